@@ -1,0 +1,363 @@
+"""Seeded synthetic inputs for the LSA decode hot path.
+
+Test and benchmark infrastructure.  This module produces the bytes that both
+the GPU path and the CPU oracle consume, and holds none of the method's
+arithmetic: no scoring, no selection, no attention.  It only draws random
+numbers, rounds them to the storage dtypes and lays them out in memory.
+
+Random numbers come from SplitMix64 evaluated as a counter-based generator
+(``draw(key, i) = mix64(key + (i + 1) * GAMMA)``), keyed per (seed, stream), so
+every tensor element can be regenerated independently of thread count or
+device.  Normal draws map the top 16 bits of a draw through a 65536-entry
+inverse-normal-CDF table (bin midpoints), which lets host C code and the HIP
+device fill produce bit-identical bf16 K/V without transcendental functions on
+either side.
+
+Workload shapes follow the paper's decode-time setting (Memory Indexer over
+64- or 128-token compressed chunks, Sec. 2.1; 1M-token serving, Sec. 2.5) and
+the five presets below.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import statistics
+import subprocess
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_HOST_SO = os.path.join(_HERE, "libsynth.so")
+_DEV_SO = os.path.join(_HERE, "libsynth_dev.so")
+
+GAMMA = 0x9E3779B97F4A7C15
+STREAM_K, STREAM_V, STREAM_Q, STREAM_E, STREAM_QE, STREAM_LEN, STREAM_QE_NOISE = 1, 2, 3, 4, 5, 6, 7
+M64 = (1 << 64) - 1
+
+
+# --------------------------------------------------------------------------- RNG
+def _mix64_int(z: int) -> int:
+    z &= M64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & M64
+    return z ^ (z >> 31)
+
+
+def stream_key(seed: int, stream: int) -> int:
+    """Key of one (seed, stream) pair."""
+    return _mix64_int((seed * GAMMA + stream * 0xD1B54A32D192ED03 + 1) & M64)
+
+
+def _mix64(z: np.ndarray) -> np.ndarray:
+    z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+    z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+    return z ^ (z >> np.uint64(31))
+
+
+def draws(key: int, start: int, n: int) -> np.ndarray:
+    """Raw 64-bit draws at counters [start, start + n)."""
+    with np.errstate(over="ignore"):
+        i = np.arange(start, start + n, dtype=np.uint64) + np.uint64(1)
+        return _mix64(np.uint64(key) + i * np.uint64(GAMMA))
+
+
+def uniform53(key: int, start: int, n: int) -> np.ndarray:
+    return (draws(key, start, n) >> np.uint64(11)).astype(np.float64) * (2.0 ** -53)
+
+
+# ----------------------------------------------------------------- rounding
+def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round-to-nearest-even from float64 straight to bf16 (no double rounding)."""
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)                      # x = m * 2**e, 0.5 <= |m| < 1
+    e = np.maximum(e, -125)                 # below the normal range the quantum stays 2**-133
+    q = np.rint(np.ldexp(x, 8 - e))         # significand on an 8-bit grid, ties to even
+    r = np.ldexp(q, e - 8).astype(np.float32)  # exact in float32
+    return (r.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f64(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+# ------------------------------------------------------------- normal table
+_TABLES: Dict[str, np.ndarray] = {}
+
+
+def normal_table_f64() -> np.ndarray:
+    """inv_cdf((u + 0.5) / 65536) for u in [0, 65536)."""
+    if "f64" not in _TABLES:
+        nd = statistics.NormalDist()
+        _TABLES["f64"] = np.array([nd.inv_cdf((u + 0.5) / 65536.0) for u in range(65536)], dtype=np.float64)
+    return _TABLES["f64"]
+
+
+def normal_table_bf16() -> np.ndarray:
+    if "bf16" not in _TABLES:
+        _TABLES["bf16"] = f64_to_bf16_bits(normal_table_f64())
+    return _TABLES["bf16"]
+
+
+def normal_f64(key: int, start: int, n: int) -> np.ndarray:
+    return normal_table_f64()[(draws(key, start, n) >> np.uint64(48)).astype(np.int64)]
+
+
+def normal_bf16(key: int, start: int, n: int) -> np.ndarray:
+    return normal_table_bf16()[(draws(key, start, n) >> np.uint64(48)).astype(np.int64)]
+
+
+def int8_uniform(key: int, start: int, n: int) -> np.ndarray:
+    """Uniform integers in [-127, 127] (multiply-shift range reduction)."""
+    hi = draws(key, start, n) >> np.uint64(32)
+    return ((hi * np.uint64(255)) >> np.uint64(32)).astype(np.int64) - 127
+
+
+# ---------------------------------------------------------------- problems
+@dataclass
+class Problem:
+    """Shape of one decode step.
+
+    ``keep`` is the per-sequence keep budget k_b (per lookahead query when
+    ``n_lookahead > 1``; the retained set is then the union of the per-query
+    top-k sets).
+    """
+    name: str
+    ctx_tokens: List[int]
+    chunk: int
+    keep: List[int]
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int = 128
+    emb_dim: int = 256
+    n_lookahead: int = 1
+    n_qtok: int = 1
+    emb_dtype: str = "bf16"          # 'f32' | 'bf16' | 'i8'
+    planted: int = 0                 # planted relevant chunks per sequence
+    q_scale: float = 1.0             # multiplier applied to q before rounding to bf16
+    qe_rho: float = 0.95             # correlation of lookahead query embeddings
+    meta: Dict[str, object] = field(default_factory=dict)
+
+    @property
+    def batch(self) -> int:
+        return len(self.ctx_tokens)
+
+    @property
+    def n_chunks(self) -> List[int]:
+        return [L // self.chunk for L in self.ctx_tokens]
+
+    @property
+    def chunk_offsets(self) -> List[int]:
+        off = [0]
+        for n in self.n_chunks:
+            off.append(off[-1] + n)
+        return off
+
+    @property
+    def total_chunks(self) -> int:
+        return self.chunk_offsets[-1]
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+    def max_sel_b(self, b: int) -> int:
+        return min(self.n_lookahead * self.keep[b], self.n_chunks[b])
+
+    @property
+    def max_sel(self) -> int:
+        return max(self.max_sel_b(b) for b in range(self.batch))
+
+    def kv_elems(self) -> int:
+        """Elements of one of K or V (whole cache)."""
+        return self.total_chunks * self.n_kv_heads * self.chunk * self.head_dim
+
+
+def planted_positions(n: int, p: int) -> np.ndarray:
+    """p positions spread evenly over n chunks: floor((2i + 1) n / (2p))."""
+    i = np.arange(p, dtype=np.int64)
+    return ((2 * i + 1) * n) // (2 * p)
+
+
+def make_problem(name: str, seed: int = 0) -> Problem:
+    """The five workload presets of the decode hot path."""
+    if name == "tiny":
+        return Problem("tiny", [4096], 64, [8], 8, 8, emb_dtype="f32", planted=3,
+                       q_scale=1.0 / math.sqrt(128.0))
+    if name == "int8":
+        return Problem("int8", [131072] * 4, 64, [256] * 4, 32, 8, emb_dtype="i8", planted=16)
+    if name == "paper1m":
+        n = 1048576 // 64
+        return Problem("paper1m", [1048576], 64, [int(0.10 * n)], 32, 8, emb_dtype="bf16", planted=64)
+    if name == "batch32":
+        u = uniform53(stream_key(seed, STREAM_LEN), 0, 32)
+        lo, hi = math.log(32768.0), math.log(524288.0)
+        lens = [64 * int(math.exp(lo + (hi - lo) * float(x)) // 64) for x in u]
+        keep = [max(1, int(0.135 * (L // 64))) for L in lens]
+        return Problem("batch32", lens, 64, keep, 32, 8, emb_dtype="bf16", planted=16)
+    if name == "lookahead":
+        return Problem("lookahead", [1048576] * 8, 128, [512] * 8, 64, 8, emb_dtype="bf16",
+                       n_lookahead=16, n_qtok=16, planted=0)
+    raise KeyError(name)
+
+
+PRESETS = ("tiny", "int8", "paper1m", "batch32", "lookahead")
+
+
+# ------------------------------------------------------------ host inputs
+def _unit_rows(x: np.ndarray) -> np.ndarray:
+    return x / np.linalg.norm(x, axis=-1, keepdims=True)
+
+
+def _store(x64: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return x64.astype(np.float32)
+    if dtype == "bf16":
+        return f64_to_bf16_bits(x64)
+    raise ValueError(dtype)
+
+
+def host_inputs(prob: Problem, seed: int) -> Dict[str, object]:
+    """Small tensors of one step, generated on the host.
+
+    Returns ``qe`` [B][Q][D], ``E`` [sum n_b][D] (float32, bf16 bits as uint16,
+    or int8), ``q`` [B][Tq][Hq][d] bf16 bits and ``planted`` (list of global-
+    per-sequence chunk ids).
+    """
+    B, Q, D = prob.batch, prob.n_lookahead, prob.emb_dim
+    offs = prob.chunk_offsets
+    kE, kQE, kN = stream_key(seed, STREAM_E), stream_key(seed, STREAM_QE), stream_key(seed, STREAM_QE_NOISE)
+    planted = [planted_positions(n, prob.planted) for n in prob.n_chunks]
+    if prob.emb_dtype == "i8":
+        E = int8_uniform(kE, 0, offs[-1] * D).reshape(offs[-1], D)
+        qe = int8_uniform(kQE, 0, B * Q * D).reshape(B, Q, D)
+        for b in range(B):
+            sign = np.where(qe[b, 0] >= 0, 127, -127)
+            for c in planted[b]:
+                E[offs[b] + c] = sign
+        E, qe = E.astype(np.int8), qe.astype(np.int8)
+    else:
+        E64 = _unit_rows(normal_f64(kE, 0, offs[-1] * D).reshape(offs[-1], D))
+        base = _unit_rows(normal_f64(kQE, 0, B * D).reshape(B, D))
+        if Q == 1:
+            qe64 = base[:, None, :]
+        else:
+            g = _unit_rows(normal_f64(kN, 0, B * Q * D).reshape(B, Q, D))
+            rho = prob.qe_rho
+            qe64 = _unit_rows(math.sqrt(rho) * base[:, None, :] + math.sqrt(1.0 - rho) * g)
+        for b in range(B):
+            rows = offs[b] + planted[b]
+            E64[rows] = _unit_rows(E64[rows] + 0.5 * base[b][None, :])
+        E, qe = _store(E64, prob.emb_dtype), _store(qe64, prob.emb_dtype)
+    nq = B * prob.n_qtok * prob.n_q_heads * prob.head_dim
+    q = normal_bf16(stream_key(seed, STREAM_Q), 0, nq)
+    if prob.q_scale != 1.0:
+        q = f64_to_bf16_bits(bf16_bits_to_f64(q) * prob.q_scale)
+    q = q.reshape(B, prob.n_qtok, prob.n_q_heads, prob.head_dim)
+    return {"qe": qe, "E": E, "q": q, "planted": planted}
+
+
+# ------------------------------------------------------------ K/V on host
+def _so(path: str, builder) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        builder()
+    return ctypes.CDLL(path)
+
+
+_host_lib: Optional[ctypes.CDLL] = None
+
+
+def host_lib() -> ctypes.CDLL:
+    global _host_lib
+    if _host_lib is None:
+        lib = _so(_HOST_SO, build_host)
+        lib.synth_kv_chunks.argtypes = [ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_void_p]
+        lib.synth_kv_chunks.restype = None
+        lib.synth_draws.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p]
+        lib.synth_stream_key.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        lib.synth_stream_key.restype = ctypes.c_uint64
+        _host_lib = lib
+    return _host_lib
+
+
+def kv_chunks(prob: Problem, seed: int, which: str, b: int, h: int, chunks) -> np.ndarray:
+    """K or V of sequence b, KV head h, for the listed (per-sequence) chunk ids.
+
+    Returns bf16 bits shaped [len(chunks)][chunk][head_dim], token-major.
+    """
+    stream = STREAM_K if which == "k" else STREAM_V
+    chunks = np.ascontiguousarray(np.asarray(chunks, dtype=np.int64) + prob.chunk_offsets[b])
+    out = np.empty((len(chunks), prob.chunk, prob.head_dim), dtype=np.uint16)
+    tab = np.ascontiguousarray(normal_table_bf16())
+    host_lib().synth_kv_chunks(stream_key(seed, stream), tab.ctypes.data, prob.n_kv_heads, h, prob.head_dim,
+                               prob.chunk, chunks.ctypes.data, len(chunks), out.ctypes.data)
+    return out
+
+
+def kv_head_sparse(prob: Problem, seed: int, which: str, b: int, h: int, chunks) -> np.ndarray:
+    """Logical token-major K or V of one (sequence, KV head): [ctx_tokens][head_dim].
+
+    Only the listed chunks are filled; every other token is zero.
+    """
+    C = prob.chunk
+    full = np.zeros((prob.ctx_tokens[b], prob.head_dim), dtype=np.uint16)
+    chunks = np.asarray(chunks, dtype=np.int64)
+    if len(chunks):
+        vals = kv_chunks(prob, seed, which, b, h, chunks)
+        full.reshape(-1, C, prob.head_dim)[chunks] = vals
+    return full
+
+
+# ------------------------------------------------------- K/V on the device
+_dev_lib: Optional[ctypes.CDLL] = None
+
+
+def dev_lib() -> ctypes.CDLL:
+    global _dev_lib
+    if _dev_lib is None:
+        lib = _so(_DEV_SO, build_device)
+        lib.synth_fill_kv_device.argtypes = [ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                             ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+        lib.synth_fill_kv_device.restype = ctypes.c_int
+        _dev_lib = lib
+    return _dev_lib
+
+
+def fill_kv_device(prob: Problem, seed: int, which: str, out_ptr: int, table_ptr: int, stream_ptr: int,
+                   chunk_stride: Optional[int] = None, head_stride: Optional[int] = None) -> None:
+    """Fill a device K (``[chunk][head][token][dim]``) or V (``[chunk][head][dim][token]``) cache.
+
+    ``table_ptr`` is a device copy of :func:`normal_table_bf16`.
+    """
+    C, d, H = prob.chunk, prob.head_dim, prob.n_kv_heads
+    hs = C * d if head_stride is None else head_stride
+    cs = H * C * d if chunk_stride is None else chunk_stride
+    stream = STREAM_K if which == "k" else STREAM_V
+    rc = dev_lib().synth_fill_kv_device(stream_key(seed, stream), table_ptr, out_ptr, prob.total_chunks, H, C, d,
+                                        cs, hs, 0 if which == "k" else 1, stream_ptr)
+    if rc != 0:
+        raise RuntimeError(f"synth_fill_kv_device failed with code {rc}")
+
+
+# ------------------------------------------------------------------ build
+def build_host() -> None:
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", os.path.join(_HERE, "synth.c"),
+                           "-o", _HOST_SO])
+
+
+def build_device() -> None:
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    subprocess.check_call([hipcc, "--offload-arch=gfx950", "-O3", "-fPIC", "-shared", "-std=c++17",
+                           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                           os.path.join(_HERE, "synth_dev.hip"), "-o", _DEV_SO],
+                          stderr=subprocess.DEVNULL if os.environ.get("LSA_QUIET_BUILD") else None)
+
+
+def build() -> None:
+    build_host()
+    build_device()

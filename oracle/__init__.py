@@ -1,0 +1,179 @@
+"""CPU oracle for the LSA decode hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s CPU-baseline leg
+may import this package.  It wraps ``lsa_oracle.c`` (float64 / int64, plain
+loops) and composes its three functions in the paper's order for one decode
+step:
+
+* O1 score -- Memory Indexer score, Sec. 2.1 Eq. 4, read as the dual-encoder dot
+  product (one head, unit gate);
+* O2 select -- top-k with lowest-index tie-break, ascending output; union of the
+  per-query sets for several lookahead queries (Sec. 2.1 Eq. corecomp and
+  Sec. 2.4 Eq. union; K_max of Sec. 2.5 is the keep budget);
+* O3 attend -- softmax(q K^T * scale) V over the tokens of the kept chunks.
+
+It shares no code with the HIP library; the only common input is the seeded
+generator in ``lsa_synth``.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+from typing import Callable, Dict, List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SO = os.path.join(_HERE, "liblsa_oracle.so")
+_lib: Optional[ctypes.CDLL] = None
+
+_P = ctypes.c_void_p
+_I32, _I64, _F64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+
+
+def build() -> None:
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math",
+                           os.path.join(_HERE, "lsa_oracle.c"), "-o", _SO, "-lm"])
+
+
+def bind(path: str) -> ctypes.CDLL:
+    """Load an oracle shared object and declare its signatures."""
+    L = ctypes.CDLL(path)
+    L.oracle_score_f32.argtypes = [_P, _P, _I64, _I32, _P]
+    L.oracle_score_bf16.argtypes = [_P, _P, _I64, _I32, _P]
+    L.oracle_score_i8.argtypes = [_P, _P, _I64, _I32, _P]
+    for f in (L.oracle_score_f32, L.oracle_score_bf16, L.oracle_score_i8):
+        f.restype = None
+    L.oracle_topk_f64.argtypes = [_P, _I64, _I64, _P]
+    L.oracle_topk_f64.restype = _I64
+    L.oracle_topk_i64.argtypes = [_P, _I64, _I64, _P]
+    L.oracle_topk_i64.restype = _I64
+    L.oracle_union.argtypes = [_P, _I32, _I64, _I64, _P]
+    L.oracle_union.restype = _I64
+    L.oracle_attention.argtypes = [_P, _I32, _P, _P, _I64, _I32, _I32, _P, _I64, _F64, _P, _P]
+    L.oracle_attention.restype = ctypes.c_int
+    return L
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO):
+            build()
+        _lib = bind(_SO)
+    return _lib
+
+
+def _c(a: np.ndarray, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+# ------------------------------------------------------------------ O1 score
+def score(qe: np.ndarray, E: np.ndarray, emb_dtype: str) -> np.ndarray:
+    """Scores of one query embedding qe [D] against chunk embeddings E [n][D].
+
+    float64 for 'f32' / 'bf16' (bf16 given as uint16 bit patterns), int64 for 'i8'.
+    """
+    n, D = E.shape
+    if emb_dtype == "i8":
+        out = np.empty(n, dtype=np.int64)
+        qe, E = _c(qe, np.int8), _c(E, np.int8)
+        lib().oracle_score_i8(qe.ctypes.data, E.ctypes.data, n, D, out.ctypes.data)
+        return out
+    out = np.empty(n, dtype=np.float64)
+    if emb_dtype == "f32":
+        qe, E = _c(qe, np.float32), _c(E, np.float32)
+        lib().oracle_score_f32(qe.ctypes.data, E.ctypes.data, n, D, out.ctypes.data)
+    elif emb_dtype == "bf16":
+        qe, E = _c(qe, np.uint16), _c(E, np.uint16)
+        lib().oracle_score_bf16(qe.ctypes.data, E.ctypes.data, n, D, out.ctypes.data)
+    else:
+        raise ValueError(emb_dtype)
+    return out
+
+
+# ----------------------------------------------------------------- O2 select
+def topk(s: np.ndarray, k: int) -> np.ndarray:
+    """The k chunk ids with the largest scores (lower id wins ties), ascending."""
+    n = len(s)
+    out = np.empty(k, dtype=np.int32)
+    if s.dtype == np.int64:
+        s = _c(s, np.int64)
+        r = lib().oracle_topk_i64(s.ctypes.data, n, k, out.ctypes.data)
+    else:
+        s = _c(s, np.float64)
+        r = lib().oracle_topk_f64(s.ctypes.data, n, k, out.ctypes.data)
+    if r != k:
+        raise ValueError(f"oracle_topk rejected n={n} k={k}")
+    return out
+
+
+def union(lists: np.ndarray, n: int) -> np.ndarray:
+    """Ascending union of the rows of ``lists`` [n_lists][k]."""
+    lists = _c(lists, np.int32)
+    out = np.empty(n, dtype=np.int32)
+    u = lib().oracle_union(lists.ctypes.data, lists.shape[0], lists.shape[1], n, out.ctypes.data)
+    if u < 0:
+        raise ValueError("oracle_union rejected its input")
+    return out[:u].copy()
+
+
+# ------------------------------------------------------------------ O3 attend
+def attention(q_rows: np.ndarray, Kh: np.ndarray, Vh: np.ndarray, sel: np.ndarray, chunk: int,
+              scale: Optional[float] = None):
+    """Attention of q_rows [R][d] over the tokens of chunks ``sel`` of one KV head.
+
+    Kh, Vh are logical token-major [n_tok][d] bf16 bit patterns.  Returns
+    (out [R][d] float64, lse [R] float64).
+    """
+    R, d = q_rows.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    q_rows, Kh, Vh = _c(q_rows, np.uint16), _c(Kh, np.uint16), _c(Vh, np.uint16)
+    sel = _c(sel, np.int32)
+    out = np.empty((R, d), dtype=np.float64)
+    lse = np.empty(R, dtype=np.float64)
+    rc = lib().oracle_attention(q_rows.ctypes.data, R, Kh.ctypes.data, Vh.ctypes.data, Kh.shape[0], d, chunk,
+                                sel.ctypes.data, len(sel), float(scale), out.ctypes.data, lse.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_attention rejected its input")
+    return out, lse
+
+
+# ---------------------------------------------------------------- O4 step
+def select_for_sequence(prob, inputs: Dict[str, object], b: int):
+    """O1 then O2 for sequence b.
+
+    Returns (scores [Q][n_b], per-query lists [Q][k_b], kept ascending chunk ids).
+    """
+    Q = prob.n_lookahead
+    lo, hi = prob.chunk_offsets[b], prob.chunk_offsets[b + 1]
+    E_b = inputs["E"][lo:hi]
+    scores = np.stack([score(inputs["qe"][b, j], E_b, prob.emb_dtype) for j in range(Q)])
+    lists = np.stack([topk(scores[j], prob.keep[b]) for j in range(Q)])
+    kept = lists[0].copy() if Q == 1 else union(lists, prob.n_chunks[b])
+    return scores, lists, kept
+
+
+def attend_rows(prob, inputs: Dict[str, object], b: int, kept: np.ndarray, rows: Sequence,
+                kv: Callable[[str, int, int, np.ndarray], np.ndarray], scale: Optional[float] = None):
+    """O3 for the (t, h) query rows of sequence b over the kept chunks.
+
+    ``kv(which, b, g, chunks)`` supplies the logical K or V of KV head g as
+    [ctx_tokens][d] (only the kept chunks need to be filled).  Returns
+    {(t, h): (out [d], lse)}.
+    """
+    G = prob.group
+    by_g: Dict[int, List] = {}
+    for (t, h) in rows:
+        by_g.setdefault(h // G, []).append((t, h))
+    res = {}
+    for g, rs in sorted(by_g.items()):
+        Kh, Vh = kv("k", b, g, kept), kv("v", b, g, kept)
+        qr = np.stack([inputs["q"][b, t, h] for (t, h) in rs])
+        out, lse = attention(qr, Kh, Vh, kept, prob.chunk, scale)
+        for j, key in enumerate(rs):
+            res[key] = (out[j], lse[j])
+    return res

@@ -1,0 +1,191 @@
+/*
+ * CPU oracle for the LSA decode hot path -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, obviously correct reference for what one decode step of
+ * Lookahead Sparse Attention computes: score every compressed chunk with the
+ * Memory Indexer, keep the top-k chunks, attend over the kept chunks only.
+ * Only the test suite, the smoke check and the benchmark's CPU baseline may
+ * load this library; the product path never links or calls it.
+ *
+ * Arithmetic is float64 (int64 for int8 embeddings), every loop runs in index
+ * order, and nothing is blocked, fused or reordered beyond the definitions.
+ * Inputs in bf16 are passed as their raw 16-bit patterns and widened here.
+ *
+ * Readings of the paper that this file encodes:
+ *  - Score (Sec. 2.1, Eq. 4): the gated multi-head form with one indexer head
+ *    and unit gate, i.e. the dual-encoder dot product s_c = qe . E_c.  The
+ *    sigmoid and ReLU of Eq. 4 are non-decreasing, so they cannot reorder
+ *    chunks with positive dot products; the keep-budget selection is taken on
+ *    the raw dot product.
+ *  - Selection (Sec. 2.1, Eq. corecomp; Sec. 2.5 bound K_max): the k chunks with
+ *    the largest score, ties broken towards the lower chunk index, reported in
+ *    ascending chunk order.  With several lookahead queries the kept set is the
+ *    union of the per-query top-k sets (the set union of Eq. union).
+ *  - Attention (Sec. 2.1, core attention over the selected entries):
+ *    softmax(q K^T * scale) V over the tokens of the kept chunks, with query
+ *    head h reading KV head floor(h / G).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+static double bf16_to_f64(uint16_t bits) {
+  uint32_t u = (uint32_t)bits << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* ---------------------------------------------------------------- O1 score */
+
+/* s[c] = sum_i qe[i] * E[c][i], float32 inputs, float64 sum (Sec. 2.1, Eq. 4). */
+void oracle_score_f32(const float* qe, const float* E, int64_t n, int32_t D, double* out) {
+  for (int64_t c = 0; c < n; ++c) {
+    double s = 0.0;
+    for (int32_t i = 0; i < D; ++i) s += (double)qe[i] * (double)E[c * D + i];
+    out[c] = s;
+  }
+}
+
+/* Same, bf16 inputs given as bit patterns. */
+void oracle_score_bf16(const uint16_t* qe, const uint16_t* E, int64_t n, int32_t D, double* out) {
+  for (int64_t c = 0; c < n; ++c) {
+    double s = 0.0;
+    for (int32_t i = 0; i < D; ++i) s += bf16_to_f64(qe[i]) * bf16_to_f64(E[c * D + i]);
+    out[c] = s;
+  }
+}
+
+/* Same, int8 inputs, exact int64 sum. */
+void oracle_score_i8(const int8_t* qe, const int8_t* E, int64_t n, int32_t D, int64_t* out) {
+  for (int64_t c = 0; c < n; ++c) {
+    int64_t s = 0;
+    for (int32_t i = 0; i < D; ++i) s += (int64_t)qe[i] * (int64_t)E[c * D + i];
+    out[c] = s;
+  }
+}
+
+/* ----------------------------------------------------------------- O2 top-k */
+
+typedef struct { double s; int64_t c; } scored_f;
+typedef struct { int64_t s; int64_t c; } scored_i;
+
+/* Larger score first; equal scores: lower chunk index first. */
+static int by_score_desc_f(const void* a, const void* b) {
+  const scored_f* x = (const scored_f*)a;
+  const scored_f* y = (const scored_f*)b;
+  if (x->s > y->s) return -1;
+  if (x->s < y->s) return 1;
+  return (x->c > y->c) - (x->c < y->c);
+}
+
+static int by_score_desc_i(const void* a, const void* b) {
+  const scored_i* x = (const scored_i*)a;
+  const scored_i* y = (const scored_i*)b;
+  if (x->s > y->s) return -1;
+  if (x->s < y->s) return 1;
+  return (x->c > y->c) - (x->c < y->c);
+}
+
+static int ascending_i32(const void* a, const void* b) {
+  const int32_t x = *(const int32_t*)a, y = *(const int32_t*)b;
+  return (x > y) - (x < y);
+}
+
+/* Top-k of float64 scores: writes the k kept chunk ids in ascending order and
+ * returns k, or -1 on a bad argument or allocation failure. */
+int64_t oracle_topk_f64(const double* s, int64_t n, int64_t k, int32_t* out) {
+  if (n <= 0 || k < 1 || k > n) return -1;
+  scored_f* v = (scored_f*)malloc((size_t)n * sizeof *v);
+  if (!v) return -1;
+  for (int64_t c = 0; c < n; ++c) { v[c].s = s[c]; v[c].c = c; }
+  qsort(v, (size_t)n, sizeof *v, by_score_desc_f);
+  for (int64_t j = 0; j < k; ++j) out[j] = (int32_t)v[j].c;
+  free(v);
+  qsort(out, (size_t)k, sizeof *out, ascending_i32);
+  return k;
+}
+
+/* Top-k of int64 scores (int8 embeddings). */
+int64_t oracle_topk_i64(const int64_t* s, int64_t n, int64_t k, int32_t* out) {
+  if (n <= 0 || k < 1 || k > n) return -1;
+  scored_i* v = (scored_i*)malloc((size_t)n * sizeof *v);
+  if (!v) return -1;
+  for (int64_t c = 0; c < n; ++c) { v[c].s = s[c]; v[c].c = c; }
+  qsort(v, (size_t)n, sizeof *v, by_score_desc_i);
+  for (int64_t j = 0; j < k; ++j) out[j] = (int32_t)v[j].c;
+  free(v);
+  qsort(out, (size_t)k, sizeof *out, ascending_i32);
+  return k;
+}
+
+/* Union of n_lists chunk-id lists of length k each (row-major), ascending.
+ * Returns the union size, or -1 on a bad argument. */
+int64_t oracle_union(const int32_t* lists, int32_t n_lists, int64_t k, int64_t n, int32_t* out) {
+  if (n <= 0 || n_lists < 1 || k < 0) return -1;
+  unsigned char* in = (unsigned char*)calloc((size_t)n, 1);
+  if (!in) return -1;
+  for (int64_t j = 0; j < (int64_t)n_lists * k; ++j) {
+    if (lists[j] < 0 || lists[j] >= n) { free(in); return -1; }
+    in[lists[j]] = 1;
+  }
+  int64_t u = 0;
+  for (int64_t c = 0; c < n; ++c)
+    if (in[c]) out[u++] = (int32_t)c;
+  free(in);
+  return u;
+}
+
+/* ------------------------------------------------------------- O3 attention */
+
+/*
+ * Attention of R query rows against the tokens of the selected chunks of one
+ * KV head.
+ *   q     [R][d]        bf16 bits
+ *   Kh,Vh [n_tok][d]    bf16 bits, logical token-major for this KV head
+ *   sel   [nsel]        chunk ids; the token list is the concatenation, over
+ *                       sel in the given order, of tokens [c*C, c*C + C)
+ *   out   [R][d]        float64,  out = sum_i w_i V_i / sum_i w_i
+ *   lse   [R]           float64,  m + log(sum_i w_i)
+ * where l_i = scale * q . K_i, m = max_i l_i and w_i = exp(l_i - m).
+ * Returns 0, or -1 on a bad argument or allocation failure.
+ */
+int oracle_attention(const uint16_t* q, int32_t R, const uint16_t* Kh, const uint16_t* Vh,
+                     int64_t n_tok, int32_t d, int32_t C, const int32_t* sel, int64_t nsel,
+                     double scale, double* out, double* lse) {
+  if (R < 1 || d < 1 || C < 1 || nsel < 1) return -1;
+  for (int64_t j = 0; j < nsel; ++j)
+    if (sel[j] < 0 || (int64_t)(sel[j] + 1) * C > n_tok) return -1;
+  const int64_t T = nsel * C;
+  double* logit = (double*)malloc((size_t)T * sizeof *logit);
+  if (!logit) return -1;
+  for (int32_t r = 0; r < R; ++r) {
+    const uint16_t* qr = q + (int64_t)r * d;
+    for (int64_t i = 0; i < T; ++i) {
+      const int64_t tok = (int64_t)sel[i / C] * C + i % C;
+      double dot = 0.0;
+      for (int32_t e = 0; e < d; ++e) dot += bf16_to_f64(qr[e]) * bf16_to_f64(Kh[tok * d + e]);
+      logit[i] = dot * scale;
+    }
+    double m = logit[0];
+    for (int64_t i = 1; i < T; ++i)
+      if (logit[i] > m) m = logit[i];
+    double Z = 0.0;
+    for (int64_t i = 0; i < T; ++i) {
+      logit[i] = exp(logit[i] - m); /* the weight w_i from here on */
+      Z += logit[i];
+    }
+    for (int32_t e = 0; e < d; ++e) {
+      double acc = 0.0;
+      for (int64_t i = 0; i < T; ++i) {
+        const int64_t tok = (int64_t)sel[i / C] * C + i % C;
+        acc += logit[i] * bf16_to_f64(Vh[tok * d + e]);
+      }
+      out[(int64_t)r * d + e] = acc / Z;
+    }
+    lse[r] = m + log(Z);
+  }
+  free(logit);
+  return 0;
+}

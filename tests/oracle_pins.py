@@ -1,0 +1,244 @@
+"""Pins that tie the CPU oracle to the paper and to mathematics, not to itself.
+
+Each ``pin_*`` function raises AssertionError when the oracle disagrees with
+an independent fact: a hand-worked example, a closed form, brute force over all
+subsets, a library routine that computes the same definition by another route,
+or an invariant the paper states (all chunks kept == dense attention, Sec. 2.5
+cold start).  ``test_oracle.py`` runs them on the real oracle and
+``test_oracle_mutants.py`` checks that planted mistakes in the oracle's C
+source make at least one of them fail.
+"""
+from __future__ import annotations
+
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import scipy.special
+import torch
+
+import lsa_synth as synth
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _bf16(x) -> np.ndarray:
+    return synth.f64_to_bf16_bits(np.asarray(x, dtype=np.float64))
+
+
+def _f64(bits) -> np.ndarray:
+    return synth.bf16_bits_to_f64(bits)
+
+
+# ------------------------------------------------------------------ scores
+def pin_score_library_matmul():
+    """O1 for f32 and bf16 equals a float64 matrix-vector product (numpy)."""
+    rng = np.random.default_rng(1)
+    for D in (64, 256):
+        E = rng.standard_normal((37, D)).astype(np.float32)
+        qe = rng.standard_normal(D).astype(np.float32)
+        ref = E.astype(np.float64) @ qe.astype(np.float64)
+        got = oracle.score(qe, E, "f32")
+        assert np.allclose(got, ref, rtol=1e-12, atol=1e-12), "f32 score != E @ qe"
+        Eb, qb = _bf16(E), _bf16(qe)
+        ref = _f64(Eb) @ _f64(qb)
+        got = oracle.score(qb, Eb, "bf16")
+        assert np.allclose(got, ref, rtol=1e-12, atol=1e-12), "bf16 score != E @ qe"
+
+
+def pin_score_int8_exact():
+    """O1 for int8 is the exact integer dot product (Python integers)."""
+    rng = np.random.default_rng(2)
+    E = rng.integers(-127, 128, size=(23, 256)).astype(np.int8)
+    qe = rng.integers(-127, 128, size=256).astype(np.int8)
+    got = oracle.score(qe, E, "i8")
+    for c in range(E.shape[0]):
+        exact = sum(int(a) * int(b) for a, b in zip(qe.tolist(), E[c].tolist()))
+        assert int(got[c]) == exact, f"int8 score of chunk {c}"
+
+
+def pin_score_closed_forms():
+    """One-hot chunk rows read out one query component; the sign-aligned
+    planted row scores 127 * sum |qe_i|; scaling qe by 2 doubles every score."""
+    D = 16
+    qe = np.arange(1, D + 1, dtype=np.float64) * np.array([(-1) ** i for i in range(D)])
+    E = np.eye(D, dtype=np.float32)
+    got = oracle.score(qe.astype(np.float32), E, "f32")
+    assert np.array_equal(got, qe), "one-hot rows must return the query components"
+    q8 = np.array([5, -3, 0, 127, -127, 1, -1, 2] * 32, dtype=np.int8)
+    row = np.where(q8 >= 0, 127, -127).astype(np.int8)[None, :]
+    s = oracle.score(q8, row, "i8")
+    assert int(s[0]) == 127 * int(np.abs(q8.astype(np.int64)).sum()), "sign-aligned planted score"
+    rng = np.random.default_rng(3)
+    E = rng.standard_normal((9, 32)).astype(np.float32)
+    q = rng.standard_normal(32).astype(np.float32)
+    assert np.array_equal(oracle.score(2 * q, E, "f32"), 2 * oracle.score(q, E, "f32")), "homogeneity"
+
+
+# -------------------------------------------------------------------- top-k
+def pin_topk_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "topk_worked.json")))
+    s = np.array(g["scores"], dtype=np.float64)
+    for case in g["cases"]:
+        got = oracle.topk(s, case["k"])
+        assert got.tolist() == case["kept"], f"worked top-k, k={case['k']}"
+        got_i = oracle.topk(s.astype(np.int64), case["k"])
+        assert got_i.tolist() == case["kept"], f"worked int top-k, k={case['k']}"
+    u = g["union"]
+    assert oracle.union(np.array(u["lists"]), u["n"]).tolist() == u["kept"], "worked union"
+
+
+def pin_topk_bruteforce():
+    """Over all C(n, k) subsets: the kept set has the largest score sum and,
+    among those, the lexicographically smallest ascending id list."""
+    rng = np.random.default_rng(4)
+    for trial in range(60):
+        n = int(rng.integers(1, 11))
+        k = int(rng.integers(1, n + 1))
+        s = rng.integers(-3, 4, size=n).astype(np.float64)  # many ties
+        best, best_sum = None, -math.inf
+        for comb in itertools.combinations(range(n), k):  # lexicographic order
+            tot = s[list(comb)].sum()
+            if tot > best_sum:
+                best, best_sum = list(comb), tot
+        assert oracle.topk(s, k).tolist() == best, f"brute force n={n} k={k} s={s.tolist()}"
+        assert oracle.topk(s.astype(np.int64), k).tolist() == best, "brute force (int)"
+
+
+def pin_topk_library_sort():
+    """Agrees with numpy's lexsort on (score desc, id asc); k=1 is numpy's
+    first argmax; k=n keeps everything; -0.0 ties +0.0."""
+    rng = np.random.default_rng(5)
+    for n, k in ((1000, 100), (2048, 256), (777, 1)):
+        s = np.round(rng.standard_normal(n), 2)  # ties
+        order = np.lexsort((np.arange(n), -s))
+        assert oracle.topk(s, k).tolist() == sorted(order[:k].tolist()), f"lexsort n={n} k={k}"
+        assert oracle.topk(s, 1).tolist() == [int(np.argmax(s))], "first argmax"
+        assert oracle.topk(s, n).tolist() == list(range(n)), "k = n"
+    s = np.array([0.0, -0.0, 0.0, -1.0, -0.0])
+    assert oracle.topk(s, 2).tolist() == [0, 1], "-0.0 and +0.0 tie"
+    assert oracle.topk(s, 4).tolist() == [0, 1, 2, 4], "-0.0 and +0.0 tie"
+
+
+def pin_union_bruteforce():
+    """Union of per-query top-k sets equals the Python set union of brute-force
+    sets, and obeys max|S_j| <= |U| <= min(sum |S_j|, n)."""
+    rng = np.random.default_rng(6)
+    for _ in range(20):
+        n, Q = int(rng.integers(4, 12)), int(rng.integers(2, 5))
+        k = int(rng.integers(1, n + 1))
+        lists = []
+        for _ in range(Q):
+            s = rng.integers(-2, 3, size=n).astype(np.float64)
+            lists.append(sorted(np.lexsort((np.arange(n), -s))[:k].tolist()))
+        u = oracle.union(np.array(lists), n).tolist()
+        assert u == sorted(set().union(*map(set, lists))), "union"
+        assert k <= len(u) <= min(Q * k, n)
+
+
+def pin_planted_selected(name: str, seeds=(0,)):
+    """Planted high-similarity chunks are always in the kept set."""
+    for seed in seeds:
+        prob = synth.make_problem(name, seed)
+        inp = synth.host_inputs(prob, seed)
+        for b in range(prob.batch):
+            _, _, kept = oracle.select_for_sequence(prob, inp, b)
+            missing = set(inp["planted"][b].tolist()) - set(kept.tolist())
+            assert not missing, f"{name} seed {seed} seq {b}: planted chunks {sorted(missing)} not kept"
+
+
+# ---------------------------------------------------------------- attention
+def pin_attention_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "attention_worked.json")))
+    out, lse = oracle.attention(_bf16(g["q"]), _bf16(g["K"]), _bf16(g["V"]), np.array(g["kept"]), g["chunk"],
+                                g["scale"])
+    assert np.allclose(out, g["out"], rtol=1e-14, atol=0), "worked attention output"
+    assert np.allclose(lse, g["lse"], rtol=1e-14, atol=0), "worked attention lse"
+
+
+def _rand_head(rng, n_tok, d, scale_k=1.0):
+    return _bf16(rng.standard_normal((n_tok, d)) * scale_k), _bf16(rng.standard_normal((n_tok, d)))
+
+
+def pin_keep_all_is_dense():
+    """With every chunk kept the result is plain dense attention (the paper's
+    cold start keeps all chunks resident and matches the baseline exactly),
+    computed here with scipy's softmax and a numpy matmul."""
+    rng = np.random.default_rng(7)
+    for (n_chunks, C, d, R) in ((6, 4, 16, 3), (3, 64, 128, 2)):
+        K, V = _rand_head(rng, n_chunks * C, d, 0.5)
+        q = _bf16(rng.standard_normal((R, d)))
+        scale = 1.0 / math.sqrt(d)
+        out, lse = oracle.attention(q, K, V, np.arange(n_chunks), C, scale)
+        logits = (_f64(q) @ _f64(K).T) * scale
+        ref = scipy.special.softmax(logits, axis=1) @ _f64(V)
+        assert np.allclose(out, ref, rtol=1e-12, atol=1e-14), "keep-all != dense"
+        assert np.allclose(lse, scipy.special.logsumexp(logits, axis=1), rtol=1e-13), "keep-all lse"
+
+
+def pin_masked_dense_sdpa():
+    """Kept-chunk attention equals PyTorch's float64 scaled_dot_product_attention
+    with a boolean mask that hides the tokens of the dropped chunks."""
+    rng = np.random.default_rng(8)
+    n_chunks, C, d, R = 10, 8, 32, 4
+    K, V = _rand_head(rng, n_chunks * C, d, 1.5)  # sharp softmax
+    q = _bf16(rng.standard_normal((R, d)))
+    kept = np.array([1, 4, 5, 9])
+    out, _ = oracle.attention(q, K, V, kept, C, None)
+    mask = torch.zeros(R, n_chunks * C, dtype=torch.bool)
+    for c in kept:
+        mask[:, c * C:(c + 1) * C] = True
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(_f64(q))[None], torch.from_numpy(_f64(K))[None], torch.from_numpy(_f64(V))[None],
+        attn_mask=mask[None])[0].numpy()
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-14), "masked dense"
+
+
+def pin_attention_closed_forms():
+    """Constant V returns that constant; q = 0 returns the mean of the kept V
+    rows and lse = log(#kept tokens); identical keys do the same for any q;
+    a single kept token returns its own V row."""
+    rng = np.random.default_rng(9)
+    n_chunks, C, d = 7, 4, 16
+    K, V = _rand_head(rng, n_chunks * C, d)
+    kept = np.array([0, 3, 6])
+    toks = np.concatenate([np.arange(c * C, (c + 1) * C) for c in kept])
+    const = _bf16(np.full((n_chunks * C, d), 0.375))
+    out, _ = oracle.attention(_bf16(rng.standard_normal((2, d))), K, const, kept, C)
+    assert np.allclose(out, 0.375, rtol=1e-14), "constant V"
+    out, lse = oracle.attention(_bf16(np.zeros((1, d))), K, V, kept, C)
+    assert np.allclose(out[0], _f64(V)[toks].mean(axis=0), rtol=1e-12, atol=1e-14), "q = 0 mean"
+    assert abs(lse[0] - math.log(len(toks))) < 1e-13, "q = 0 lse"
+    Ksame = np.tile(K[:1], (n_chunks * C, 1))
+    out, _ = oracle.attention(_bf16(rng.standard_normal((1, d))), Ksame, V, kept, C)
+    assert np.allclose(out[0], _f64(V)[toks].mean(axis=0), rtol=1e-12, atol=1e-14), "equal keys mean"
+    out, lse = oracle.attention(_bf16(rng.standard_normal((1, d))), K, V, np.array([5]), 1)
+    assert np.array_equal(out[0], _f64(V)[5]), "single token"
+
+
+def pin_gqa_mapping():
+    """Query head h reads KV head floor(h / G): KV head g holds constant V = g + 1."""
+    prob = synth.Problem("gqa", [256], 64, [2], n_q_heads=8, n_kv_heads=2, head_dim=32, emb_dim=64,
+                         emb_dtype="f32")
+    rng = np.random.default_rng(10)
+    inp = {"q": _bf16(rng.standard_normal((1, 1, 8, 32))).reshape(1, 1, 8, 32)}
+
+    def kv(which, b, g, chunks):
+        if which == "v":
+            return _bf16(np.full((256, 32), g + 1.0))
+        return _bf16(rng.standard_normal((256, 32)))
+
+    res = oracle.attend_rows(prob, inp, 0, np.array([0, 3]), [(0, h) for h in range(8)], kv)
+    for h in range(8):
+        assert np.allclose(res[(0, h)][0], h // 4 + 1.0), f"head {h} must read KV head {h // 4}"
+
+
+ALL_PINS = [
+    pin_score_library_matmul, pin_score_int8_exact, pin_score_closed_forms,
+    pin_topk_worked_example, pin_topk_bruteforce, pin_topk_library_sort, pin_union_bruteforce,
+    pin_attention_worked_example, pin_keep_all_is_dense, pin_masked_dense_sdpa, pin_attention_closed_forms,
+    pin_gqa_mapping,
+]

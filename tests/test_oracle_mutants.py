@@ -1,0 +1,71 @@
+"""Planted mistakes in the oracle must be caught by its pins.
+
+Each mutant is a one-line textual change to ``oracle/lsa_oracle.c`` -- a
+reversed tie-break, a dropped scale, a wrong sign, a wrong token or dimension
+index, a dropped term -- compiled on the CPU into a throw-away library.  The
+test passes when at least one pin fails for every mutant, which shows the pins
+can tell a plausible slip in the oracle from the real thing.
+"""
+import os
+import subprocess
+import tempfile
+
+import pytest
+
+import oracle
+import oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "lsa_oracle.c")
+
+MUTANTS = {
+    "tie_break_reversed_f": ("  return (x->c > y->c) - (x->c < y->c);\n}\n\nstatic int by_score_desc_i",
+                             "  return (x->c < y->c) - (x->c > y->c);\n}\n\nstatic int by_score_desc_i"),
+    "tie_break_reversed_i": ("  return (x->c > y->c) - (x->c < y->c);\n}\n\nstatic int ascending_i32",
+                             "  return (x->c < y->c) - (x->c > y->c);\n}\n\nstatic int ascending_i32"),
+    "smallest_first": ("  if (x->s > y->s) return -1;\n  if (x->s < y->s) return 1;\n  return (x->c > y->c) - (x->c < y->c);\n}\n\nstatic int by_score_desc_i",
+                       "  if (x->s > y->s) return 1;\n  if (x->s < y->s) return -1;\n  return (x->c > y->c) - (x->c < y->c);\n}\n\nstatic int by_score_desc_i"),
+    "output_not_ascending": ("  free(v);\n  qsort(out, (size_t)k, sizeof *out, ascending_i32);\n  return k;\n}\n\n/* Top-k of int64",
+                             "  free(v);\n  return k;\n}\n\n/* Top-k of int64"),
+    "score_f32_dropped_term": ("for (int32_t i = 0; i < D; ++i) s += (double)qe[i]",
+                               "for (int32_t i = 1; i < D; ++i) s += (double)qe[i]"),
+    "score_bf16_wrong_sign": ("s += bf16_to_f64(qe[i]) * bf16_to_f64(E[c * D + i]);",
+                              "s -= bf16_to_f64(qe[i]) * bf16_to_f64(E[c * D + i]);"),
+    "score_i8_reversed_dims": ("(int64_t)qe[i] * (int64_t)E[c * D + i]",
+                               "(int64_t)qe[i] * (int64_t)E[c * D + (D - 1 - i)]"),
+    "union_drops_last_list": ("j < (int64_t)n_lists * k; ++j", "j < (int64_t)(n_lists - 1) * k; ++j"),
+    "attn_dropped_scale": ("logit[i] = dot * scale;", "logit[i] = dot;"),
+    "attn_exp_wrong_sign": ("logit[i] = exp(logit[i] - m);", "logit[i] = exp(m - logit[i]);"),
+    "attn_k_token_index": ("const int64_t tok = (int64_t)sel[i / C] * C + i % C;\n      double dot",
+                           "const int64_t tok = (int64_t)sel[i / C] + i % C;\n      double dot"),
+    "attn_v_token_index": ("const int64_t tok = (int64_t)sel[i / C] * C + i % C;\n        acc",
+                           "const int64_t tok = (int64_t)sel[i / C] + i % C;\n        acc"),
+    "attn_k_transposed_dims": ("bf16_to_f64(Kh[tok * d + e])", "bf16_to_f64(Kh[tok * d + (d - 1 - e)])"),
+    "attn_v_transposed_dims": ("bf16_to_f64(Vh[tok * d + e])", "bf16_to_f64(Vh[tok * d + (d - 1 - e)])"),
+    "attn_lse_dropped_max": ("lse[r] = m + log(Z);", "lse[r] = log(Z);"),
+    "attn_unnormalised": ("out[(int64_t)r * d + e] = acc / Z;", "out[(int64_t)r * d + e] = acc;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique/present"
+    path = tmp_path / "mutant.c"
+    path.write_text(src.replace(old, new))
+    so = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", str(path), "-o", str(so), "-lm"])
+    saved = oracle._lib
+    oracle._lib = oracle.bind(str(so))
+    failed = []
+    try:
+        for pin in P.ALL_PINS:
+            try:
+                pin()
+            except AssertionError:
+                failed.append(pin.__name__)
+            except ValueError:
+                failed.append(pin.__name__)
+    finally:
+        oracle._lib = saved
+    assert failed, f"no pin catches mutant {name}"
