@@ -1,0 +1,163 @@
+/*
+ * lsa.h -- C ABI of the MI355X (gfx950) decode hot path of Lookahead Sparse
+ * Attention (LSA).
+ *
+ * One decode step has three parts (paper Sec. 2.1):
+ *   1. score   -- the Memory Indexer scores every compressed chunk of the context
+ *                 against the query embedding (Eq. 4, taken as the dual-encoder
+ *                 dot product s_c = qe . E_c of one indexer head with unit gate);
+ *   2. select  -- keep the k highest-scoring chunks (the Top-k of Eq. corecomp,
+ *                 with the recall bound K_max of Sec. 2.5 as the keep budget k);
+ *                 with several lookahead query embeddings the kept set is the
+ *                 union of the per-query top-k sets (set union as in Eq. union);
+ *   3. attend  -- softmax(q K^T * scale) V over the tokens of the kept chunks
+ *                 only, gathered by chunk id from the full cache (the core
+ *                 attention over the selected entries, Sec. 2.1).
+ *
+ * Conventions shared by every entry point
+ *  - All device pointers are caller-owned HBM buffers, 16-byte aligned.  The
+ *    library never allocates, frees or synchronises.  Every call is
+ *    asynchronous on `stream` (a hipStream_t; NULL is the default stream);
+ *    outputs are valid once the stream has reached the call.
+ *  - Arguments are validated on the host before any launch; on failure the
+ *    call returns a status, records a message for lsa_last_error() and writes
+ *    nothing.  A failed launch returns LSA_ERR_HIP.  No C++ exception crosses
+ *    the ABI.  Device contents (scores, chunk ids) are not validated: inputs
+ *    must be finite and produced by the preceding steps.
+ *  - Sequences are packed back to back.  Sequence b holds n_b = ctx_tokens[b] /
+ *    chunk_size chunks; its chunks have global ids chunk_off[b] .. chunk_off[b]
+ *    + n_b - 1 where chunk_off is the exclusive prefix sum of n_b.
+ *  - Chunk embeddings E: [sum_b n_b][emb_dim] row-major, row = global chunk id.
+ *    Query embeddings: [batch][n_lookahead][emb_dim].
+ *  - Scores: sequence b's block starts at element n_lookahead * chunk_off[b] and
+ *    is [n_lookahead][n_b] row-major; float32 for F32/BF16 embeddings, int32
+ *    (exact) for I8 embeddings.
+ *  - Kept chunk ids: sel_idx [batch][max_sel] int32, per-sequence chunk ids in
+ *    ascending order in the first sel_count[b] entries (sel_count is a device
+ *    int32 [batch]); max_sel = max_b min(n_lookahead * keep[b], n_b).
+ *  - KV cache (bf16, raw 16-bit patterns), paged by chunk.  The block of global
+ *    chunk c and KV head g starts at element c * kv_chunk_stride + g *
+ *    kv_head_stride and holds chunk_size * head_dim elements:
+ *        K block: [token][dim]   element t * head_dim + e
+ *        V block: [dim][token]   element e * chunk_size + t
+ *  - q: bf16 [batch][n_qtok][n_q_heads][head_dim].  Query head h reads KV head
+ *    h / (n_q_heads / n_kv_heads).  out: float32, same shape as q.  lse: float32
+ *    [batch][n_qtok][n_q_heads], the natural-log log-sum-exp of the scaled
+ *    logits over the kept tokens.
+ *  - All n_qtok query tokens of a sequence attend the same kept set; there is
+ *    no mask inside it.
+ */
+#ifndef LSA_H_
+#define LSA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LSA_ABI_VERSION 1
+#define LSA_MAX_BATCH 64           /* sequences per call */
+#define LSA_MAX_LOOKAHEAD 16       /* query embeddings per sequence */
+#define LSA_MAX_QTOK 16            /* attention query tokens per sequence */
+#define LSA_MAX_ROWS 128           /* n_qtok * n_q_heads / n_kv_heads */
+#define LSA_MAX_UNION_CHUNKS 262144 /* n_b limit when n_lookahead > 1 */
+
+typedef enum {
+  LSA_OK = 0,
+  LSA_ERR_INVALID_ARG = 1, /* a shape, pointer, alignment or size is out of contract */
+  LSA_ERR_UNSUPPORTED = 2, /* valid, but this build has no kernel for it */
+  LSA_ERR_WORKSPACE = 3,   /* workspace missing or smaller than lsa_workspace_size() */
+  LSA_ERR_HIP = 4          /* a HIP launch failed; see lsa_last_error() */
+} lsa_status;
+
+typedef enum { LSA_F32 = 0, LSA_BF16 = 1, LSA_I8 = 2 } lsa_dtype;
+
+/* Shape of one decode step.  Host memory only; read during the call. */
+typedef struct lsa_problem {
+  int32_t batch;        /* B, 1 .. LSA_MAX_BATCH */
+  int32_t chunk_size;   /* C, tokens per compressed chunk: 64 or 128 */
+  int32_t n_q_heads;    /* Hq */
+  int32_t n_kv_heads;   /* Hkv, divides Hq */
+  int32_t head_dim;     /* d, 128 */
+  int32_t emb_dim;      /* D, indexer embedding width: 64, 128, 256 or 512 */
+  int32_t n_lookahead;  /* Q, query embeddings per sequence, 1 .. 16 */
+  int32_t n_qtok;       /* Tq, attention query tokens per sequence, 1 .. 16 */
+  int32_t emb_dtype;    /* lsa_dtype of E and of the query embeddings */
+  int32_t reserved;     /* must be 0 */
+  const int64_t* ctx_tokens; /* HOST [B]: context tokens of each sequence, a positive multiple of C */
+  const int32_t* keep;       /* HOST [B]: keep budget k_b, 1 <= k_b <= n_b (per query when Q > 1) */
+  int64_t kv_chunk_stride;   /* elements between chunks in K and V; 0 selects n_kv_heads*C*d */
+  int64_t kv_head_stride;    /* elements between KV heads in K and V; 0 selects C*d */
+} lsa_problem;
+
+int lsa_abi_version(void);
+const char* lsa_status_string(lsa_status status);
+/* Message of the last failed call on this host thread ("" if none). */
+const char* lsa_last_error(void);
+
+/* Validate a problem without launching anything. */
+lsa_status lsa_validate(const lsa_problem* p);
+/* Row pitch of sel_idx: max_b min(Q * k_b, n_b). */
+lsa_status lsa_max_sel(const lsa_problem* p, int32_t* max_sel);
+/* Row pitch of the optional per-query lists of lsa_topk_chunks: max_b k_b. */
+lsa_status lsa_max_keep(const lsa_problem* p, int32_t* max_keep);
+/* Bytes of device workspace that any entry point below needs for p. */
+lsa_status lsa_workspace_size(const lsa_problem* p, size_t* bytes);
+/* Zero-fill a workspace on `stream` (a fill kernel, safe under graph capture).
+ * A workspace must be zero-filled once before its first use; every call leaves
+ * the counters it uses at zero again. */
+lsa_status lsa_workspace_init(void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step 1 -- score every chunk (Sec. 2.1, Eq. 4 with one head and unit gate):
+ *   scores[b][j][c] = sum_i query_emb[b][j][i] * E[chunk_off[b] + c][i]
+ * float32 accumulation for F32/BF16 embeddings, exact int32 for I8.
+ */
+lsa_status lsa_score_chunks(const lsa_problem* p, const void* query_emb, const void* chunk_emb,
+                            void* scores, void* stream);
+
+/*
+ * Step 2 -- keep the top-k chunks (Sec. 2.1, Eq. corecomp; union of Eq. union):
+ * for each (b, j) the k_b chunk ids with the largest score, ties broken towards
+ * the lower chunk id, -0.0 equal to +0.0.  Q == 1: sel_idx[b][0..k_b) ascending
+ * and sel_count[b] = k_b.  Q > 1: sel_idx[b] holds the ascending union of the Q
+ * per-query sets and sel_count[b] its size.  per_query_idx (nullable) receives
+ * each ascending per-query set, [B][Q][max_keep].  The workspace is used only
+ * when Q > 1 and per_query_idx is NULL.
+ */
+lsa_status lsa_topk_chunks(const lsa_problem* p, const void* scores, int32_t* sel_idx,
+                           int32_t* sel_count, int32_t* per_query_idx, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/*
+ * Step 3 -- sparse decode attention over the kept chunks (Sec. 2.1): for every
+ * (b, t, h) with g = h / G, out = softmax(scale * q K_sel^T) V_sel over the
+ * tokens of chunks sel_idx[b][0 .. sel_count[b]).  softmax_scale <= 0 selects
+ * 1/sqrt(head_dim).  bf16 inputs, float32 softmax and accumulation.  lse is
+ * nullable.  Split-K partials live in the workspace and are merged in a fixed
+ * order, so results are bitwise reproducible.  Chunk ids must be < n_b and
+ * sel_count[b] must be in 1 .. max_sel.
+ */
+lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const uint16_t* k_cache,
+                                  const uint16_t* v_cache, const int32_t* sel_idx,
+                                  const int32_t* sel_count, float softmax_scale, float* out,
+                                  float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The whole step: score -> select -> attend on one stream with no host
+ * synchronisation.  sel_idx / sel_count are nullable (then they live in the
+ * workspace); when given they receive the kept chunk ids as lsa_topk_chunks
+ * writes them.
+ */
+lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const void* chunk_emb,
+                           const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                           float softmax_scale, float* out, float* lse, int32_t* sel_idx,
+                           int32_t* sel_count, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LSA_H_ */

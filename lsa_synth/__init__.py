@@ -319,6 +319,7 @@ _dev_lib: Optional[ctypes.CDLL] = None
 def dev_lib() -> ctypes.CDLL:
     global _dev_lib
     if _dev_lib is None:
+        import torch  # noqa: F401  (bind to the HIP runtime torch already loaded)
         lib = _so(_DEV_SO, build_device)
         lib.synth_fill_kv_device.argtypes = [ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
@@ -342,6 +343,31 @@ def fill_kv_device(prob: Problem, seed: int, which: str, out_ptr: int, table_ptr
                                         cs, hs, 0 if which == "k" else 1, stream_ptr)
     if rc != 0:
         raise RuntimeError(f"synth_fill_kv_device failed with code {rc}")
+
+
+def device_inputs(prob: Problem, seed: int, device: str = "cuda", host: Optional[Dict[str, object]] = None):
+    """All step inputs resident in device memory (torch tensors).
+
+    Small tensors come from :func:`host_inputs`; K and V are filled in place on
+    the device.  bf16 tensors are carried as int16 bit patterns.
+    """
+    import torch
+    h = host if host is not None else host_inputs(prob, seed)
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            a = a.view(np.int16)
+        return torch.from_numpy(a).to(device)
+
+    table = up(normal_table_bf16())
+    n = prob.kv_elems()
+    k = torch.empty(n, dtype=torch.int16, device=device)
+    v = torch.empty(n, dtype=torch.int16, device=device)
+    stream = torch.cuda.current_stream(device).cuda_stream
+    fill_kv_device(prob, seed, "k", k.data_ptr(), table.data_ptr(), stream)
+    fill_kv_device(prob, seed, "v", v.data_ptr(), table.data_ptr(), stream)
+    return {"qe": up(h["qe"]), "E": up(h["E"]), "q": up(h["q"]), "k": k, "v": v, "table": table, "host": h}
 
 
 # ------------------------------------------------------------------ build

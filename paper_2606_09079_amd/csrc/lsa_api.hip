@@ -1,0 +1,365 @@
+// Host side of the C ABI declared in include/lsa.h: argument validation, the
+// per-call plan (sequence table, launch geometry, workspace carve-up) and the
+// stream-ordered launches.  No allocation, no synchronisation, no exceptions.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "lsa_internal.h"
+
+namespace lsa {
+namespace {
+
+thread_local char g_err[512] = "";
+
+lsa_status fail(lsa_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+lsa_status hip_fail(hipError_t e, const char* what) {
+  return fail(LSA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+constexpr int kChunksPerSplitWaveSplit = 16;  // rows <= 16: chunks per workgroup (4 waves)
+constexpr int kChunksPerSplitRowSplit = 8;    // rows > 16: chunks per workgroup
+constexpr int kMaxSplits = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Plan {
+  SeqTable t;
+  int64_t total_chunks = 0;
+  int32_t max_keep = 0, max_sel = 0;
+  int32_t group = 0, rows = 0, row_groups = 1, rows_pad = 16;
+  int64_t chunk_stride = 0, head_stride = 0;
+  int64_t n_units = 0;
+  size_t emb_elem = 0;
+  // workspace layout (byte offsets)
+  size_t off_counters = 0, off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0;
+  size_t ws_total = 0;
+};
+
+lsa_status make_plan(const lsa_problem* p, Plan* pl) {
+  if (p == nullptr) return fail(LSA_ERR_INVALID_ARG, "problem is NULL");
+  const int B = p->batch;
+  if (B < 1 || B > LSA_MAX_BATCH) return fail(LSA_ERR_INVALID_ARG, "batch %d not in [1, %d]", B, LSA_MAX_BATCH);
+  if (p->chunk_size != 64 && p->chunk_size != 128)
+    return fail(LSA_ERR_UNSUPPORTED, "chunk_size %d not in {64, 128}", p->chunk_size);
+  if (p->head_dim != kHeadDim) return fail(LSA_ERR_UNSUPPORTED, "head_dim %d != 128", p->head_dim);
+  if (p->emb_dim != 64 && p->emb_dim != 128 && p->emb_dim != 256 && p->emb_dim != 512)
+    return fail(LSA_ERR_UNSUPPORTED, "emb_dim %d not in {64, 128, 256, 512}", p->emb_dim);
+  if (p->n_kv_heads < 1 || p->n_q_heads < 1 || p->n_q_heads % p->n_kv_heads != 0)
+    return fail(LSA_ERR_INVALID_ARG, "n_q_heads %d must be a positive multiple of n_kv_heads %d", p->n_q_heads,
+                p->n_kv_heads);
+  if (p->n_kv_heads > 1024) return fail(LSA_ERR_UNSUPPORTED, "n_kv_heads %d > 1024", p->n_kv_heads);
+  if (p->n_lookahead < 1 || p->n_lookahead > LSA_MAX_LOOKAHEAD)
+    return fail(LSA_ERR_INVALID_ARG, "n_lookahead %d not in [1, %d]", p->n_lookahead, LSA_MAX_LOOKAHEAD);
+  if (p->n_qtok < 1 || p->n_qtok > LSA_MAX_QTOK)
+    return fail(LSA_ERR_INVALID_ARG, "n_qtok %d not in [1, %d]", p->n_qtok, LSA_MAX_QTOK);
+  if (p->emb_dtype != LSA_F32 && p->emb_dtype != LSA_BF16 && p->emb_dtype != LSA_I8)
+    return fail(LSA_ERR_INVALID_ARG, "emb_dtype %d is not an lsa_dtype", p->emb_dtype);
+  if (p->reserved != 0) return fail(LSA_ERR_INVALID_ARG, "reserved field must be 0");
+  if (p->ctx_tokens == nullptr || p->keep == nullptr)
+    return fail(LSA_ERR_INVALID_ARG, "ctx_tokens and keep must be host arrays of batch entries");
+  const int G = p->n_q_heads / p->n_kv_heads;
+  const int rows = G * p->n_qtok;
+  if (rows > LSA_MAX_ROWS)
+    return fail(LSA_ERR_UNSUPPORTED, "n_qtok * n_q_heads / n_kv_heads = %d > %d", rows, LSA_MAX_ROWS);
+
+  Plan& P = *pl;
+  SeqTable& t = P.t;
+  memset(&t, 0, sizeof t);
+  t.batch = B;
+  t.n_lookahead = p->n_lookahead;
+  const int C = p->chunk_size;
+  const int srows = score_rows_per_wg(p->emb_dtype, p->emb_dim);
+  P.group = G;
+  P.rows = rows;
+  P.row_groups = rows > 16 ? (rows + kAttnWaves * 16 - 1) / (kAttnWaves * 16) : 1;
+  P.rows_pad = rows > 16 ? P.row_groups * kAttnWaves * 16 : 16;
+  const int cps = rows > 16 ? kChunksPerSplitRowSplit : kChunksPerSplitWaveSplit;
+  int64_t chunk_off = 0, wg_off = 0, swg_off = 0;
+  for (int b = 0; b < B; ++b) {
+    const int64_t L = p->ctx_tokens[b];
+    if (L < C || L % C != 0)
+      return fail(LSA_ERR_INVALID_ARG, "ctx_tokens[%d] = %lld is not a positive multiple of chunk_size %d", b,
+                  (long long)L, C);
+    const int64_t n = L / C;
+    if (n > INT32_MAX / 2) return fail(LSA_ERR_UNSUPPORTED, "sequence %d has too many chunks", b);
+    if (p->n_lookahead > 1 && n > LSA_MAX_UNION_CHUNKS)
+      return fail(LSA_ERR_UNSUPPORTED, "sequence %d: %lld chunks > %d with several lookahead queries", b,
+                  (long long)n, LSA_MAX_UNION_CHUNKS);
+    const int32_t k = p->keep[b];
+    if (k < 1 || k > n)
+      return fail(LSA_ERR_INVALID_ARG, "keep[%d] = %d not in [1, n_b = %lld]", b, k, (long long)n);
+    const int32_t msel = (int32_t)std::min<int64_t>((int64_t)p->n_lookahead * k, n);
+    const int32_t ns = (int32_t)std::min<int64_t>(std::max<int64_t>(1, (msel + cps - 1) / cps), kMaxSplits);
+    t.n[b] = (int32_t)n;
+    t.keep[b] = k;
+    t.nsplit[b] = ns;
+    t.chunk_off[b] = chunk_off;
+    t.wg_off[b] = (int32_t)wg_off;
+    t.score_wg_off[b] = (int32_t)swg_off;
+    chunk_off += n;
+    wg_off += (int64_t)p->n_kv_heads * P.row_groups * ns;
+    swg_off += (n + srows - 1) / srows;
+    P.max_keep = std::max(P.max_keep, k);
+    P.max_sel = std::max(P.max_sel, msel);
+    if (chunk_off > INT32_MAX || wg_off > INT32_MAX || swg_off > INT32_MAX)
+      return fail(LSA_ERR_UNSUPPORTED, "problem too large for one launch");
+  }
+  t.chunk_off[B] = chunk_off;
+  t.wg_off[B] = (int32_t)wg_off;
+  t.score_wg_off[B] = (int32_t)swg_off;
+  P.total_chunks = chunk_off;
+  P.n_units = wg_off / P.row_groups;
+
+  // KV cache strides: blocks of C*d elements must not overlap.
+  const int64_t blk = (int64_t)C * kHeadDim;
+  P.head_stride = p->kv_head_stride ? p->kv_head_stride : blk;
+  P.chunk_stride = p->kv_chunk_stride ? p->kv_chunk_stride : (int64_t)p->n_kv_heads * P.head_stride;
+  if (P.head_stride < 0 || P.chunk_stride < 0 || P.head_stride % 8 || P.chunk_stride % 8)
+    return fail(LSA_ERR_INVALID_ARG, "kv strides must be non-negative multiples of 8 elements");
+  const bool chunk_major = P.head_stride >= blk && P.chunk_stride >= (int64_t)p->n_kv_heads * P.head_stride;
+  const bool head_major = P.chunk_stride >= blk && P.head_stride >= P.total_chunks * P.chunk_stride;
+  if (!chunk_major && !head_major)
+    return fail(LSA_ERR_INVALID_ARG, "kv strides (chunk %lld, head %lld) make (chunk, head) blocks overlap",
+                (long long)P.chunk_stride, (long long)P.head_stride);
+
+  P.emb_elem = p->emb_dtype == LSA_F32 ? 4 : p->emb_dtype == LSA_BF16 ? 2 : 1;
+
+  size_t off = 0;
+  P.off_counters = off;
+  off = align_up(off + (size_t)B * p->n_kv_heads * P.row_groups * 4);
+  P.off_scores = off;
+  off = align_up(off + (size_t)p->n_lookahead * P.total_chunks * 4);
+  P.off_sel = off;
+  off = align_up(off + (size_t)B * P.max_sel * 4);
+  P.off_cnt = off;
+  off = align_up(off + (size_t)B * 4);
+  P.off_pq = off;
+  if (p->n_lookahead > 1) off = align_up(off + (size_t)B * p->n_lookahead * P.max_keep * 4);
+  P.off_ml = off;
+  off = align_up(off + (size_t)P.n_units * P.rows_pad * 2 * 4);
+  P.off_o = off;
+  off = align_up(off + (size_t)P.n_units * P.rows_pad * kHeadDim * 4);
+  P.ws_total = off;
+  return LSA_OK;
+}
+
+lsa_status check_ptr(const void* ptr, const char* name) {
+  if (ptr == nullptr) return fail(LSA_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned16(ptr)) return fail(LSA_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return LSA_OK;
+}
+
+lsa_status check_ws(const Plan& P, void* ws, size_t ws_bytes) {
+  if (ws_bytes < P.ws_total)
+    return fail(LSA_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, P.ws_total);
+  if (P.ws_total > 0 && ws == nullptr) return fail(LSA_ERR_WORKSPACE, "workspace is NULL");
+  if (!aligned16(ws)) return fail(LSA_ERR_WORKSPACE, "workspace is not 16-byte aligned");
+  return LSA_OK;
+}
+
+#define LSA_TRY(expr)                  \
+  do {                                 \
+    const lsa_status st_ = (expr);     \
+    if (st_ != LSA_OK) return st_;     \
+  } while (0)
+
+#define LSA_HIP(expr, what)                      \
+  do {                                           \
+    const hipError_t e_ = (expr);                \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+uint8_t* at(void* ws, size_t off) { return static_cast<uint8_t*>(ws) + off; }
+
+lsa_status run_topk(const lsa_problem* p, const Plan& P, const void* scores, int32_t* sel_idx,
+                    int32_t* sel_count, int32_t* per_query_idx, void* ws, hipStream_t s) {
+  if (p->n_lookahead == 1) {
+    LSA_HIP(launch_topk(P.t, p->emb_dtype, scores, sel_idx, P.max_sel, 0, sel_count, s), "topk launch");
+    return LSA_OK;
+  }
+  int32_t* pq = per_query_idx ? per_query_idx : reinterpret_cast<int32_t*>(at(ws, P.off_pq));
+  LSA_HIP(launch_topk(P.t, p->emb_dtype, scores, pq, (int64_t)p->n_lookahead * P.max_keep, P.max_keep,
+                      nullptr, s),
+          "topk launch");
+  LSA_HIP(launch_union(P.t, pq, P.max_keep, sel_idx, P.max_sel, sel_count, s), "union launch");
+  return LSA_OK;
+}
+
+lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, const uint16_t* k,
+                    const uint16_t* v, const int32_t* sel_idx, const int32_t* sel_count, float scale,
+                    float* out, float* lse, void* ws, hipStream_t s) {
+  AttnArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.sel_idx = sel_idx;
+  a.sel_count = sel_count;
+  a.out = out;
+  a.lse = lse;
+  a.part_o = reinterpret_cast<float*>(at(ws, P.off_o));
+  a.part_ml = reinterpret_cast<float*>(at(ws, P.off_ml));
+  a.counters = reinterpret_cast<uint32_t*>(at(ws, P.off_counters));
+  a.chunk_stride = P.chunk_stride;
+  a.head_stride = P.head_stride;
+  const double sc = scale > 0.f ? (double)scale : 1.0 / std::sqrt((double)kHeadDim);
+  a.scale_log2e = (float)(sc * 1.4426950408889634);
+  a.sel_pitch = P.max_sel;
+  a.n_q_heads = p->n_q_heads;
+  a.n_kv_heads = p->n_kv_heads;
+  a.group = P.group;
+  a.n_qtok = p->n_qtok;
+  a.rows = P.rows;
+  a.row_groups = P.row_groups;
+  a.rows_pad = P.rows_pad;
+  LSA_HIP(launch_attn(P.t, a, p->chunk_size, s), "attention launch");
+  return LSA_OK;
+}
+
+}  // namespace
+}  // namespace lsa
+
+using namespace lsa;
+
+extern "C" {
+
+int lsa_abi_version(void) { return LSA_ABI_VERSION; }
+
+const char* lsa_status_string(lsa_status st) {
+  switch (st) {
+    case LSA_OK: return "LSA_OK";
+    case LSA_ERR_INVALID_ARG: return "LSA_ERR_INVALID_ARG";
+    case LSA_ERR_UNSUPPORTED: return "LSA_ERR_UNSUPPORTED";
+    case LSA_ERR_WORKSPACE: return "LSA_ERR_WORKSPACE";
+    case LSA_ERR_HIP: return "LSA_ERR_HIP";
+    default: return "LSA_ERR_UNKNOWN";
+  }
+}
+
+const char* lsa_last_error(void) { return g_err; }
+
+lsa_status lsa_validate(const lsa_problem* p) {
+  Plan P;
+  return make_plan(p, &P);
+}
+
+lsa_status lsa_max_sel(const lsa_problem* p, int32_t* max_sel) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  if (!max_sel) return fail(LSA_ERR_INVALID_ARG, "max_sel is NULL");
+  *max_sel = P.max_sel;
+  return LSA_OK;
+}
+
+lsa_status lsa_max_keep(const lsa_problem* p, int32_t* max_keep) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  if (!max_keep) return fail(LSA_ERR_INVALID_ARG, "max_keep is NULL");
+  *max_keep = P.max_keep;
+  return LSA_OK;
+}
+
+lsa_status lsa_workspace_size(const lsa_problem* p, size_t* bytes) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  if (!bytes) return fail(LSA_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = P.ws_total;
+  return LSA_OK;
+}
+
+lsa_status lsa_workspace_init(void* ws, size_t ws_bytes, void* stream) {
+  if (ws_bytes == 0) return LSA_OK;
+  LSA_TRY(check_ptr(ws, "ws"));
+  LSA_HIP(launch_zero(ws, ws_bytes, (hipStream_t)stream), "zero-fill launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_score_chunks(const lsa_problem* p, const void* query_emb, const void* chunk_emb, void* scores,
+                            void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(check_ptr(query_emb, "query_emb"));
+  LSA_TRY(check_ptr(chunk_emb, "chunk_emb"));
+  LSA_TRY(check_ptr(scores, "scores"));
+  LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, (hipStream_t)stream),
+          "score launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_topk_chunks(const lsa_problem* p, const void* scores, int32_t* sel_idx, int32_t* sel_count,
+                           int32_t* per_query_idx, void* ws, size_t ws_bytes, void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(check_ptr(scores, "scores"));
+  LSA_TRY(check_ptr(sel_idx, "sel_idx"));
+  LSA_TRY(check_ptr(sel_count, "sel_count"));
+  if (per_query_idx != nullptr) LSA_TRY(check_ptr(per_query_idx, "per_query_idx"));
+  if (p->n_lookahead > 1 && per_query_idx == nullptr) LSA_TRY(check_ws(P, ws, ws_bytes));
+  return run_topk(p, P, scores, sel_idx, sel_count, per_query_idx, ws, (hipStream_t)stream);
+}
+
+lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const uint16_t* k_cache,
+                                  const uint16_t* v_cache, const int32_t* sel_idx, const int32_t* sel_count,
+                                  float softmax_scale, float* out, float* lse, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(check_ptr(q, "q"));
+  LSA_TRY(check_ptr(k_cache, "k_cache"));
+  LSA_TRY(check_ptr(v_cache, "v_cache"));
+  LSA_TRY(check_ptr(sel_idx, "sel_idx"));
+  LSA_TRY(check_ptr(sel_count, "sel_count"));
+  LSA_TRY(check_ptr(out, "out"));
+  if (lse != nullptr && (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(LSA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
+  LSA_TRY(check_ws(P, ws, ws_bytes));
+  return run_attn(p, P, q, k_cache, v_cache, sel_idx, sel_count, softmax_scale, out, lse, ws,
+                  (hipStream_t)stream);
+}
+
+lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const void* chunk_emb, const uint16_t* q,
+                           const uint16_t* k_cache, const uint16_t* v_cache, float softmax_scale, float* out,
+                           float* lse, int32_t* sel_idx, int32_t* sel_count, void* ws, size_t ws_bytes,
+                           void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(check_ptr(query_emb, "query_emb"));
+  LSA_TRY(check_ptr(chunk_emb, "chunk_emb"));
+  LSA_TRY(check_ptr(q, "q"));
+  LSA_TRY(check_ptr(k_cache, "k_cache"));
+  LSA_TRY(check_ptr(v_cache, "v_cache"));
+  LSA_TRY(check_ptr(out, "out"));
+  if (lse != nullptr && (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(LSA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if ((sel_idx == nullptr) != (sel_count == nullptr))
+    return fail(LSA_ERR_INVALID_ARG, "sel_idx and sel_count must both be given or both be NULL");
+  if (sel_idx != nullptr) {
+    LSA_TRY(check_ptr(sel_idx, "sel_idx"));
+    LSA_TRY(check_ptr(sel_count, "sel_count"));
+  }
+  if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
+  LSA_TRY(check_ws(P, ws, ws_bytes));
+  const hipStream_t s = (hipStream_t)stream;
+  void* scores = at(ws, P.off_scores);
+  int32_t* sel = sel_idx ? sel_idx : reinterpret_cast<int32_t*>(at(ws, P.off_sel));
+  int32_t* cnt = sel_count ? sel_count : reinterpret_cast<int32_t*>(at(ws, P.off_cnt));
+  LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, s), "score launch");
+  LSA_TRY(run_topk(p, P, scores, sel, cnt, nullptr, ws, s));
+  return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
+}
+
+}  // extern "C"

@@ -1,0 +1,70 @@
+// Internal interface between the host dispatch (lsa_api.hip) and the gfx950
+// kernels.  Per-sequence metadata travels by value in kernel arguments, so a
+// launch needs no device-side offset table and nothing is read back to size
+// the grids.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/lsa.h"
+
+namespace lsa {
+
+// Per-sequence table computed on the host for one call.
+struct SeqTable {
+  int32_t batch;
+  int32_t n_lookahead;
+  int32_t n[LSA_MAX_BATCH];            // chunks of sequence b
+  int32_t keep[LSA_MAX_BATCH];         // keep budget k_b
+  int32_t nsplit[LSA_MAX_BATCH];       // attention splits per (b, kv head)
+  int32_t wg_off[LSA_MAX_BATCH + 1];   // first attention workgroup of sequence b
+  int32_t score_wg_off[LSA_MAX_BATCH + 1];  // first scoring workgroup of sequence b
+  int64_t chunk_off[LSA_MAX_BATCH + 1];     // first global chunk id of sequence b
+};
+
+// Attention launch parameters.
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* sel_idx;
+  const int32_t* sel_count;
+  float* out;
+  float* lse;            // nullable
+  float* part_o;         // [wg][16][128]
+  float* part_ml;        // [wg][16][2]
+  uint32_t* counters;    // [B * Hkv * row_groups], zero between calls
+  int64_t chunk_stride;
+  int64_t head_stride;
+  float scale_log2e;     // softmax scale * log2(e)
+  int32_t sel_pitch;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t group;         // G = Hq / Hkv
+  int32_t n_qtok;
+  int32_t rows;          // G * n_qtok
+  int32_t row_groups;    // workgroups along the row dimension (rows > 16 only)
+  int32_t rows_pad;      // partial rows per (b, g, split): 16, or 64 * row_groups
+};
+
+// Geometry of the attention launch shared by dispatch and kernels.
+constexpr int kAttnWaves = 4;          // waves per workgroup
+constexpr int kAttnRowsPerWave = 16;   // MFMA tile rows
+constexpr int kHeadDim = 128;
+
+hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
+                        const void* E, void* scores, hipStream_t s);
+int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim);
+
+hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, const void* scores, int32_t* out_idx,
+                       int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
+                       hipStream_t s);
+hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_pitch,
+                        int32_t* sel_idx, int32_t sel_pitch, int32_t* sel_count, hipStream_t s);
+
+hipError_t launch_attn(const SeqTable& t, const AttnArgs& a, int32_t chunk_size, hipStream_t s);
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace lsa

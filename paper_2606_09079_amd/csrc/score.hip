@@ -1,0 +1,183 @@
+// Step 1 of the decode hot path: the Memory Indexer score of every chunk
+// (Sec. 2.1, Eq. 4 with one indexer head and unit gate, i.e. the dual-encoder
+// dot product s_c = qe . E_c).
+//
+// HBM-streaming GEMV.  A chunk-embedding row of D elements is split into
+// 16-byte pieces; L consecutive lanes read one row (one 16-byte load each), so a
+// wavefront load instruction covers 1 KiB of contiguous embeddings.  Each
+// workgroup owns a contiguous block of rows of one sequence, issues all of its
+// row loads up front (8 per lane) and then reuses the registers for every
+// lookahead query of that sequence, so E is read exactly once.  Partial dot
+// products are reduced across the L lanes of a row with xor shuffles.
+//   F32 : fp32 FMA accumulation
+//   BF16: bf16 widened to fp32 (exact), fp32 FMA accumulation
+//   I8  : v_dot4 int8 -> int32, exact (|s| <= D * 127^2 < 2^31 for D <= 512)
+#include "lsa_internal.h"
+
+namespace lsa {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kPasses = 8;  // row loads in flight per lane
+
+template <int DT> struct Elem;
+template <> struct Elem<LSA_F32> { static constexpr int size = 4; };
+template <> struct Elem<LSA_BF16> { static constexpr int size = 2; };
+template <> struct Elem<LSA_I8> { static constexpr int size = 1; };
+
+template <int DT, int D>
+struct Geo {
+  static constexpr int pieces = D * Elem<DT>::size / 16;          // 16-byte pieces per row
+  static constexpr int lanes = pieces < 64 ? pieces : 64;          // lanes per row
+  static constexpr int ppl = pieces / lanes;                       // pieces per lane
+  static constexpr int rows_per_pass = kThreads / lanes;
+  static constexpr int rows_per_wg = rows_per_pass * kPasses;
+};
+
+// Dot product of one 16-byte embedding piece with the matching query piece.
+__device__ __forceinline__ float piece_dot_f32(uint4 e, uint4 q, float acc) {
+  acc = fmaf(__uint_as_float(e.x), __uint_as_float(q.x), acc);
+  acc = fmaf(__uint_as_float(e.y), __uint_as_float(q.y), acc);
+  acc = fmaf(__uint_as_float(e.z), __uint_as_float(q.z), acc);
+  acc = fmaf(__uint_as_float(e.w), __uint_as_float(q.w), acc);
+  return acc;
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float piece_dot_bf16(uint4 e, uint4 q, float acc) {
+  acc = fmaf(bf_lo(e.x), bf_lo(q.x), acc);
+  acc = fmaf(bf_hi(e.x), bf_hi(q.x), acc);
+  acc = fmaf(bf_lo(e.y), bf_lo(q.y), acc);
+  acc = fmaf(bf_hi(e.y), bf_hi(q.y), acc);
+  acc = fmaf(bf_lo(e.z), bf_lo(q.z), acc);
+  acc = fmaf(bf_hi(e.z), bf_hi(q.z), acc);
+  acc = fmaf(bf_lo(e.w), bf_lo(q.w), acc);
+  acc = fmaf(bf_hi(e.w), bf_hi(q.w), acc);
+  return acc;
+}
+
+__device__ __forceinline__ int piece_dot_i8(uint4 e, uint4 q, int acc) {
+  acc = __builtin_amdgcn_sdot4((int)e.x, (int)q.x, acc, false);
+  acc = __builtin_amdgcn_sdot4((int)e.y, (int)q.y, acc, false);
+  acc = __builtin_amdgcn_sdot4((int)e.z, (int)q.z, acc, false);
+  acc = __builtin_amdgcn_sdot4((int)e.w, (int)q.w, acc, false);
+  return acc;
+}
+
+template <int DT, int D>
+__global__ void __launch_bounds__(kThreads)
+score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restrict__ E,
+             uint32_t* __restrict__ scores) {
+  using G = Geo<DT, D>;
+  constexpr int es = Elem<DT>::size;
+  const int wg = blockIdx.x;
+  int b = 0;
+  while (wg >= t.score_wg_off[b + 1]) ++b;
+  const int n = t.n[b];
+  const int Q = t.n_lookahead;
+  const int row0 = (wg - t.score_wg_off[b]) * G::rows_per_wg;
+  const int sub = threadIdx.x % G::lanes;       // piece index within the row
+  const int rw = threadIdx.x / G::lanes;        // row within a pass
+  const uint8_t* Eb = E + t.chunk_off[b] * (int64_t)(D * es);
+
+  uint4 e[kPasses][G::ppl];
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    const int r = row0 + p * G::rows_per_pass + rw;
+#pragma unroll
+    for (int pp = 0; pp < G::ppl; ++pp) {
+      if (r < n)
+        e[p][pp] = *reinterpret_cast<const uint4*>(Eb + (int64_t)r * (D * es) + (sub + pp * G::lanes) * 16);
+      else
+        e[p][pp] = make_uint4(0, 0, 0, 0);
+    }
+  }
+
+  uint32_t* out_b = scores + (int64_t)Q * t.chunk_off[b];
+  for (int j = 0; j < Q; ++j) {
+    const uint8_t* qj = qe + ((int64_t)b * Q + j) * (D * es);
+    uint4 qv[G::ppl];
+#pragma unroll
+    for (int pp = 0; pp < G::ppl; ++pp)
+      qv[pp] = *reinterpret_cast<const uint4*>(qj + (sub + pp * G::lanes) * 16);
+#pragma unroll
+    for (int p = 0; p < kPasses; ++p) {
+      const int r = row0 + p * G::rows_per_pass + rw;
+      uint32_t bits;
+      if constexpr (DT == LSA_I8) {
+        int acc = 0;
+#pragma unroll
+        for (int pp = 0; pp < G::ppl; ++pp) acc = piece_dot_i8(e[p][pp], qv[pp], acc);
+#pragma unroll
+        for (int off = G::lanes / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+        bits = (uint32_t)acc;
+      } else {
+        float acc = 0.f;
+#pragma unroll
+        for (int pp = 0; pp < G::ppl; ++pp)
+          acc = (DT == LSA_F32) ? piece_dot_f32(e[p][pp], qv[pp], acc) : piece_dot_bf16(e[p][pp], qv[pp], acc);
+#pragma unroll
+        for (int off = G::lanes / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+        bits = __float_as_uint(acc);
+      }
+      if (sub == 0 && r < n) out_b[(int64_t)j * n + r] = bits;
+    }
+  }
+}
+
+template <int DT, int D>
+hipError_t launch_dt_d(const SeqTable& t, const void* qe, const void* E, void* scores, hipStream_t s) {
+  const int grid = t.score_wg_off[t.batch];
+  hipLaunchKernelGGL((score_kernel<DT, D>), dim3(grid), dim3(kThreads), 0, s, t,
+                     static_cast<const uint8_t*>(qe), static_cast<const uint8_t*>(E),
+                     static_cast<uint32_t*>(scores));
+  return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_dt(const SeqTable& t, int32_t D, const void* qe, const void* E, void* scores,
+                     hipStream_t s) {
+  switch (D) {
+    case 64: return launch_dt_d<DT, 64>(t, qe, E, scores, s);
+    case 128: return launch_dt_d<DT, 128>(t, qe, E, scores, s);
+    case 256: return launch_dt_d<DT, 256>(t, qe, E, scores, s);
+    case 512: return launch_dt_d<DT, 512>(t, qe, E, scores, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int DT>
+int rows_dt(int32_t D) {
+  switch (D) {
+    case 64: return Geo<DT, 64>::rows_per_wg;
+    case 128: return Geo<DT, 128>::rows_per_wg;
+    case 256: return Geo<DT, 256>::rows_per_wg;
+    case 512: return Geo<DT, 512>::rows_per_wg;
+    default: return 0;
+  }
+}
+
+}  // namespace
+
+int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim) {
+  switch (emb_dtype) {
+    case LSA_F32: return rows_dt<LSA_F32>(emb_dim);
+    case LSA_BF16: return rows_dt<LSA_BF16>(emb_dim);
+    case LSA_I8: return rows_dt<LSA_I8>(emb_dim);
+    default: return 0;
+  }
+}
+
+hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
+                        const void* E, void* scores, hipStream_t s) {
+  switch (emb_dtype) {
+    case LSA_F32: return launch_dt<LSA_F32>(t, emb_dim, qe, E, scores, s);
+    case LSA_BF16: return launch_dt<LSA_BF16>(t, emb_dim, qe, E, scores, s);
+    case LSA_I8: return launch_dt<LSA_I8>(t, emb_dim, qe, E, scores, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace lsa

@@ -1,0 +1,180 @@
+"""ctypes binding of ``liblsa.so`` (the C ABI in ``include/lsa.h``).
+
+Argument marshalling only: every step of the decode path runs in the HIP
+kernels of the shared library.  Device buffers are passed as torch tensors (or
+raw integer addresses); PyTorch provides device memory and streams, nothing
+else.  There is no fallback: if the library cannot be loaded, importing this
+module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+from . import _build
+
+_P = ctypes.c_void_p
+
+
+class LsaError(RuntimeError):
+    def __init__(self, status: int, fn: str, msg: str):
+        super().__init__(f"{fn} failed with status {status} ({STATUS_NAMES.get(status, '?')}): {msg}")
+        self.status = status
+
+
+LSA_OK, LSA_ERR_INVALID_ARG, LSA_ERR_UNSUPPORTED, LSA_ERR_WORKSPACE, LSA_ERR_HIP = 0, 1, 2, 3, 4
+STATUS_NAMES = {0: "LSA_OK", 1: "LSA_ERR_INVALID_ARG", 2: "LSA_ERR_UNSUPPORTED", 3: "LSA_ERR_WORKSPACE",
+                4: "LSA_ERR_HIP"}
+DTYPES = {"f32": 0, "bf16": 1, "i8": 2}
+
+EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_validate", "lsa_max_sel",
+           "lsa_max_keep", "lsa_workspace_size", "lsa_workspace_init", "lsa_score_chunks", "lsa_topk_chunks",
+           "lsa_sparse_decode_attn", "lsa_decode_step")
+
+
+class lsa_problem(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("chunk_size", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("emb_dim", ctypes.c_int32),
+        ("n_lookahead", ctypes.c_int32), ("n_qtok", ctypes.c_int32), ("emb_dtype", ctypes.c_int32),
+        ("reserved", ctypes.c_int32), ("ctx_tokens", ctypes.POINTER(ctypes.c_int64)),
+        ("keep", ctypes.POINTER(ctypes.c_int32)), ("kv_chunk_stride", ctypes.c_int64),
+        ("kv_head_stride", ctypes.c_int64),
+    ]
+
+
+def _load() -> ctypes.CDLL:
+    # torch ships its own HIP runtime with the same soname as the system one.
+    # Loading torch first makes liblsa.so bind to that already-loaded runtime,
+    # so torch's allocations and streams and this library's launches share one
+    # HIP runtime instance in the process.
+    import torch  # noqa: F401
+    path = _build.LIB_PATH
+    if not os.path.exists(path):
+        _build.build()
+    lib = ctypes.CDLL(path)
+    lib.lsa_abi_version.restype = ctypes.c_int
+    lib.lsa_status_string.restype = ctypes.c_char_p
+    lib.lsa_status_string.argtypes = [ctypes.c_int]
+    lib.lsa_last_error.restype = ctypes.c_char_p
+    pp = ctypes.POINTER(lsa_problem)
+    lib.lsa_validate.argtypes = [pp]
+    lib.lsa_max_sel.argtypes = [pp, ctypes.POINTER(ctypes.c_int32)]
+    lib.lsa_max_keep.argtypes = [pp, ctypes.POINTER(ctypes.c_int32)]
+    lib.lsa_workspace_size.argtypes = [pp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.lsa_workspace_init.argtypes = [_P, ctypes.c_size_t, _P]
+    lib.lsa_score_chunks.argtypes = [pp, _P, _P, _P, _P]
+    lib.lsa_topk_chunks.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+    lib.lsa_sparse_decode_attn.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
+    lib.lsa_decode_step.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+    for name in EXPORTS[3:]:
+        getattr(lib, name).restype = ctypes.c_int
+    if lib.lsa_abi_version() != 1:
+        raise RuntimeError(f"liblsa ABI version {lib.lsa_abi_version()} != 1")
+    return lib
+
+
+LIB = _load()
+
+
+class Problem:
+    """Shape of one decode step (mirrors ``lsa_problem``; keeps its host arrays alive)."""
+
+    def __init__(self, ctx_tokens: Sequence[int], chunk_size: int, keep: Sequence[int], n_q_heads: int,
+                 n_kv_heads: int, head_dim: int = 128, emb_dim: int = 256, n_lookahead: int = 1,
+                 n_qtok: int = 1, emb_dtype: str = "bf16", kv_chunk_stride: int = 0, kv_head_stride: int = 0):
+        B = len(ctx_tokens)
+        self._ctx = (ctypes.c_int64 * max(B, 1))(*ctx_tokens)
+        self._keep = (ctypes.c_int32 * max(len(keep), 1))(*keep)
+        self.c = lsa_problem(B, chunk_size, n_q_heads, n_kv_heads, head_dim, emb_dim, n_lookahead, n_qtok,
+                             DTYPES[emb_dtype] if isinstance(emb_dtype, str) else int(emb_dtype), 0,
+                             ctypes.cast(self._ctx, ctypes.POINTER(ctypes.c_int64)),
+                             ctypes.cast(self._keep, ctypes.POINTER(ctypes.c_int32)), kv_chunk_stride,
+                             kv_head_stride)
+
+    @classmethod
+    def from_synth(cls, prob, **kw) -> "Problem":
+        return cls(prob.ctx_tokens, prob.chunk, prob.keep, prob.n_q_heads, prob.n_kv_heads, prob.head_dim,
+                   prob.emb_dim, prob.n_lookahead, prob.n_qtok, prob.emb_dtype, **kw)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(rc: int, fn: str) -> None:
+    if rc != LSA_OK:
+        raise LsaError(rc, fn, LIB.lsa_last_error().decode())
+
+
+def last_error() -> str:
+    return LIB.lsa_last_error().decode()
+
+
+def lsa_validate(p: Problem) -> int:
+    return LIB.lsa_validate(p.ref)
+
+
+def lsa_max_sel(p: Problem) -> int:
+    v = ctypes.c_int32()
+    _check(LIB.lsa_max_sel(p.ref, ctypes.byref(v)), "lsa_max_sel")
+    return v.value
+
+
+def lsa_max_keep(p: Problem) -> int:
+    v = ctypes.c_int32()
+    _check(LIB.lsa_max_keep(p.ref, ctypes.byref(v)), "lsa_max_keep")
+    return v.value
+
+
+def lsa_workspace_size(p: Problem) -> int:
+    v = ctypes.c_size_t()
+    _check(LIB.lsa_workspace_size(p.ref, ctypes.byref(v)), "lsa_workspace_size")
+    return v.value
+
+
+def lsa_workspace_init(ws, nbytes: int, stream=None) -> None:
+    _check(LIB.lsa_workspace_init(_ptr(ws), nbytes, _stream(stream)), "lsa_workspace_init")
+
+
+def lsa_score_chunks(p: Problem, query_emb, chunk_emb, scores, stream=None) -> None:
+    _check(LIB.lsa_score_chunks(p.ref, _ptr(query_emb), _ptr(chunk_emb), _ptr(scores), _stream(stream)),
+           "lsa_score_chunks")
+
+
+def lsa_topk_chunks(p: Problem, scores, sel_idx, sel_count, per_query_idx=None, ws=None, ws_bytes: int = 0,
+                    stream=None) -> None:
+    _check(LIB.lsa_topk_chunks(p.ref, _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(per_query_idx), _ptr(ws),
+                               ws_bytes, _stream(stream)), "lsa_topk_chunks")
+
+
+def lsa_sparse_decode_attn(p: Problem, q, k_cache, v_cache, sel_idx, sel_count, softmax_scale: float, out,
+                           lse=None, ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(LIB.lsa_sparse_decode_attn(p.ref, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(sel_idx),
+                                      _ptr(sel_count), float(softmax_scale), _ptr(out), _ptr(lse), _ptr(ws),
+                                      ws_bytes, _stream(stream)), "lsa_sparse_decode_attn")
+
+
+def lsa_decode_step(p: Problem, query_emb, chunk_emb, q, k_cache, v_cache, softmax_scale: float, out, lse=None,
+                    sel_idx=None, sel_count=None, ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(LIB.lsa_decode_step(p.ref, _ptr(query_emb), _ptr(chunk_emb), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                               float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx), _ptr(sel_count), _ptr(ws),
+                               ws_bytes, _stream(stream)), "lsa_decode_step")

@@ -1,0 +1,116 @@
+"""The C ABI on the CPU: every symbol that include/lsa.h declares is exported,
+and argument validation rejects bad problems and buffers before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_09079_amd as L
+from paper_2606_09079_amd import lsa as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "lsa.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_ ]*?[\s\*]+(lsa_[a-z_]+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_four_steps():
+    names = declared_functions()
+    for n in ("lsa_score_chunks", "lsa_topk_chunks", "lsa_sparse_decode_attn", "lsa_decode_step"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(B._build.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in lsa.h but not exported"
+    assert set(declared_functions()) == set(B.EXPORTS)
+
+
+def test_abi_version_and_status_strings():
+    assert L.LIB.lsa_abi_version() == 1
+    assert L.LIB.lsa_status_string(0) == b"LSA_OK"
+    assert L.LIB.lsa_status_string(3) == b"LSA_ERR_WORKSPACE"
+
+
+def good(**kw):
+    args = dict(ctx_tokens=[64 * 100, 64 * 10], chunk_size=64, keep=[10, 3], n_q_heads=8, n_kv_heads=2)
+    args.update(kw)
+    return L.Problem(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ctx_tokens=[]), B.LSA_ERR_INVALID_ARG),
+    (dict(ctx_tokens=[64] * 65, keep=[1] * 65), B.LSA_ERR_INVALID_ARG),
+    (dict(chunk_size=32, ctx_tokens=[3200, 640]), B.LSA_ERR_UNSUPPORTED),
+    (dict(ctx_tokens=[6401, 640]), B.LSA_ERR_INVALID_ARG),
+    (dict(ctx_tokens=[0, 640]), B.LSA_ERR_INVALID_ARG),
+    (dict(keep=[0, 3]), B.LSA_ERR_INVALID_ARG),
+    (dict(keep=[101, 3]), B.LSA_ERR_INVALID_ARG),
+    (dict(n_q_heads=9), B.LSA_ERR_INVALID_ARG),
+    (dict(head_dim=64), B.LSA_ERR_UNSUPPORTED),
+    (dict(emb_dim=100), B.LSA_ERR_UNSUPPORTED),
+    (dict(n_lookahead=17), B.LSA_ERR_INVALID_ARG),
+    (dict(n_qtok=0), B.LSA_ERR_INVALID_ARG),
+    (dict(n_q_heads=64, n_kv_heads=1, n_qtok=4), B.LSA_ERR_UNSUPPORTED),
+    (dict(emb_dtype=7), B.LSA_ERR_INVALID_ARG),
+    (dict(kv_head_stride=64 * 128, kv_chunk_stride=64 * 128), B.LSA_ERR_INVALID_ARG),
+    (dict(kv_head_stride=100), B.LSA_ERR_INVALID_ARG),
+    (dict(n_lookahead=2, ctx_tokens=[64 * 300000, 64], keep=[1, 1]), B.LSA_ERR_UNSUPPORTED),
+])
+def test_validation_rejects(kw, status):
+    p = good(**kw)
+    assert L.lsa_validate(p) == status
+    assert L.last_error() != ""
+
+
+def test_validation_accepts_presets_and_head_major_strides():
+    import lsa_synth
+    for name in lsa_synth.PRESETS:
+        assert L.lsa_validate(L.Problem.from_synth(lsa_synth.make_problem(name, 0))) == 0
+    total = 110
+    p = good(kv_head_stride=total * 64 * 128, kv_chunk_stride=64 * 128)
+    assert L.lsa_validate(p) == 0
+
+
+def test_sizes():
+    p = good()
+    assert L.lsa_max_sel(p) == 10
+    assert L.lsa_max_keep(p) == 10
+    q = good(n_lookahead=4)
+    assert L.lsa_max_sel(q) == 40 and L.lsa_max_keep(q) == 10
+    assert L.lsa_workspace_size(q) > L.lsa_workspace_size(p) > 0
+
+
+FAKE = 1 << 20          # 16-byte aligned, never dereferenced: calls fail validation first
+MISALIGNED = FAKE + 4
+
+
+def _rc(fn, *args):
+    return fn(*args)
+
+
+def test_entry_points_reject_bad_buffers_without_launching():
+    p = good()
+    ws = L.lsa_workspace_size(p)
+    lib = L.LIB
+    assert lib.lsa_score_chunks(p.ref, None, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_score_chunks(p.ref, MISALIGNED, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_topk_chunks(p.ref, FAKE, None, FAKE, None, FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_sparse_decode_attn(p.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, FAKE, ws - 1,
+                                      None) == B.LSA_ERR_WORKSPACE
+    assert lib.lsa_sparse_decode_attn(p.ref, FAKE, FAKE, FAKE, FAKE, FAKE, float("nan"), FAKE, None, FAKE, ws,
+                                      None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_sparse_decode_attn(p.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, ws,
+                                      None) == B.LSA_ERR_WORKSPACE
+    assert lib.lsa_decode_step(p.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, FAKE, None, FAKE, ws,
+                               None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_decode_step(p.ref, FAKE, FAKE, FAKE, FAKE, MISALIGNED, 0.0, FAKE, None, None, None, FAKE,
+                               ws, None) == B.LSA_ERR_INVALID_ARG
+    q = good(n_lookahead=3)
+    assert lib.lsa_topk_chunks(q.ref, FAKE, FAKE, FAKE, None, FAKE, 16, None) == B.LSA_ERR_WORKSPACE
+    with pytest.raises(L.LsaError):
+        L.lsa_score_chunks(p, None, FAKE, FAKE, stream=0)

@@ -1,0 +1,177 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, on the GPU.
+
+Small problems are checked element by element on every row; they span many
+MFMA tiles, several splits, ragged batches, both chunk sizes, every embedding
+dtype and width, GQA groups of 1 to 8, several query tokens and lookahead
+queries, and the degenerate cases (k = 1, k = n, one chunk, tied and signed-zero
+scores).  The five full-size workloads run in the launch configuration the
+benchmark times and are checked on every score and kept id and on sampled
+attention rows.
+"""
+import numpy as np
+import pytest
+
+import lsa_synth as synth
+from gpu_case import log, run_case
+
+pytestmark = pytest.mark.gpu
+
+
+def _lib():
+    import paper_2606_09079_amd as L
+    return L
+
+
+def P(name, ctx, chunk, keep, hq, hkv, emb_dim=256, dtype="bf16", Q=1, Tq=1, planted=0):
+    return synth.Problem(name, list(ctx), chunk, list(keep), hq, hkv, emb_dim=emb_dim, emb_dtype=dtype,
+                         n_lookahead=Q, n_qtok=Tq, planted=planted)
+
+
+SMALL = [
+    P("f32_g1", [64 * 37], 64, [5], 4, 4, dtype="f32", planted=2),
+    P("bf16_g4_ragged", [64 * 50, 64 * 3, 64, 64 * 129], 64, [7, 3, 1, 40], 16, 4),
+    P("i8_keep_all", [64 * 300, 64 * 300], 64, [30, 300], 8, 2, dtype="i8", planted=4),
+    P("c128_tq4_rows16", [128 * 40], 128, [9], 8, 2, emb_dim=128, Tq=4),
+    P("rows20_d512", [64 * 33, 64 * 20], 64, [6, 20], 40, 8, emb_dim=512, Tq=4),
+    P("lookahead_rows128", [128 * 70, 128 * 45], 128, [6, 9], 16, 2, Q=4, Tq=16),
+    P("i8_d64_q3_tq2", [64 * 90], 64, [10], 2, 1, emb_dim=64, dtype="i8", Q=3, Tq=2),
+    P("f32_d512_q2", [64 * 61], 64, [11], 8, 4, emb_dim=512, dtype="f32", Q=2),
+    P("many_splits", [64 * 4000], 64, [3000], 8, 8),
+    P("keys_beyond_lds", [64 * 20000], 64, [2000], 8, 8, dtype="f32"),
+    P("batch64", [64 * (3 + (b * 7) % 23) for b in range(64)], 64, [1 + (b % 3) for b in range(64)], 4, 1),
+    P("single_chunk", [64, 128], 64, [1, 2], 4, 2),
+]
+
+
+@pytest.mark.parametrize("prob", SMALL, ids=lambda p: p.name)
+def test_small_problem(prob):
+    r = run_case(prob, seed=11)
+    assert r["worst_attn"] <= 2e-3
+
+
+def test_device_fill_matches_host_generator():
+    import torch
+    prob = P("fill", [64 * 5, 64 * 3], 64, [1, 1], 4, 2)
+    dev = synth.device_inputs(prob, 3)
+    k = dev["k"].cpu().numpy().view(np.uint16).reshape(prob.total_chunks, 2, 64, 128)
+    v = dev["v"].cpu().numpy().view(np.uint16).reshape(prob.total_chunks, 2, 128, 64)
+    for b in range(2):
+        for g in range(2):
+            ch = np.arange(prob.n_chunks[b])
+            hk = synth.kv_chunks(prob, 3, "k", b, g, ch)
+            hv = synth.kv_chunks(prob, 3, "v", b, g, ch)
+            o = prob.chunk_offsets[b]
+            assert np.array_equal(k[o:o + len(ch), g], hk)
+            assert np.array_equal(v[o:o + len(ch), g], np.transpose(hv, (0, 2, 1)))
+    torch.cuda.synchronize()
+
+
+def test_topk_ties_and_signed_zero():
+    """Tied scores go to the lower chunk id; -0.0 ties +0.0 (given scores)."""
+    import torch
+    import oracle
+    L = _lib()
+    n = 4096
+    rng = np.random.default_rng(5)
+    s = np.round(rng.standard_normal(n), 1).astype(np.float32)   # heavy ties
+    s[::7] = 0.0
+    s[3::7] = -0.0
+    for k in (1, 5, 100, 1000, 2047, n):
+        prob = L.Problem([64 * n], 64, [k], 4, 4)
+        sc = torch.from_numpy(s).cuda()
+        sel = torch.full((1, k), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+        L.lsa_topk_chunks(prob, sc, sel, cnt)
+        torch.cuda.synchronize()
+        ref = oracle.topk(s.astype(np.float64), k)
+        assert cnt.item() == k
+        assert np.array_equal(sel.cpu().numpy()[0], ref), f"k={k}"
+
+
+def test_int_scores_extremes():
+    """int32 keys at the extremes of the range and all-equal scores."""
+    import torch
+    import oracle
+    L = _lib()
+    n = 3000
+    s = np.full(n, 7, dtype=np.int32)
+    s[10] = 2**31 - 1
+    s[20] = -2**31
+    s[30] = -1
+    s[40] = 0
+    for k in (1, 2, 3, 500, n - 1, n):
+        prob = L.Problem([64 * n], 64, [k], 4, 4, emb_dtype="i8")
+        sc = torch.from_numpy(s).cuda()
+        sel = torch.full((1, k), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+        L.lsa_topk_chunks(prob, sc, sel, cnt)
+        torch.cuda.synchronize()
+        assert np.array_equal(sel.cpu().numpy()[0], oracle.topk(s.astype(np.int64), k)), f"k={k}"
+
+
+def test_step_is_deterministic_and_workspace_reusable():
+    """Two fused steps give bitwise-equal results; a workspace reused by a
+    different problem in between still gives the same answer (the split
+    counters are left at zero by every call)."""
+    import torch
+    L = _lib()
+    prob = P("det", [64 * 3000], 64, [700], 32, 8)
+    other = P("other", [64 * 100, 64 * 50], 64, [20, 5], 8, 2)
+    dev = synth.device_inputs(prob, 1)
+    dev2 = synth.device_inputs(other, 2)
+    Pp, Po = L.Problem.from_synth(prob), L.Problem.from_synth(other)
+    ws_bytes = max(L.lsa_workspace_size(Pp), L.lsa_workspace_size(Po))
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    outs = []
+    for it in range(3):
+        out = torch.empty(1, 1, 32, 128, dtype=torch.float32, device="cuda")
+        lse = torch.empty(1, 1, 32, dtype=torch.float32, device="cuda")
+        L.lsa_decode_step(Pp, dev["qe"], dev["E"], dev["q"], dev["k"], dev["v"], 0.0, out, lse, ws=ws,
+                          ws_bytes=ws_bytes)
+        if it == 1:
+            o2 = torch.empty(2, 1, 8, 128, dtype=torch.float32, device="cuda")
+            L.lsa_decode_step(Po, dev2["qe"], dev2["E"], dev2["q"], dev2["k"], dev2["v"], 0.0, o2, ws=ws,
+                              ws_bytes=ws_bytes)
+        torch.cuda.synchronize()
+        outs.append((out.cpu().numpy().copy(), lse.cpu().numpy().copy()))
+    for o, l in outs[1:]:
+        assert np.array_equal(o.view(np.uint32), outs[0][0].view(np.uint32))
+        assert np.array_equal(l.view(np.uint32), outs[0][1].view(np.uint32))
+    assert torch.count_nonzero(ws[:256 * 4]).item() >= 0  # workspace stays usable
+
+
+# ---------------------------------------------------------------- full size
+def _sample_rows(prob, n_rows):
+    rng = np.random.default_rng(0)
+    allr = [(t, h) for t in range(prob.n_qtok) for h in range(prob.n_q_heads)]
+    idx = sorted(rng.choice(len(allr), size=min(n_rows, len(allr)), replace=False).tolist())
+    return [allr[i] for i in idx]
+
+
+def test_preset_tiny():
+    prob = synth.make_problem("tiny", 0)
+    r = run_case(prob, 0)
+    assert r["modes"][0] == "exact"
+
+
+def test_preset_int8():
+    prob = synth.make_problem("int8", 0)
+    r = run_case(prob, 0, seqs=[0, 3], rows=_sample_rows(prob, 8))
+    assert all(m == "exact" for m in r["modes"].values())
+
+
+def test_preset_paper1m():
+    prob = synth.make_problem("paper1m", 0)
+    run_case(prob, 0)
+
+
+def test_preset_batch32():
+    prob = synth.make_problem("batch32", 0)
+    big = int(np.argmax(prob.ctx_tokens))
+    run_case(prob, 0, seqs=sorted({0, big, 31}), rows=_sample_rows(prob, 6))
+
+
+def test_preset_lookahead():
+    prob = synth.make_problem("lookahead", 0)
+    rows = [(t, h) for t in (0, 15) for h in range(0, 64, 9)]
+    run_case(prob, 0, seqs=[0, 7], rows=rows)
