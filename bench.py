@@ -1,0 +1,245 @@
+"""Benchmark of the LSA decode hot path on one MI355X.
+
+One step = the whole hot path -- score every chunk, keep the top-k, sparse
+decode attention over the kept chunks -- as one ``lsa_decode_step`` call on
+inputs already resident in HBM.  Workload: the paper-scale single sequence, a
+1,048,576-token context in 16,384 chunks of 64 tokens, keep 1,638 chunks (10%),
+32 query heads over 8 KV heads of dim 128, bf16 K/V, bf16 indexer embeddings of
+dim 256.  Four query sets (query embedding and attention query) rotate from
+step to step so that each step keeps a different chunk set and the 256 MB
+Infinity Cache cannot serve a previous step's bytes.
+
+Prints one JSON line: steps/s, plus a ``roofline`` object for the dominant
+kernel (sparse attention: algorithmic bytes = kept K/V + q + out, divided by
+its HIP-event-timed average launch duration on the launch stream) and a
+``cpu_baseline`` object (the CPU oracle on a bounded sample of the same
+workload, on the host cores of this run).
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode steps/sec for score+top-k+sparse attn at 1M ctx; achieved HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+WORKLOADS = {
+    "paper1m": "paper1m: 1,048,576-token context, 64-token chunks (16,384), keep 1,638 (10%), "
+               "32 query / 8 KV heads, head_dim 128, bf16 K/V, bf16 indexer dim 256, batch 1",
+}
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "attn_kernel_paper1m_traffic.md")
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def attn_source_sha() -> str:
+    with open(os.path.join(ROOT, "paper_2606_09079_amd", "csrc", "attn.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the committed rocprofv3 counter summary,
+    or None when the summary is missing or was taken on other kernel source."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    text = open(PMC_SUMMARY).read()
+    m = re.search(r"attn\.hip sha256\[:16\]:\s*([0-9a-f]{16})", text)
+    t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m or not t or m.group(1) != attn_source_sha():
+        return None
+    return float(t.group(1))
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="paper1m", choices=sorted(WORKLOADS))
+    ap.add_argument("--rotations", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="bound on the oracle sample's CPU time")
+    ap.add_argument("--only", choices=["step", "attn"], default=None,
+                    help="profiling aid: launch only this entry point in the timed loop")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="profiling aid: also run one plain copy of this many MiB (known bytes)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported by this build "
+              f"(the hot path is measured per GPU, see the sharding notes in DESIGN.md)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import lsa_synth as synth
+    import paper_2606_09079_amd as L
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    prob = synth.make_problem(args.workload, 0)
+    t_setup = time.time()
+    host0 = synth.host_inputs(prob, 0)
+    dev = synth.device_inputs(prob, 0, host=host0)
+    rot = []
+    for r in range(args.rotations):
+        h = host0 if r == 0 else synth.host_inputs(prob, 1000 + r)
+        qe = torch.from_numpy(np.ascontiguousarray(h["qe"]).view(np.int16)).cuda()
+        q = torch.from_numpy(np.ascontiguousarray(h["q"]).view(np.int16)).cuda()
+        rot.append((qe, q))
+    P = L.Problem.from_synth(prob)
+    B, Tq, Hq, d = prob.batch, prob.n_qtok, prob.n_q_heads, prob.head_dim
+    ws_bytes = L.lsa_workspace_size(P)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty(B, Tq, Hq, d, dtype=torch.float32, device="cuda")
+    lse = torch.empty(B, Tq, Hq, dtype=torch.float32, device="cuda")
+    max_sel = L.lsa_max_sel(P)
+    sels = [torch.empty(B, max_sel, dtype=torch.int32, device="cuda") for _ in rot]
+    cnts = [torch.empty(B, dtype=torch.int32, device="cuda") for _ in rot]
+    torch.cuda.synchronize()
+    log(f"[bench] setup {time.time() - t_setup:.1f}s, workspace {ws_bytes / 2**20:.1f} MiB")
+
+    def step(i: int) -> None:
+        qe, q = rot[i % len(rot)]
+        L.lsa_decode_step(P, qe, dev["E"], q, dev["k"], dev["v"], 0.0, out, lse, sels[i % len(rot)],
+                          cnts[i % len(rot)], ws, ws_bytes, stream)
+
+    def attn(i: int) -> None:
+        _, q = rot[i % len(rot)]
+        L.lsa_sparse_decode_attn(P, q, dev["k"], dev["v"], sels[i % len(rot)], cnts[i % len(rot)], 0.0, out, lse,
+                                 ws, ws_bytes, stream)
+
+    # every rotation's kept set exists before any attention-only launch
+    for i in range(len(rot)):
+        step(i)
+    torch.cuda.synchronize()
+
+    if args.copy_calibration_mib:
+        nbytes = args.copy_calibration_mib << 20
+        src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        synth.copy_device(src.data_ptr(), dst.data_ptr(), nbytes, stream.cuda_stream)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {nbytes} bytes done")
+
+    fn = attn if args.only == "attn" else step
+    for i in range(args.warmup):
+        fn(i)
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps, synchronised on both sides
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        fn(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = ev0.elapsed_time(ev1)
+    ms_per_step = ms_total / args.steps
+    log(f"[bench] timed {args.steps} x {fn.__name__}: {ms_per_step * 1e3:.2f} us/step (wall {wall:.3f}s)")
+
+    # ---- dominant kernel: per-launch HIP events around the attention launch
+    n_att = max(args.steps, 20)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_att)]
+    for i in range(n_att):
+        evs[i][0].record(stream)
+        attn(i)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    att_ms = [a.elapsed_time(b) for a, b in evs]
+    att_avg_us = 1e3 * sum(att_ms) / len(att_ms)
+
+    counts = [int(c.cpu().sum()) for c in cnts]
+    C, Hkv = prob.chunk, prob.n_kv_heads
+    kv_bytes = [n * C * Hkv * d * 2 * 2 for n in counts]
+    attn_bytes = sum(kv_bytes) / len(kv_bytes) + B * Tq * Hq * d * (2 + 4) + B * Tq * Hq * 4 + max(counts) * 4
+    emb_bytes = prob.total_chunks * prob.emb_dim * 2 + B * prob.n_lookahead * prob.emb_dim * 2
+    step_bytes = attn_bytes + emb_bytes
+    achieved = attn_bytes / (att_avg_us * 1e-6) / 1e9
+    traffic = measured_traffic()
+
+    result = {
+        "metric": METRIC,
+        "value": round(1e3 / ms_per_step, 2) if args.only in (None, "step") else None,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.workload], "global_batch": B, "seq_len": prob.ctx_tokens[0],
+                   "parallelism": "single GPU", "kept_chunks_per_step": counts[0], "rotations": len(rot)},
+        "step_gbs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "step_roofline_frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "kernel": "attn_kernel (lsa_sparse_decode_attn)", "avg_launch_us": round(att_avg_us, 2),
+                     "algorithmic_bytes_per_launch": int(attn_bytes)},
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(prob, host0, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def cpu_baseline(prob, host, budget_s: float):
+    """The CPU oracle, as it stands, on one full step of the same workload
+    (score all chunks, top-k, attention for every query head), repeated while
+    the time bound allows.  Independent KV-head groups run on parallel threads."""
+    import numpy as np
+
+    import lsa_synth as synth
+    import oracle
+
+    t_prep = time.time()
+    _, _, kept = oracle.select_for_sequence(prob, host, 0)
+    Hkv, G = prob.n_kv_heads, prob.group
+    kv = {(w, g): synth.kv_head_sparse(prob, 0, w, 0, g, kept) for g in range(Hkv) for w in ("k", "v")}
+    log(f"[bench] cpu baseline inputs prepared in {time.time() - t_prep:.1f}s")
+    threads = min(Hkv, os.cpu_count() or 1)
+
+    def one_step():
+        _, _, kept_s = oracle.select_for_sequence(prob, host, 0)
+
+        def head(g):
+            qr = np.stack([host["q"][0, 0, g * G + j] for j in range(G)])
+            return oracle.attention(qr, kv[("k", g)], kv[("v", g)], kept_s, prob.chunk)
+
+        with cf.ThreadPoolExecutor(threads) as ex:
+            list(ex.map(head, range(Hkv)))
+
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        one_step()
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or el / reps * (reps + 1) > 3 * budget_s:
+            break
+    return {"value": round(reps / el, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full step(s) of the same 1M-token workload (score 16,384 chunks, top-k 1,638, "
+                      f"fp64 attention for all 32 query heads) in {el:.1f}s; KV-head groups on {threads} threads"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -37,9 +37,15 @@
  *    int32 [batch]); max_sel = max_b min(n_lookahead * keep[b], n_b).
  *  - KV cache (bf16, raw 16-bit patterns), paged by chunk.  The block of global
  *    chunk c and KV head g starts at element c * kv_chunk_stride + g *
- *    kv_head_stride and holds chunk_size * head_dim elements:
- *        K block: [token][dim]   element t * head_dim + e
- *        V block: [dim][token]   element e * chunk_size + t
+ *    kv_head_stride and holds the chunk_size x 128 values of that chunk and
+ *    head in MFMA operand order, so that every 1 KiB of the block is exactly
+ *    what one wavefront load feeds to one v_mfma_f32_16x16x32_bf16.  Token t
+ *    (0 <= t < chunk_size) and dimension e (0 <= e < 128) sit at element
+ *        K block: ((((t/32*2 + t/4%2)*4 + e/32)*4 + e/8%4)*16 + t%32/8*4 + t%4)*8 + e%8
+ *        V block: (((t/32*8 + e/16)*4 + t%32/8)*16 + e%16)*8 + t%8
+ *    (integer division).  A serving system writes each new token's K and V
+ *    rows into these positions once; every decode step then streams whole,
+ *    contiguous 16 KiB (C = 64) or 32 KiB (C = 128) blocks.
  *  - q: bf16 [batch][n_qtok][n_q_heads][head_dim].  Query head h reads KV head
  *    h / (n_q_heads / n_kv_heads).  out: float32, same shape as q.  lse: float32
  *    [batch][n_qtok][n_q_heads], the natural-log log-sum-exp of the scaled
@@ -106,8 +112,8 @@ lsa_status lsa_max_keep(const lsa_problem* p, int32_t* max_keep);
 /* Bytes of device workspace that any entry point below needs for p. */
 lsa_status lsa_workspace_size(const lsa_problem* p, size_t* bytes);
 /* Zero-fill a workspace on `stream` (a fill kernel, safe under graph capture).
- * A workspace must be zero-filled once before its first use; every call leaves
- * the counters it uses at zero again. */
+ * Optional: no entry point needs a zeroed workspace; it only makes the
+ * workspace contents deterministic before a first call. */
 lsa_status lsa_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
 /*

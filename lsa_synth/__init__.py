@@ -325,15 +325,18 @@ def dev_lib() -> ctypes.CDLL:
                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
         lib.synth_fill_kv_device.restype = ctypes.c_int
+        lib.synth_copy_device.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        lib.synth_copy_device.restype = ctypes.c_int
         _dev_lib = lib
     return _dev_lib
 
 
 def fill_kv_device(prob: Problem, seed: int, which: str, out_ptr: int, table_ptr: int, stream_ptr: int,
                    chunk_stride: Optional[int] = None, head_stride: Optional[int] = None) -> None:
-    """Fill a device K (``[chunk][head][token][dim]``) or V (``[chunk][head][dim][token]``) cache.
+    """Fill a device K or V cache in the library's chunk-paged, MFMA-ordered block layout.
 
-    ``table_ptr`` is a device copy of :func:`normal_table_bf16`.
+    ``table_ptr`` is a device copy of :func:`normal_table_bf16`.  See
+    :func:`block_offset` for where token t, dim e of a block lands.
     """
     C, d, H = prob.chunk, prob.head_dim, prob.n_kv_heads
     hs = C * d if head_stride is None else head_stride
@@ -343,6 +346,23 @@ def fill_kv_device(prob: Problem, seed: int, which: str, out_ptr: int, table_ptr
                                         cs, hs, 0 if which == "k" else 1, stream_ptr)
     if rc != 0:
         raise RuntimeError(f"synth_fill_kv_device failed with code {rc}")
+
+
+def block_offset(which: str, t, e):
+    """Element offset of (token t, dim e) inside one (chunk, KV head) block of the
+    K (``which='k'``) or V cache, head_dim 128.  Works on numpy arrays."""
+    t = np.asarray(t, dtype=np.int64)
+    e = np.asarray(e, dtype=np.int64)
+    if which == "k":
+        return ((((t // 32 * 2 + t // 4 % 2) * 4 + e // 32) * 4 + e // 8 % 4) * 16 + t % 32 // 8 * 4 + t % 4) * 8 + e % 8
+    return (((t // 32 * 8 + e // 16) * 4 + t % 32 // 8) * 16 + e % 16) * 8 + t % 8
+
+
+def copy_device(src_ptr: int, dst_ptr: int, nbytes: int, stream_ptr: int) -> None:
+    """A plain device copy of known size (for calibrating byte counters)."""
+    rc = dev_lib().synth_copy_device(src_ptr, dst_ptr, nbytes, stream_ptr)
+    if rc != 0:
+        raise RuntimeError(f"synth_copy_device failed with code {rc}")
 
 
 def device_inputs(prob: Problem, seed: int, device: str = "cuda", host: Optional[Dict[str, object]] = None):

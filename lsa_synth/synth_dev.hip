@@ -6,10 +6,13 @@
 // dimension e is table[draw(key, (tau * hkv + h) * d + e) >> 48], with draw the
 // SplitMix64 counter generator (Steele, Lea, Flood, OOPSLA 2014).
 //
-// Physical layout of one (chunk, head) block of chunk*d elements:
-//   inner_transposed == 0 : [token][dim]  (element t*d + e)
-//   inner_transposed == 1 : [dim][token]  (element e*chunk + t)
-// The block of global chunk c and head h starts at c*chunk_stride + h*head_stride.
+// The block of global chunk c and KV head h starts at c*chunk_stride +
+// h*head_stride and holds chunk*128 bf16 values in the MFMA operand order of
+// the decode-attention library (head_dim 128, chunk a multiple of 32):
+//   K (value_block == 0): token t, dim e at
+//     ((((t/32*2 + t/4%2)*4 + e/32)*4 + e/8%4)*16 + t%32/8*4 + t%4)*8 + e%8
+//   V (value_block == 1): token t, dim e at
+//     (((t/32*8 + e/16)*4 + t%32/8)*16 + e%16)*8 + t%8
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -26,7 +29,7 @@ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
 __global__ void __launch_bounds__(256)
 fill_kv(uint64_t key, const uint16_t* __restrict__ table, uint16_t* __restrict__ out,
         int64_t total_chunks, int32_t hkv, int32_t chunk, int32_t d,
-        int64_t chunk_stride, int64_t head_stride, int32_t inner_transposed) {
+        int64_t chunk_stride, int64_t head_stride, int32_t value_block) {
   const int64_t block_elems = (int64_t)chunk * d;
   const int64_t groups_per_block = block_elems / 8;
   const int64_t total = total_chunks * hkv * groups_per_block;
@@ -40,9 +43,17 @@ fill_kv(uint64_t key, const uint16_t* __restrict__ table, uint16_t* __restrict__
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int64_t inner = inner0 + j;
+      const int64_t w = inner % 8, n16 = (inner / 8) % 16, kg = (inner / 128) % 4;
       int64_t t, e;
-      if (inner_transposed) { e = inner / chunk; t = inner - e * chunk; }
-      else { t = inner / d; e = inner - t * d; }
+      if (value_block) {
+        const int64_t nb = (inner / 512) % 8, tt = inner / 4096;
+        t = 32 * tt + 8 * kg + w;
+        e = 16 * nb + n16;
+      } else {
+        const int64_t jj = (inner / 512) % 4, hf = (inner / 2048) % 2, tt = inner / 4096;
+        t = 32 * tt + 8 * (n16 / 4) + 4 * hf + n16 % 4;
+        e = 8 * (kg + 4 * jj) + w;
+      }
       const int64_t tau = c * chunk + t;
       const uint64_t idx = (uint64_t)((tau * hkv + h) * d + e);
       v[j] = table[mix64(key + (idx + 1ULL) * kGamma) >> 48];
@@ -56,14 +67,32 @@ fill_kv(uint64_t key, const uint16_t* __restrict__ table, uint16_t* __restrict__
   }
 }
 
+// Plain 16-byte copy, used only to calibrate hardware byte counters against a
+// kernel whose traffic is known exactly (n16 * 16 bytes read and written).
+__global__ void __launch_bounds__(256) copy16(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n16) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
 }  // namespace
+
+extern "C" int synth_copy_device(const void* src, void* dst, int64_t bytes, void* stream) {
+  if (!src || !dst || bytes <= 0 || bytes % 16 != 0) return 1;
+  if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) return 1;
+  const int64_t n16 = bytes / 16;
+  int64_t blocks = (n16 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(copy16, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                     static_cast<const uint4*>(src), static_cast<uint4*>(dst), n16);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 // Returns 0 on success, 1 on a bad argument, 2 on a HIP launch error.
 extern "C" int synth_fill_kv_device(uint64_t key, const uint16_t* table, uint16_t* out,
                                     int64_t total_chunks, int32_t hkv, int32_t chunk,
                                     int32_t d, int64_t chunk_stride, int64_t head_stride,
-                                    int32_t inner_transposed, void* stream) {
-  if (!table || !out || total_chunks <= 0 || hkv <= 0 || chunk <= 0 || d <= 0) return 1;
+                                    int32_t value_block, void* stream) {
+  if (!table || !out || total_chunks <= 0 || hkv <= 0 || chunk <= 0 || chunk % 32 != 0 || d != 128) return 1;
   if (((int64_t)chunk * d) % 8 != 0 || chunk_stride % 8 != 0 || head_stride % 8 != 0) return 1;
   if ((reinterpret_cast<uintptr_t>(out) & 15) != 0) return 1;
   const int64_t total = total_chunks * hkv * ((int64_t)chunk * d / 8);
@@ -71,6 +100,6 @@ extern "C" int synth_fill_kv_device(uint64_t key, const uint16_t* table, uint16_
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(fill_kv, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, key,
                      table, out, total_chunks, hkv, chunk, d, chunk_stride, head_stride,
-                     inner_transposed);
+                     value_block);
   return hipGetLastError() == hipSuccess ? 0 : 2;
 }

@@ -4,7 +4,9 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
-LIB_PATH = os.path.join(HERE, "liblsa.so")
+# LSA_LIB points the binding at another build of the same sources (for example an
+# installed copy); by default the in-tree library is used.
+LIB_PATH = os.environ.get("LSA_LIB") or os.path.join(HERE, "liblsa.so")
 SOURCES = ("score.hip", "topk.hip", "attn.hip", "lsa_api.hip")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

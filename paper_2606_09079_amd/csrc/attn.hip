@@ -2,34 +2,35 @@
 // the tokens of the kept chunks only (Sec. 2.1, core attention over the
 // selected entries), gathered by chunk id from the paged bf16 cache.
 //
-// Flash-decoding with split-K over the kept-chunk list.  Work unit = (sequence
-// b, KV head g, split s); a split owns a contiguous range of the kept list.
-// All G * Tq query rows that read KV head g are handled together, so each K/V
-// byte is fetched from HBM once.
+// Flash-decoding with split-K over the kept-chunk list, in two kernels:
 //
-// Both products run on MFMA v_mfma_f32_16x16x32_bf16 with no data shuffles:
-//  * QK computes S^T = K Q^T with 16 tokens as the M dimension and 16 query rows
-//    as N.  The M rows of the two 16-token MFMAs of a 32-token tile are permuted
-//    (tokens 8a+0..3 and 8a+4..7) so that after the product each lane holds the
-//    8 consecutive tokens 8*(lane/16)..+7 of query row lane%16 -- exactly the
-//    A-operand layout the PV MFMA wants for P.
-//  * PV computes O = P V with the 32 tokens as K and 16 head dims per MFMA as N;
-//    the V block is stored [dim][token], so every B operand is one 16-byte load.
-//  * P is split into bf16 hi + lo parts (two MFMAs), keeping ~16 significant
-//    bits of the probabilities; logits, the running max/sum and O stay fp32.
-// Every operand load is a 16-byte global load; per instruction a wavefront
-// reads 16 rows x 64 contiguous bytes.
+// attn_split_kernel -- work unit = (sequence b, KV head g, split s).  The kept
+//   list of (b, g) is cut into 32-token tiles and each split owns a contiguous,
+//   equal share of them; the split count is sized so that the whole grid is one
+//   resident round on MI355X (256 CUs x 2 workgroups).  All G * Tq query rows
+//   that read KV head g are handled together, so every K/V byte is fetched from
+//   HBM once.  Both products run on v_mfma_f32_16x16x32_bf16:
+//   * QK computes S^T = K Q^T with 16 tokens as M and 16 query rows as N.  The
+//     cache stores each (chunk, head) block in MFMA operand order, and the M
+//     rows of the two 16-token MFMAs of a tile are tokens 8a+0..3 and 8a+4..7,
+//     so after the product each lane holds the 8 consecutive tokens
+//     8*(lane/16)..+7 of query row lane%16 -- the A-operand layout PV needs.
+//   * PV computes O = P V with the tile's 32 tokens as K and 16 head dims per
+//     MFMA as N.  P is split into bf16 hi + lo parts (two MFMAs), keeping ~16
+//     significant bits; logits, the running max / sum and O stay fp32.
+//   Every load instruction reads 1 KiB of contiguous cache, and two tiles are
+//   in flight per wave (the next tile loads while the current one computes).
+//   Rows <= 16: the 4 waves of a workgroup take consecutive quarters of the
+//   split's tiles and merge their (m, l, O) states through LDS.  Rows > 16:
+//   each wave owns one 16-row block and walks all tiles of the split; the
+//   workgroup's waves read the same cache lines back to back, so only the first
+//   read reaches HBM.  Partials (m, l, O) go to the workspace.
 //
-// Rows <= 16 (one 16-row block): the 4 waves of a workgroup take alternate
-// chunks of the split and merge their (m, l, O) states through LDS.  Rows > 16:
-// each wave owns one 16-row block and walks every chunk of the split; the
-// workgroup's waves read the same K/V lines back to back, so only the first
-// read reaches HBM.
-//
-// Split partials (m, l, O) go to the workspace; the last workgroup of each
-// (b, g, row group) -- detected with a device-scope counter, released and
-// acquired with fences -- merges them in split order, so results are bitwise
-// reproducible, and resets the counter to zero for the next call.
+// attn_combine_kernel -- one workgroup per output row (b, t, h) merges the
+//   splits of its (b, g) in split order: weights exp2(m_s - M), then O as a
+//   weighted sum of float4 slices, each thread holding a strided subset of the
+//   splits so that all its loads are in flight at once.  Fixed order throughout,
+//   so results are bitwise reproducible.
 #include "lsa_internal.h"
 
 namespace lsa {
@@ -41,6 +42,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kThreads = kAttnWaves * 64;
 constexpr int kOPad = 132;  // LDS row pitch (floats) of the wave merge
+constexpr int kCombineGroups = kThreads / (kHeadDim / 4);  // split groups in the combine
 
 __device__ __forceinline__ bf16x8 load8(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
@@ -48,37 +50,53 @@ __device__ __forceinline__ bf16x8 load8(const uint16_t* p) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// (sequence, kv head, row group, split) of attention workgroup wg
+struct Unit {
+  int b, g, rg, s, ns;
+};
+
+__device__ __forceinline__ Unit unit_of(const SeqTable& t, int RG, int wg) {
+  Unit u;
+  int b = 0;
+  while (wg >= t.wg_off[b + 1]) ++b;
+  const int ns = t.nsplit[b];
+  const int local = wg - t.wg_off[b];
+  u.b = b;
+  u.ns = ns;
+  u.g = local / (ns * RG);
+  u.rg = (local / ns) % RG;
+  u.s = local % ns;
+  return u;
+}
+
 template <int C, bool ROW_SPLIT>
-__global__ void __launch_bounds__(kThreads)
-attn_kernel(SeqTable t, AttnArgs a) {
+__global__ void __launch_bounds__(kThreads, 2)  // 2 waves per SIMD: <= 256 registers
+attn_split_kernel(SeqTable t, AttnArgs a) {
   __shared__ float sm_o[ROW_SPLIT ? 1 : kAttnWaves][16][kOPad];
   __shared__ float sm_m[kAttnWaves][16], sm_l[kAttnWaves][16];
-  __shared__ int sh_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n16 = lane & 15, kg = lane >> 4;
+  const int RG = a.row_groups, G = a.group;
+  const Unit u = unit_of(t, RG, blockIdx.x);
+  const int b = u.b, g = u.g, s = u.s, ns = u.ns;
 
-  // ---- which (sequence, kv head, row group, split) this workgroup owns
-  const int wg = blockIdx.x;
-  int b = 0;
-  while (wg >= t.wg_off[b + 1]) ++b;
-  const int ns = t.nsplit[b];
-  const int RG = a.row_groups;
-  const int local = wg - t.wg_off[b];
-  const int g = local / (ns * RG);
-  const int rg = (local / ns) % RG;
-  const int s = local % ns;
   // sel_count and the chunk ids are clamped so that malformed device inputs
   // can only give wrong numbers, never an out-of-bounds access.
+  constexpr int TPC = C / 32;  // 32-token tiles per chunk
   const int cnt = min(max(a.sel_count[b], 0), a.sel_pitch);
   const int n_b = t.n[b];
-  const int lo = (int)(((int64_t)s * cnt) / ns);
-  const int hi = (int)(((int64_t)(s + 1) * cnt) / ns);
-  const int G = a.group;
+  const int nTall = cnt * TPC;
+  const int T0 = (int)(((int64_t)s * nTall) / ns), T1 = (int)(((int64_t)(s + 1) * nTall) / ns);
+  int Tb = T0, Te = T1;
+  if constexpr (!ROW_SPLIT) {
+    Tb = T0 + (int)(((int64_t)wave * (T1 - T0)) / kAttnWaves);
+    Te = T0 + (int)(((int64_t)(wave + 1) * (T1 - T0)) / kAttnWaves);
+  }
 
   // ---- query operand: row n16 of this wave's 16-row block
-  const int rblock = ROW_SPLIT ? rg * kAttnWaves + wave : 0;
+  const int rblock = ROW_SPLIT ? u.rg * kAttnWaves + wave : 0;
   const bool block_live = rblock * 16 < a.rows;
   bf16x8 qb[4];
   {
@@ -99,84 +117,103 @@ attn_kernel(SeqTable t, AttnArgs a) {
   for (int nb = 0; nb < 8; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int c_first = ROW_SPLIT ? lo : lo + wave;
-  const int c_step = ROW_SPLIT ? 1 : kAttnWaves;
-  const int32_t* sel = a.sel_idx + (int64_t)b * a.sel_pitch;
-  const int tokA = 8 * (n16 >> 2) + (n16 & 3);  // token of this lane's A row in the first QK MFMA
+  // Tiles Tb..Te-1 of the kept list; tile T is tile T % TPC of kept chunk T / TPC.
+  // Chunk ids are fetched 64 at a time into a register (one per lane) and read
+  // back with readlane, so no scalar load sits between consecutive tiles.
+  const int nT = block_live && Te > Tb ? Te - Tb : 0;
+  const int pos0 = Tb / TPC;
+  const int npos = nT > 0 ? (Te - 1) / TPC - pos0 + 1 : 0;
+  const int32_t* sel = a.sel_idx + (int64_t)b * a.sel_pitch + pos0;
+  int sel_base = 0;
+  int sel_lane = lane < npos ? sel[lane] : 0;
+  const uint16_t* kbase = a.k + t.chunk_off[b] * a.chunk_stride + g * a.head_stride + lane * 8;
+  const uint16_t* vbase = a.v + t.chunk_off[b] * a.chunk_stride + g * a.head_stride + lane * 8;
 
-  if (block_live) {
-    for (int pos = c_first; pos < hi; pos += c_step) {
-      const int c = min(max(__builtin_amdgcn_readfirstlane(sel[pos]), 0), n_b - 1);
-      const int64_t gc = t.chunk_off[b] + c;
-      const uint16_t* kb = a.k + gc * a.chunk_stride + g * a.head_stride;
-      const uint16_t* vb = a.v + gc * a.chunk_stride + g * a.head_stride;
+  // K and V tiles are 8 KiB each and contiguous in the MFMA-ordered block
+  // layout: load instruction q of a tile reads bytes [1024 q, 1024 q + 1024).
+  auto load_tile = [&](int i, bf16x8(&kt)[8], bf16x8(&vt)[8]) {
+    const int T = Tb + i;
+    const int j = T / TPC - pos0, tt = T % TPC;
+    if (j - sel_base >= 64) {  // wave-uniform: next window of chunk ids
+      sel_base = j & ~63;
+      sel_lane = sel_base + lane < npos ? sel[sel_base + lane] : 0;
+    }
+    const int c = min(max(__builtin_amdgcn_readlane(sel_lane, j - sel_base), 0), n_b - 1);
+    const int64_t off = (int64_t)c * a.chunk_stride + tt * (32 * kHeadDim);
+    const uint16_t* kp = kbase + off;
+    const uint16_t* vp = vbase + off;
 #pragma unroll
-      for (int tt = 0; tt < C / 32; ++tt) {
-        bf16x8 ka[2][4], vv[8];
+    for (int q = 0; q < 8; ++q) kt[q] = load8(kp + q * 512);
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
-            ka[hf][jj] = load8(kb + (32 * tt + tokA + 4 * hf) * kHeadDim + 8 * kg + 32 * jj);
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb) vv[nb] = load8(vb + (16 * nb + n16) * C + 32 * tt + 8 * kg);
+    for (int q = 0; q < 8; ++q) vt[q] = load8(vp + q * 512);
+  };
 
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+  auto compute_tile = [&](const bf16x8(&kt)[8], const bf16x8(&vt)[8]) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[0][jj], qb[jj], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[1][jj], qb[jj], s1, 0, 0, 0);
-        }
-        // lane holds logits of query row n16 for tokens 32tt + 8kg + 0..7
-        float x[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
-        float mx = -INFINITY;
+    for (int jj = 0; jj < 4; ++jj) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[jj], qb[jj], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[4 + jj], qb[jj], s1, 0, 0, 0);
+    }
+    // lane holds logits of query row n16 for tile tokens 8kg + 0..7
+    float x[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+    float mx = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          x[i] *= a.scale_log2e;
-          mx = fmaxf(mx, x[i]);
-        }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = fast_exp2(m_run - m_new);
-        float p[8], psum = 0.f;
+    for (int i = 0; i < 8; ++i) {
+      x[i] *= a.scale_log2e;
+      mx = fmaxf(mx, x[i]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = fast_exp2(m_run - m_new);
+    float p[8], psum = 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          p[i] = fast_exp2(x[i] - m_new);
-          psum += p[i];
-        }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-        if (__ballot(alpha != 1.f) != 0ull) {
-          // O rows of this lane are 4kg..4kg+3; their alphas live in lanes 4kg+r
+    for (int i = 0; i < 8; ++i) {
+      p[i] = fast_exp2(x[i] - m_new);
+      psum += p[i];
+    }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    if (__ballot(alpha != 1.f) != 0ull) {
+      // O rows of this lane are 4kg..4kg+3; their alphas live in lanes 4kg+r
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float ar = __shfl(alpha, 4 * kg + r);
+      for (int r = 0; r < 4; ++r) {
+        const float ar = __shfl(alpha, 4 * kg + r);
 #pragma unroll
-            for (int nb = 0; nb < 8; ++nb) o[nb][r] *= ar;
-          }
-        }
-        bf16x8 ph, pl;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          ph[i] = (__bf16)p[i];
-          pl[i] = (__bf16)(p[i] - (float)ph[i]);
-        }
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb) {
-          o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vv[nb], o[nb], 0, 0, 0);
-          o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vv[nb], o[nb], 0, 0, 0);
-        }
+        for (int nb = 0; nb < 8; ++nb) o[nb][r] *= ar;
       }
+    }
+    bf16x8 ph, pl;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      ph[i] = (__bf16)p[i];
+      pl[i] = (__bf16)(p[i] - (float)ph[i]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) {
+      o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vt[nb], o[nb], 0, 0, 0);
+      o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vt[nb], o[nb], 0, 0, 0);
+    }
+  };
+
+  // Two tile buffers: the loads of tile i+1 are in flight while tile i computes.
+  bf16x8 ka[8], va[8], kb2[8], vb2[8];
+  if (nT > 0) load_tile(0, ka, va);
+  for (int i = 0; i < nT; i += 2) {
+    if (i + 1 < nT) load_tile(i + 1, kb2, vb2);
+    compute_tile(ka, va);
+    if (i + 1 < nT) {
+      if (i + 2 < nT) load_tile(i + 2, ka, va);
+      compute_tile(kb2, vb2);
     }
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
 
-  // ---- write this workgroup's split partials
+  // ---- this split's partials: rows of the (b, g) group, [unit][rows_pad]
   const int rows_pad = a.rows_pad;
-  const int64_t unit0 = (int64_t)t.wg_off[b] / RG + (int64_t)g * ns;  // split 0 of (b, g)
-  const int64_t unit = unit0 + s;
+  const int64_t unit = (int64_t)t.wg_off[b] / RG + (int64_t)g * ns + s;
   if constexpr (ROW_SPLIT) {
     if (block_live) {
       const int64_t rbase = unit * rows_pad + rblock * 16;
@@ -221,47 +258,104 @@ attn_kernel(SeqTable t, AttnArgs a) {
       }
     }
   }
+}
 
-  // ---- the last split of (b, g, rg) to finish merges all splits in order
-  __threadfence();
+__global__ void __launch_bounds__(kThreads)
+attn_combine_kernel(SeqTable t, AttnArgs a) {
+  __shared__ float sm_w[kMaxSplits];
+  __shared__ float4 sm_red[kCombineGroups][kHeadDim / 4];
+  __shared__ float sm_lw[kAttnWaves];
+  __shared__ float sh_M;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = a.group;
+  const int rows_per_b = a.n_qtok * a.n_q_heads;
+  const int b = blockIdx.x / rows_per_b;
+  const int rem = blockIdx.x - b * rows_per_b;
+  const int tq = rem / a.n_q_heads, h = rem - tq * a.n_q_heads;
+  const int g = h / G, r = tq * G + h % G;  // row within the (b, g) group
+  const int ns = t.nsplit[b];
+  const int64_t unit0 = (int64_t)t.wg_off[b] / a.row_groups + (int64_t)g * ns;
+  const int rows_pad = a.rows_pad;
+
+  // split weights exp2(m_s - M) in LDS and L = sum_s w_s l_s (one round of loads)
+  float m_s = -INFINITY, l_s = 0.f;
+  if (tid < ns) {
+    const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + ((unit0 + tid) * rows_pad + r) * 2);
+    m_s = ml.x;
+    l_s = ml.y;
+  }
+  float mw = m_s;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mw = fmaxf(mw, __shfl_xor(mw, off));
+  if (lane == 0) sm_lw[wave] = mw;
   __syncthreads();
-  const int64_t cidx = ((int64_t)b * a.n_kv_heads + g) * RG + rg;
   if (tid == 0) {
-    const uint32_t prev = atomicAdd(&a.counters[cidx], 1u);
-    sh_last = (prev == (uint32_t)(ns - 1));
+    float M = sm_lw[0];
+    for (int w = 1; w < kAttnWaves; ++w) M = fmaxf(M, sm_lw[w]);
+    sh_M = M;
   }
   __syncthreads();
-  if (!sh_last) return;
-  __threadfence();
-  if (tid == 0) atomicExch(&a.counters[cidx], 0u);
+  const float M = sh_M;
+  const float f = (tid < ns && m_s != -INFINITY) ? fast_exp2(m_s - M) : 0.f;
+  if (tid < ns) sm_w[tid] = f;
+  float lf = f * l_s;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) lf += __shfl_xor(lf, off);
+  __syncthreads();  // sm_lw is reused
+  if (lane == 0) sm_lw[wave] = lf;
+  __syncthreads();
+  float L = sm_lw[0];
+  for (int w = 1; w < kAttnWaves; ++w) L += sm_lw[w];
+  const float invL = 1.f / L;
 
-  const int row_begin = ROW_SPLIT ? rg * kAttnWaves * 16 : 0;
-  const int row_end = ROW_SPLIT ? min(row_begin + kAttnWaves * 16, a.rows) : a.rows;
-  for (int idx = tid; idx < (row_end - row_begin) * kHeadDim; idx += kThreads) {
-    const int r = row_begin + idx / kHeadDim, e = idx % kHeadDim;
-    float M = -INFINITY;
-    for (int s2 = 0; s2 < ns; ++s2) M = fmaxf(M, a.part_ml[((unit0 + s2) * rows_pad + r) * 2]);
-    float acc = 0.f, L = 0.f;
-    for (int s2 = 0; s2 < ns; ++s2) {
-      const float ms = a.part_ml[((unit0 + s2) * rows_pad + r) * 2];
-      const float f = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M);
-      acc += f * a.part_o[((unit0 + s2) * rows_pad + r) * kHeadDim + e];
-      L += f * a.part_ml[((unit0 + s2) * rows_pad + r) * 2 + 1];
-    }
-    const int tq = r / G, h = g * G + r % G;
-    const int64_t orow = ((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h;
-    a.out[orow * kHeadDim + e] = acc / L;
-    if (e == 0 && a.lse != nullptr) a.lse[orow] = (M + __log2f(L)) * kLn2;
+  // O = sum_s w_s O_s: thread (group sg, slice e4) sums splits sg, sg + 8, ...
+  const int sg = tid / (kHeadDim / 4), e4 = (tid % (kHeadDim / 4)) * 4;
+  const float* src = a.part_o + (unit0 * rows_pad + r) * kHeadDim + e4;
+  const int64_t sstride = (int64_t)rows_pad * kHeadDim;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+  for (int s2 = sg; s2 < ns; s2 += kCombineGroups) {
+    const float4 v = *reinterpret_cast<const float4*>(src + s2 * sstride);
+    const float w = sm_w[s2];
+    acc.x += w * v.x;
+    acc.y += w * v.y;
+    acc.z += w * v.z;
+    acc.w += w * v.w;
   }
+  sm_red[sg][e4 / 4] = acc;
+  __syncthreads();
+  const int64_t orow = ((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h;
+  if (tid < kHeadDim / 4) {
+    float4 sum = sm_red[0][tid];
+#pragma unroll
+    for (int q = 1; q < kCombineGroups; ++q) {
+      const float4 v = sm_red[q][tid];
+      sum.x += v.x;
+      sum.y += v.y;
+      sum.z += v.z;
+      sum.w += v.w;
+    }
+    sum.x *= invL;
+    sum.y *= invL;
+    sum.z *= invL;
+    sum.w *= invL;
+    *reinterpret_cast<float4*>(a.out + orow * kHeadDim + tid * 4) = sum;
+  }
+  if (tid == 0 && a.lse != nullptr) a.lse[orow] = (M + __log2f(L)) * kLn2;
 }
 
 template <int C>
 hipError_t launch_c(const SeqTable& t, const AttnArgs& a, hipStream_t s) {
   const dim3 grid(t.wg_off[t.batch]);
   if (a.rows > 16)
-    hipLaunchKernelGGL((attn_kernel<C, true>), grid, dim3(kThreads), 0, s, t, a);
+    hipLaunchKernelGGL((attn_split_kernel<C, true>), grid, dim3(kThreads), 0, s, t, a);
   else
-    hipLaunchKernelGGL((attn_kernel<C, false>), grid, dim3(kThreads), 0, s, t, a);
+    hipLaunchKernelGGL((attn_split_kernel<C, false>), grid, dim3(kThreads), 0, s, t, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(t.batch * a.n_qtok * a.n_q_heads), dim3(kThreads), 0, s, t,
+                     a);
   return hipGetLastError();
 }
 

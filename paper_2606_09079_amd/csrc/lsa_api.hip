@@ -28,9 +28,6 @@ lsa_status hip_fail(hipError_t e, const char* what) {
 }
 
 constexpr size_t kAlign = 256;
-constexpr int kChunksPerSplitWaveSplit = 16;  // rows <= 16: chunks per workgroup (4 waves)
-constexpr int kChunksPerSplitRowSplit = 8;    // rows > 16: chunks per workgroup
-constexpr int kMaxSplits = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -45,7 +42,7 @@ struct Plan {
   int64_t n_units = 0;
   size_t emb_elem = 0;
   // workspace layout (byte offsets)
-  size_t off_counters = 0, off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0;
+  size_t off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0;
   size_t ws_total = 0;
 };
 
@@ -87,7 +84,14 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   P.rows = rows;
   P.row_groups = rows > 16 ? (rows + kAttnWaves * 16 - 1) / (kAttnWaves * 16) : 1;
   P.rows_pad = rows > 16 ? P.row_groups * kAttnWaves * 16 : 16;
-  const int cps = rows > 16 ? kChunksPerSplitRowSplit : kChunksPerSplitWaveSplit;
+  // First pass: shapes and the total kept-chunk bound, which sizes the splits.
+  int64_t sel_total = 0;
+  for (int b = 0; b < B; ++b) {
+    const int64_t L = p->ctx_tokens[b];
+    if (L >= C && L % C == 0 && p->keep[b] >= 1)
+      sel_total += std::min<int64_t>((int64_t)p->n_lookahead * p->keep[b], L / C);
+  }
+  const int tpc = C / 32;
   int64_t chunk_off = 0, wg_off = 0, swg_off = 0;
   for (int b = 0; b < B; ++b) {
     const int64_t L = p->ctx_tokens[b];
@@ -103,7 +107,12 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
     if (k < 1 || k > n)
       return fail(LSA_ERR_INVALID_ARG, "keep[%d] = %d not in [1, n_b = %lld]", b, k, (long long)n);
     const int32_t msel = (int32_t)std::min<int64_t>((int64_t)p->n_lookahead * k, n);
-    const int32_t ns = (int32_t)std::min<int64_t>(std::max<int64_t>(1, (msel + cps - 1) / cps), kMaxSplits);
+    // splits of sequence b in proportion to its share of the kept chunks, so the
+    // whole grid is about kTargetWorkgroups; at least one 32-token tile per split
+    const double share = (double)kTargetWorkgroups * (double)msel /
+                         ((double)p->n_kv_heads * P.row_groups * (double)std::max<int64_t>(sel_total, 1));
+    const int32_t ns = (int32_t)std::max<int64_t>(
+        1, std::min<int64_t>({std::llround(share), (int64_t)kMaxSplits, (int64_t)msel * tpc}));
     t.n[b] = (int32_t)n;
     t.keep[b] = k;
     t.nsplit[b] = ns;
@@ -139,8 +148,6 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   P.emb_elem = p->emb_dtype == LSA_F32 ? 4 : p->emb_dtype == LSA_BF16 ? 2 : 1;
 
   size_t off = 0;
-  P.off_counters = off;
-  off = align_up(off + (size_t)B * p->n_kv_heads * P.row_groups * 4);
   P.off_scores = off;
   off = align_up(off + (size_t)p->n_lookahead * P.total_chunks * 4);
   P.off_sel = off;
@@ -212,7 +219,6 @@ lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, cons
   a.lse = lse;
   a.part_o = reinterpret_cast<float*>(at(ws, P.off_o));
   a.part_ml = reinterpret_cast<float*>(at(ws, P.off_ml));
-  a.counters = reinterpret_cast<uint32_t*>(at(ws, P.off_counters));
   a.chunk_stride = P.chunk_stride;
   a.head_stride = P.head_stride;
   const double sc = scale > 0.f ? (double)scale : 1.0 / std::sqrt((double)kHeadDim);

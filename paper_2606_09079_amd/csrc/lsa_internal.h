@@ -32,9 +32,8 @@ struct AttnArgs {
   const int32_t* sel_count;
   float* out;
   float* lse;            // nullable
-  float* part_o;         // [wg][16][128]
-  float* part_ml;        // [wg][16][2]
-  uint32_t* counters;    // [B * Hkv * row_groups], zero between calls
+  float* part_o;         // [unit][rows_pad][128]
+  float* part_ml;        // [unit][rows_pad][2]
   int64_t chunk_stride;
   int64_t head_stride;
   float scale_log2e;     // softmax scale * log2(e)
@@ -52,6 +51,10 @@ struct AttnArgs {
 constexpr int kAttnWaves = 4;          // waves per workgroup
 constexpr int kAttnRowsPerWave = 16;   // MFMA tile rows
 constexpr int kHeadDim = 128;
+// Split-K sizing: the attention grid is sized to one resident round of the
+// MI355X (256 CUs x 2 workgroups of 256 threads at <= 256 registers).
+constexpr int kTargetWorkgroups = 512;
+constexpr int kMaxSplits = 256;  // splits per (sequence, kv head, row group)
 
 hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
                         const void* E, void* scores, hipStream_t s);

@@ -53,16 +53,19 @@ def test_device_fill_matches_host_generator():
     import torch
     prob = P("fill", [64 * 5, 64 * 3], 64, [1, 1], 4, 2)
     dev = synth.device_inputs(prob, 3)
-    k = dev["k"].cpu().numpy().view(np.uint16).reshape(prob.total_chunks, 2, 64, 128)
-    v = dev["v"].cpu().numpy().view(np.uint16).reshape(prob.total_chunks, 2, 128, 64)
+    k = dev["k"].cpu().numpy().view(np.uint16).reshape(prob.total_chunks, 2, 64 * 128)
+    v = dev["v"].cpu().numpy().view(np.uint16).reshape(prob.total_chunks, 2, 64 * 128)
+    tt, ee = np.meshgrid(np.arange(64), np.arange(128), indexing="ij")
+    ko, vo = synth.block_offset("k", tt, ee), synth.block_offset("v", tt, ee)
+    assert sorted(ko.ravel().tolist()) == list(range(64 * 128)) == sorted(vo.ravel().tolist())
     for b in range(2):
         for g in range(2):
             ch = np.arange(prob.n_chunks[b])
             hk = synth.kv_chunks(prob, 3, "k", b, g, ch)
             hv = synth.kv_chunks(prob, 3, "v", b, g, ch)
             o = prob.chunk_offsets[b]
-            assert np.array_equal(k[o:o + len(ch), g], hk)
-            assert np.array_equal(v[o:o + len(ch), g], np.transpose(hv, (0, 2, 1)))
+            assert np.array_equal(k[o:o + len(ch), g][:, ko], hk)
+            assert np.array_equal(v[o:o + len(ch), g][:, vo], hv)
     torch.cuda.synchronize()
 
 
