@@ -18,8 +18,9 @@
 //   * PV computes O = P V with the tile's 32 tokens as K and 16 head dims per
 //     MFMA as N.  P is split into bf16 hi + lo parts (two MFMAs), keeping ~16
 //     significant bits; logits, the running max / sum and O stay fp32.
-//   Every load instruction reads 1 KiB of contiguous cache, and two tiles are
-//   in flight per wave (the next tile loads while the current one computes).
+//   Every load instruction reads 1 KiB of contiguous cache with a nontemporal
+//   (streaming) hint, and two tiles are in flight per wave (the next tile loads
+//   while the current one computes).
 //   Rows <= 16: the 4 waves of a workgroup take consecutive quarters of the
 //   split's tiles and merge their (m, l, O) states through LDS.  Rows > 16:
 //   each wave owns one 16-row block and walks all tiles of the split; the
@@ -44,8 +45,16 @@ constexpr int kThreads = kAttnWaves * 64;
 constexpr int kOPad = 132;  // LDS row pitch (floats) of the wave merge
 constexpr int kCombineGroups = kThreads / (kHeadDim / 4);  // split groups in the combine
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ bf16x8 load8(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+}
+
+// K/V stream: every byte is read exactly once per step, so the loads are
+// nontemporal (streaming) and do not displace other data in the caches.
+__device__ __forceinline__ bf16x8 load8_stream(const uint16_t* p) {
+  return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -143,9 +152,9 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
     const uint16_t* kp = kbase + off;
     const uint16_t* vp = vbase + off;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) kt[q] = load8(kp + q * 512);
+    for (int q = 0; q < 8; ++q) kt[q] = load8_stream(kp + q * 512);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) vt[q] = load8(vp + q * 512);
+    for (int q = 0; q < 8; ++q) vt[q] = load8_stream(vp + q * 512);
   };
 
   auto compute_tile = [&](const bf16x8(&kt)[8], const bf16x8(&vt)[8]) {
