@@ -6,12 +6,14 @@
 // One 1024-thread workgroup per (sequence, query).  Scores map to 32-bit keys
 // whose unsigned order is the score order (fp32: -0.0 folded onto +0.0, sign
 // bit set for positives, all bits flipped for negatives; int32: sign bit
-// flipped).  A 4-pass, 8-bit-digit radix select over keys staged in LDS finds
-// the k-th largest key T and how many keys equal to T must be taken.  The
-// final pass walks the scores in index order: keys above T are kept, and keys
-// equal to T are kept while the tie quota lasts, so ties go to the lower chunk
-// id and the output comes out ascending with no sort.  Histograms are split
-// four ways by wave to cut LDS atomic contention on concentrated digits.
+// flipped).  Each thread keeps a contiguous segment of keys in registers (all
+// of its loads in flight at once), and a radix select with 12-, 12- and 8-bit
+// digits over 4096-bin LDS histograms finds the k-th largest key T and how many
+// keys equal to T must be taken.  The compaction walks the register segments
+// in index order: keys above T are kept, keys equal to T are kept while the tie
+// quota lasts, so ties go to the lower chunk id and the output comes out
+// ascending with no sort.  Contexts longer than 64K chunks use a slower path
+// that re-reads the scores from memory in every pass.
 #include "lsa_internal.h"
 
 namespace lsa {
@@ -145,6 +147,188 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
   if (sel_count != nullptr && tid == 0) sel_count[b] = k;
 }
 
+// ---------------------------------------------------------------------------
+// LDS-resident selection for up to 16384 chunks per (sequence, query).  The
+// kernel runs once per step, so its code is kept compact (loops, not long
+// unrolled straight-line code): instruction fetch, not arithmetic, is what a
+// single-pass workgroup waits on.
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelMaxN = 16384;
+constexpr int kSelKPT = kSelMaxN / kSelThreads;  // 16 keys per thread
+constexpr int kSelCand = 4096;                   // threshold-bin keys packed for the last digits
+
+// key i lives at LDS word i + i / 16, so the 16 keys of one thread's segment
+// (read in the compaction) spread over the banks
+__device__ __forceinline__ int kpos(int i) { return i + (i >> 4); }
+
+// Inclusive prefix sum across the 64 lanes of a wave with DPP row shifts and
+// row broadcasts (no LDS round trips).
+__device__ __forceinline__ uint32_t wave_scan_incl(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
+
+// Inclusive prefix sum over the workgroup; *total receives the block sum.
+__device__ __forceinline__ uint32_t sel_scan(uint32_t v, uint32_t* wave_tot, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t incl = wave_scan_incl(v);
+  if (lane == 63) wave_tot[wave] = incl;
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+#pragma unroll 4
+  for (int w = 0; w < kSelWaves; ++w) {
+    const uint32_t x = wave_tot[w];
+    before += (w < wave) ? x : 0u;
+    tot += x;
+  }
+  *total = tot;
+  __syncthreads();  // wave_tot is reused by the next scan
+  return incl + before;
+}
+
+// Among 4096 bins (thread t owns bins 4t .. 4t+3), the bin holding the
+// krem-th largest counted key, the keys to take from it and its size, written
+// to LDS and read by every thread after the call.
+__device__ __forceinline__ void sel_find_bin(const uint32_t* hist, uint32_t krem, uint32_t* wave_tot,
+                                             uint32_t* sh) {
+  const int tid = threadIdx.x;
+  const uint4 c4 = reinterpret_cast<const uint4*>(hist)[tid];
+  const uint32_t c[4] = {c4.x, c4.y, c4.z, c4.w};
+  uint32_t total;
+  const uint32_t incl = sel_scan(c4.x + c4.y + c4.z + c4.w, wave_tot, &total);
+  uint32_t cum = total - incl;  // keys in bins above this thread's
+  for (int q = 3; q >= 0; --q) {
+    if (cum < krem && cum + c[q] >= krem) {
+      sh[0] = 4u * tid + q;
+      sh[1] = krem - cum;
+      sh[2] = c[q];
+    }
+    cum += c[q];
+  }
+  __syncthreads();
+}
+
+template <bool INT_KEYS>
+__global__ void __launch_bounds__(kSelThreads)
+topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict__ out_idx,
+                   int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count) {
+  __shared__ uint32_t keys[kSelMaxN + kSelMaxN / 16];
+  __shared__ uint32_t hist[4096];
+  __shared__ uint32_t cand[kSelCand];
+  __shared__ uint32_t wave_tot[kSelWaves];
+  __shared__ uint32_t sh[4];
+
+  const int Q = t.n_lookahead;
+  const int b = blockIdx.x / Q, j = blockIdx.x % Q;
+  const int n = t.n[b], k = t.keep[b];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * n;
+  int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
+
+  reinterpret_cast<uint4*>(hist)[tid] = make_uint4(0u, 0u, 0u, 0u);
+  if (tid == 0) sh[3] = 0u;
+  __syncthreads();
+
+  // Coalesced loads, all issued before use (indices clamped into range), then
+  // keys to LDS and the histogram of their top 12 bits.  Keys past the end are
+  // 0 (the smallest key): never above the threshold and, having the highest
+  // chunk ids, never reached by the tie quota (which counts real keys only).
+  {
+    uint32_t raw[kSelKPT];
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) raw[q] = s[min(q * kSelThreads + tid, n - 1)];
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) {
+      const int i = q * kSelThreads + tid;
+      const uint32_t kk = i < n ? order_key<INT_KEYS>(raw[q]) : 0u;
+      keys[kpos(i)] = kk;
+      if (i < n) atomicAdd(&hist[kk >> 20], 1u);
+    }
+  }
+  __syncthreads();
+
+  sel_find_bin(hist, (uint32_t)k, wave_tot, sh);
+  const uint32_t B0 = sh[0], m = sh[2];
+  uint32_t krem = sh[1];
+  uint32_t prefix = B0 << 20, pmask = 0xFFF00000u;
+
+  // Remaining 20 bits: two more radix digits (12 and 8 bits) under prefix B0.
+  // The keys of bin B0 are first packed into LDS (one atomic per wave and
+  // iteration) when they fit, so those passes touch only them.
+  const bool packed = m <= (uint32_t)kSelCand;
+  if (packed) {
+    __syncthreads();  // sh[] has been read by every thread
+#pragma unroll 1
+    for (int q = 0; q < kSelKPT; ++q) {
+      const int i = q * kSelThreads + tid;
+      const uint32_t kk = keys[kpos(i)];
+      const bool pred = i < n && (kk >> 20) == B0;
+      const uint64_t mask = __ballot(pred);
+      if (mask == 0ull) continue;
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(&sh[3], (uint32_t)__popcll(mask));
+      base = __shfl(base, 0);
+      if (pred)
+        cand[base + __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u))] = kk;
+    }
+  }
+#pragma unroll 1
+  for (int pass = 0; pass < 2; ++pass) {
+    const int shift = pass == 0 ? 8 : 0;
+    const uint32_t dmask = pass == 0 ? 0xFFFu : 0xFFu;
+    reinterpret_cast<uint4*>(hist)[tid] = make_uint4(0u, 0u, 0u, 0u);
+    __syncthreads();
+    if (packed) {
+      for (int c = tid; c < (int)m; c += kSelThreads) {
+        const uint32_t kk = cand[c];
+        if ((kk & pmask) == prefix) atomicAdd(&hist[(kk >> shift) & dmask], 1u);
+      }
+    } else {
+      for (int i = tid; i < n; i += kSelThreads) {
+        const uint32_t kk = keys[kpos(i)];
+        if ((kk & pmask) == prefix) atomicAdd(&hist[(kk >> shift) & dmask], 1u);
+      }
+    }
+    __syncthreads();
+    sel_find_bin(hist, krem, wave_tot, sh);
+    prefix |= sh[0] << shift;
+    pmask |= dmask << shift;
+    krem = sh[1];
+    __syncthreads();
+  }
+
+  // T is the k-th largest key; every key above T is kept, and the first krem
+  // keys equal to T in chunk order.  Thread t walks its segment [16t, 16t+16).
+  const uint32_t T = prefix;
+  const int i0 = tid * kSelKPT;
+  uint32_t gt = 0, eq = 0;
+#pragma unroll 4
+  for (int q = 0; q < kSelKPT; ++q) {
+    const uint32_t kk = keys[kpos(i0 + q)];
+    gt += kk > T;
+    eq += kk == T;
+  }
+  uint32_t tot2;
+  const uint32_t both = sel_scan((gt << 16) | eq, wave_tot, &tot2) - ((gt << 16) | eq);
+  uint32_t pgt = both >> 16, peq = both & 0xFFFFu;
+#pragma unroll 1
+  for (int q = 0; q < kSelKPT; ++q) {
+    const uint32_t kk = keys[kpos(i0 + q)];
+    const bool g1 = kk > T, e1 = kk == T;
+    const uint32_t pos = pgt + min(peq, krem);
+    if ((g1 || (e1 && peq < krem)) && pos < (uint32_t)k) out[pos] = i0 + q;
+    pgt += g1;
+    peq += e1;
+  }
+  if (sel_count != nullptr && tid == 0) sel_count[b] = k;
+}
+
 // Ascending union of the Q per-query lists of each sequence via an LDS bitmap.
 __global__ void __launch_bounds__(kThreads)
 union_kernel(SeqTable t, const int32_t* __restrict__ per_query, int32_t k_pitch,
@@ -189,19 +373,31 @@ __global__ void zero_kernel(uint4* p, size_t n16, uint8_t* tail, size_t ntail) {
 
 }  // namespace
 
+namespace {
+
+template <bool INT_KEYS>
+hipError_t launch_topk_keys(const SeqTable& t, const uint32_t* scores, int32_t* out_idx, int64_t pitch_seq,
+                            int64_t pitch_q, int32_t* sel_count, hipStream_t s) {
+  int n_max = 0;
+  for (int b = 0; b < t.batch; ++b) n_max = max(n_max, t.n[b]);
+  const dim3 grid(t.batch * t.n_lookahead);
+  if (n_max <= kSelMaxN)
+    hipLaunchKernelGGL((topk_select_kernel<INT_KEYS>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
+                       pitch_seq, pitch_q, sel_count);
+  else
+    hipLaunchKernelGGL((topk_kernel<INT_KEYS>), grid, dim3(kThreads), 0, s, t, scores, out_idx, pitch_seq,
+                       pitch_q, sel_count);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, const void* scores, int32_t* out_idx,
                        int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
                        hipStream_t s) {
-  const dim3 grid(t.batch * t.n_lookahead);
-  if (emb_dtype == LSA_I8)
-    hipLaunchKernelGGL(topk_kernel<true>, grid, dim3(kThreads), 0, s, t,
-                       static_cast<const uint32_t*>(scores), out_idx, out_pitch_seq, out_pitch_query,
-                       sel_count);
-  else
-    hipLaunchKernelGGL(topk_kernel<false>, grid, dim3(kThreads), 0, s, t,
-                       static_cast<const uint32_t*>(scores), out_idx, out_pitch_seq, out_pitch_query,
-                       sel_count);
-  return hipGetLastError();
+  const uint32_t* sc = static_cast<const uint32_t*>(scores);
+  if (emb_dtype == LSA_I8) return launch_topk_keys<true>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
+  return launch_topk_keys<false>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
 }
 
 hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_pitch,

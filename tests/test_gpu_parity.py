@@ -69,17 +69,18 @@ def test_device_fill_matches_host_generator():
     torch.cuda.synchronize()
 
 
-def test_topk_ties_and_signed_zero():
-    """Tied scores go to the lower chunk id; -0.0 ties +0.0 (given scores)."""
+@pytest.mark.parametrize("n", [300, 4096, 70000])
+def test_topk_ties_and_signed_zero(n):
+    """Tied scores go to the lower chunk id; -0.0 ties +0.0 (given scores).
+    70000 chunks exceeds the register-resident path and takes the streaming one."""
     import torch
     import oracle
     L = _lib()
-    n = 4096
     rng = np.random.default_rng(5)
     s = np.round(rng.standard_normal(n), 1).astype(np.float32)   # heavy ties
     s[::7] = 0.0
     s[3::7] = -0.0
-    for k in (1, 5, 100, 1000, 2047, n):
+    for k in (1, 5, 100, min(1000, n), n // 2 - 1, n):
         prob = L.Problem([64 * n], 64, [k], 4, 4)
         sc = torch.from_numpy(s).cuda()
         sel = torch.full((1, k), -1, dtype=torch.int32, device="cuda")
