@@ -6,10 +6,10 @@
  *   1. score   -- the Memory Indexer scores every compressed chunk of the context
  *                 against the query embedding (Eq. 4, taken as the dual-encoder
  *                 dot product s_c = qe . E_c of one indexer head with unit gate);
- *   2. select  -- keep the k highest-scoring chunks (the Top-k of Eq. corecomp,
+ *   2. select  -- keep the k highest-scoring chunks (the Top-k of Eq. 6,
  *                 with the recall bound K_max of Sec. 2.5 as the keep budget k);
  *                 with several lookahead query embeddings the kept set is the
- *                 union of the per-query top-k sets (set union as in Eq. union);
+ *                 union of the per-query top-k sets (set union as in Eq. 13);
  *   3. attend  -- softmax(q K^T * scale) V over the tokens of the kept chunks
  *                 only, gathered by chunk id from the full cache (the core
  *                 attention over the selected entries, Sec. 2.1).
@@ -125,7 +125,7 @@ lsa_status lsa_score_chunks(const lsa_problem* p, const void* query_emb, const v
                             void* scores, void* stream);
 
 /*
- * Step 2 -- keep the top-k chunks (Sec. 2.1, Eq. corecomp; union of Eq. union):
+ * Step 2 -- keep the top-k chunks (Sec. 2.1, Eq. 6; union of Eq. 13):
  * for each (b, j) the k_b chunk ids with the largest score, ties broken towards
  * the lower chunk id, -0.0 equal to +0.0.  Q == 1: sel_idx[b][0..k_b) ascending
  * and sel_count[b] = k_b.  Q > 1: sel_idx[b] holds the ascending union of the Q

@@ -8,8 +8,8 @@ step:
 * O1 score -- Memory Indexer score, Sec. 2.1 Eq. 4, read as the dual-encoder dot
   product (one head, unit gate);
 * O2 select -- top-k with lowest-index tie-break, ascending output; union of the
-  per-query sets for several lookahead queries (Sec. 2.1 Eq. corecomp and
-  Sec. 2.4 Eq. union; K_max of Sec. 2.5 is the keep budget);
+  per-query sets for several lookahead queries (Sec. 2.1 Eq. 6 and
+  Sec. 2.4 Eq. 13; K_max of Sec. 2.5 is the keep budget);
 * O3 attend -- softmax(q K^T * scale) V over the tokens of the kept chunks.
 
 It shares no code with the HIP library; the only common input is the seeded

@@ -17,10 +17,10 @@
  *    sigmoid and ReLU of Eq. 4 are non-decreasing, so they cannot reorder
  *    chunks with positive dot products; the keep-budget selection is taken on
  *    the raw dot product.
- *  - Selection (Sec. 2.1, Eq. corecomp; Sec. 2.5 bound K_max): the k chunks with
+ *  - Selection (Sec. 2.1, Eq. 6; Sec. 2.5 bound K_max): the k chunks with
  *    the largest score, ties broken towards the lower chunk index, reported in
  *    ascending chunk order.  With several lookahead queries the kept set is the
- *    union of the per-query top-k sets (the set union of Eq. union).
+ *    union of the per-query top-k sets (the set union of Eq. 13).
  *  - Attention (Sec. 2.1, core attention over the selected entries):
  *    softmax(q K^T * scale) V over the tokens of the kept chunks, with query
  *    head h reading KV head floor(h / G).

@@ -1,19 +1,24 @@
 // Step 2 of the decode hot path: keep the k highest-scoring chunks (the Top-k
-// of Sec. 2.1, Eq. corecomp, with the K_max recall bound of Sec. 2.5 as k) and,
+// of Sec. 2.1, Eq. 6, with the K_max recall bound of Sec. 2.5 as k) and,
 // with several lookahead queries, the union of the per-query sets (the set
-// union of Sec. 2.4, Eq. union).
+// union of Sec. 2.4, Eq. 13).
 //
 // One 1024-thread workgroup per (sequence, query).  Scores map to 32-bit keys
 // whose unsigned order is the score order (fp32: -0.0 folded onto +0.0, sign
 // bit set for positives, all bits flipped for negatives; int32: sign bit
-// flipped).  Each thread keeps a contiguous segment of keys in registers (all
-// of its loads in flight at once), and a radix select with 12-, 12- and 8-bit
-// digits over 4096-bin LDS histograms finds the k-th largest key T and how many
-// keys equal to T must be taken.  The compaction walks the register segments
-// in index order: keys above T are kept, keys equal to T are kept while the tie
-// quota lasts, so ties go to the lower chunk id and the output comes out
-// ascending with no sort.  Contexts longer than 64K chunks use a slower path
-// that re-reads the scores from memory in every pass.
+// flipped).  A radix select finds the k-th largest key T and how many keys
+// equal to T must be taken; the compaction then walks the keys in index order,
+// keeping keys above T and keys equal to T while the tie quota lasts, so ties
+// go to the lower chunk id and the output comes out ascending with no sort.
+//
+// topk_select_kernel (up to 16384 chunks): every key is loaded once into LDS
+//   (16 per thread, all loads in flight together).  The first digit is the top
+//   12 bits (4096-bin histogram); the keys of the threshold bin are then packed
+//   into a candidate list, and the last 20 bits are resolved with 12- and 8-bit
+//   digits over that list only (over all keys if the bin holds more than 4096).
+//   The compaction scans each thread's contiguous 16-key segment.
+// topk_kernel (longer contexts): 8-bit digits, with the keys staged in LDS when
+//   they fit and re-read from memory in every pass otherwise.
 #include "lsa_internal.h"
 
 namespace lsa {
