@@ -192,15 +192,16 @@ lsa_status check_ws(const Plan& P, void* ws, size_t ws_bytes) {
 
 uint8_t* at(void* ws, size_t off) { return static_cast<uint8_t*>(ws) + off; }
 
-lsa_status run_topk(const lsa_problem* p, const Plan& P, const void* scores, int32_t* sel_idx,
+lsa_status run_topk(const lsa_problem* p, const Plan& P, bool keys_ready, const void* scores, int32_t* sel_idx,
                     int32_t* sel_count, int32_t* per_query_idx, void* ws, hipStream_t s) {
   if (p->n_lookahead == 1) {
-    LSA_HIP(launch_topk(P.t, p->emb_dtype, scores, sel_idx, P.max_sel, 0, sel_count, s), "topk launch");
+    LSA_HIP(launch_topk(P.t, p->emb_dtype, keys_ready, scores, sel_idx, P.max_sel, 0, sel_count, s),
+            "topk launch");
     return LSA_OK;
   }
   int32_t* pq = per_query_idx ? per_query_idx : reinterpret_cast<int32_t*>(at(ws, P.off_pq));
-  LSA_HIP(launch_topk(P.t, p->emb_dtype, scores, pq, (int64_t)p->n_lookahead * P.max_keep, P.max_keep,
-                      nullptr, s),
+  LSA_HIP(launch_topk(P.t, p->emb_dtype, keys_ready, scores, pq, (int64_t)p->n_lookahead * P.max_keep,
+                      P.max_keep, nullptr, s),
           "topk launch");
   LSA_HIP(launch_union(P.t, pq, P.max_keep, sel_idx, P.max_sel, sel_count, s), "union launch");
   return LSA_OK;
@@ -300,7 +301,7 @@ lsa_status lsa_score_chunks(const lsa_problem* p, const void* query_emb, const v
   LSA_TRY(check_ptr(query_emb, "query_emb"));
   LSA_TRY(check_ptr(chunk_emb, "chunk_emb"));
   LSA_TRY(check_ptr(scores, "scores"));
-  LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, (hipStream_t)stream),
+  LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, false, (hipStream_t)stream),
           "score launch");
   return LSA_OK;
 }
@@ -314,7 +315,7 @@ lsa_status lsa_topk_chunks(const lsa_problem* p, const void* scores, int32_t* se
   LSA_TRY(check_ptr(sel_count, "sel_count"));
   if (per_query_idx != nullptr) LSA_TRY(check_ptr(per_query_idx, "per_query_idx"));
   if (p->n_lookahead > 1 && per_query_idx == nullptr) LSA_TRY(check_ws(P, ws, ws_bytes));
-  return run_topk(p, P, scores, sel_idx, sel_count, per_query_idx, ws, (hipStream_t)stream);
+  return run_topk(p, P, false, scores, sel_idx, sel_count, per_query_idx, ws, (hipStream_t)stream);
 }
 
 lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const uint16_t* k_cache,
@@ -363,8 +364,10 @@ lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const vo
   void* scores = at(ws, P.off_scores);
   int32_t* sel = sel_idx ? sel_idx : reinterpret_cast<int32_t*>(at(ws, P.off_sel));
   int32_t* cnt = sel_count ? sel_count : reinterpret_cast<int32_t*>(at(ws, P.off_cnt));
-  LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, s), "score launch");
-  LSA_TRY(run_topk(p, P, scores, sel, cnt, nullptr, ws, s));
+  // the scores stay in the workspace, so the scoring kernel writes them as
+  // order keys and the selection reads them without converting
+  LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, true, s), "score launch");
+  LSA_TRY(run_topk(p, P, true, scores, sel, cnt, nullptr, ws, s));
   return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
 }
 

@@ -56,12 +56,33 @@ constexpr int kHeadDim = 128;
 constexpr int kTargetWorkgroups = 512;
 constexpr int kMaxSplits = 256;  // splits per (sequence, kv head, row group)
 
+// How the selection reads its scores: raw float32 scores, raw int32 scores, or
+// scores the scoring kernel has already mapped to keys (the fused step).
+enum KeyMode : int { kKeysFromF32 = 0, kKeysFromI32 = 1, kKeysReady = 2 };
+
+// 32-bit key whose unsigned order is the score order.  float32: -0.0 is folded
+// onto +0.0, then positives get the sign bit set and negatives have every bit
+// flipped; int32: the sign bit is flipped.
+template <int MODE>
+__device__ __forceinline__ uint32_t order_key(uint32_t bits) {
+  if constexpr (MODE == kKeysReady) {
+    return bits;
+  } else if constexpr (MODE == kKeysFromI32) {
+    return bits ^ 0x80000000u;
+  } else {
+    if (bits == 0x80000000u) bits = 0u;
+    return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+  }
+}
+
+// keys == true writes order keys instead of scores (for the fused step).
 hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
-                        const void* E, void* scores, hipStream_t s);
+                        const void* E, void* scores, bool keys, hipStream_t s);
 int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim);
 
-hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, const void* scores, int32_t* out_idx,
-                       int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
+// keys_ready == true: `scores` holds keys written by launch_score(keys = true).
+hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, bool keys_ready, const void* scores,
+                       int32_t* out_idx, int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
                        hipStream_t s);
 hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_pitch,
                         int32_t* sel_idx, int32_t sel_pitch, int32_t* sel_count, hipStream_t s);

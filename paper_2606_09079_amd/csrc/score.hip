@@ -66,7 +66,7 @@ __device__ __forceinline__ int piece_dot_i8(uint4 e, uint4 q, int acc) {
   return acc;
 }
 
-template <int DT, int D>
+template <int DT, int D, bool KEYS>
 __global__ void __launch_bounds__(kThreads)
 score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restrict__ E,
              uint32_t* __restrict__ scores) {
@@ -122,28 +122,33 @@ score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restri
         for (int off = G::lanes / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
         bits = __float_as_uint(acc);
       }
+      if constexpr (KEYS) bits = order_key<DT == LSA_I8 ? kKeysFromI32 : kKeysFromF32>(bits);
       if (sub == 0 && r < n) out_b[(int64_t)j * n + r] = bits;
     }
   }
 }
 
 template <int DT, int D>
-hipError_t launch_dt_d(const SeqTable& t, const void* qe, const void* E, void* scores, hipStream_t s) {
+hipError_t launch_dt_d(const SeqTable& t, const void* qe, const void* E, void* scores, bool keys, hipStream_t s) {
   const int grid = t.score_wg_off[t.batch];
-  hipLaunchKernelGGL((score_kernel<DT, D>), dim3(grid), dim3(kThreads), 0, s, t,
-                     static_cast<const uint8_t*>(qe), static_cast<const uint8_t*>(E),
-                     static_cast<uint32_t*>(scores));
+  const auto* q8 = static_cast<const uint8_t*>(qe);
+  const auto* e8 = static_cast<const uint8_t*>(E);
+  auto* out = static_cast<uint32_t*>(scores);
+  if (keys)
+    hipLaunchKernelGGL((score_kernel<DT, D, true>), dim3(grid), dim3(kThreads), 0, s, t, q8, e8, out);
+  else
+    hipLaunchKernelGGL((score_kernel<DT, D, false>), dim3(grid), dim3(kThreads), 0, s, t, q8, e8, out);
   return hipGetLastError();
 }
 
 template <int DT>
-hipError_t launch_dt(const SeqTable& t, int32_t D, const void* qe, const void* E, void* scores,
+hipError_t launch_dt(const SeqTable& t, int32_t D, const void* qe, const void* E, void* scores, bool keys,
                      hipStream_t s) {
   switch (D) {
-    case 64: return launch_dt_d<DT, 64>(t, qe, E, scores, s);
-    case 128: return launch_dt_d<DT, 128>(t, qe, E, scores, s);
-    case 256: return launch_dt_d<DT, 256>(t, qe, E, scores, s);
-    case 512: return launch_dt_d<DT, 512>(t, qe, E, scores, s);
+    case 64: return launch_dt_d<DT, 64>(t, qe, E, scores, keys, s);
+    case 128: return launch_dt_d<DT, 128>(t, qe, E, scores, keys, s);
+    case 256: return launch_dt_d<DT, 256>(t, qe, E, scores, keys, s);
+    case 512: return launch_dt_d<DT, 512>(t, qe, E, scores, keys, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -171,11 +176,11 @@ int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim) {
 }
 
 hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
-                        const void* E, void* scores, hipStream_t s) {
+                        const void* E, void* scores, bool keys, hipStream_t s) {
   switch (emb_dtype) {
-    case LSA_F32: return launch_dt<LSA_F32>(t, emb_dim, qe, E, scores, s);
-    case LSA_BF16: return launch_dt<LSA_BF16>(t, emb_dim, qe, E, scores, s);
-    case LSA_I8: return launch_dt<LSA_I8>(t, emb_dim, qe, E, scores, s);
+    case LSA_F32: return launch_dt<LSA_F32>(t, emb_dim, qe, E, scores, keys, s);
+    case LSA_BF16: return launch_dt<LSA_BF16>(t, emb_dim, qe, E, scores, keys, s);
+    case LSA_I8: return launch_dt<LSA_I8>(t, emb_dim, qe, E, scores, keys, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -4,19 +4,23 @@
 // union of Sec. 2.4, Eq. 13).
 //
 // One 1024-thread workgroup per (sequence, query).  Scores map to 32-bit keys
-// whose unsigned order is the score order (fp32: -0.0 folded onto +0.0, sign
-// bit set for positives, all bits flipped for negatives; int32: sign bit
-// flipped).  A radix select finds the k-th largest key T and how many keys
-// equal to T must be taken; the compaction then walks the keys in index order,
-// keeping keys above T and keys equal to T while the tie quota lasts, so ties
-// go to the lower chunk id and the output comes out ascending with no sort.
+// whose unsigned order is the score order (order_key; the fused step receives
+// them already mapped from the scoring kernel).  A radix select finds the k-th
+// largest key T and how many keys equal to T must be taken; every key above T
+// is kept, and keys equal to T in chunk order while the tie quota lasts, so
+// ties go to the lower chunk id and the output is ascending with no sort.
 //
-// topk_select_kernel (up to 16384 chunks): every key is loaded once into LDS
-//   (16 per thread, all loads in flight together).  The first digit is the top
-//   12 bits (4096-bin histogram); the keys of the threshold bin are then packed
-//   into a candidate list, and the last 20 bits are resolved with 12- and 8-bit
-//   digits over that list only (over all keys if the bin holds more than 4096).
-//   The compaction scans each thread's contiguous 16-key segment.
+// topk_select_kernel (up to 16384 chunks) runs on one compute unit, where every
+// instruction executed by all 1024 threads costs 16 cycles, so the design
+// minimises per-key work:
+//   - keys stay in registers (16 per thread, coalesced buffer loads);
+//   - first digit: top 12 bits into an LDS histogram whose atomic return
+//     values double as each key's rank in its bin, so the keys of the
+//     threshold bin are packed into a candidate list without a scan;
+//   - the last 20 bits: two 10-bit digits resolved by one wavefront over the
+//     candidates, with no barriers;
+//   - the kept set is built as bitmaps straight from wavefront ballots, and
+//     512 threads emit the set bits of their 32-chunk words in order.
 // topk_kernel (longer contexts): 8-bit digits, with the keys staged in LDS when
 //   they fit and re-read from memory in every pass otherwise.
 #include "lsa_internal.h"
@@ -28,16 +32,6 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kLdsKeys = 16384;
 constexpr int kSubHist = 4;
-
-template <bool INT_KEYS>
-__device__ __forceinline__ uint32_t order_key(uint32_t bits) {
-  if constexpr (INT_KEYS) {
-    return bits ^ 0x80000000u;
-  } else {
-    if (bits == 0x80000000u) bits = 0u;  // -0.0 ties +0.0
-    return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
-  }
-}
 
 // Exclusive block-wide prefix sum of a 64-bit value (two 32-bit counters).
 __device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t* wave_tot) {
@@ -63,7 +57,7 @@ __device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t* w
   return incl - v + wave_tot[wave];
 }
 
-template <bool INT_KEYS>
+template <int MODE>
 __global__ void __launch_bounds__(kThreads)
 topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict__ out_idx,
             int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count) {
@@ -81,7 +75,7 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
   const bool staged = n <= kLdsKeys;
 
   if (staged)
-    for (int i = tid; i < n; i += kThreads) keys[i] = order_key<INT_KEYS>(s[i]);
+    for (int i = tid; i < n; i += kThreads) keys[i] = order_key<MODE>(s[i]);
 
   uint32_t prefix = 0, pmask = 0, krem = (uint32_t)k;
   uint32_t* hflat = &hist[0][0];
@@ -90,7 +84,7 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
     for (int i = tid; i < kSubHist * 256; i += kThreads) hflat[i] = 0u;
     __syncthreads();
     for (int i = tid; i < n; i += kThreads) {
-      const uint32_t key = staged ? keys[i] : order_key<INT_KEYS>(s[i]);
+      const uint32_t key = staged ? keys[i] : order_key<MODE>(s[i]);
       if ((key & pmask) == prefix) atomicAdd(&hist[sub][(key >> shift) & 255u], 1u);
     }
     __syncthreads();
@@ -132,14 +126,14 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
   const int i0 = min(tid * seg, n), i1 = min(i0 + seg, n);
   uint32_t gt = 0, eq = 0;
   for (int i = i0; i < i1; ++i) {
-    const uint32_t key = order_key<INT_KEYS>(s[i]);
+    const uint32_t key = order_key<MODE>(s[i]);
     gt += key > T;
     eq += key == T;
   }
   const uint64_t base = block_exclusive_scan(((uint64_t)gt << 32) | eq, wave_tot);
   uint32_t pgt = (uint32_t)(base >> 32), peq = (uint32_t)base;
   for (int i = i0; i < i1; ++i) {
-    const uint32_t key = order_key<INT_KEYS>(s[i]);
+    const uint32_t key = order_key<MODE>(s[i]);
     if (key > T) {
       const uint32_t pos = pgt + min(peq, krem);
       if (pos < (uint32_t)k) out[pos] = i;
@@ -154,18 +148,15 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
 
 // ---------------------------------------------------------------------------
 // LDS-resident selection for up to 16384 chunks per (sequence, query).  The
-// kernel runs once per step, so its code is kept compact (loops, not long
-// unrolled straight-line code): instruction fetch, not arithmetic, is what a
-// single-pass workgroup waits on.
+// kernel runs once per step on a single compute unit, so what it waits on is
+// latency: every phase is a short chain of independent memory operations, and
+// the tail of the radix select runs in one wavefront with no barriers.
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelMaxN = 16384;
 constexpr int kSelKPT = kSelMaxN / kSelThreads;  // 16 keys per thread
 constexpr int kSelCand = 4096;                   // threshold-bin keys packed for the last digits
-
-// key i lives at LDS word i + i / 16, so the 16 keys of one thread's segment
-// (read in the compaction) spread over the banks
-__device__ __forceinline__ int kpos(int i) { return i + (i >> 4); }
+constexpr int kSelSub = 4;                       // sub-histograms of the first digit (lane / 16)
 
 // Inclusive prefix sum across the 64 lanes of a wave with DPP row shifts and
 // row broadcasts (no LDS round trips).
@@ -179,157 +170,217 @@ __device__ __forceinline__ uint32_t wave_scan_incl(uint32_t x) {
   return x;
 }
 
-// Inclusive prefix sum over the workgroup; *total receives the block sum.
-__device__ __forceinline__ uint32_t sel_scan(uint32_t v, uint32_t* wave_tot, uint32_t* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t incl = wave_scan_incl(v);
-  if (lane == 63) wave_tot[wave] = incl;
-  __syncthreads();
-  uint32_t before = 0, tot = 0;
-#pragma unroll 4
-  for (int w = 0; w < kSelWaves; ++w) {
-    const uint32_t x = wave_tot[w];
-    before += (w < wave) ? x : 0u;
-    tot += x;
-  }
-  *total = tot;
-  __syncthreads();  // wave_tot is reused by the next scan
-  return incl + before;
+__device__ __forceinline__ uint32_t lane_bcast(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
-// Among 4096 bins (thread t owns bins 4t .. 4t+3), the bin holding the
-// krem-th largest counted key, the keys to take from it and its size, written
-// to LDS and read by every thread after the call.
-__device__ __forceinline__ void sel_find_bin(const uint32_t* hist, uint32_t krem, uint32_t* wave_tot,
-                                             uint32_t* sh) {
-  const int tid = threadIdx.x;
-  const uint4 c4 = reinterpret_cast<const uint4*>(hist)[tid];
-  const uint32_t c[4] = {c4.x, c4.y, c4.z, c4.w};
-  uint32_t total;
-  const uint32_t incl = sel_scan(c4.x + c4.y + c4.z + c4.w, wave_tot, &total);
-  uint32_t cum = total - incl;  // keys in bins above this thread's
-  for (int q = 3; q >= 0; --q) {
-    if (cum < krem && cum + c[q] >= krem) {
-      sh[0] = 4u * tid + q;
-      sh[1] = krem - cum;
-      sh[2] = c[q];
-    }
-    cum += c[q];
+// One wavefront: among the keys src[0 .. m) that match (prefix, pmask), find
+// the bin of the next 10-bit digit (below bit `shift`) holding the kr-th
+// largest; h is a private LDS area of 1024 words and src is readable up to the
+// next multiple of 512 past m.  Returns the digit and updates kr to the number
+// of keys still to take from that bin.
+__device__ __forceinline__ uint32_t wave_digit(const uint32_t* src, int m, uint32_t prefix, uint32_t pmask,
+                                               int shift, uint32_t& kr, uint32_t* h) {
+  const int lane = threadIdx.x & 63;
+  uint4* h4 = reinterpret_cast<uint4*>(h) + lane * 4;  // lane l owns bins 16l .. 16l+15
+#pragma unroll
+  for (int q = 0; q < 4; ++q) h4[q] = make_uint4(0u, 0u, 0u, 0u);
+  __builtin_amdgcn_wave_barrier();
+  // candidates in batches of 8 per lane: all reads of a batch are issued
+  // before its atomics
+  for (int c0 = 0; c0 < m; c0 += 8 * 64) {
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = src[c0 + u * 64 + lane];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (c0 + u * 64 + lane < m && (v[u] & pmask) == prefix) atomicAdd(&h[(v[u] >> shift) & 1023u], 1u);
   }
-  __syncthreads();
+  __builtin_amdgcn_wave_barrier();
+  uint32_t sum = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint4 x = h4[q];
+    sum += x.x + x.y + x.z + x.w;
+  }
+  const uint32_t incl = wave_scan_incl(sum);
+  const uint32_t above = lane_bcast(incl, 63) - incl;  // keys in the bins of higher lanes
+  const int L = __builtin_ctzll(__ballot(above < kr && above + sum >= kr));
+  const uint32_t krl = kr - lane_bcast(above, L);
+  // lane i < 16 takes bin 16L + 15 - i (descending), then a row scan
+  const uint32_t c = lane < 16 ? h[16 * L + 15 - lane] : 0u;
+  uint32_t ci = c;
+  ci += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)ci, 0x111, 0xF, 0xF, false);  // row_shr:1
+  ci += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)ci, 0x112, 0xF, 0xF, false);  // row_shr:2
+  ci += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)ci, 0x114, 0xF, 0xF, false);  // row_shr:4
+  ci += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)ci, 0x118, 0xF, 0xF, false);  // row_shr:8
+  const int i = __builtin_ctzll(__ballot(lane < 16 && ci >= krl && ci - c < krl));
+  kr = krl - (lane_bcast(ci, i) - lane_bcast(c, i));
+  return (uint32_t)(16 * L + 15 - i);
 }
 
-template <bool INT_KEYS>
+// Raw 32-bit buffer view of `bytes` bytes at p (gfx9 buffer descriptor: no
+// stride, 32-bit data format); loads past the end return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+template <int MODE>
 __global__ void __launch_bounds__(kSelThreads)
 topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict__ out_idx,
                    int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count) {
-  __shared__ uint32_t keys[kSelMaxN + kSelMaxN / 16];
-  __shared__ uint32_t hist[4096];
-  __shared__ uint32_t cand[kSelCand];
-  __shared__ uint32_t wave_tot[kSelWaves];
+  // First-digit histogram, 4 counters per bin (one per lane quarter, adjacent
+  // words so that equal bins of different quarters fall in different banks).
+  __shared__ __align__(16) uint32_t hist[4096 * kSelSub];
+  __shared__ uint32_t cand[kSelCand + 512];  // + the read-ahead of the last batch
+  __shared__ uint32_t keys[kSelMaxN];  // used only when the threshold bin is too large to pack
+  __shared__ __align__(16) uint32_t tot[kSelWaves];
+  __shared__ __align__(16) uint32_t bm_gt[kSelMaxN / 32];  // chunks above T, bit i % 32 of word i / 32
+  __shared__ __align__(16) uint32_t bm_eq[kSelMaxN / 32];  // chunks equal to T
   __shared__ uint32_t sh[4];
 
   const int Q = t.n_lookahead;
   const int b = blockIdx.x / Q, j = blockIdx.x % Q;
   const int n = t.n[b], k = t.keep[b];
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane >> 4;
   const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * n;
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
 
-  reinterpret_cast<uint4*>(hist)[tid] = make_uint4(0u, 0u, 0u, 0u);
-  if (tid == 0) sh[3] = 0u;
+  // Key i = q * 1024 + tid sits in slot q of thread tid: coalesced buffer loads,
+  // all in flight while the histogram is cleared.  Slots past the end hold key
+  // 0, the smallest key.  They are counted in bin 0 like real keys, which
+  // changes neither the threshold nor the tie quota (k <= n real keys all lie
+  // at or above them), and the emission drops their chunk ids.
+  const __amdgpu_buffer_rsrc_t src = raw_buffer(s, (uint32_t)n * 4u);
+  uint32_t kk[kSelKPT];
+#pragma unroll
+  for (int q = 0; q < kSelKPT; ++q)
+    kk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
+#pragma unroll
+  for (int q = 0; q < kSelSub; ++q)
+    reinterpret_cast<uint4*>(hist)[q * kSelThreads + tid] = make_uint4(0u, 0u, 0u, 0u);
+  if (tid < kSelMaxN / 128) reinterpret_cast<uint4*>(bm_eq)[tid] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
 
-  // Coalesced loads, all issued before use (indices clamped into range), then
-  // keys to LDS and the histogram of their top 12 bits.  Keys past the end are
-  // 0 (the smallest key): never above the threshold and, having the highest
-  // chunk ids, never reached by the tie quota (which counts real keys only).
-  {
-    uint32_t raw[kSelKPT];
+  // First digit (top 12 bits).  The atomic returns the key's rank among the
+  // keys of its bin and quarter, which later places it in the candidate list.
+  uint32_t bin[kSelKPT], rk[kSelKPT];
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q) raw[q] = s[min(q * kSelThreads + tid, n - 1)];
-#pragma unroll
-    for (int q = 0; q < kSelKPT; ++q) {
-      const int i = q * kSelThreads + tid;
-      const uint32_t kk = i < n ? order_key<INT_KEYS>(raw[q]) : 0u;
-      keys[kpos(i)] = kk;
-      if (i < n) atomicAdd(&hist[kk >> 20], 1u);
-    }
+  for (int q = 0; q < kSelKPT; ++q) {
+    if constexpr (MODE != kKeysReady) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
+    bin[q] = kk[q] >> 20;
+    rk[q] = atomicAdd(&hist[bin[q] * kSelSub + sub], 1u);
   }
   __syncthreads();
 
-  sel_find_bin(hist, (uint32_t)k, wave_tot, sh);
+  // Bin B0 holding the k-th largest key: thread t owns bins 4t .. 4t+3.
+  {
+    const uint4* h4 = reinterpret_cast<const uint4*>(hist) + 4 * tid;
+    uint32_t c[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint4 x = h4[q];
+      c[q] = x.x + x.y + x.z + x.w;
+    }
+    const uint32_t mine = c[0] + c[1] + c[2] + c[3];
+    const uint32_t incl = wave_scan_incl(mine);
+    if (lane == 63) tot[wave] = incl;
+    __syncthreads();
+    // keys in the bins of higher waves: lane w < 16 holds wave w's total
+    const uint32_t wt = lane < kSelWaves ? tot[lane] : 0u;
+    const uint32_t after = lane_bcast(wave_scan_incl(lane > wave ? wt : 0u), 63);
+    uint32_t cum = after + lane_bcast(incl, 63) - incl;  // keys in the bins above this thread's
+    const uint32_t kr = (uint32_t)k;
+#pragma unroll
+    for (int q = 3; q >= 0; --q) {
+      if (cum < kr && cum + c[q] >= kr) {
+        sh[0] = 4u * tid + q;
+        sh[1] = kr - cum;
+        sh[2] = c[q];
+      }
+      cum += c[q];
+    }
+  }
+  __syncthreads();
   const uint32_t B0 = sh[0], m = sh[2];
   uint32_t krem = sh[1];
-  uint32_t prefix = B0 << 20, pmask = 0xFFF00000u;
 
-  // Remaining 20 bits: two more radix digits (12 and 8 bits) under prefix B0.
-  // The keys of bin B0 are first packed into LDS (one atomic per wave and
-  // iteration) when they fit, so those passes touch only them.
+  // Keys of bin B0 to the candidate list at (keys of lower quarters) + rank.
   const bool packed = m <= (uint32_t)kSelCand;
   if (packed) {
-    __syncthreads();  // sh[] has been read by every thread
-#pragma unroll 1
-    for (int q = 0; q < kSelKPT; ++q) {
-      const int i = q * kSelThreads + tid;
-      const uint32_t kk = keys[kpos(i)];
-      const bool pred = i < n && (kk >> 20) == B0;
-      const uint64_t mask = __ballot(pred);
-      if (mask == 0ull) continue;
-      uint32_t base = 0;
-      if (lane == 0) base = atomicAdd(&sh[3], (uint32_t)__popcll(mask));
-      base = __shfl(base, 0);
-      if (pred)
-        cand[base + __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u))] = kk;
+    const uint4 bc = reinterpret_cast<const uint4*>(hist)[B0];
+    const uint32_t off = (sub > 0 ? bc.x : 0u) + (sub > 1 ? bc.y : 0u) + (sub > 2 ? bc.z : 0u);
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q)
+      if (bin[q] == B0) cand[off + rk[q]] = kk[q];
+  } else {
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) keys[q * kSelThreads + tid] = kk[q];
+  }
+  __syncthreads();
+
+  // Last 20 bits: two 10-bit digits resolved by wave 0 alone, over the packed
+  // candidates (or over all keys when the bin was too large to pack).
+  if (wave == 0) {
+    uint32_t prefix = B0 << 20, kr = krem;
+    const uint32_t* cs = packed ? cand : keys;
+    const int lim = packed ? (int)m : kSelMaxN;
+    prefix |= wave_digit(cs, lim, prefix, 0xFFF00000u, 10, kr, hist) << 10;
+    prefix |= wave_digit(cs, lim, prefix, 0xFFFFFC00u, 0, kr, hist);
+    if (lane == 0) {
+      sh[0] = prefix;
+      sh[1] = kr;
     }
   }
-#pragma unroll 1
-  for (int pass = 0; pass < 2; ++pass) {
-    const int shift = pass == 0 ? 8 : 0;
-    const uint32_t dmask = pass == 0 ? 0xFFFu : 0xFFu;
-    reinterpret_cast<uint4*>(hist)[tid] = make_uint4(0u, 0u, 0u, 0u);
-    __syncthreads();
-    if (packed) {
-      for (int c = tid; c < (int)m; c += kSelThreads) {
-        const uint32_t kk = cand[c];
-        if ((kk & pmask) == prefix) atomicAdd(&hist[(kk >> shift) & dmask], 1u);
-      }
-    } else {
-      for (int i = tid; i < n; i += kSelThreads) {
-        const uint32_t kk = keys[kpos(i)];
-        if ((kk & pmask) == prefix) atomicAdd(&hist[(kk >> shift) & dmask], 1u);
-      }
-    }
-    __syncthreads();
-    sel_find_bin(hist, krem, wave_tot, sh);
-    prefix |= sh[0] << shift;
-    pmask |= dmask << shift;
-    krem = sh[1];
-    __syncthreads();
-  }
+  __syncthreads();
 
   // T is the k-th largest key; every key above T is kept, and the first krem
-  // keys equal to T in chunk order.  Thread t walks its segment [16t, 16t+16).
-  const uint32_t T = prefix;
-  const int i0 = tid * kSelKPT;
-  uint32_t gt = 0, eq = 0;
-#pragma unroll 4
+  // keys equal to T in chunk order.  The ballot of one wave and slot covers the
+  // 64 consecutive chunks q * 1024 + 64 * wave + lane, so the ballots are the
+  // kept bitmaps, stored by lane 0 (the equal-to-T bitmap, cleared at the
+  // start, only where it is not empty).
+  const uint32_t T = sh[0];
+  krem = sh[1];
+  uint64_t* gdst = reinterpret_cast<uint64_t*>(bm_gt) + wave;
+  uint64_t* edst = reinterpret_cast<uint64_t*>(bm_eq) + wave;
+#pragma unroll
   for (int q = 0; q < kSelKPT; ++q) {
-    const uint32_t kk = keys[kpos(i0 + q)];
-    gt += kk > T;
-    eq += kk == T;
+    const uint64_t g = __ballot(kk[q] > T);
+    const uint64_t e = __ballot(kk[q] == T);
+    if (lane == 0) {
+      gdst[q * kSelWaves] = g;
+      if (e != 0ull) edst[q * kSelWaves] = e;
+    }
   }
-  uint32_t tot2;
-  const uint32_t both = sel_scan((gt << 16) | eq, wave_tot, &tot2) - ((gt << 16) | eq);
-  uint32_t pgt = both >> 16, peq = both & 0xFFFFu;
-#pragma unroll 1
-  for (int q = 0; q < kSelKPT; ++q) {
-    const uint32_t kk = keys[kpos(i0 + q)];
-    const bool g1 = kk > T, e1 = kk == T;
-    const uint32_t pos = pgt + min(peq, krem);
-    if ((g1 || (e1 && peq < krem)) && pos < (uint32_t)k) out[pos] = i0 + q;
-    pgt += g1;
-    peq += e1;
+  __syncthreads();
+
+  // Emission in chunk order: thread v < 512 owns chunks 32v .. 32v+31.
+  const bool emits = tid < kSelMaxN / 32;
+  uint32_t g = 0, e = 0;
+  if (emits) {
+    const int valid = n - 32 * tid;  // chunk ids past n are padding
+    const uint32_t live = valid >= 32 ? 0xFFFFFFFFu : valid > 0 ? (1u << valid) - 1u : 0u;
+    g = bm_gt[tid] & live;
+    e = bm_eq[tid] & live;
+  }
+  const uint32_t cnt = ((uint32_t)__popc(g) << 16) | (uint32_t)__popc(e);  // both <= 16384
+  const uint32_t incl = wave_scan_incl(cnt);
+  if (lane == 63) tot[wave] = incl;
+  __syncthreads();
+  if (emits) {
+    const uint32_t wt = lane < kSelWaves ? tot[lane] : 0u;
+    const uint32_t excl = lane_bcast(wave_scan_incl(lane < wave ? wt : 0u), 63) + incl - cnt;
+    const uint32_t gb = excl >> 16, eb = excl & 0xFFFFu;
+    uint32_t kept = g;
+    for (uint32_t r = eb < krem ? krem - eb : 0u; e != 0u && r != 0u; --r) {
+      kept |= e & (0u - e);  // lowest remaining chunk equal to T
+      e &= e - 1u;
+    }
+    uint32_t pos = gb + min(eb, krem);
+    while (kept != 0u) {
+      out[pos++] = 32 * tid + __builtin_ctz(kept);
+      kept &= kept - 1u;
+    }
   }
   if (sel_count != nullptr && tid == 0) sel_count[b] = k;
 }
@@ -380,29 +431,32 @@ __global__ void zero_kernel(uint4* p, size_t n16, uint8_t* tail, size_t ntail) {
 
 namespace {
 
-template <bool INT_KEYS>
+template <int MODE>
 hipError_t launch_topk_keys(const SeqTable& t, const uint32_t* scores, int32_t* out_idx, int64_t pitch_seq,
                             int64_t pitch_q, int32_t* sel_count, hipStream_t s) {
   int n_max = 0;
   for (int b = 0; b < t.batch; ++b) n_max = max(n_max, t.n[b]);
   const dim3 grid(t.batch * t.n_lookahead);
   if (n_max <= kSelMaxN)
-    hipLaunchKernelGGL((topk_select_kernel<INT_KEYS>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
+    hipLaunchKernelGGL((topk_select_kernel<MODE>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
                        pitch_seq, pitch_q, sel_count);
   else
-    hipLaunchKernelGGL((topk_kernel<INT_KEYS>), grid, dim3(kThreads), 0, s, t, scores, out_idx, pitch_seq,
+    hipLaunchKernelGGL((topk_kernel<MODE>), grid, dim3(kThreads), 0, s, t, scores, out_idx, pitch_seq,
                        pitch_q, sel_count);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, const void* scores, int32_t* out_idx,
-                       int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
+hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, bool keys_ready, const void* scores,
+                       int32_t* out_idx, int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
                        hipStream_t s) {
   const uint32_t* sc = static_cast<const uint32_t*>(scores);
-  if (emb_dtype == LSA_I8) return launch_topk_keys<true>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
-  return launch_topk_keys<false>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
+  if (keys_ready)
+    return launch_topk_keys<kKeysReady>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
+  if (emb_dtype == LSA_I8)
+    return launch_topk_keys<kKeysFromI32>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
+  return launch_topk_keys<kKeysFromF32>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
 }
 
 hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_pitch,
