@@ -2,14 +2,13 @@
 // the tokens of the kept chunks only (Sec. 2.1, core attention over the
 // selected entries), gathered by chunk id from the paged bf16 cache.
 //
-// Flash-decoding with split-K over the kept-chunk list, in two kernels:
-//
-// attn_split_kernel -- work unit = (sequence b, KV head g, split s).  The kept
-//   list of (b, g) is cut into 32-token tiles and each split owns a contiguous,
-//   equal share of them; the split count is sized so that the whole grid is one
-//   resident round on MI355X (256 CUs x 2 workgroups).  All G * Tq query rows
-//   that read KV head g are handled together, so every K/V byte is fetched from
-//   HBM once.  Both products run on v_mfma_f32_16x16x32_bf16:
+// Flash-decoding with split-K over the kept-chunk list.  The kept list of
+// each (sequence b, KV head g) is cut into 32-token tiles, and each split owns
+// a contiguous, equal share of them; the split count is sized so that the whole
+// grid is one resident round on MI355X (256 CUs x 2 workgroups).  All G * Tq
+// query rows that read KV head g are handled by the same workgroup, so every
+// K/V byte is fetched from HBM once.  Both products run on
+// v_mfma_f32_16x16x32_bf16:
 //   * QK computes S^T = K Q^T with 16 tokens as M and 16 query rows as N.  The
 //     cache stores each (chunk, head) block in MFMA operand order, and the M
 //     rows of the two 16-token MFMAs of a tile are tokens 8a+0..3 and 8a+4..7,
@@ -18,20 +17,22 @@
 //   * PV computes O = P V with the tile's 32 tokens as K and 16 head dims per
 //     MFMA as N.  P is split into bf16 hi + lo parts (two MFMAs), keeping ~16
 //     significant bits; logits, the running max / sum and O stay fp32.
-//   Every load instruction reads 1 KiB of contiguous cache with a nontemporal
-//   (streaming) hint, and two tiles are in flight per wave (the next tile loads
-//   while the current one computes).
-//   Rows <= 16: the 4 waves of a workgroup take consecutive quarters of the
-//   split's tiles and merge their (m, l, O) states through LDS.  Rows > 16:
-//   each wave owns one 16-row block and walks all tiles of the split; the
-//   workgroup's waves read the same cache lines back to back, so only the first
-//   read reaches HBM.  Partials (m, l, O) go to the workspace.
+//
+// attn_split_kernel (rows <= 16): the 4 waves of a workgroup take consecutive
+//   quarters of the split's tiles, each streaming its own tiles straight into
+//   registers (1 KiB per load instruction, nontemporal hint, two tiles in
+//   flight per wave), and merge their (m, l, O) states through LDS.
+// attn_rows_kernel (rows > 16): every wave owns one or two 16-row blocks and
+//   needs every tile, so tiles are staged once per workgroup in LDS by
+//   global->LDS copies, three tiles ahead, and each wave writes its own rows.
 //
 // attn_combine_kernel -- one workgroup per output row (b, t, h) merges the
-//   splits of its (b, g) in split order: weights exp2(m_s - M), then O as a
-//   weighted sum of float4 slices, each thread holding a strided subset of the
-//   splits so that all its loads are in flight at once.  Fixed order throughout,
-//   so results are bitwise reproducible.
+//   splits of its (b, g): weights exp2(m_s - M), O as the weighted sum of the
+//   split outputs, divided by L = sum_s exp2(m_s - M) l_s.  Every wave computes
+//   M and L itself from all splits' (m, l), so the loads of (m, l) and of the
+//   thread's O slices go out in one round and only the final merge of the 8
+//   split groups needs a barrier.  The summation order is fixed, so results
+//   are bitwise reproducible.
 #include "lsa_internal.h"
 
 namespace lsa {
@@ -43,7 +44,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kThreads = kAttnWaves * 64;
 constexpr int kOPad = 132;  // LDS row pitch (floats) of the wave merge
-constexpr int kCombineGroups = kThreads / (kHeadDim / 4);  // split groups in the combine
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -59,12 +59,35 @@ __device__ __forceinline__ bf16x8 load8_stream(const uint16_t* p) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// (sequence, kv head, row group, split) of attention workgroup wg
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+// Softmax weights as the two bf16 A operands of P V: p = hi + lo to about 16
+// significant bits.  hi is p truncated to bf16 (so converting it is exact) and
+// lo is the exact remainder p - hi rounded to bf16.
+__device__ __forceinline__ void split_bf16(const f32x8& p, bf16x8& ph, bf16x8& pl) {
+  f32x8 hi;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) hi[e] = __uint_as_float(__float_as_uint(p[e]) & 0xFFFF0000u);
+  ph = __builtin_convertvector(hi, bf16x8);
+  pl = __builtin_convertvector(p - hi, bf16x8);
+}
+
+// max over the lanes l, l ^ 16, l ^ 32, l ^ 48 (the four 16-lane rows of a
+// column), with the cross-row swaps of gfx950
+__device__ __forceinline__ float col_max(float x) {
+  const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
+  const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+}
+
+// (sequence, kv head, split) of attention workgroup wg; workgroups of sequence
+// b start at t.wg_off[b] and run head-major
 struct Unit {
-  int b, g, rg, s, ns;
+  int b, g, s, ns;
 };
 
-__device__ __forceinline__ Unit unit_of(const SeqTable& t, int RG, int wg) {
+__device__ __forceinline__ Unit unit_of(const SeqTable& t, int wg) {
   Unit u;
   int b = 0;
   while (wg >= t.wg_off[b + 1]) ++b;
@@ -72,23 +95,22 @@ __device__ __forceinline__ Unit unit_of(const SeqTable& t, int RG, int wg) {
   const int local = wg - t.wg_off[b];
   u.b = b;
   u.ns = ns;
-  u.g = local / (ns * RG);
-  u.rg = (local / ns) % RG;
+  u.g = local / ns;
   u.s = local % ns;
   return u;
 }
 
-template <int C, bool ROW_SPLIT>
+template <int C>
 __global__ void __launch_bounds__(kThreads, 2)  // 2 waves per SIMD: <= 256 registers
 attn_split_kernel(SeqTable t, AttnArgs a) {
-  __shared__ float sm_o[ROW_SPLIT ? 1 : kAttnWaves][16][kOPad];
+  __shared__ float sm_o[kAttnWaves][16][kOPad];
   __shared__ float sm_m[kAttnWaves][16], sm_l[kAttnWaves][16];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n16 = lane & 15, kg = lane >> 4;
-  const int RG = a.row_groups, G = a.group;
-  const Unit u = unit_of(t, RG, blockIdx.x);
+  const int G = a.group;
+  const Unit u = unit_of(t, blockIdx.x);
   const int b = u.b, g = u.g, s = u.s, ns = u.ns;
 
   // sel_count and the chunk ids are clamped so that malformed device inputs
@@ -98,18 +120,13 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   const int n_b = t.n[b];
   const int nTall = cnt * TPC;
   const int T0 = (int)(((int64_t)s * nTall) / ns), T1 = (int)(((int64_t)(s + 1) * nTall) / ns);
-  int Tb = T0, Te = T1;
-  if constexpr (!ROW_SPLIT) {
-    Tb = T0 + (int)(((int64_t)wave * (T1 - T0)) / kAttnWaves);
-    Te = T0 + (int)(((int64_t)(wave + 1) * (T1 - T0)) / kAttnWaves);
-  }
+  const int Tb = T0 + (int)(((int64_t)wave * (T1 - T0)) / kAttnWaves);
+  const int Te = T0 + (int)(((int64_t)(wave + 1) * (T1 - T0)) / kAttnWaves);
 
-  // ---- query operand: row n16 of this wave's 16-row block
-  const int rblock = ROW_SPLIT ? u.rg * kAttnWaves + wave : 0;
-  const bool block_live = rblock * 16 < a.rows;
+  // ---- query operand: row n16 (rows <= 16 here)
   bf16x8 qb[4];
   {
-    const int row = rblock * 16 + n16;
+    const int row = n16;
     if (row < a.rows) {
       const int tq = row / G, h = g * G + row % G;
       const uint16_t* qp = a.q + (((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h) * kHeadDim + 8 * kg;
@@ -129,7 +146,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   // Tiles Tb..Te-1 of the kept list; tile T is tile T % TPC of kept chunk T / TPC.
   // Chunk ids are fetched 64 at a time into a register (one per lane) and read
   // back with readlane, so no scalar load sits between consecutive tiles.
-  const int nT = block_live && Te > Tb ? Te - Tb : 0;
+  const int nT = Te > Tb ? Te - Tb : 0;
   const int pos0 = Tb / TPC;
   const int npos = nT > 0 ? (Te - 1) / TPC - pos0 + 1 : 0;
   const int32_t* sel = a.sel_idx + (int64_t)b * a.sel_pitch + pos0;
@@ -172,11 +189,11 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
       x[i] *= a.scale_log2e;
       mx = fmaxf(mx, x[i]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = col_max(mx);
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
-    float p[8], psum = 0.f;
+    f32x8 p;
+    float psum = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       p[i] = fast_exp2(x[i] - m_new);
@@ -194,11 +211,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
       }
     }
     bf16x8 ph, pl;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      ph[i] = (__bf16)p[i];
-      pl[i] = (__bf16)(p[i] - (float)ph[i]);
-    }
+    split_bf16(p, ph, pl);
 #pragma unroll
     for (int nb = 0; nb < 8; ++nb) {
       o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vt[nb], o[nb], 0, 0, 0);
@@ -222,21 +235,8 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
 
   // ---- this split's partials: rows of the (b, g) group, [unit][rows_pad]
   const int rows_pad = a.rows_pad;
-  const int64_t unit = (int64_t)t.wg_off[b] / RG + (int64_t)g * ns + s;
-  if constexpr (ROW_SPLIT) {
-    if (block_live) {
-      const int64_t rbase = unit * rows_pad + rblock * 16;
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb)
-          a.part_o[(rbase + 4 * kg + r) * kHeadDim + 16 * nb + n16] = o[nb][r];
-      if (kg == 0) {
-        a.part_ml[(rbase + n16) * 2 + 0] = m_run;
-        a.part_ml[(rbase + n16) * 2 + 1] = l_run;
-      }
-    }
-  } else {
+  const int64_t unit = (int64_t)t.wg_off[b] + (int64_t)g * ns + s;
+  {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -269,14 +269,251 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   }
 }
 
+// s_waitcnt immediates (gfx9 encoding) that wait for the vector-memory counter
+// only: at most N of this wave's loads still outstanding.
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+// More than 16 query rows per KV head (rows = G * n_qtok, up to 128).  One
+// workgroup per (sequence, kv head, split) serves all the rows, so each K/V
+// tile is fetched from HBM once: every wave copies 4 of the tile's 16 one-KiB
+// pieces (K pieces 0-7, V pieces 8-15) straight into LDS with
+// global_load_lds_dwordx4, kRowBufs - 1 tiles ahead of the tile being
+// consumed, and every wave then reads the whole tile from LDS for its own row
+// blocks (w and w + 4; RBW of them).  Each wave keeps an online softmax per row
+// block and writes its rows' partials itself.
+constexpr int kRowBufs = 4;  // LDS tile buffers per workgroup (16 KiB each)
+
+// This lane's slice of 8 staged pieces (K: pieces 0-7, V: pieces 8-15 of a
+// tile).  The reads are issued as one assembly block that ends with its own LDS
+// wait: the compiler cannot tell the staged buffers apart and would otherwise
+// make every read wait for all global->LDS copies still in flight, draining
+// the prefetch.
+__device__ __forceinline__ void read_pieces(const uint4 (&tb)[16][64], int first, int lane, bf16x8 (&out)[8]) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)&tb[first][lane];
+  uint4 v[8];
+  asm volatile(
+      "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
+      "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
+      "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
+      "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), "=&v"(v[7])
+      : "v"(a)
+      : "memory");
+#pragma unroll
+  for (int q = 0; q < 8; ++q) out[q] = __builtin_bit_cast(bf16x8, v[q]);
+}
+
+
+typedef const __attribute__((address_space(4))) int32_t* kept_ids_t;  // read-only during the kernel
+
+template <int C, int RBW>
+__global__ void __launch_bounds__(kThreads, 2)
+attn_rows_kernel(SeqTable t, AttnArgs a) {
+  // four distinct LDS objects, always named statically, so that the compiler
+  // can tell the tile being read from the tiles still being copied in
+  __shared__ uint4 buf0[16][64], buf1[16][64], buf2[16][64], buf3[16][64];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n16 = lane & 15, kg = lane >> 4;
+  const int G = a.group;
+  const Unit u = unit_of(t, blockIdx.x);
+  const int b = u.b, g = u.g, s = u.s, ns = u.ns;
+
+  constexpr int TPC = C / 32;
+  const int cnt = min(max(a.sel_count[b], 0), a.sel_pitch);
+  const int n_b = t.n[b];
+  const int nTall = cnt * TPC;
+  const int Tb = (int)(((int64_t)s * nTall) / ns), Te = (int)(((int64_t)(s + 1) * nTall) / ns);
+  const int nT = Te > Tb ? Te - Tb : 0;
+
+  // query operands and online-softmax state of this wave's row blocks
+  bool rb_live[RBW];
+  bf16x8 qb[RBW][4];
+  f32x4 o[RBW][8];
+  float m_run[RBW], l_run[RBW];
+#pragma unroll
+  for (int r = 0; r < RBW; ++r) {
+    rb_live[r] = (wave + 4 * r) * 16 < a.rows;  // wave-uniform
+    const int row = (wave + 4 * r) * 16 + n16;
+    if (row < a.rows) {
+      const int tq = row / G, h = g * G + row % G;
+      const uint16_t* qp = a.q + (((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h) * kHeadDim + 8 * kg;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) qb[r][jj] = load8(qp + 32 * jj);
+    } else {
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) qb[r][jj] = bf16x8{};
+    }
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) o[r][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run[r] = -INFINITY;
+    l_run[r] = 0.f;
+  }
+
+  // the query operands are in registers before any tile copy starts (so that no
+  // wait in the loop is ever for them); chunk ids come through the scalar cache
+  // (wave-uniform loads), so the tile copies are the only vector loads in flight
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  const kept_ids_t sel = (kept_ids_t)(uintptr_t)(a.sel_idx + (int64_t)b * a.sel_pitch);
+  // this wave's quarter of a tile: K or V (waves 0-1 / 2-3), first or second half
+  const uint16_t* src = (wave < 2 ? a.k : a.v) + t.chunk_off[b] * a.chunk_stride + g * a.head_stride +
+                        (wave & 1) * (4 * 512) + lane * 8;
+
+  // chunk id of the next tile to issue, loaded one issue ahead
+  int c_next = nT > 0 ? sel[Tb / TPC] : 0;
+  auto issue = [&](int i, uint4(&dst)[16][64]) {  // this wave's pieces of tile i -> dst
+    const int T = Tb + i;
+    const int tt = T % TPC;
+    const int c = min(max(c_next, 0), n_b - 1);
+    if (i + 1 < nT) c_next = sel[(T + 1) / TPC];
+    const uint16_t* p = src + (int64_t)c * a.chunk_stride + tt * (32 * kHeadDim);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_global_load_lds((const void*)(p + q * 512),
+                                       (void __attribute__((address_space(3)))*)&dst[4 * wave + q][0], 16, 0, 0);
+  };
+
+  // tile i is consumed from buffer i % 4 while tiles i + 1 .. i + 3 are being
+  // copied into the other three
+  auto step = [&](int i, const uint4(&tb)[16][64], uint4(&next)[16][64]) {
+    // tile i has landed once at most `ahead` younger tiles of this wave are in flight
+    const int ahead = min(nT - 1 - i, kRowBufs - 2);
+    if (ahead >= 2)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(8));
+    else if (ahead == 1)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(4));
+    else
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    // every wave's pieces of tile i are in; every wave is done with tile i - 1
+    // (a bare barrier: a fenced one would also wait for the tiles still in flight)
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+    if (i + kRowBufs - 1 < nT) issue(i + kRowBufs - 1, next);  // the buffer of tile i - 1
+    bf16x8 kt[8], vt[8];
+    read_pieces(tb, 0, lane, kt);
+    f32x4 sc[RBW][2];
+#pragma unroll
+    for (int r = 0; r < RBW; ++r) {
+      sc[r][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+      sc[r][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (!rb_live[r]) continue;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        sc[r][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[jj], qb[r][jj], sc[r][0], 0, 0, 0);
+        sc[r][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[4 + jj], qb[r][jj], sc[r][1], 0, 0, 0);
+      }
+    }
+    // the V reads go out while the QK products execute
+    __builtin_amdgcn_sched_barrier(0);
+    read_pieces(tb, 8, lane, vt);
+#pragma unroll
+    for (int r = 0; r < RBW; ++r) {
+      if (!rb_live[r]) continue;
+      // lane holds logits of query row n16 for tile tokens 8kg + 0..7
+      const float x[8] = {sc[r][0][0], sc[r][0][1], sc[r][0][2], sc[r][0][3],
+                          sc[r][1][0], sc[r][1][1], sc[r][1][2], sc[r][1][3]};
+      float mx = x[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, x[e]);
+      mx = col_max(mx);
+      // max over raw logits (the scale is positive), then p = exp2(x * scale - m)
+      const float m_new = fmaxf(m_run[r], mx * a.scale_log2e);
+      const float alpha = fast_exp2(m_run[r] - m_new);
+      f32x8 p;
+      float psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[e] = fast_exp2(fmaf(x[e], a.scale_log2e, -m_new));
+        psum += p[e];
+      }
+      l_run[r] = l_run[r] * alpha + psum;
+      m_run[r] = m_new;
+      if (__ballot(alpha != 1.f) != 0ull) {
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const float ar = __shfl(alpha, 4 * kg + rr);
+#pragma unroll
+          for (int nb = 0; nb < 8; ++nb) o[r][nb][rr] *= ar;
+        }
+      }
+      bf16x8 ph, pl;
+      split_bf16(p, ph, pl);
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        o[r][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vt[nb], o[r][nb], 0, 0, 0);
+        o[r][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vt[nb], o[r][nb], 0, 0, 0);
+      }
+    }
+  };
+
+  if (nT > 0) issue(0, buf0);
+  if (nT > 1) issue(1, buf1);
+  if (nT > 2) issue(2, buf2);
+  int i = 0;
+  for (; i + 4 <= nT; i += 4) {
+    step(i, buf0, buf3);
+    step(i + 1, buf1, buf0);
+    step(i + 2, buf2, buf1);
+    step(i + 3, buf3, buf2);
+  }
+  if (i < nT) step(i, buf0, buf3);
+  if (i + 1 < nT) step(i + 1, buf1, buf0);
+  if (i + 2 < nT) step(i + 2, buf2, buf1);
+
+  // partials of this wave's row blocks, [unit][rows_pad]
+  const int64_t unit = (int64_t)blockIdx.x;
+#pragma unroll
+  for (int r = 0; r < RBW; ++r) {
+    if (!rb_live[r]) continue;
+    float l = l_run[r];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    const int64_t rbase = unit * a.rows_pad + (wave + 4 * r) * 16;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) a.part_o[(rbase + 4 * kg + rr) * kHeadDim + 16 * nb + n16] = o[r][nb][rr];
+    if (kg == 0) {
+      a.part_ml[(rbase + n16) * 2 + 0] = m_run[r];
+      a.part_ml[(rbase + n16) * 2 + 1] = l;
+    }
+  }
+}
+
+// Wave-wide reductions with DPP row shifts and row broadcasts; the result is
+// read from lane 63.
+__device__ __forceinline__ float wave_max(float x) {
+  const int ninf = (int)0xFF800000u;
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x111, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x112, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x114, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x118, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x142, 0xA, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x143, 0xC, 0xF, false)));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x111, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x112, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x114, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x118, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xA, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xC, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
 __global__ void __launch_bounds__(kThreads)
 attn_combine_kernel(SeqTable t, AttnArgs a) {
-  __shared__ float sm_w[kMaxSplits];
-  __shared__ float4 sm_red[kCombineGroups][kHeadDim / 4];
-  __shared__ float sm_lw[kAttnWaves];
-  __shared__ float sh_M;
+  constexpr int kSlices = kHeadDim / 4;              // float4 slices of a row
+  constexpr int kGroups = kThreads / kSlices;        // split groups (8)
+  constexpr int kBatch = 8;                          // splits per thread and round of loads
+  __shared__ float4 sm_red[kGroups][kSlices];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int G = a.group;
   const int rows_per_b = a.n_qtok * a.n_q_heads;
   const int b = blockIdx.x / rows_per_b;
@@ -284,67 +521,74 @@ attn_combine_kernel(SeqTable t, AttnArgs a) {
   const int tq = rem / a.n_q_heads, h = rem - tq * a.n_q_heads;
   const int g = h / G, r = tq * G + h % G;  // row within the (b, g) group
   const int ns = t.nsplit[b];
-  const int64_t unit0 = (int64_t)t.wg_off[b] / a.row_groups + (int64_t)g * ns;
-  const int rows_pad = a.rows_pad;
+  const int64_t unit0 = (int64_t)t.wg_off[b] + (int64_t)g * ns;
+  const int64_t rows_pad = a.rows_pad;
+  const float2* ml = reinterpret_cast<const float2*>(a.part_ml) + unit0 * rows_pad + r;  // split s at s * rows_pad
+  const int sg = tid / kSlices, e4 = (tid % kSlices) * 4;
+  const float* po = a.part_o + (unit0 * rows_pad + r) * kHeadDim + e4;
+  const int64_t ostride = rows_pad * kHeadDim;
 
-  // split weights exp2(m_s - M) in LDS and L = sum_s w_s l_s (one round of loads)
-  float m_s = -INFINITY, l_s = 0.f;
-  if (tid < ns) {
-    const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + ((unit0 + tid) * rows_pad + r) * 2);
-    m_s = ml.x;
-    l_s = ml.y;
-  }
-  float mw = m_s;
+  // Every load of the first round is issued up front: (m, l) of all splits
+  // (each wave reads them all, lane l splits l, l + 64, ...), and this
+  // thread's first batch of O slices (splits sg, sg + 8, ...).
+  float2 mls[kMaxSplits / 64];
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) mw = fmaxf(mw, __shfl_xor(mw, off));
-  if (lane == 0) sm_lw[wave] = mw;
-  __syncthreads();
-  if (tid == 0) {
-    float M = sm_lw[0];
-    for (int w = 1; w < kAttnWaves; ++w) M = fmaxf(M, sm_lw[w]);
-    sh_M = M;
+  for (int i = 0; i < kMaxSplits / 64; ++i) {
+    const int sp = lane + 64 * i;
+    mls[i] = sp < ns ? ml[sp * rows_pad] : make_float2(-INFINITY, 0.f);
   }
-  __syncthreads();
-  const float M = sh_M;
-  const float f = (tid < ns && m_s != -INFINITY) ? fast_exp2(m_s - M) : 0.f;
-  if (tid < ns) sm_w[tid] = f;
-  float lf = f * l_s;
+  float4 ov[kBatch];
+  float mo[kBatch];
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) lf += __shfl_xor(lf, off);
-  __syncthreads();  // sm_lw is reused
-  if (lane == 0) sm_lw[wave] = lf;
-  __syncthreads();
-  float L = sm_lw[0];
-  for (int w = 1; w < kAttnWaves; ++w) L += sm_lw[w];
-  const float invL = 1.f / L;
+  for (int i = 0; i < kBatch; ++i) {
+    const int sp = sg + kGroups * i;
+    ov[i] = sp < ns ? *reinterpret_cast<const float4*>(po + sp * ostride) : make_float4(0.f, 0.f, 0.f, 0.f);
+    mo[i] = sp < ns ? ml[sp * rows_pad].x : -INFINITY;
+  }
 
-  // O = sum_s w_s O_s: thread (group sg, slice e4) sums splits sg, sg + 8, ...
-  const int sg = tid / (kHeadDim / 4), e4 = (tid % (kHeadDim / 4)) * 4;
-  const float* src = a.part_o + (unit0 * rows_pad + r) * kHeadDim + e4;
-  const int64_t sstride = (int64_t)rows_pad * kHeadDim;
+  // M = max_s m_s and L = sum_s exp2(m_s - M) l_s, in a fixed order
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kMaxSplits / 64; ++i) mx = fmaxf(mx, mls[i].x);
+  const float M = wave_max(mx);
+  float lx = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxSplits / 64; ++i) lx += mls[i].x == -INFINITY ? 0.f : fast_exp2(mls[i].x - M) * mls[i].y;
+  const float L = wave_sum(lx);
+
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 8
-  for (int s2 = sg; s2 < ns; s2 += kCombineGroups) {
-    const float4 v = *reinterpret_cast<const float4*>(src + s2 * sstride);
-    const float w = sm_w[s2];
-    acc.x += w * v.x;
-    acc.y += w * v.y;
-    acc.z += w * v.z;
-    acc.w += w * v.w;
+  for (int base = 0;;) {
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const float w = mo[i] == -INFINITY ? 0.f : fast_exp2(mo[i] - M);
+      acc.x += w * ov[i].x;
+      acc.y += w * ov[i].y;
+      acc.z += w * ov[i].z;
+      acc.w += w * ov[i].w;
+    }
+    base += kGroups * kBatch;
+    if (base >= ns) break;
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const int sp = base + sg + kGroups * i;
+      ov[i] = sp < ns ? *reinterpret_cast<const float4*>(po + sp * ostride) : make_float4(0.f, 0.f, 0.f, 0.f);
+      mo[i] = sp < ns ? ml[sp * rows_pad].x : -INFINITY;
+    }
   }
-  sm_red[sg][e4 / 4] = acc;
+  sm_red[sg][tid % kSlices] = acc;
   __syncthreads();
   const int64_t orow = ((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h;
-  if (tid < kHeadDim / 4) {
+  if (tid < kSlices) {
     float4 sum = sm_red[0][tid];
 #pragma unroll
-    for (int q = 1; q < kCombineGroups; ++q) {
+    for (int q = 1; q < kGroups; ++q) {
       const float4 v = sm_red[q][tid];
       sum.x += v.x;
       sum.y += v.y;
       sum.z += v.z;
       sum.w += v.w;
     }
+    const float invL = 1.f / L;
     sum.x *= invL;
     sum.y *= invL;
     sum.z *= invL;
@@ -357,10 +601,12 @@ attn_combine_kernel(SeqTable t, AttnArgs a) {
 template <int C>
 hipError_t launch_c(const SeqTable& t, const AttnArgs& a, hipStream_t s) {
   const dim3 grid(t.wg_off[t.batch]);
-  if (a.rows > 16)
-    hipLaunchKernelGGL((attn_split_kernel<C, true>), grid, dim3(kThreads), 0, s, t, a);
+  if (a.rows > 4 * 16)
+    hipLaunchKernelGGL((attn_rows_kernel<C, 2>), grid, dim3(kThreads), 0, s, t, a);
+  else if (a.rows > 16)
+    hipLaunchKernelGGL((attn_rows_kernel<C, 1>), grid, dim3(kThreads), 0, s, t, a);
   else
-    hipLaunchKernelGGL((attn_split_kernel<C, false>), grid, dim3(kThreads), 0, s, t, a);
+    hipLaunchKernelGGL((attn_split_kernel<C>), grid, dim3(kThreads), 0, s, t, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(attn_combine_kernel, dim3(t.batch * a.n_qtok * a.n_q_heads), dim3(kThreads), 0, s, t,

@@ -37,7 +37,7 @@ struct Plan {
   SeqTable t;
   int64_t total_chunks = 0;
   int32_t max_keep = 0, max_sel = 0;
-  int32_t group = 0, rows = 0, row_groups = 1, rows_pad = 16;
+  int32_t group = 0, rows = 0, rows_pad = 16;
   int64_t chunk_stride = 0, head_stride = 0;
   int64_t n_units = 0;
   size_t emb_elem = 0;
@@ -82,8 +82,7 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   const int srows = score_rows_per_wg(p->emb_dtype, p->emb_dim);
   P.group = G;
   P.rows = rows;
-  P.row_groups = rows > 16 ? (rows + kAttnWaves * 16 - 1) / (kAttnWaves * 16) : 1;
-  P.rows_pad = rows > 16 ? P.row_groups * kAttnWaves * 16 : 16;
+  P.rows_pad = (rows + 15) / 16 * 16;  // partial rows per unit: whole 16-row MFMA blocks
   // First pass: shapes and the total kept-chunk bound, which sizes the splits.
   int64_t sel_total = 0;
   for (int b = 0; b < B; ++b) {
@@ -110,7 +109,7 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
     // splits of sequence b in proportion to its share of the kept chunks, so the
     // whole grid is about kTargetWorkgroups; at least one 32-token tile per split
     const double share = (double)kTargetWorkgroups * (double)msel /
-                         ((double)p->n_kv_heads * P.row_groups * (double)std::max<int64_t>(sel_total, 1));
+                         ((double)p->n_kv_heads * (double)std::max<int64_t>(sel_total, 1));
     const int32_t ns = (int32_t)std::max<int64_t>(
         1, std::min<int64_t>({std::llround(share), (int64_t)kMaxSplits, (int64_t)msel * tpc}));
     t.n[b] = (int32_t)n;
@@ -120,7 +119,7 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
     t.wg_off[b] = (int32_t)wg_off;
     t.score_wg_off[b] = (int32_t)swg_off;
     chunk_off += n;
-    wg_off += (int64_t)p->n_kv_heads * P.row_groups * ns;
+    wg_off += (int64_t)p->n_kv_heads * ns;
     swg_off += (n + srows - 1) / srows;
     P.max_keep = std::max(P.max_keep, k);
     P.max_sel = std::max(P.max_sel, msel);
@@ -131,7 +130,7 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   t.wg_off[B] = (int32_t)wg_off;
   t.score_wg_off[B] = (int32_t)swg_off;
   P.total_chunks = chunk_off;
-  P.n_units = wg_off / P.row_groups;
+  P.n_units = wg_off;
 
   // KV cache strides: blocks of C*d elements must not overlap.
   const int64_t blk = (int64_t)C * kHeadDim;
@@ -230,7 +229,6 @@ lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, cons
   a.group = P.group;
   a.n_qtok = p->n_qtok;
   a.rows = P.rows;
-  a.row_groups = P.row_groups;
   a.rows_pad = P.rows_pad;
   LSA_HIP(launch_attn(P.t, a, p->chunk_size, s), "attention launch");
   return LSA_OK;

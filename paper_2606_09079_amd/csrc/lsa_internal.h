@@ -43,8 +43,7 @@ struct AttnArgs {
   int32_t group;         // G = Hq / Hkv
   int32_t n_qtok;
   int32_t rows;          // G * n_qtok
-  int32_t row_groups;    // workgroups along the row dimension (rows > 16 only)
-  int32_t rows_pad;      // partial rows per (b, g, split): 16, or 64 * row_groups
+  int32_t rows_pad;      // partial rows per (b, g, split): rows rounded up to 16
 };
 
 // Geometry of the attention launch shared by dispatch and kernels.
