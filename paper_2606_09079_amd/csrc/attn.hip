@@ -24,7 +24,8 @@
 //   flight per wave), and merge their (m, l, O) states through LDS.
 // attn_rows_kernel (rows > 16): every wave owns one or two 16-row blocks and
 //   needs every tile, so tiles are staged once per workgroup in LDS by
-//   global->LDS copies, three tiles ahead, and each wave writes its own rows.
+//   global->LDS copies, two tiles ahead, with three workgroups per CU, and
+//   each wave writes its own rows.
 //
 // attn_combine_kernel -- one workgroup per output row (b, t, h) merges the
 //   splits of its (b, g): weights exp2(m_s - M), O as the weighted sum of the
@@ -281,7 +282,7 @@ constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 
 // consumed, and every wave then reads the whole tile from LDS for its own row
 // blocks (w and w + 4; RBW of them).  Each wave keeps an online softmax per row
 // block and writes its rows' partials itself.
-constexpr int kRowBufs = 4;  // LDS tile buffers per workgroup (16 KiB each)
+constexpr int kRowBufs = 5;  // LDS tile buffers per workgroup (16 KiB each; 2 workgroups fill a CU's LDS)
 
 // This lane's slice of 8 staged pieces (K: pieces 0-7, V: pieces 8-15 of a
 // tile).  The reads are issued as one assembly block that ends with its own LDS
@@ -307,16 +308,27 @@ __device__ __forceinline__ void read_pieces(const uint4 (&tb)[16][64], int first
 
 typedef const __attribute__((address_space(4))) int32_t* kept_ids_t;  // read-only during the kernel
 
-template <int C, int RBW>
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Token held in MFMA row m of the QK product.  With this order the 32x32
+// result leaves register r of lane j holding token 16 (r / 8) + 8 (j / 32) +
+// r % 8 of query row j % 32, which is exactly the P^T operand of the PV
+// product for 16-token step r / 8.
+__device__ __forceinline__ int qk_token(int m) {
+  return 16 * (m / 16) + 8 * ((m / 4) % 2) + 4 * ((m / 8) % 2) + m % 4;
+}
+
+template <int C>
 __global__ void __launch_bounds__(kThreads, 2)
 attn_rows_kernel(SeqTable t, AttnArgs a) {
   // four distinct LDS objects, always named statically, so that the compiler
-  // can tell the tile being read from the tiles still being copied in
-  __shared__ uint4 buf0[16][64], buf1[16][64], buf2[16][64], buf3[16][64];
+  // can tell the tile being read from the tiles still being copied in.  A
+  // staged tile holds, in MFMA operand order, K pieces d = 0..7 (QK step d)
+  // and V pieces 8 + 4 s + n (PV token half s, 32-dim block n).
+  __shared__ uint4 buf0[16][64], buf1[16][64], buf2[16][64], buf3[16][64], buf4[16][64];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n16 = lane & 15, kg = lane >> 4;
   const int G = a.group;
   const Unit u = unit_of(t, blockIdx.x);
   const int b = u.b, g = u.g, s = u.s, ns = u.ns;
@@ -328,28 +340,42 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   const int Tb = (int)(((int64_t)s * nTall) / ns), Te = (int)(((int64_t)(s + 1) * nTall) / ns);
   const int nT = Te > Tb ? Te - Tb : 0;
 
-  // query operands and online-softmax state of this wave's row blocks
-  bool rb_live[RBW];
-  bf16x8 qb[RBW][4];
-  f32x4 o[RBW][8];
-  float m_run[RBW], l_run[RBW];
+  // this wave's 32 query rows: lane j serves row 32 * wave + j % 32
+  const bool live = 32 * wave < a.rows;  // wave-uniform
+  const int row = 32 * wave + (lane & 31);
+  bf16x8 qb[8];  // Q^T operand of QK step d: dims 16 d + 8 (lane / 32) .. + 7
+  if (row < a.rows) {
+    const int tq = row / G, h = g * G + row % G;
+    const uint16_t* qp = a.q + (((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h) * kHeadDim + 8 * (lane >> 5);
 #pragma unroll
-  for (int r = 0; r < RBW; ++r) {
-    rb_live[r] = (wave + 4 * r) * 16 < a.rows;  // wave-uniform
-    const int row = (wave + 4 * r) * 16 + n16;
-    if (row < a.rows) {
-      const int tq = row / G, h = g * G + row % G;
-      const uint16_t* qp = a.q + (((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h) * kHeadDim + 8 * kg;
+    for (int d = 0; d < 8; ++d) qb[d] = load8(qp + 16 * d);
+  } else {
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) qb[r][jj] = load8(qp + 32 * jj);
-    } else {
+    for (int d = 0; d < 8; ++d) qb[d] = bf16x8{};
+  }
+  f32x16 o[4];  // O^T, 32-dim block n: dims 32 n + 8 (r / 4) + 4 (lane / 32) + r % 4
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) qb[r][jj] = bf16x8{};
+  for (int n = 0; n < 4; ++n)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[n][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // Each wave copies 4 of a tile's 16 pieces; lane i of piece q gathers the 16
+  // bytes of the cache block that MFMA lane i needs (element offsets within
+  // the tile's 32-token slice of the chunk block).
+  int goff[4];
+  {
+    const int i = lane, hi = lane >> 5;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (wave < 2) {  // K piece d: token qk_token(i % 32), dims 16 d + 8 hi .. + 7
+        const int d = 4 * wave + q, tk = qk_token(i & 31), e0 = 16 * d + 8 * hi;
+        goff[q] = (((((tk / 4) % 2) * 4 + e0 / 32) * 4 + (e0 / 8) % 4) * 16 + (tk / 8) * 4 + tk % 4) * 8;
+      } else {  // V piece (s, n): dim 32 n + i % 32, tokens 16 s + 8 hi .. + 7
+        const int sh = wave - 2, n = q, e = 32 * n + (i & 31), t0 = 16 * sh + 8 * hi;
+        goff[q] = (((e / 16) * 4 + t0 / 8) * 16 + e % 16) * 8;
+      }
     }
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb) o[r][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m_run[r] = -INFINITY;
-    l_run[r] = 0.f;
   }
 
   // the query operands are in registers before any tile copy starts (so that no
@@ -357,9 +383,7 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   // (wave-uniform loads), so the tile copies are the only vector loads in flight
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   const kept_ids_t sel = (kept_ids_t)(uintptr_t)(a.sel_idx + (int64_t)b * a.sel_pitch);
-  // this wave's quarter of a tile: K or V (waves 0-1 / 2-3), first or second half
-  const uint16_t* src = (wave < 2 ? a.k : a.v) + t.chunk_off[b] * a.chunk_stride + g * a.head_stride +
-                        (wave & 1) * (4 * 512) + lane * 8;
+  const uint16_t* src = (wave < 2 ? a.k : a.v) + t.chunk_off[b] * a.chunk_stride + g * a.head_stride;
 
   // chunk id of the next tile to issue, loaded one issue ahead
   int c_next = nT > 0 ? sel[Tb / TPC] : 0;
@@ -371,114 +395,149 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     const uint16_t* p = src + (int64_t)c * a.chunk_stride + tt * (32 * kHeadDim);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      __builtin_amdgcn_global_load_lds((const void*)(p + q * 512),
+      __builtin_amdgcn_global_load_lds((const void*)(p + goff[q]),
                                        (void __attribute__((address_space(3)))*)&dst[4 * wave + q][0], 16, 0, 0);
   };
 
-  // tile i is consumed from buffer i % 4 while tiles i + 1 .. i + 3 are being
-  // copied into the other three
-  auto step = [&](int i, const uint4(&tb)[16][64], uint4(&next)[16][64]) {
-    // tile i has landed once at most `ahead` younger tiles of this wave are in flight
-    const int ahead = min(nT - 1 - i, kRowBufs - 2);
+  // Software pipeline over tiles.  Step j (after the barrier that makes tile j
+  // visible) issues the copy of tile j + 3, the QK products of tile j, and
+  // then the softmax and PV products of tile j - 1, so the VALU softmax of one
+  // tile runs while the MFMA unit works on the next tile's QK.  Tile j lives in
+  // buffer j % 5: the copy of tile j + 3 reuses the buffer of tile j - 2, whose
+  // last reader (step j - 1) is behind the barrier.
+  // logits of the tile whose softmax is pending, as the two QK accumulators
+  // (summed only when the softmax runs, a step after the products were issued)
+  f32x16 s_cur0, s_cur1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    s_cur0[r] = 0.f;
+    s_cur1[r] = 0.f;
+  }
+
+  auto qk = [&](const uint4(&tb)[16][64], f32x16& s0, f32x16& s1) {
+    bf16x8 kp[8];
+    read_pieces(tb, 0, lane, kp);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      s0[r] = 0.f;
+      s1[r] = 0.f;
+    }
+#pragma unroll
+    for (int d = 0; d < 8; d += 2) {
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kp[d], qb[d], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kp[d + 1], qb[d + 1], s1, 0, 0, 0);
+    }
+  };
+
+  auto softmax_pv = [&](const f32x16& x0, const f32x16& x1, const uint4(&tb)[16][64]) {
+    bf16x8 vp[8];
+    read_pieces(tb, 8, lane, vp);
+    const f32x16 x = x0 + x1;
+    // online softmax: lanes j and j ^ 32 share row j % 32 and split its tokens
+    float mx = x[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    // max over raw logits (the scale is positive), then p = exp2(x * scale - m)
+    const float m_new = fmaxf(m_run, mx * a.scale_log2e);
+    const float alpha = fast_exp2(m_run - m_new);
+    f32x8 p0, p1;
+    float psum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      p0[r] = fast_exp2(fmaf(x[r], a.scale_log2e, -m_new));
+      p1[r] = fast_exp2(fmaf(x[8 + r], a.scale_log2e, -m_new));
+      psum += p0[r] + p1[r];
+    }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    if (__ballot(alpha != 1.f) != 0ull) {  // every O register of a lane belongs to its row
+#pragma unroll
+      for (int n = 0; n < 4; ++n) o[n] *= alpha;
+    }
+    bf16x8 ph0, pl0, ph1, pl1;
+    split_bf16(p0, ph0, pl0);
+    split_bf16(p1, ph1, pl1);
+    // O^T += V^T P^T, token half s of the tile, 32-dim block n
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      o[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[n], ph0, o[n], 0, 0, 0);
+      o[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[n], pl0, o[n], 0, 0, 0);
+      o[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[4 + n], ph1, o[n], 0, 0, 0);
+      o[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[4 + n], pl1, o[n], 0, 0, 0);
+    }
+  };
+
+  auto step = [&](int j, const uint4(&cur)[16][64], const uint4(&prev)[16][64], uint4(&dma)[16][64]) {
+    // tile j has landed once at most `ahead` younger tiles of this wave are in flight
+    const int ahead = min(nT - 1 - j, kRowBufs - 3);
     if (ahead >= 2)
       __builtin_amdgcn_s_waitcnt(waitcnt_vm(8));
     else if (ahead == 1)
       __builtin_amdgcn_s_waitcnt(waitcnt_vm(4));
     else
       __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
-    // every wave's pieces of tile i are in; every wave is done with tile i - 1
+    // every wave's pieces of tile j are in; every wave is done with tile j - 2
     // (a bare barrier: a fenced one would also wait for the tiles still in flight)
     __asm__ volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     __asm__ volatile("" ::: "memory");
-    if (i + kRowBufs - 1 < nT) issue(i + kRowBufs - 1, next);  // the buffer of tile i - 1
-    bf16x8 kt[8], vt[8];
-    read_pieces(tb, 0, lane, kt);
-    f32x4 sc[RBW][2];
-#pragma unroll
-    for (int r = 0; r < RBW; ++r) {
-      sc[r][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-      sc[r][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (!rb_live[r]) continue;
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        sc[r][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[jj], qb[r][jj], sc[r][0], 0, 0, 0);
-        sc[r][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[4 + jj], qb[r][jj], sc[r][1], 0, 0, 0);
-      }
-    }
-    // the V reads go out while the QK products execute
-    __builtin_amdgcn_sched_barrier(0);
-    read_pieces(tb, 8, lane, vt);
-#pragma unroll
-    for (int r = 0; r < RBW; ++r) {
-      if (!rb_live[r]) continue;
-      // lane holds logits of query row n16 for tile tokens 8kg + 0..7
-      const float x[8] = {sc[r][0][0], sc[r][0][1], sc[r][0][2], sc[r][0][3],
-                          sc[r][1][0], sc[r][1][1], sc[r][1][2], sc[r][1][3]};
-      float mx = x[0];
-#pragma unroll
-      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, x[e]);
-      mx = col_max(mx);
-      // max over raw logits (the scale is positive), then p = exp2(x * scale - m)
-      const float m_new = fmaxf(m_run[r], mx * a.scale_log2e);
-      const float alpha = fast_exp2(m_run[r] - m_new);
-      f32x8 p;
-      float psum = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p[e] = fast_exp2(fmaf(x[e], a.scale_log2e, -m_new));
-        psum += p[e];
-      }
-      l_run[r] = l_run[r] * alpha + psum;
-      m_run[r] = m_new;
-      if (__ballot(alpha != 1.f) != 0ull) {
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const float ar = __shfl(alpha, 4 * kg + rr);
-#pragma unroll
-          for (int nb = 0; nb < 8; ++nb) o[r][nb][rr] *= ar;
-        }
-      }
-      bf16x8 ph, pl;
-      split_bf16(p, ph, pl);
-#pragma unroll
-      for (int nb = 0; nb < 8; ++nb) {
-        o[r][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vt[nb], o[r][nb], 0, 0, 0);
-        o[r][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vt[nb], o[r][nb], 0, 0, 0);
-      }
-    }
+    if (j + kRowBufs - 2 < nT) issue(j + kRowBufs - 2, dma);
+    if (!live) return;
+    f32x16 n0, n1;
+    qk(cur, n0, n1);
+    if (j > 0) softmax_pv(s_cur0, s_cur1, prev);
+    s_cur0 = n0;
+    s_cur1 = n1;
   };
 
   if (nT > 0) issue(0, buf0);
   if (nT > 1) issue(1, buf1);
   if (nT > 2) issue(2, buf2);
-  int i = 0;
-  for (; i + 4 <= nT; i += 4) {
-    step(i, buf0, buf3);
-    step(i + 1, buf1, buf0);
-    step(i + 2, buf2, buf1);
-    step(i + 3, buf3, buf2);
+  int j = 0;
+  for (; j + 5 <= nT; j += 5) {
+    step(j, buf0, buf4, buf3);
+    step(j + 1, buf1, buf0, buf4);
+    step(j + 2, buf2, buf1, buf0);
+    step(j + 3, buf3, buf2, buf1);
+    step(j + 4, buf4, buf3, buf2);
   }
-  if (i < nT) step(i, buf0, buf3);
-  if (i + 1 < nT) step(i + 1, buf1, buf0);
-  if (i + 2 < nT) step(i + 2, buf2, buf1);
+  if (j < nT) step(j, buf0, buf4, buf3);
+  if (j + 1 < nT) step(j + 1, buf1, buf0, buf4);
+  if (j + 2 < nT) step(j + 2, buf2, buf1, buf0);
+  if (j + 3 < nT) step(j + 3, buf3, buf2, buf1);
+  // the last tile's softmax and PV (its buffer is nT - 1 mod 5)
+  if (nT > 0 && live) {
+    switch ((nT - 1) % 5) {
+      case 0: softmax_pv(s_cur0, s_cur1, buf0); break;
+      case 1: softmax_pv(s_cur0, s_cur1, buf1); break;
+      case 2: softmax_pv(s_cur0, s_cur1, buf2); break;
+      case 3: softmax_pv(s_cur0, s_cur1, buf3); break;
+      default: softmax_pv(s_cur0, s_cur1, buf4); break;
+    }
+  }
 
-  // partials of this wave's row blocks, [unit][rows_pad]
-  const int64_t unit = (int64_t)blockIdx.x;
+  // partials of this wave's rows, [unit][rows_pad]; lanes j and j ^ 32 hold
+  // halves of row j % 32's sum and disjoint dims of its output
+  if (live) {
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run), false, false);
+    const float l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+    if (row < a.rows) {
+      const int64_t rbase = (int64_t)blockIdx.x * a.rows_pad + row;
+      float* po = a.part_o + rbase * kHeadDim + 4 * (lane >> 5);
 #pragma unroll
-  for (int r = 0; r < RBW; ++r) {
-    if (!rb_live[r]) continue;
-    float l = l_run[r];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int64_t rbase = unit * a.rows_pad + (wave + 4 * r) * 16;
+      for (int n = 0; n < 4; ++n)
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr)
-#pragma unroll
-      for (int nb = 0; nb < 8; ++nb) a.part_o[(rbase + 4 * kg + rr) * kHeadDim + 16 * nb + n16] = o[r][nb][rr];
-    if (kg == 0) {
-      a.part_ml[(rbase + n16) * 2 + 0] = m_run[r];
-      a.part_ml[(rbase + n16) * 2 + 1] = l;
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<float4*>(po + 32 * n + 8 * q) =
+              make_float4(o[n][4 * q], o[n][4 * q + 1], o[n][4 * q + 2], o[n][4 * q + 3]);
+      if (lane < 32) {
+        a.part_ml[rbase * 2 + 0] = m_run;
+        a.part_ml[rbase * 2 + 1] = l;
+      }
     }
   }
 }
@@ -601,10 +660,8 @@ attn_combine_kernel(SeqTable t, AttnArgs a) {
 template <int C>
 hipError_t launch_c(const SeqTable& t, const AttnArgs& a, hipStream_t s) {
   const dim3 grid(t.wg_off[t.batch]);
-  if (a.rows > 4 * 16)
-    hipLaunchKernelGGL((attn_rows_kernel<C, 2>), grid, dim3(kThreads), 0, s, t, a);
-  else if (a.rows > 16)
-    hipLaunchKernelGGL((attn_rows_kernel<C, 1>), grid, dim3(kThreads), 0, s, t, a);
+  if (a.rows > 16)
+    hipLaunchKernelGGL((attn_rows_kernel<C>), grid, dim3(kThreads), 0, s, t, a);
   else
     hipLaunchKernelGGL((attn_split_kernel<C>), grid, dim3(kThreads), 0, s, t, a);
   const hipError_t e = hipGetLastError();
