@@ -657,6 +657,65 @@ attn_combine_kernel(SeqTable t, AttnArgs a) {
   if (tid == 0 && a.lse != nullptr) a.lse[orow] = (M + __log2f(L)) * kLn2;
 }
 
+// Few splits per row (at most kFewSplits): one thread per (output row, float4
+// slice of the head dim) walks every split itself -- (m, l) of all splits for
+// M and L, then its own O slices -- so a row needs no cross-thread reduction
+// and a 256-thread workgroup merges 8 rows.  Same arithmetic order for every
+// thread of a row, so results stay bitwise reproducible.
+constexpr int kFewSplits = 16;
+
+__global__ void __launch_bounds__(kThreads)
+attn_combine_few_kernel(SeqTable t, AttnArgs a, int n_rows) {
+  constexpr int kSlices = kHeadDim / 4;
+  const int gid = blockIdx.x * kThreads + threadIdx.x;
+  const int orow = gid / kSlices, slice = gid % kSlices;
+  if (orow >= n_rows) return;
+  const int G = a.group;
+  const int rows_per_b = a.n_qtok * a.n_q_heads;
+  const int b = orow / rows_per_b;
+  const int rem = orow - b * rows_per_b;
+  const int tq = rem / a.n_q_heads, h = rem - tq * a.n_q_heads;
+  const int g = h / G, r = tq * G + h % G;  // row within the (b, g) group
+  const int ns = min(t.nsplit[b], kFewSplits);
+  const int64_t unit0 = (int64_t)t.wg_off[b] + (int64_t)g * ns;
+  const int64_t rows_pad = a.rows_pad;
+  const float2* ml = reinterpret_cast<const float2*>(a.part_ml) + unit0 * rows_pad + r;
+  const float* po = a.part_o + (unit0 * rows_pad + r) * kHeadDim + 4 * slice;
+  float2 v[kFewSplits];
+  float4 ov[kFewSplits];
+#pragma unroll
+  for (int sp = 0; sp < kFewSplits; ++sp) {
+    if (sp < ns) {
+      v[sp] = ml[sp * rows_pad];
+      ov[sp] = *reinterpret_cast<const float4*>(po + sp * rows_pad * kHeadDim);
+    }
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int sp = 0; sp < kFewSplits; ++sp)
+    if (sp < ns) M = fmaxf(M, v[sp].x);
+  float L = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int sp = 0; sp < kFewSplits; ++sp) {
+    if (sp < ns && v[sp].x != -INFINITY) {
+      const float w = fast_exp2(v[sp].x - M);
+      L += w * v[sp].y;
+      acc.x += w * ov[sp].x;
+      acc.y += w * ov[sp].y;
+      acc.z += w * ov[sp].z;
+      acc.w += w * ov[sp].w;
+    }
+  }
+  const float invL = 1.f / L;
+  acc.x *= invL;
+  acc.y *= invL;
+  acc.z *= invL;
+  acc.w *= invL;
+  *reinterpret_cast<float4*>(a.out + (int64_t)orow * kHeadDim + 4 * slice) = acc;
+  if (slice == 0 && a.lse != nullptr) a.lse[orow] = (M + __log2f(L)) * kLn2;
+}
+
 template <int C>
 hipError_t launch_c(const SeqTable& t, const AttnArgs& a, hipStream_t s) {
   const dim3 grid(t.wg_off[t.batch]);
@@ -666,8 +725,16 @@ hipError_t launch_c(const SeqTable& t, const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((attn_split_kernel<C>), grid, dim3(kThreads), 0, s, t, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(t.batch * a.n_qtok * a.n_q_heads), dim3(kThreads), 0, s, t,
-                     a);
+  const int n_rows = t.batch * a.n_qtok * a.n_q_heads;
+  int ns_max = 0;
+  for (int b = 0; b < t.batch; ++b) ns_max = max(ns_max, t.nsplit[b]);
+  if (ns_max <= kFewSplits) {
+    const int per_wg = kThreads / (kHeadDim / 4);
+    hipLaunchKernelGGL(attn_combine_few_kernel, dim3((n_rows + per_wg - 1) / per_wg), dim3(kThreads), 0, s, t,
+                       a, n_rows);
+  } else {
+    hipLaunchKernelGGL(attn_combine_kernel, dim3(n_rows), dim3(kThreads), 0, s, t, a);
+  }
   return hipGetLastError();
 }
 

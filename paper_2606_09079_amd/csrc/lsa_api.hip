@@ -79,7 +79,7 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   t.batch = B;
   t.n_lookahead = p->n_lookahead;
   const int C = p->chunk_size;
-  const int srows = score_rows_per_wg(p->emb_dtype, p->emb_dim);
+  const int srows = score_rows_per_wg(p->emb_dtype, p->emb_dim, p->n_lookahead);
   P.group = G;
   P.rows = rows;
   P.rows_pad = (rows + 15) / 16 * 16;  // partial rows per unit: whole 16-row MFMA blocks

@@ -77,7 +77,7 @@ __device__ __forceinline__ uint32_t order_key(uint32_t bits) {
 // keys == true writes order keys instead of scores (for the fused step).
 hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
                         const void* E, void* scores, bool keys, hipStream_t s);
-int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim);
+int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim, int32_t n_lookahead);
 
 // keys_ready == true: `scores` holds keys written by launch_score(keys = true).
 hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, bool keys_ready, const void* scores,

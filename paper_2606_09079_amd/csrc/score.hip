@@ -128,6 +128,77 @@ score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restri
   }
 }
 
+// Several lookahead queries with bf16 embeddings: the scores of a sequence are
+// the product S^T = E qe^T of its [n_b x D] chunk embeddings with the [D x Q]
+// query embeddings, a real dense contraction, so it runs on
+// v_mfma_f32_16x16x32_bf16: each wave takes 16 chunks (A operand: 16 rows of E,
+// 32 dims per step, loaded straight from HBM) against all Q <= 16 queries
+// (B operand, in registers), D / 32 steps.  E is still read exactly once.
+constexpr int kMfmaMinQueries = 4;
+constexpr int kMfmaRowsPerWg = 64;  // 4 waves x 16 chunks
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int D, bool KEYS>
+__global__ void __launch_bounds__(kThreads)
+score_mfma_kernel(SeqTable t, const uint16_t* __restrict__ qe, const uint16_t* __restrict__ E,
+                  uint32_t* __restrict__ scores) {
+  constexpr int kSteps = D / 32;
+  const int wg = blockIdx.x;
+  int b = 0;
+  while (wg >= t.score_wg_off[b + 1]) ++b;
+  const int n = t.n[b], Q = t.n_lookahead;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c0 = (wg - t.score_wg_off[b]) * kMfmaRowsPerWg + wave * 16;
+  if (c0 >= n) return;
+  // A operand rows: chunk c0 + lane % 16 (clamped; its scores are not stored)
+  const int crow = min(c0 + (lane & 15), n - 1);
+  const uint16_t* er = E + (t.chunk_off[b] + crow) * (int64_t)D + 8 * (lane >> 4);
+  bf16x8 ea[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st)
+    ea[st] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(er + 32 * st));
+  // B operand: query lane % 16 (zero beyond Q), dims 32 st + 8 (lane / 16) .. + 7
+  const int jq = lane & 15;
+  bf16x8 qb[kSteps];
+  const uint16_t* qp = qe + ((int64_t)b * Q + min(jq, Q - 1)) * D + 8 * (lane >> 4);
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st)
+    qb[st] = jq < Q ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qp + 32 * st)) : bf16x8{};
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ea[st], qb[st], acc, 0, 0, 0);
+  // acc[r] = score of chunk c0 + 4 (lane / 16) + r for query lane % 16
+  if (jq < Q) {
+    uint32_t* out = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)jq * n;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int c = c0 + 4 * (lane >> 4) + r;
+      uint32_t bits = __float_as_uint(acc[r]);
+      if constexpr (KEYS) bits = order_key<kKeysFromF32>(bits);
+      if (c < n) out[c] = bits;
+    }
+  }
+}
+
+template <int D>
+hipError_t launch_mfma_d(const SeqTable& t, const void* qe, const void* E, void* scores, bool keys, hipStream_t s) {
+  const int grid = t.score_wg_off[t.batch];
+  const auto* q16 = static_cast<const uint16_t*>(qe);
+  const auto* e16 = static_cast<const uint16_t*>(E);
+  auto* out = static_cast<uint32_t*>(scores);
+  if (keys)
+    hipLaunchKernelGGL((score_mfma_kernel<D, true>), dim3(grid), dim3(kThreads), 0, s, t, q16, e16, out);
+  else
+    hipLaunchKernelGGL((score_mfma_kernel<D, false>), dim3(grid), dim3(kThreads), 0, s, t, q16, e16, out);
+  return hipGetLastError();
+}
+
+bool use_mfma(int32_t emb_dtype, int32_t n_lookahead) {
+  return emb_dtype == LSA_BF16 && n_lookahead >= kMfmaMinQueries;
+}
+
 template <int DT, int D>
 hipError_t launch_dt_d(const SeqTable& t, const void* qe, const void* E, void* scores, bool keys, hipStream_t s) {
   const int grid = t.score_wg_off[t.batch];
@@ -166,7 +237,8 @@ int rows_dt(int32_t D) {
 
 }  // namespace
 
-int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim) {
+int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim, int32_t n_lookahead) {
+  if (use_mfma(emb_dtype, n_lookahead)) return kMfmaRowsPerWg;
   switch (emb_dtype) {
     case LSA_F32: return rows_dt<LSA_F32>(emb_dim);
     case LSA_BF16: return rows_dt<LSA_BF16>(emb_dim);
@@ -177,6 +249,15 @@ int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim) {
 
 hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
                         const void* E, void* scores, bool keys, hipStream_t s) {
+  if (use_mfma(emb_dtype, t.n_lookahead)) {
+    switch (emb_dim) {
+      case 64: return launch_mfma_d<64>(t, qe, E, scores, keys, s);
+      case 128: return launch_mfma_d<128>(t, qe, E, scores, keys, s);
+      case 256: return launch_mfma_d<256>(t, qe, E, scores, keys, s);
+      case 512: return launch_mfma_d<512>(t, qe, E, scores, keys, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (emb_dtype) {
     case LSA_F32: return launch_dt<LSA_F32>(t, emb_dim, qe, E, scores, keys, s);
     case LSA_BF16: return launch_dt<LSA_BF16>(t, emb_dim, qe, E, scores, keys, s);
