@@ -9,6 +9,8 @@ dim 256.  Four query sets (query embedding and attention query) rotate from
 step to step so that each step keeps a different chunk set and the 256 MB
 Infinity Cache cannot serve a previous step's bytes.
 
+The other workloads (``--workload``) use the same loop, for profiling.
+
 Prints one JSON line: steps/s, plus a ``roofline`` object for the dominant
 kernel (sparse attention: algorithmic bytes = kept K/V + q + out, divided by
 its HIP-event-timed average launch duration on the launch stream) and a
@@ -35,7 +37,17 @@ HBM_PEAK_GBS = 8000.0
 WORKLOADS = {
     "paper1m": "paper1m: 1,048,576-token context, 64-token chunks (16,384), keep 1,638 (10%), "
                "32 query / 8 KV heads, head_dim 128, bf16 K/V, bf16 indexer dim 256, batch 1",
+    "lookahead": "lookahead: 8 sequences x 1,048,576 tokens, 128-token chunks (8,192 each), 16 lookahead "
+                 "query embeddings, union of per-query top-512, 16 query tokens, 64 query / 8 KV heads, "
+                 "head_dim 128, bf16 K/V, bf16 indexer dim 256",
+    "batch32": "batch32: 32 sequences, log-uniform 32K-512K tokens, 64-token chunks, keep 13.5%, "
+               "32 query / 8 KV heads, head_dim 128, bf16 K/V, bf16 indexer dim 256",
+    "int8": "int8: 4 sequences x 131,072 tokens, 64-token chunks (2,048 each), keep 256, 32 query / 8 KV heads, "
+            "head_dim 128, bf16 K/V, int8 indexer dim 256",
+    "tiny": "tiny: 4,096 tokens, 64-token chunks (64), keep 8, 8 query / 8 KV heads, head_dim 128, bf16 K/V, "
+            "fp32 indexer dim 256",
 }
+EMB_BYTES = {"f32": 4, "bf16": 2, "i8": 1}
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "attn_kernel_paper1m_traffic.md")
 
 
@@ -168,10 +180,10 @@ def main() -> int:
     C, Hkv = prob.chunk, prob.n_kv_heads
     kv_bytes = [n * C * Hkv * d * 2 * 2 for n in counts]
     attn_bytes = sum(kv_bytes) / len(kv_bytes) + B * Tq * Hq * d * (2 + 4) + B * Tq * Hq * 4 + max(counts) * 4
-    emb_bytes = prob.total_chunks * prob.emb_dim * 2 + B * prob.n_lookahead * prob.emb_dim * 2
+    emb_bytes = (prob.total_chunks + B * prob.n_lookahead) * prob.emb_dim * EMB_BYTES[prob.emb_dtype]
     step_bytes = attn_bytes + emb_bytes
     achieved = attn_bytes / (att_avg_us * 1e-6) / 1e9
-    traffic = measured_traffic()
+    traffic = measured_traffic() if args.workload == "paper1m" else None
 
     result = {
         "metric": METRIC,
@@ -236,9 +248,12 @@ def cpu_baseline(prob, host, budget_s: float):
         el = time.perf_counter() - t0
         if el >= budget_s or el / reps * (reps + 1) > 3 * budget_s:
             break
+    full = prob.batch == 1 and prob.n_qtok == 1
+    what = ("full step(s) of the same workload" if full else
+            "step(s) of sequence 0 of the same workload, attention for its first query token only")
     return {"value": round(reps / el, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{reps} full step(s) of the same 1M-token workload (score 16,384 chunks, top-k 1,638, "
-                      f"fp64 attention for all 32 query heads) in {el:.1f}s; KV-head groups on {threads} threads"}
+            "sample": f"{reps} {what} (score {prob.n_chunks[0]:,} chunks, top-{prob.keep[0]:,}, fp64 attention "
+                      f"for {prob.n_q_heads} query heads) in {el:.1f}s; KV-head groups on {threads} threads"}
 
 
 if __name__ == "__main__":
