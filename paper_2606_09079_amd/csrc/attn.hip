@@ -7,33 +7,40 @@
 // a contiguous, equal share of them; the split count is sized so that the whole
 // grid is one resident round on MI355X (256 CUs x 2 workgroups).  All G * Tq
 // query rows that read KV head g are handled by the same workgroup, so every
-// K/V byte is fetched from HBM once.  Both products run on
-// v_mfma_f32_16x16x32_bf16:
+// K/V byte is fetched from HBM once.  Logits, the running max / sum and O stay
+// fp32; the softmax weights P enter the PV product as bf16 hi + lo parts (two
+// MFMAs per product), which keeps ~16 significant bits.
+//
+// attn_split_kernel (rows <= 16) on v_mfma_f32_16x16x32_bf16.  The 4 waves of
+//   a workgroup take consecutive quarters of the split's tiles, each streaming
+//   its own tiles straight into registers (1 KiB per load instruction,
+//   nontemporal hint, two tiles in flight per wave), and merge their (m, l, O)
+//   states through LDS.
 //   * QK computes S^T = K Q^T with 16 tokens as M and 16 query rows as N.  The
 //     cache stores each (chunk, head) block in MFMA operand order, and the M
 //     rows of the two 16-token MFMAs of a tile are tokens 8a+0..3 and 8a+4..7,
 //     so after the product each lane holds the 8 consecutive tokens
 //     8*(lane/16)..+7 of query row lane%16 -- the A-operand layout PV needs.
 //   * PV computes O = P V with the tile's 32 tokens as K and 16 head dims per
-//     MFMA as N.  P is split into bf16 hi + lo parts (two MFMAs), keeping ~16
-//     significant bits; logits, the running max / sum and O stay fp32.
+//     MFMA as N.
+// attn_rows_kernel (17..128 rows) on v_mfma_f32_32x32x16_bf16.  Every wave
+//   owns 32 rows and needs every tile, so each tile is copied once per
+//   workgroup from HBM into LDS (global->LDS copies into MFMA operand order,
+//   three tiles ahead, five 16 KiB buffers).  QK computes S^T = K Q^T and PV
+//   computes O^T = V^T P^T, so a lane's O registers all belong to its own row
+//   and the softmax rescale needs no exchange; the QK products of tile j are
+//   issued before the softmax and PV of tile j - 1, so VALU and MFMA overlap.
 //
-// attn_split_kernel (rows <= 16): the 4 waves of a workgroup take consecutive
-//   quarters of the split's tiles, each streaming its own tiles straight into
-//   registers (1 KiB per load instruction, nontemporal hint, two tiles in
-//   flight per wave), and merge their (m, l, O) states through LDS.
-// attn_rows_kernel (rows > 16): every wave owns one or two 16-row blocks and
-//   needs every tile, so tiles are staged once per workgroup in LDS by
-//   global->LDS copies, two tiles ahead, with three workgroups per CU, and
-//   each wave writes its own rows.
-//
-// attn_combine_kernel -- one workgroup per output row (b, t, h) merges the
-//   splits of its (b, g): weights exp2(m_s - M), O as the weighted sum of the
-//   split outputs, divided by L = sum_s exp2(m_s - M) l_s.  Every wave computes
-//   M and L itself from all splits' (m, l), so the loads of (m, l) and of the
-//   thread's O slices go out in one round and only the final merge of the 8
-//   split groups needs a barrier.  The summation order is fixed, so results
-//   are bitwise reproducible.
+// attn_combine_kernel (more than 16 splits) -- one workgroup per output row
+//   (b, t, h) merges the splits of its (b, g): weights exp2(m_s - M), O as the
+//   weighted sum of the split outputs, divided by L = sum_s exp2(m_s - M) l_s.
+//   Every wave computes M and L itself from all splits' (m, l), so the loads of
+//   (m, l) and of the thread's O slices go out in one round and only the final
+//   merge of the 8 split groups needs a barrier.
+// attn_combine_few_kernel (at most 16 splits) -- the same merge with one thread
+//   per (output row, float4 slice of O) walking every split itself.
+// The summation order of both combines is fixed, so results are bitwise
+// reproducible.
 #include "lsa_internal.h"
 
 namespace lsa {

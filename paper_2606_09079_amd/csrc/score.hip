@@ -12,6 +12,8 @@
 //   F32 : fp32 FMA accumulation
 //   BF16: bf16 widened to fp32 (exact), fp32 FMA accumulation
 //   I8  : v_dot4 int8 -> int32, exact (|s| <= D * 127^2 < 2^31 for D <= 512)
+// With bf16 embeddings and at least 4 lookahead queries the same product is a
+// dense [n_b x D] x [D x Q] contraction and runs on MFMA (score_mfma_kernel).
 #include "lsa_internal.h"
 
 namespace lsa {
