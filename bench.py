@@ -90,6 +90,13 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="bound on the oracle sample's CPU time")
     ap.add_argument("--only", choices=["step", "attn"], default=None,
                     help="profiling aid: launch only this entry point in the timed loop")
+    ap.add_argument("--read-ceiling-mib", type=int, default=2048,
+                    help="size of the plain streaming read that measures the read-bandwidth ceiling "
+                         "(a multiple of 32; 0: skip)")
+    ap.add_argument("--flush-mib", type=int, default=None,
+                    help="untimed streaming read between the per-step samples of the step-time distribution, "
+                         "so that the 256 MB Infinity Cache cannot serve a previous step's bytes "
+                         "(a multiple of 32; default: 1024 for workloads below 1 GB per step, else 0)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="profiling aid: also run one plain copy of this many MiB (known bytes)")
     args = ap.parse_args()
@@ -171,6 +178,18 @@ def main() -> int:
     ms_per_step = ms_total / args.steps
     log(f"[bench] timed {args.steps} x {fn.__name__}: {ms_per_step * 1e3:.2f} us/step (wall {wall:.3f}s)")
 
+    # ---- distribution of single-step times (HIP events around each step, outside
+    # the timed region), with an optional untimed cache flush between samples
+    flush_mib = args.flush_mib
+    sink = torch.empty(synth.read_sink_words(), dtype=torch.int32, device="cuda")
+    n_dist = max(args.steps, 100)
+    dist_bufs = None
+    step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_dist)]
+
+    def flush() -> None:
+        if dist_bufs is not None:
+            synth.read_device(dist_bufs.data_ptr(), dist_bufs.numel(), sink.data_ptr(), stream.cuda_stream)
+
     # ---- dominant kernel: per-launch HIP events around the attention launch
     n_att = max(args.steps, 20)
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_att)]
@@ -183,6 +202,39 @@ def main() -> int:
     att_avg_us = 1e3 * sum(att_ms) / len(att_ms)
 
     counts = [int(c.cpu().sum()) for c in cnts]
+    C_, Hkv_ = prob.chunk, prob.n_kv_heads
+    approx_step_bytes = sum(counts) / len(counts) * C_ * Hkv_ * d * 4
+    if flush_mib is None:
+        flush_mib = 1024 if approx_step_bytes < 1e9 else 0
+    if flush_mib:
+        dist_bufs = torch.empty(flush_mib << 20, dtype=torch.uint8, device="cuda")
+    fn_dist = attn if args.only == "attn" else step
+    for i in range(n_dist):
+        flush()
+        step_ev[i][0].record(stream)
+        fn_dist(i)
+        step_ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    step_us = sorted(1e3 * a.elapsed_time(b) for a, b in step_ev)
+
+    def pct(p: float) -> float:
+        return round(step_us[min(len(step_us) - 1, int(p * len(step_us)))], 2)
+
+    dist_bufs = None
+
+    # ---- read-bandwidth ceiling of this device: a plain streaming read
+    read_gbs = None
+    if args.read_ceiling_mib:
+        rbuf = torch.ones(args.read_ceiling_mib << 20, dtype=torch.uint8, device="cuda")
+        rev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(6)]
+        for a_, b_ in rev:
+            a_.record(stream)
+            synth.read_device(rbuf.data_ptr(), rbuf.numel(), sink.data_ptr(), stream.cuda_stream)
+            b_.record(stream)
+        torch.cuda.synchronize()
+        best_ms = min(a_.elapsed_time(b_) for a_, b_ in rev[1:])
+        read_gbs = rbuf.numel() / (best_ms * 1e-3) / 1e9
+        del rbuf
     C, Hkv = prob.chunk, prob.n_kv_heads
     kv_bytes = [n * C * Hkv * d * 2 * 2 for n in counts]
     attn_bytes = sum(kv_bytes) / len(kv_bytes) + B * Tq * Hq * d * (2 + 4) + B * Tq * Hq * 4 + max(counts) * 4
@@ -208,10 +260,15 @@ def main() -> int:
                    "parallelism": "single GPU", "kept_chunks_per_step": counts[0], "rotations": len(rot)},
         "step_gbs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "step_roofline_frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "step_us": {"p10": pct(0.10), "median": pct(0.50), "p90": pct(0.90), "samples": n_dist,
+                    "flush_mib_between_samples": flush_mib},
+        "read_ceiling_gbs": round(read_gbs, 1) if read_gbs else None,
+        "step_frac_of_read_ceiling": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / read_gbs, 4) if read_gbs else None,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "attn_kernel (lsa_sparse_decode_attn)", "avg_launch_us": round(att_avg_us, 2),
-                     "algorithmic_bytes_per_launch": int(attn_bytes)},
+                     "algorithmic_bytes_per_launch": int(attn_bytes),
+                     "frac_of_read_ceiling": round(achieved / read_gbs, 4) if read_gbs else None},
     }
 
     if not args.no_cpu_baseline:

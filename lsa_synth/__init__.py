@@ -327,6 +327,9 @@ def dev_lib() -> ctypes.CDLL:
         lib.synth_fill_kv_device.restype = ctypes.c_int
         lib.synth_copy_device.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
         lib.synth_copy_device.restype = ctypes.c_int
+        lib.synth_read_device.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        lib.synth_read_device.restype = ctypes.c_int
+        lib.synth_read_sink_words.restype = ctypes.c_int
         _dev_lib = lib
     return _dev_lib
 
@@ -363,6 +366,18 @@ def copy_device(src_ptr: int, dst_ptr: int, nbytes: int, stream_ptr: int) -> Non
     rc = dev_lib().synth_copy_device(src_ptr, dst_ptr, nbytes, stream_ptr)
     if rc != 0:
         raise RuntimeError(f"synth_copy_device failed with code {rc}")
+
+
+def read_device(src_ptr: int, nbytes: int, sink_ptr: int, stream_ptr: int) -> None:
+    """A plain streaming read of known size (for the read-bandwidth ceiling);
+    ``sink`` holds :func:`read_sink_words` uint32 words of device memory."""
+    rc = dev_lib().synth_read_device(src_ptr, nbytes, sink_ptr, stream_ptr)
+    if rc != 0:
+        raise RuntimeError(f"synth_read_device failed with code {rc}")
+
+
+def read_sink_words() -> int:
+    return int(dev_lib().synth_read_sink_words())
 
 
 def device_inputs(prob: Problem, seed: int, device: str = "cuda", host: Optional[Dict[str, object]] = None):

@@ -74,7 +74,45 @@ __global__ void __launch_bounds__(256) copy16(const uint4* __restrict__ src, uin
     dst[i] = src[i];
 }
 
+// Plain streaming read, used only to measure the read-bandwidth ceiling of
+// the device.  Workgroup g reads its own contiguous slice; per step a wave
+// loads 4 x 1 KiB (nontemporal 16-byte loads), two steps in flight.  Each
+// workgroup folds what it read into one word of `sink`, so the loads cannot be
+// dropped.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kReadBlocks = 1024;
+constexpr int64_t kReadStep16 = 1024;  // 16 KiB per workgroup step, in 16-byte units
+__global__ void __launch_bounds__(256) read16(const u32x4* __restrict__ src, int64_t per_wg16, uint32_t* __restrict__ sink) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const u32x4* base = src + (int64_t)blockIdx.x * per_wg16 + w * 256 + lane;
+  const int64_t steps = per_wg16 / kReadStep16;  // even: the host checks
+  uint32_t acc = 0;
+  for (int64_t i = 0; i < steps; i += 2) {
+    u32x4 v[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = __builtin_nontemporal_load(base + i * kReadStep16 + q * 64);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[4 + q] = __builtin_nontemporal_load(base + (i + 1) * kReadStep16 + q * 64);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc ^= v[q].x ^ v[q].y ^ v[q].z ^ v[q].w;
+  }
+  acc |= __shfl_xor(acc, 1);
+  if (threadIdx.x == 0) sink[blockIdx.x] = acc;
+}
+
 }  // namespace
+
+// Returns 0 on success, 1 on a bad argument (bytes must be a positive
+// multiple of 32 MiB), 2 on a HIP launch error.  `sink` must hold
+// synth_read_sink_words() words.
+extern "C" int synth_read_sink_words() { return kReadBlocks; }
+extern "C" int synth_read_device(const void* src, int64_t bytes, uint32_t* sink, void* stream) {
+  constexpr int64_t kUnit = (int64_t)kReadBlocks * 2 * kReadStep16 * 16;
+  if (!src || !sink || bytes <= 0 || bytes % kUnit != 0 || (reinterpret_cast<uintptr_t>(src) & 15)) return 1;
+  hipLaunchKernelGGL(read16, dim3(kReadBlocks), dim3(256), 0, (hipStream_t)stream, static_cast<const u32x4*>(src),
+                     bytes / 16 / kReadBlocks, sink);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 extern "C" int synth_copy_device(const void* src, void* dst, int64_t bytes, void* stream) {
   if (!src || !dst || bytes <= 0 || bytes % 16 != 0) return 1;
