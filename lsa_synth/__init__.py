@@ -35,6 +35,7 @@ _DEV_SO = os.path.join(_HERE, "libsynth_dev.so")
 
 GAMMA = 0x9E3779B97F4A7C15
 STREAM_K, STREAM_V, STREAM_Q, STREAM_E, STREAM_QE, STREAM_LEN, STREAM_QE_NOISE = 1, 2, 3, 4, 5, 6, 7
+STREAM_IDX_Q, STREAM_IDX_K, STREAM_IDX_W = 8, 9, 10
 M64 = (1 << 64) - 1
 
 
@@ -138,6 +139,13 @@ class Problem:
     planted: int = 0                 # planted relevant chunks per sequence
     q_scale: float = 1.0             # multiplier applied to q before rounding to bf16
     qe_rho: float = 0.95             # correlation of lookahead query embeddings
+    # recall path (full Memory Indexer): layers OR-ed together (0 = not used),
+    # indexer heads per layer, index-key width, and the fraction of entries each
+    # layer's gate weights are drawn to recall; keep[b] is then the bound K_max
+    idx_layers: int = 0
+    idx_heads: int = 64
+    idx_dim: int = 128
+    idx_rate: float = 0.05
     meta: Dict[str, object] = field(default_factory=dict)
 
     @property
@@ -200,10 +208,21 @@ def make_problem(name: str, seed: int = 0) -> Problem:
     if name == "lookahead":
         return Problem("lookahead", [1048576] * 8, 128, [512] * 8, 64, 8, emb_dtype="bf16",
                        n_lookahead=16, n_qtok=16, planted=0)
+    if name == "recall_tiny":
+        return Problem("recall_tiny", [4096], 64, [12], 8, 8, emb_dtype="bf16", idx_layers=3, idx_heads=16,
+                       idx_dim=64, idx_rate=0.05)
+    if name == "recall_batch":
+        return Problem("recall_batch", [131072] * 4, 64, [2048] * 4, 32, 8, emb_dtype="bf16", idx_layers=2,
+                       idx_heads=32, idx_dim=128, idx_rate=0.08)
+    if name == "recall1m":
+        n = 1048576 // 64
+        return Problem("recall1m", [1048576], 64, [int(0.10 * n)], 32, 8, emb_dtype="bf16", idx_layers=3,
+                       idx_heads=64, idx_dim=128, idx_rate=0.05)
     raise KeyError(name)
 
 
 PRESETS = ("tiny", "int8", "paper1m", "batch32", "lookahead")
+RECALL_PRESETS = ("recall_tiny", "recall_batch", "recall1m")
 
 
 # ------------------------------------------------------------ host inputs
@@ -219,12 +238,53 @@ def _store(x64: np.ndarray, dtype: str) -> np.ndarray:
     raise ValueError(dtype)
 
 
+def _gate_shift(g: np.ndarray, sig: np.ndarray, rate: float) -> float:
+    """Shift beta of gate weights w_h = g_h - beta such that, for random unit
+    index keys, sum_h w_h ReLU(z_h) with independent z_h ~ N(0, sig_h^2) is >= 0
+    with probability about ``rate`` (normal approximation of the sum; the
+    realised recall is whatever the drawn keys give)."""
+    z = statistics.NormalDist().inv_cdf(1.0 - rate)
+    mean_relu = sig / math.sqrt(2.0 * math.pi)
+    var_relu = sig * sig * (0.5 - 1.0 / (2.0 * math.pi))
+
+    def f(beta: float) -> float:
+        w = g - beta
+        return float((w * mean_relu).sum()) + z * math.sqrt(float((w * w * var_relu).sum()))
+
+    lo, hi = -100.0, 100.0
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if f(mid) > 0.0:
+            lo = mid
+        else:
+            hi = mid
+    return 0.5 * (lo + hi)
+
+
+def _recall_inputs(prob: Problem, seed: int) -> Dict[str, np.ndarray]:
+    """Indexer queries [B][L][n_h][c] (bf16 bits, N(0, 1)), gate weights
+    [B][L][n_h] (float32) and unit-norm index keys [L][sum n_b][c] (bf16 bits)."""
+    B, L, H, c = prob.batch, prob.idx_layers, prob.idx_heads, prob.idx_dim
+    n = prob.total_chunks
+    q = normal_bf16(stream_key(seed, STREAM_IDX_Q), 0, B * L * H * c).reshape(B, L, H, c)
+    K = f64_to_bf16_bits(_unit_rows(normal_f64(stream_key(seed, STREAM_IDX_K), 0, L * n * c).reshape(L * n, c)))
+    g = normal_f64(stream_key(seed, STREAM_IDX_W), 0, B * L * H).reshape(B, L, H)
+    qf = bf16_bits_to_f64(q)
+    w = np.empty((B, L, H), dtype=np.float32)
+    for b in range(B):
+        for l in range(L):
+            sig = np.linalg.norm(qf[b, l], axis=-1) / math.sqrt(c)
+            w[b, l] = (g[b, l] - _gate_shift(g[b, l], sig, prob.idx_rate)).astype(np.float32)
+    return {"idx_q": q, "idx_w": w, "idx_k": K.reshape(L, n, c)}
+
+
 def host_inputs(prob: Problem, seed: int) -> Dict[str, object]:
     """Small tensors of one step, generated on the host.
 
     Returns ``qe`` [B][Q][D], ``E`` [sum n_b][D] (float32, bf16 bits as uint16,
     or int8), ``q`` [B][Tq][Hq][d] bf16 bits and ``planted`` (list of global-
-    per-sequence chunk ids).
+    per-sequence chunk ids); with ``idx_layers > 0`` also the recall inputs
+    ``idx_q``, ``idx_w`` and ``idx_k`` of :func:`_recall_inputs`.
     """
     B, Q, D = prob.batch, prob.n_lookahead, prob.emb_dim
     offs = prob.chunk_offsets
@@ -256,7 +316,10 @@ def host_inputs(prob: Problem, seed: int) -> Dict[str, object]:
     if prob.q_scale != 1.0:
         q = f64_to_bf16_bits(bf16_bits_to_f64(q) * prob.q_scale)
     q = q.reshape(B, prob.n_qtok, prob.n_q_heads, prob.head_dim)
-    return {"qe": qe, "E": E, "q": q, "planted": planted}
+    out = {"qe": qe, "E": E, "q": q, "planted": planted}
+    if prob.idx_layers > 0:
+        out.update(_recall_inputs(prob, seed))
+    return out
 
 
 # ------------------------------------------------------------ K/V on host
@@ -402,7 +465,11 @@ def device_inputs(prob: Problem, seed: int, device: str = "cuda", host: Optional
     stream = torch.cuda.current_stream(device).cuda_stream
     fill_kv_device(prob, seed, "k", k.data_ptr(), table.data_ptr(), stream)
     fill_kv_device(prob, seed, "v", v.data_ptr(), table.data_ptr(), stream)
-    return {"qe": up(h["qe"]), "E": up(h["E"]), "q": up(h["q"]), "k": k, "v": v, "table": table, "host": h}
+    out = {"qe": up(h["qe"]), "E": up(h["E"]), "q": up(h["q"]), "k": k, "v": v, "table": table, "host": h}
+    for name in ("idx_q", "idx_w", "idx_k"):
+        if name in h:
+            out[name] = up(h[name])
+    return out
 
 
 # ------------------------------------------------------------------ build

@@ -10,7 +10,15 @@ step:
 * O2 select -- top-k with lowest-index tie-break, ascending output; union of the
   per-query sets for several lookahead queries (Sec. 2.1 Eq. 6 and
   Sec. 2.4 Eq. 13; K_max of Sec. 2.5 is the keep budget);
-* O3 attend -- softmax(q K^T * scale) V over the tokens of the kept chunks.
+* O3 attend -- softmax(q K^T * scale) V over the tokens of the kept chunks
+  (an empty kept set gives out = 0, lse = -inf).
+
+and, for the recall path, the full Memory Indexer in the paper's order:
+
+* R1 index score -- x = sum_h w_h ReLU(q_h . K_s) per indexer layer (the
+  argument of the sigmoid of Sec. 2.1 Eq. 4);
+* R2 recall -- sigmoid(x) >= 1/2 per layer (Eq. 5), OR over the layers
+  (Eq. 13), at most K_max entries (Sec. 2.5), then O3 over the recalled set.
 
 It shares no code with the HIP library; the only common input is the seeded
 generator in ``lsa_synth``.
@@ -54,6 +62,10 @@ def bind(path: str) -> ctypes.CDLL:
     L.oracle_union.restype = _I64
     L.oracle_attention.argtypes = [_P, _I32, _P, _P, _I64, _I32, _I32, _P, _I64, _F64, _P, _P]
     L.oracle_attention.restype = ctypes.c_int
+    L.oracle_index_score_bf16.argtypes = [_P, _P, _P, _I64, _I32, _I32, _P]
+    L.oracle_index_score_bf16.restype = None
+    L.oracle_recall.argtypes = [_P, _I32, _I64, _I64, _P]
+    L.oracle_recall.restype = _I64
     return L
 
 
@@ -140,6 +152,39 @@ def attention(q_rows: np.ndarray, Kh: np.ndarray, Vh: np.ndarray, sel: np.ndarra
     if rc != 0:
         raise ValueError("oracle_attention rejected its input")
     return out, lse
+
+
+# ------------------------------------------------------------ R1 / R2 recall
+def index_score(q: np.ndarray, w: np.ndarray, K: np.ndarray) -> np.ndarray:
+    """x[s] = sum_h w[h] ReLU(q[h] . K[s]) in float64 (Sec. 2.1 Eq. 4 before the
+    sigmoid).  q [n_h][c] and K [n][c] are bf16 bit patterns, w [n_h] float32."""
+    n_h, c = q.shape
+    n = K.shape[0]
+    q, K, w = _c(q, np.uint16), _c(K, np.uint16), _c(w, np.float32)
+    out = np.empty(n, dtype=np.float64)
+    lib().oracle_index_score_bf16(q.ctypes.data, w.ctypes.data, K.ctypes.data, n, n_h, c, out.ctypes.data)
+    return out
+
+
+def recall(x: np.ndarray, kmax: int) -> np.ndarray:
+    """Recalled entry ids, ascending, from the sigmoid arguments x [L][n]
+    (threshold 1/2 per layer, OR over layers, at most kmax entries)."""
+    x = _c(np.atleast_2d(x), np.float64)
+    L, n = x.shape
+    out = np.empty(n, dtype=np.int32)
+    m = lib().oracle_recall(x.ctypes.data, L, n, kmax, out.ctypes.data)
+    if m < 0:
+        raise ValueError(f"oracle_recall rejected L={L} n={n} kmax={kmax}")
+    return out[:m].copy()
+
+
+def recall_for_sequence(prob, inputs: Dict[str, object], b: int):
+    """R1 then R2 for sequence b: returns (x [L][n_b], recalled ascending ids)."""
+    lo, hi = prob.chunk_offsets[b], prob.chunk_offsets[b + 1]
+    L = prob.idx_layers
+    x = np.stack([index_score(inputs["idx_q"][b, l], inputs["idx_w"][b, l], inputs["idx_k"][l, lo:hi])
+                  for l in range(L)])
+    return x, recall(x, prob.keep[b])
 
 
 # ---------------------------------------------------------------- O4 step

@@ -23,7 +23,14 @@
  *    union of the per-query top-k sets (the set union of Eq. 13).
  *  - Attention (Sec. 2.1, core attention over the selected entries):
  *    softmax(q K^T * scale) V over the tokens of the kept chunks, with query
- *    head h reading KV head floor(h / G).
+ *    head h reading KV head floor(h / G).  An empty kept set gives out = 0 and
+ *    lse = -inf (the empty sum), which only the recall path below can produce.
+ *  - Recall (the full Memory Indexer of Sec. 2.1 Eq. 4, the threshold of Eq. 5,
+ *    the OR over indexer layers of Eq. 13 and the K_max bound of Sec. 2.5):
+ *    layer l recalls entry s when sigma(x_l(s)) >= 1/2 with
+ *    x_l(s) = sum_h w_h ReLU(q_h . K_s); the recalled set is the OR over the
+ *    layers; when it holds more than K_max entries, the K_max with the largest
+ *    max_l x_l(s) are kept (lower id first on ties).
  */
 #include <math.h>
 #include <stdint.h>
@@ -154,7 +161,12 @@ int64_t oracle_union(const int32_t* lists, int32_t n_lists, int64_t k, int64_t n
 int oracle_attention(const uint16_t* q, int32_t R, const uint16_t* Kh, const uint16_t* Vh,
                      int64_t n_tok, int32_t d, int32_t C, const int32_t* sel, int64_t nsel,
                      double scale, double* out, double* lse) {
-  if (R < 1 || d < 1 || C < 1 || nsel < 1) return -1;
+  if (R < 1 || d < 1 || C < 1 || nsel < 0) return -1;
+  if (nsel == 0) { /* nothing to attend: the empty sum */
+    for (int64_t i = 0; i < (int64_t)R * d; ++i) out[i] = 0.0;
+    for (int32_t r = 0; r < R; ++r) lse[r] = -INFINITY;
+    return 0;
+  }
   for (int64_t j = 0; j < nsel; ++j)
     if (sel[j] < 0 || (int64_t)(sel[j] + 1) * C > n_tok) return -1;
   const int64_t T = nsel * C;
@@ -188,4 +200,66 @@ int oracle_attention(const uint16_t* q, int32_t R, const uint16_t* Kh, const uin
   }
   free(logit);
   return 0;
+}
+
+/* ---------------------------------------------------------------- R recall */
+
+/*
+ * Gated multi-head index score of one indexer layer, the argument of the
+ * sigmoid in Sec. 2.1 Eq. 4:
+ *   x[s] = sum_h w[h] * ReLU(q[h] . K[s])
+ *   q [n_h][c] bf16 bits, w [n_h] float32, K [n][c] bf16 bits, x [n] float64.
+ */
+void oracle_index_score_bf16(const uint16_t* q, const float* w, const uint16_t* K, int64_t n, int32_t n_h,
+                             int32_t c, double* out) {
+  for (int64_t s = 0; s < n; ++s) {
+    double x = 0.0;
+    for (int32_t h = 0; h < n_h; ++h) {
+      double dot = 0.0;
+      for (int32_t i = 0; i < c; ++i) dot += bf16_to_f64(q[(int64_t)h * c + i]) * bf16_to_f64(K[s * c + i]);
+      const double relu = dot > 0.0 ? dot : 0.0;
+      x += (double)w[h] * relu;
+    }
+    out[s] = x;
+  }
+}
+
+/*
+ * Recall of the Memory Indexers of L layers over n entries (Sec. 2.1 Eq. 5,
+ * the OR of Eq. 13, the K_max bound of Sec. 2.5).  x [L][n] float64 holds the
+ * sigmoid arguments.  Layer l recalls entry s when sigma(x[l][s]) >= 1/2; the
+ * sigmoid is increasing with sigma(0) = 1/2, so that is exactly x[l][s] >= 0
+ * (-0.0 included), and taking it on x keeps the decision free of the rounding
+ * of a computed sigmoid.  An entry is recalled when any layer recalls it.  If
+ * more than kmax entries are recalled, the kmax with the largest max_l x[l][s]
+ * stay (lower id first on ties).  Writes the kept ids in ascending order and
+ * returns their count, 0 .. kmax, or -1 on a bad argument or allocation failure.
+ */
+int64_t oracle_recall(const double* x, int32_t L, int64_t n, int64_t kmax, int32_t* out) {
+  if (L < 1 || n <= 0 || kmax < 1) return -1;
+  scored_f* v = (scored_f*)malloc((size_t)n * sizeof *v);
+  if (!v) return -1;
+  int64_t m = 0;
+  for (int64_t s = 0; s < n; ++s) {
+    int recalled = 0;
+    double best = x[s];
+    for (int32_t l = 0; l < L; ++l) {
+      const double xl = x[(int64_t)l * n + s];
+      if (xl >= 0.0) recalled = 1;
+      if (xl > best) best = xl;
+    }
+    if (recalled) {
+      v[m].s = best;
+      v[m].c = s;
+      ++m;
+    }
+  }
+  if (m > kmax) {
+    qsort(v, (size_t)m, sizeof *v, by_score_desc_f);
+    m = kmax;
+  }
+  for (int64_t j = 0; j < m; ++j) out[j] = (int32_t)v[j].c;
+  free(v);
+  qsort(out, (size_t)m, sizeof *out, ascending_i32);
+  return m;
 }

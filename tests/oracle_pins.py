@@ -236,9 +236,132 @@ def pin_gqa_mapping():
         assert np.allclose(res[(0, h)][0], h // 4 + 1.0), f"head {h} must read KV head {h // 4}"
 
 
+def pin_attention_empty_set():
+    """An empty kept set (only the recall path can produce one) gives the empty
+    sum: out = 0 and lse = -inf."""
+    rng = np.random.default_rng(11)
+    K, V = _rand_head(rng, 16, 8)
+    out, lse = oracle.attention(_bf16(rng.standard_normal((3, 8))), K, V, np.array([], dtype=np.int32), 4)
+    assert np.array_equal(out, np.zeros((3, 8))), "empty set output"
+    assert np.all(np.isneginf(lse)), "empty set lse"
+
+
+# ------------------------------------------------------------------- recall
+def pin_recall_worked_example():
+    """Hand-worked two-layer example: scores, the threshold at exactly 0, the OR
+    over layers and the K_max bound."""
+    g = json.load(open(os.path.join(GOLDEN, "recall_worked.json")))
+    q, K = _bf16(g["q"]), _bf16(g["K"])
+    x = np.stack([oracle.index_score(q, np.array(w, dtype=np.float32), K) for w in g["w"]])
+    assert np.array_equal(x, np.array(g["x"])), "worked index scores"
+    for case in g["cases"]:
+        got = oracle.recall(x[case["layers"]], case["kmax"])
+        assert got.tolist() == case["kept"], f"worked recall {case}"
+
+
+def pin_index_score_single_head():
+    """One head with unit gate is ReLU of the dual-encoder dot product (the
+    already pinned O1 score); a gate w scales it by w."""
+    rng = np.random.default_rng(12)
+    K = _bf16(rng.standard_normal((40, 64)))
+    q = _bf16(rng.standard_normal((1, 64)))
+    dot = oracle.score(q[0], K, "bf16")
+    for w in (1.0, -0.75, 2.5):
+        x = oracle.index_score(q, np.array([w], dtype=np.float32), K)
+        assert np.array_equal(x, w * np.maximum(dot, 0.0)), f"single head, w = {w}"
+
+
+def pin_index_score_relu_identities():
+    """ReLU(a) - ReLU(-a) = a and ReLU(a) + ReLU(-a) = |a| turn the score into
+    plain matrix products: x(q) - x(-q) = K (w Q) and x(q) + x(-q) = |K Q^T| w
+    (numpy, float64, on the widened bf16 values)."""
+    rng = np.random.default_rng(13)
+    for n_h, c in ((16, 64), (64, 128), (3, 8)):
+        Q = _bf16(rng.standard_normal((n_h, c)))
+        K = _bf16(rng.standard_normal((50, c)))
+        w = rng.standard_normal(n_h).astype(np.float32)
+        xp = oracle.index_score(Q, w, K)
+        xm = oracle.index_score(Q ^ np.uint16(0x8000), w, K)  # -q: flip the bf16 sign bits
+        Qf, Kf, wf = _f64(Q), _f64(K), w.astype(np.float64)
+        assert np.allclose(xp - xm, Kf @ (wf @ Qf), rtol=1e-10, atol=1e-10), f"x(q) - x(-q), n_h={n_h}"
+        assert np.allclose(xp + xm, np.abs(Kf @ Qf.T) @ wf, rtol=1e-10, atol=1e-10), f"x(q) + x(-q), n_h={n_h}"
+
+
+def pin_index_score_head_permutation():
+    """Heads are a sum: permuting (q_h, w_h) pairs together leaves x unchanged."""
+    rng = np.random.default_rng(14)
+    Q = _bf16(rng.standard_normal((32, 64)))
+    K = _bf16(rng.standard_normal((30, 64)))
+    w = rng.standard_normal(32).astype(np.float32)
+    perm = rng.permutation(32)
+    a = oracle.index_score(Q, w, K)
+    b = oracle.index_score(Q[perm], w[perm], K)
+    assert np.allclose(a, b, rtol=1e-12, atol=1e-12), "head permutation"
+
+
+def pin_recall_sigmoid_threshold():
+    """One layer, no bound: the recalled set is {s : sigmoid(x_s) >= 1/2}
+    (scipy's expit), including x = +0.0 and -0.0."""
+    rng = np.random.default_rng(15)
+    x = rng.standard_normal(500)
+    x[np.abs(x) < 1e-6] = 1e-3
+    x[::37] = 0.0
+    x[5::41] = -0.0
+    want = np.nonzero(scipy.special.expit(x) >= 0.5)[0]
+    assert oracle.recall(x[None, :], len(x)).tolist() == want.tolist(), "sigmoid threshold"
+
+
+def pin_recall_or_bruteforce():
+    """OR over layers is the Python set union of the per-layer recalls; with a
+    bound, brute force over all subsets of the union: the kept set has the
+    largest sum of max_l x and, among those, the smallest ascending id list."""
+    rng = np.random.default_rng(16)
+    for _ in range(80):
+        L, n = int(rng.integers(1, 5)), int(rng.integers(1, 11))
+        x = rng.integers(-3, 3, size=(L, n)).astype(np.float64)
+        union = sorted(set().union(*[{s for s in range(n) if x[l, s] >= 0} for l in range(L)]))
+        assert oracle.recall(x, n).tolist() == union, f"OR over layers, x={x.tolist()}"
+        r = x.max(axis=0)
+        for kmax in range(1, n + 1):
+            if len(union) <= kmax:
+                want = union
+            else:
+                want, best = None, -math.inf
+                for comb in itertools.combinations(union, kmax):
+                    tot = r[list(comb)].sum()
+                    if tot > best:
+                        want, best = list(comb), tot
+            assert oracle.recall(x, kmax).tolist() == want, f"bound {kmax}, x={x.tolist()}"
+
+
+def pin_recall_boundaries():
+    """Cases the paper's threshold fixes: with every gate >= 0 every entry is
+    recalled; when every head's ReLU is 0 the score is exactly 0 and the entry
+    is recalled (sigmoid(0) = 1/2); with heads q and -q and negative gates every
+    score is < 0 and nothing is recalled."""
+    rng = np.random.default_rng(17)
+    Q = _bf16(rng.standard_normal((8, 32)))
+    K = _bf16(rng.standard_normal((25, 32)))
+    x = oracle.index_score(Q, np.abs(rng.standard_normal(8)).astype(np.float32), K)
+    assert oracle.recall(x[None, :], 25).tolist() == list(range(25)), "non-negative gates recall all"
+    Kneg = _bf16(-np.abs(rng.standard_normal((25, 32))))
+    Qpos = _bf16(np.abs(rng.standard_normal((8, 32))))
+    x = oracle.index_score(Qpos, rng.standard_normal(8).astype(np.float32), Kneg)
+    assert np.array_equal(x, np.zeros(25)), "all ReLUs zero"
+    assert oracle.recall(x[None, :], 25).tolist() == list(range(25)), "score 0 is on the threshold"
+    q0 = rng.standard_normal((1, 32))
+    Qpm = _bf16(np.concatenate([q0, -q0]))
+    x = oracle.index_score(Qpm, np.array([-1.0, -1.0], dtype=np.float32), K)
+    assert np.all(x < 0), "q and -q with negative gates"
+    assert oracle.recall(x[None, :], 25).tolist() == [], "nothing recalled"
+
+
 ALL_PINS = [
     pin_score_library_matmul, pin_score_int8_exact, pin_score_closed_forms,
     pin_topk_worked_example, pin_topk_bruteforce, pin_topk_library_sort, pin_union_bruteforce,
     pin_attention_worked_example, pin_keep_all_is_dense, pin_masked_dense_sdpa, pin_attention_closed_forms,
-    pin_gqa_mapping,
+    pin_gqa_mapping, pin_attention_empty_set,
+    pin_recall_worked_example, pin_index_score_single_head, pin_index_score_relu_identities,
+    pin_index_score_head_permutation, pin_recall_sigmoid_threshold, pin_recall_or_bruteforce,
+    pin_recall_boundaries,
 ]

@@ -43,6 +43,18 @@ MUTANTS = {
     "attn_v_transposed_dims": ("bf16_to_f64(Vh[tok * d + e])", "bf16_to_f64(Vh[tok * d + (d - 1 - e)])"),
     "attn_lse_dropped_max": ("lse[r] = m + log(Z);", "lse[r] = log(Z);"),
     "attn_unnormalised": ("out[(int64_t)r * d + e] = acc / Z;", "out[(int64_t)r * d + e] = acc;"),
+    "attn_empty_lse_zero": ("for (int32_t r = 0; r < R; ++r) lse[r] = -INFINITY;",
+                            "for (int32_t r = 0; r < R; ++r) lse[r] = 0.0;"),
+    "idx_dropped_relu": ("const double relu = dot > 0.0 ? dot : 0.0;", "const double relu = dot;"),
+    "idx_gate_inside_relu": ("x += (double)w[h] * relu;",
+                             "x += (double)w[h] * dot > 0.0 ? (double)w[h] * dot : 0.0;"),
+    "idx_wrong_head_weight": ("x += (double)w[h] * relu;", "x += (double)w[(h + 1) % n_h] * relu;"),
+    "idx_k_reversed_dims": ("bf16_to_f64(K[s * c + i])", "bf16_to_f64(K[s * c + (c - 1 - i)])"),
+    "recall_strict_threshold": ("if (xl >= 0.0) recalled = 1;", "if (xl > 0.0) recalled = 1;"),
+    "recall_first_layer_only": ("for (int32_t l = 0; l < L; ++l) {\n      const double xl",
+                                "for (int32_t l = 0; l < 1; ++l) {\n      const double xl"),
+    "recall_ranks_first_layer": ("if (xl > best) best = xl;", "if (xl > best && l < 0) best = xl;"),
+    "recall_bound_ignored": ("  if (m > kmax) {", "  if (m > n) {"),
 }
 
 
