@@ -52,6 +52,11 @@
  *    logits over the kept tokens.
  *  - All n_qtok query tokens of a sequence attend the same kept set; there is
  *    no mask inside it.
+ *
+ * Recall path (lsa_recall_*): the paper's full Memory Indexer in place of
+ * steps 1 and 2 -- a gated multi-head score per indexer layer (Eq. 4), the
+ * sigmoid threshold 1/2 (Eq. 5), the OR over L indexer layers (Eq. 13) and
+ * the bound K_max on the recalled set (Sec. 2.5) -- followed by step 3.
  */
 #ifndef LSA_H_
 #define LSA_H_
@@ -69,6 +74,7 @@ extern "C" {
 #define LSA_MAX_QTOK 16            /* attention query tokens per sequence */
 #define LSA_MAX_ROWS 128           /* n_qtok * n_q_heads / n_kv_heads */
 #define LSA_MAX_UNION_CHUNKS 262144 /* n_b limit when n_lookahead > 1 */
+#define LSA_MAX_IDX_LAYERS 4       /* indexer layers OR-ed by the recall path */
 
 typedef enum {
   LSA_OK = 0,
@@ -97,6 +103,14 @@ typedef struct lsa_problem {
   int64_t kv_chunk_stride;   /* elements between chunks in K and V; 0 selects n_kv_heads*C*d */
   int64_t kv_head_stride;    /* elements between KV heads in K and V; 0 selects C*d */
 } lsa_problem;
+
+/* Memory Indexer of the recall path.  Host memory only; read during the call. */
+typedef struct lsa_indexer {
+  int32_t n_layers;  /* L, indexer layers whose recalls are OR-ed, 1 .. LSA_MAX_IDX_LAYERS */
+  int32_t n_heads;   /* n_h, indexer heads per layer: 16, 32 or 64 */
+  int32_t key_dim;   /* c, width of the indexer queries and compressed index keys: 64 or 128 */
+  int32_t reserved;  /* must be 0 */
+} lsa_indexer;
 
 int lsa_abi_version(void);
 const char* lsa_status_string(lsa_status status);
@@ -144,7 +158,8 @@ lsa_status lsa_topk_chunks(const lsa_problem* p, const void* scores, int32_t* se
  * 1/sqrt(head_dim).  bf16 inputs, float32 softmax and accumulation.  lse is
  * nullable.  Split-K partials live in the workspace and are merged in a fixed
  * order, so results are bitwise reproducible.  Chunk ids must be < n_b and
- * sel_count[b] must be in 1 .. max_sel.
+ * sel_count[b] must be in 0 .. max_sel; an empty kept set (which only the
+ * recall path produces) gives out = 0 and lse = -inf.
  */
 lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const uint16_t* k_cache,
                                   const uint16_t* v_cache, const int32_t* sel_idx,
@@ -161,6 +176,42 @@ lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const vo
                            const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
                            float softmax_scale, float* out, float* lse, int32_t* sel_idx,
                            int32_t* sel_count, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Recall path.  Shapes: the problem must have n_lookahead == 1 (one query token
+ * fires the indexers) and keep[b] is the bound K_max of sequence b; emb_dim and
+ * emb_dtype are not used.  Inputs, all device memory:
+ *   idx_q  bf16 [B][L][n_h][c]        indexer queries q_{t,h} of every layer
+ *   idx_w  float32 [B][L][n_h]        gate weights w_{t,h} of every layer
+ *   idx_k  bf16 [L][sum_b n_b][c]     compressed index keys, row = global chunk id
+ * R1 -- gated multi-head index score (Sec. 2.1, Eq. 4, the argument of the
+ * sigmoid), float32 accumulation of exact bf16 products:
+ *   scores[l][chunk_off[b] + s] = sum_h idx_w[b][l][h] * ReLU(idx_q[b][l][h] . idx_k[l][chunk_off[b] + s])
+ */
+lsa_status lsa_recall_scores(const lsa_problem* p, const lsa_indexer* ix, const void* idx_q, const float* idx_w,
+                             const void* idx_k, float* scores, void* stream);
+
+/*
+ * R2 -- recall from scores as lsa_recall_scores writes them, float32
+ * [L][sum_b n_b]: layer l recalls entry s when sigmoid(x) >= 1/2, i.e. x >= 0
+ * (Eq. 5; -0.0 counts as 0), and s is recalled when any layer recalls it
+ * (Eq. 13).  When more than keep[b] entries are recalled, the keep[b] with the
+ * largest max_l x stay, ties towards the lower chunk id (K_max, Sec. 2.5).
+ * sel_idx[b] receives the recalled ids in ascending order (row pitch
+ * lsa_max_sel()) and sel_count[b] their number, 0 .. keep[b].  No workspace.
+ */
+lsa_status lsa_recall_select(const lsa_problem* p, const lsa_indexer* ix, const float* scores, int32_t* sel_idx,
+                             int32_t* sel_count, void* stream);
+
+/*
+ * R1 -> R2 -> step 3 on one stream with no host synchronisation.  The scores
+ * stay in the workspace; sel_idx / sel_count are nullable as in
+ * lsa_decode_step.  Sequences with nothing recalled get out = 0, lse = -inf.
+ */
+lsa_status lsa_recall_step(const lsa_problem* p, const lsa_indexer* ix, const void* idx_q, const float* idx_w,
+                           const void* idx_k, const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                           float softmax_scale, float* out, float* lse, int32_t* sel_idx, int32_t* sel_count,
+                           void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,11 +1,13 @@
 """MI355X (gfx950) decode hot path of Lookahead Sparse Attention.
 
 score every compressed chunk (Memory Indexer dot product) -> keep the top-k
-chunks -> sparse decode attention over the kept chunks, as hand-written HIP
+chunks -> sparse decode attention over the kept chunks, and the recall path
+(full gated multi-head Memory Indexer, sigmoid threshold, OR over indexer
+layers, K_max bound) in front of the same attention, as hand-written HIP
 kernels behind the C ABI of ``include/lsa.h``.  The Python layer is the thin
 ctypes binding in :mod:`.lsa`; importing it loads ``liblsa.so`` and raises if
 that is not possible.
 """
-from .lsa import (LIB, LsaError, Problem, lsa_decode_step, lsa_max_keep, lsa_max_sel,  # noqa: F401
-                  lsa_score_chunks, lsa_sparse_decode_attn, lsa_topk_chunks, lsa_validate, lsa_workspace_init,
-                  lsa_workspace_size, last_error)
+from .lsa import (LIB, Indexer, LsaError, Problem, lsa_decode_step, lsa_max_keep, lsa_max_sel,  # noqa: F401
+                  lsa_recall_scores, lsa_recall_select, lsa_recall_step, lsa_score_chunks, lsa_sparse_decode_attn,
+                  lsa_topk_chunks, lsa_validate, lsa_workspace_init, lsa_workspace_size, last_error)

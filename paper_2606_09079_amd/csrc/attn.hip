@@ -654,7 +654,7 @@ attn_combine_kernel(SeqTable t, AttnArgs a) {
       sum.z += v.z;
       sum.w += v.w;
     }
-    const float invL = 1.f / L;
+    const float invL = L > 0.f ? 1.f / L : 0.f;  // an empty kept set gives out = 0, lse = -inf
     sum.x *= invL;
     sum.y *= invL;
     sum.z *= invL;
@@ -714,7 +714,7 @@ attn_combine_few_kernel(SeqTable t, AttnArgs a, int n_rows) {
       acc.w += w * ov[sp].w;
     }
   }
-  const float invL = 1.f / L;
+  const float invL = L > 0.f ? 1.f / L : 0.f;  // an empty kept set gives out = 0, lse = -inf
   acc.x *= invL;
   acc.y *= invL;
   acc.z *= invL;

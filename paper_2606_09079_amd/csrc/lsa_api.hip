@@ -234,6 +234,53 @@ lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, cons
   return LSA_OK;
 }
 
+lsa_status check_indexer(const lsa_problem* p, const lsa_indexer* ix) {
+  if (ix == nullptr) return fail(LSA_ERR_INVALID_ARG, "indexer is NULL");
+  if (ix->n_layers < 1 || ix->n_layers > LSA_MAX_IDX_LAYERS)
+    return fail(LSA_ERR_INVALID_ARG, "indexer n_layers %d not in [1, %d]", ix->n_layers, LSA_MAX_IDX_LAYERS);
+  if (ix->n_heads != 16 && ix->n_heads != 32 && ix->n_heads != 64)
+    return fail(LSA_ERR_UNSUPPORTED, "indexer n_heads %d not in {16, 32, 64}", ix->n_heads);
+  if (ix->key_dim != 64 && ix->key_dim != 128)
+    return fail(LSA_ERR_UNSUPPORTED, "indexer key_dim %d not in {64, 128}", ix->key_dim);
+  if (ix->reserved != 0) return fail(LSA_ERR_INVALID_ARG, "indexer reserved field must be 0");
+  if (p->n_lookahead != 1)
+    return fail(LSA_ERR_INVALID_ARG, "the recall path takes one query token: n_lookahead %d != 1", p->n_lookahead);
+  return LSA_OK;
+}
+
+// The sequence table with scoring workgroups of kRecallRowsPerWg entries.
+SeqTable recall_table(const Plan& P) {
+  SeqTable t = P.t;
+  int32_t off = 0;
+  for (int b = 0; b < t.batch; ++b) {
+    t.score_wg_off[b] = off;
+    off += (t.n[b] + kRecallRowsPerWg - 1) / kRecallRowsPerWg;
+  }
+  t.score_wg_off[t.batch] = off;
+  return t;
+}
+
+RecallArgs recall_args(const Plan& P, const lsa_indexer* ix, const void* idx_q, const float* idx_w,
+                       const void* idx_k) {
+  RecallArgs r;
+  r.q = static_cast<const uint16_t*>(idx_q);
+  r.w = idx_w;
+  r.k = static_cast<const uint16_t*>(idx_k);
+  r.total = P.total_chunks;
+  r.layer_stride = P.total_chunks * ix->key_dim;
+  r.n_layers = ix->n_layers;
+  r.n_heads = ix->n_heads;
+  r.key_dim = ix->key_dim;
+  return r;
+}
+
+lsa_status check_recall_inputs(const void* idx_q, const float* idx_w, const void* idx_k) {
+  LSA_TRY(check_ptr(idx_q, "idx_q"));
+  LSA_TRY(check_ptr(idx_w, "idx_w"));
+  LSA_TRY(check_ptr(idx_k, "idx_k"));
+  return LSA_OK;
+}
+
 }  // namespace
 }  // namespace lsa
 
@@ -366,6 +413,72 @@ lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const vo
   // order keys and the selection reads them without converting
   LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, true, s), "score launch");
   LSA_TRY(run_topk(p, P, true, scores, sel, cnt, nullptr, ws, s));
+  return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
+}
+
+lsa_status lsa_recall_scores(const lsa_problem* p, const lsa_indexer* ix, const void* idx_q, const float* idx_w,
+                             const void* idx_k, float* scores, void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(check_indexer(p, ix));
+  LSA_TRY(check_recall_inputs(idx_q, idx_w, idx_k));
+  LSA_TRY(check_ptr(scores, "scores"));
+  LSA_HIP(launch_recall_score(recall_table(P), recall_args(P, ix, idx_q, idx_w, idx_k), scores, false,
+                              (hipStream_t)stream),
+          "recall score launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_recall_select(const lsa_problem* p, const lsa_indexer* ix, const float* scores, int32_t* sel_idx,
+                             int32_t* sel_count, void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(check_indexer(p, ix));
+  LSA_TRY(check_ptr(scores, "scores"));
+  LSA_TRY(check_ptr(sel_idx, "sel_idx"));
+  LSA_TRY(check_ptr(sel_count, "sel_count"));
+  SelectArgs sa;
+  sa.recall = true;
+  sa.n_layers = ix->n_layers;
+  sa.layer_stride = P.total_chunks;
+  LSA_HIP(launch_topk(P.t, LSA_F32, false, scores, sel_idx, P.max_sel, 0, sel_count, (hipStream_t)stream, sa),
+          "recall select launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_recall_step(const lsa_problem* p, const lsa_indexer* ix, const void* idx_q, const float* idx_w,
+                           const void* idx_k, const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                           float softmax_scale, float* out, float* lse, int32_t* sel_idx, int32_t* sel_count,
+                           void* ws, size_t ws_bytes, void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(check_indexer(p, ix));
+  LSA_TRY(check_recall_inputs(idx_q, idx_w, idx_k));
+  LSA_TRY(check_ptr(q, "q"));
+  LSA_TRY(check_ptr(k_cache, "k_cache"));
+  LSA_TRY(check_ptr(v_cache, "v_cache"));
+  LSA_TRY(check_ptr(out, "out"));
+  if (lse != nullptr && (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(LSA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if ((sel_idx == nullptr) != (sel_count == nullptr))
+    return fail(LSA_ERR_INVALID_ARG, "sel_idx and sel_count must both be given or both be NULL");
+  if (sel_idx != nullptr) {
+    LSA_TRY(check_ptr(sel_idx, "sel_idx"));
+    LSA_TRY(check_ptr(sel_count, "sel_count"));
+  }
+  if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
+  LSA_TRY(check_ws(P, ws, ws_bytes));
+  const hipStream_t s = (hipStream_t)stream;
+  void* keys = at(ws, P.off_scores);  // n_lookahead == 1: one key per chunk
+  int32_t* sel = sel_idx ? sel_idx : reinterpret_cast<int32_t*>(at(ws, P.off_sel));
+  int32_t* cnt = sel_count ? sel_count : reinterpret_cast<int32_t*>(at(ws, P.off_cnt));
+  // the scoring kernel writes the order key of max_l x_l, which the selection
+  // reads as ready keys
+  LSA_HIP(launch_recall_score(recall_table(P), recall_args(P, ix, idx_q, idx_w, idx_k), keys, true, s),
+          "recall score launch");
+  SelectArgs sa;
+  sa.recall = true;
+  LSA_HIP(launch_topk(P.t, LSA_F32, true, keys, sel, P.max_sel, 0, cnt, s, sa), "recall select launch");
   return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
 }
 

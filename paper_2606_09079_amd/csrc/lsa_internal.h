@@ -79,14 +79,41 @@ hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, c
                         const void* E, void* scores, bool keys, hipStream_t s);
 int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim, int32_t n_lookahead);
 
-// keys_ready == true: `scores` holds keys written by launch_score(keys = true).
+// Selection variants.  recall: k_b becomes min(keep[b], number of keys >= the
+// key of +0.0), i.e. the entries whose sigmoid score reaches 1/2, bounded by
+// K_max = keep[b]; n_layers > 1 reads that many score arrays layer_stride
+// elements apart and selects on their per-entry maximum (the OR over layers).
+struct SelectArgs {
+  bool recall = false;
+  int32_t n_layers = 1;
+  int64_t layer_stride = 0;
+};
+
+// keys_ready == true: `scores` holds keys written by launch_score(keys = true)
+// or launch_recall_score(keys = true).
 hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, bool keys_ready, const void* scores,
                        int32_t* out_idx, int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
-                       hipStream_t s);
+                       hipStream_t s, const SelectArgs& sa = SelectArgs());
 hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_pitch,
                         int32_t* sel_idx, int32_t sel_pitch, int32_t* sel_count, hipStream_t s);
 
 hipError_t launch_attn(const SeqTable& t, const AttnArgs& a, int32_t chunk_size, hipStream_t s);
+
+// Recall path: the full Memory Indexer score of L layers.
+constexpr int kMaxIdxLayers = LSA_MAX_IDX_LAYERS;
+constexpr int kRecallRowsPerWg = 64;  // entries per scoring workgroup (4 waves x 16)
+struct RecallArgs {
+  const uint16_t* q;     // bf16 [B][L][n_h][c]
+  const float* w;        // [B][L][n_h]
+  const uint16_t* k;     // bf16 [L][total][c]
+  int64_t layer_stride;  // total * c
+  int64_t total;         // sum_b n_b
+  int32_t n_layers, n_heads, key_dim;
+};
+// t.score_wg_off must count kRecallRowsPerWg entries per workgroup.  keys ==
+// false writes x [L][total] float32; keys == true writes the order key of
+// max_l x_l per entry, [total] (the input of the recall selection).
+hipError_t launch_recall_score(const SeqTable& t, const RecallArgs& r, void* out, bool keys, hipStream_t s);
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 

@@ -57,25 +57,33 @@ __device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t* w
   return incl - v + wave_tot[wave];
 }
 
-template <int MODE>
+template <int MODE, bool RECALL>
 __global__ void __launch_bounds__(kThreads)
 topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict__ out_idx,
-            int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count) {
+            int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count, SelectArgs sa) {
   __shared__ uint32_t keys[kLdsKeys];
   __shared__ uint32_t hist[kSubHist][256];
   __shared__ uint64_t wave_tot[kWaves];
-  __shared__ uint32_t sh_digit, sh_krem;
+  __shared__ uint32_t sh_digit, sh_krem, sh_k;
 
   const int Q = t.n_lookahead;
   const int b = blockIdx.x / Q, j = blockIdx.x % Q;
-  const int n = t.n[b], k = t.keep[b];
+  const int n = t.n[b];
+  int k = t.keep[b];
   const int tid = threadIdx.x;
   const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * n;
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
   const bool staged = n <= kLdsKeys;
+  // key of entry i; for the recall, the largest over the indexer layers
+  auto key_at = [&](int i) -> uint32_t {
+    uint32_t key = order_key<MODE>(s[i]);
+    if constexpr (RECALL)
+      for (int l = 1; l < sa.n_layers; ++l) key = max(key, order_key<MODE>(s[l * sa.layer_stride + i]));
+    return key;
+  };
 
   if (staged)
-    for (int i = tid; i < n; i += kThreads) keys[i] = order_key<MODE>(s[i]);
+    for (int i = tid; i < n; i += kThreads) keys[i] = key_at(i);
 
   uint32_t prefix = 0, pmask = 0, krem = (uint32_t)k;
   uint32_t* hflat = &hist[0][0];
@@ -84,7 +92,7 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
     for (int i = tid; i < kSubHist * 256; i += kThreads) hflat[i] = 0u;
     __syncthreads();
     for (int i = tid; i < n; i += kThreads) {
-      const uint32_t key = staged ? keys[i] : order_key<MODE>(s[i]);
+      const uint32_t key = staged ? keys[i] : key_at(i);
       if ((key & pmask) == prefix) atomicAdd(&hist[sub][(key >> shift) & 255u], 1u);
     }
     __syncthreads();
@@ -105,6 +113,13 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
         if (tid + off < 64) suffix += y;
       }
       uint32_t cum = suffix - tot;  // keys in higher bins
+      if constexpr (RECALL) {
+        if (shift == 24) {
+          // keys at or above the key of +0.0 fill bins 128 .. 255 (lanes 32 .. 63)
+          krem = min(krem, (uint32_t)__shfl((int)suffix, 32));
+          if (tid == 0) sh_k = krem;
+        }
+      }
 #pragma unroll
       for (int q = 3; q >= 0; --q) {
         if (cum < krem && cum + c[q] >= krem) {
@@ -115,6 +130,15 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
       }
     }
     __syncthreads();
+    if constexpr (RECALL) {
+      if (shift == 24) {
+        k = (int)sh_k;
+        if (k == 0) {  // nothing recalled (uniform across the workgroup)
+          if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+          return;
+        }
+      }
+    }
     prefix |= sh_digit << shift;
     pmask |= 0xFFu << shift;
     krem = sh_krem;
@@ -126,14 +150,14 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
   const int i0 = min(tid * seg, n), i1 = min(i0 + seg, n);
   uint32_t gt = 0, eq = 0;
   for (int i = i0; i < i1; ++i) {
-    const uint32_t key = order_key<MODE>(s[i]);
+    const uint32_t key = key_at(i);
     gt += key > T;
     eq += key == T;
   }
   const uint64_t base = block_exclusive_scan(((uint64_t)gt << 32) | eq, wave_tot);
   uint32_t pgt = (uint32_t)(base >> 32), peq = (uint32_t)base;
   for (int i = i0; i < i1; ++i) {
-    const uint32_t key = order_key<MODE>(s[i]);
+    const uint32_t key = key_at(i);
     if (key > T) {
       const uint32_t pos = pgt + min(peq, krem);
       if (pos < (uint32_t)k) out[pos] = i;
@@ -225,10 +249,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(const void* p, uint
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-template <int MODE>
+template <int MODE, bool RECALL>
 __global__ void __launch_bounds__(kSelThreads)
 topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict__ out_idx,
-                   int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count) {
+                   int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count, SelectArgs sa) {
   // First-digit histogram, 4 counters per bin (one per lane quarter, adjacent
   // words so that equal bins of different quarters fall in different banks).
   __shared__ __align__(16) uint32_t hist[4096 * kSelSub];
@@ -238,10 +262,12 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   __shared__ __align__(16) uint32_t bm_gt[kSelMaxN / 32];  // chunks above T, bit i % 32 of word i / 32
   __shared__ __align__(16) uint32_t bm_eq[kSelMaxN / 32];  // chunks equal to T
   __shared__ uint32_t sh[4];
+  __shared__ uint32_t nonneg[kSelWaves];  // recall: keys >= the key of +0.0, per wave
 
   const int Q = t.n_lookahead;
   const int b = blockIdx.x / Q, j = blockIdx.x % Q;
-  const int n = t.n[b], k = t.keep[b];
+  const int n = t.n[b];
+  int k = t.keep[b];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane >> 4;
   const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * n;
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
@@ -256,6 +282,19 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
 #pragma unroll
   for (int q = 0; q < kSelKPT; ++q)
     kk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
+  if constexpr (RECALL) {
+    // keys of the first layer, then the largest over the other indexer layers
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
+    for (int l = 1; l < sa.n_layers; ++l) {
+      const __amdgpu_buffer_rsrc_t srcl = raw_buffer(s + l * sa.layer_stride, (uint32_t)n * 4u);
+#pragma unroll
+      for (int q = 0; q < kSelKPT; ++q) {
+        const uint32_t v = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(srcl, tid * 4, q * kSelThreads * 4, 0);
+        if (q * kSelThreads + tid < n) kk[q] = max(kk[q], order_key<MODE>(v));
+      }
+    }
+  }
 #pragma unroll
   for (int q = 0; q < kSelSub; ++q)
     reinterpret_cast<uint4*>(hist)[q * kSelThreads + tid] = make_uint4(0u, 0u, 0u, 0u);
@@ -267,11 +306,26 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   uint32_t bin[kSelKPT], rk[kSelKPT];
 #pragma unroll
   for (int q = 0; q < kSelKPT; ++q) {
-    if constexpr (MODE != kKeysReady) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
+    if constexpr (MODE != kKeysReady && !RECALL) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
     bin[q] = kk[q] >> 20;
     rk[q] = atomicAdd(&hist[bin[q] * kSelSub + sub], 1u);
   }
+  if constexpr (RECALL) {
+    uint32_t nn = 0;
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) nn += (uint32_t)__popcll(__ballot(kk[q] >= 0x80000000u));
+    if (lane == 0) nonneg[wave] = nn;
+  }
   __syncthreads();
+  if constexpr (RECALL) {
+    // recalled entries: sigmoid >= 1/2, i.e. key >= key(+0.0); at most K_max = keep[b]
+    const uint32_t c = lane < kSelWaves ? nonneg[lane] : 0u;
+    k = min(k, (int)lane_bcast(wave_scan_incl(c), 63));
+    if (k == 0) {  // nothing recalled (uniform across the workgroup)
+      if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+      return;
+    }
+  }
 
   // Bin B0 holding the k-th largest key: thread t owns bins 4t .. 4t+3.
   {
@@ -431,18 +485,18 @@ __global__ void zero_kernel(uint4* p, size_t n16, uint8_t* tail, size_t ntail) {
 
 namespace {
 
-template <int MODE>
+template <int MODE, bool RECALL>
 hipError_t launch_topk_keys(const SeqTable& t, const uint32_t* scores, int32_t* out_idx, int64_t pitch_seq,
-                            int64_t pitch_q, int32_t* sel_count, hipStream_t s) {
+                            int64_t pitch_q, int32_t* sel_count, const SelectArgs& sa, hipStream_t s) {
   int n_max = 0;
   for (int b = 0; b < t.batch; ++b) n_max = max(n_max, t.n[b]);
   const dim3 grid(t.batch * t.n_lookahead);
   if (n_max <= kSelMaxN)
-    hipLaunchKernelGGL((topk_select_kernel<MODE>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
-                       pitch_seq, pitch_q, sel_count);
+    hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
+                       pitch_seq, pitch_q, sel_count, sa);
   else
-    hipLaunchKernelGGL((topk_kernel<MODE>), grid, dim3(kThreads), 0, s, t, scores, out_idx, pitch_seq,
-                       pitch_q, sel_count);
+    hipLaunchKernelGGL((topk_kernel<MODE, RECALL>), grid, dim3(kThreads), 0, s, t, scores, out_idx, pitch_seq,
+                       pitch_q, sel_count, sa);
   return hipGetLastError();
 }
 
@@ -450,13 +504,18 @@ hipError_t launch_topk_keys(const SeqTable& t, const uint32_t* scores, int32_t* 
 
 hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, bool keys_ready, const void* scores,
                        int32_t* out_idx, int64_t out_pitch_seq, int64_t out_pitch_query, int32_t* sel_count,
-                       hipStream_t s) {
+                       hipStream_t s, const SelectArgs& sa) {
   const uint32_t* sc = static_cast<const uint32_t*>(scores);
+  if (sa.recall) {
+    if (keys_ready)
+      return launch_topk_keys<kKeysReady, true>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, sa, s);
+    return launch_topk_keys<kKeysFromF32, true>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, sa, s);
+  }
   if (keys_ready)
-    return launch_topk_keys<kKeysReady>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
+    return launch_topk_keys<kKeysReady, false>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, sa, s);
   if (emb_dtype == LSA_I8)
-    return launch_topk_keys<kKeysFromI32>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
-  return launch_topk_keys<kKeysFromF32>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, s);
+    return launch_topk_keys<kKeysFromI32, false>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, sa, s);
+  return launch_topk_keys<kKeysFromF32, false>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, sa, s);
 }
 
 hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_pitch,

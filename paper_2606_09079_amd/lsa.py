@@ -30,7 +30,8 @@ DTYPES = {"f32": 0, "bf16": 1, "i8": 2}
 
 EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_validate", "lsa_max_sel",
            "lsa_max_keep", "lsa_workspace_size", "lsa_workspace_init", "lsa_score_chunks", "lsa_topk_chunks",
-           "lsa_sparse_decode_attn", "lsa_decode_step")
+           "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
+           "lsa_recall_step")
 
 
 class lsa_problem(ctypes.Structure):
@@ -42,6 +43,11 @@ class lsa_problem(ctypes.Structure):
         ("keep", ctypes.POINTER(ctypes.c_int32)), ("kv_chunk_stride", ctypes.c_int64),
         ("kv_head_stride", ctypes.c_int64),
     ]
+
+
+class lsa_indexer(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("key_dim", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 def _load() -> ctypes.CDLL:
@@ -68,6 +74,11 @@ def _load() -> ctypes.CDLL:
     lib.lsa_topk_chunks.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
     lib.lsa_sparse_decode_attn.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
     lib.lsa_decode_step.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+    ip = ctypes.POINTER(lsa_indexer)
+    lib.lsa_recall_scores.argtypes = [pp, ip, _P, _P, _P, _P, _P]
+    lib.lsa_recall_select.argtypes = [pp, ip, _P, _P, _P, _P]
+    lib.lsa_recall_step.argtypes = [pp, ip, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P,
+                                    ctypes.c_size_t, _P]
     for name in EXPORTS[3:]:
         getattr(lib, name).restype = ctypes.c_int
     if lib.lsa_abi_version() != 1:
@@ -97,6 +108,21 @@ class Problem:
     def from_synth(cls, prob, **kw) -> "Problem":
         return cls(prob.ctx_tokens, prob.chunk, prob.keep, prob.n_q_heads, prob.n_kv_heads, prob.head_dim,
                    prob.emb_dim, prob.n_lookahead, prob.n_qtok, prob.emb_dtype, **kw)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+class Indexer:
+    """Memory Indexer of the recall path (mirrors ``lsa_indexer``)."""
+
+    def __init__(self, n_layers: int, n_heads: int, key_dim: int):
+        self.c = lsa_indexer(n_layers, n_heads, key_dim, 0)
+
+    @classmethod
+    def from_synth(cls, prob) -> "Indexer":
+        return cls(prob.idx_layers, prob.idx_heads, prob.idx_dim)
 
     @property
     def ref(self):
@@ -178,3 +204,20 @@ def lsa_decode_step(p: Problem, query_emb, chunk_emb, q, k_cache, v_cache, softm
     _check(LIB.lsa_decode_step(p.ref, _ptr(query_emb), _ptr(chunk_emb), _ptr(q), _ptr(k_cache), _ptr(v_cache),
                                float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx), _ptr(sel_count), _ptr(ws),
                                ws_bytes, _stream(stream)), "lsa_decode_step")
+
+
+def lsa_recall_scores(p: Problem, ix: Indexer, idx_q, idx_w, idx_k, scores, stream=None) -> None:
+    _check(LIB.lsa_recall_scores(p.ref, ix.ref, _ptr(idx_q), _ptr(idx_w), _ptr(idx_k), _ptr(scores),
+                                 _stream(stream)), "lsa_recall_scores")
+
+
+def lsa_recall_select(p: Problem, ix: Indexer, scores, sel_idx, sel_count, stream=None) -> None:
+    _check(LIB.lsa_recall_select(p.ref, ix.ref, _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _stream(stream)),
+           "lsa_recall_select")
+
+
+def lsa_recall_step(p: Problem, ix: Indexer, idx_q, idx_w, idx_k, q, k_cache, v_cache, softmax_scale: float, out,
+                    lse=None, sel_idx=None, sel_count=None, ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(LIB.lsa_recall_step(p.ref, ix.ref, _ptr(idx_q), _ptr(idx_w), _ptr(idx_k), _ptr(q), _ptr(k_cache),
+                               _ptr(v_cache), float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx),
+                               _ptr(sel_count), _ptr(ws), ws_bytes, _stream(stream)), "lsa_recall_step")

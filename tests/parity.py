@@ -9,6 +9,15 @@ Tolerances (written here, derived in the design notes):
   scores differ by less than 1e-4 relative; inside that band the GPU set must
   contain every chunk scoring above the band, lie inside the band's closure and
   have k members;
+* recall index scores x_l[s] = sum_h w_h ReLU(q_h . K_s):
+  |gpu - oracle| <= (c + n_h + 4) * 2**-24 * sum_h |w_h| sum_i |q_hi K_si|, the
+  float32 bound for c-term dot products of exact products, the ReLU (which
+  cannot grow an error), one product with the gate and an n_h-term sum;
+* recalled sets: identical to the oracle's unless an entry's max-over-layers
+  score lies within that bound of the threshold 0 or, when the K_max bound
+  cuts, of the cut; otherwise the GPU set must hold every entry surely
+  recalled (up to the bound), no entry that cannot be recalled, and must never
+  leave out an entry clearly above one it kept;
 * attention: max relative error 2e-3 per (b, t, h) row, normwise
   (max_e |o - r| / max_e |r|), bf16 inputs with fp32 accumulation; lse within
   2e-3 absolute.
@@ -89,3 +98,48 @@ def check_attention(gpu_out: np.ndarray, gpu_lse, ref_out: np.ndarray, ref_lse, 
             d = abs(float(gpu_lse[i]) - float(ref_lse[i]))
             assert d <= LSE_ABS_TOL, f"{what}: row {i} lse error {d:.3e}"
     return worst
+
+
+def index_score_tolerance(q: np.ndarray, w: np.ndarray, K: np.ndarray) -> np.ndarray:
+    """Bound on |gpu - oracle| of one layer's recall scores; q [n_h][c] and K
+    [n][c] are bf16 bit patterns, w [n_h] float32."""
+    import lsa_synth
+    q64, K64 = np.abs(lsa_synth.bf16_bits_to_f64(q)), np.abs(lsa_synth.bf16_bits_to_f64(K))
+    n_h, c = q.shape
+    return (c + n_h + 4) * 2.0 ** -24 * ((K64 @ q64.T) @ np.abs(w.astype(np.float64))) + 1e-30
+
+
+def check_index_scores(gpu: np.ndarray, ref: np.ndarray, tol: np.ndarray, what: str) -> float:
+    err = np.abs(gpu.astype(np.float64) - ref)
+    bad = np.nonzero(err > tol)[0]
+    assert len(bad) == 0, f"{what}: recall scores off at {bad[:10]} err {err[bad[:5]]} tol {tol[bad[:5]]}"
+    return float(err.max()) if len(err) else 0.0
+
+
+def check_recall(gpu_sel: np.ndarray, ref_x: np.ndarray, tol: np.ndarray, kmax: int, what: str) -> str:
+    """Band rule for a recalled set.  ref_x, tol: [L][n] oracle scores and their
+    bounds.  Returns 'exact' when the GPU set equals the oracle's."""
+    import oracle
+    gpu_sel = np.asarray(gpu_sel, dtype=np.int64)
+    n = ref_x.shape[1]
+    assert len(gpu_sel) <= kmax, f"{what}: {len(gpu_sel)} recalled > K_max {kmax}"
+    assert np.all(np.diff(gpu_sel) > 0), f"{what}: recalled ids not strictly ascending"
+    assert len(gpu_sel) == 0 or (gpu_sel[0] >= 0 and gpu_sel[-1] < n), f"{what}: recalled id out of range"
+    want = oracle.recall(ref_x, kmax)
+    if np.array_equal(gpu_sel, want):
+        return "exact"
+    hi = (ref_x + tol).max(axis=0)    # largest score each entry could have on the GPU
+    lo = (ref_x - tol).max(axis=0)    # smallest
+    G = set(gpu_sel.tolist())
+    possible = set(np.nonzero(hi >= 0)[0].tolist())
+    sure = set(np.nonzero(lo > 0)[0].tolist())
+    assert G <= possible, f"{what}: entries {sorted(G - possible)[:10]} cannot be recalled"
+    assert len(G) >= min(kmax, len(sure)), f"{what}: {len(G)} recalled, {len(sure)} surely recalled"
+    if len(G) < kmax:
+        assert sure <= G, f"{what}: surely recalled entries {sorted(sure - G)[:10]} missing"
+    out = sorted(possible - G)
+    if G and out:
+        weakest_in = min(hi[g] for g in G)
+        clearly = [s for s in out if lo[s] > weakest_in]
+        assert not clearly, f"{what}: entries {clearly[:10]} left out but surely above a kept one"
+    return "band"

@@ -114,3 +114,44 @@ def test_entry_points_reject_bad_buffers_without_launching():
     assert lib.lsa_topk_chunks(q.ref, FAKE, FAKE, FAKE, None, FAKE, 16, None) == B.LSA_ERR_WORKSPACE
     with pytest.raises(L.LsaError):
         L.lsa_score_chunks(p, None, FAKE, FAKE, stream=0)
+
+
+@pytest.mark.parametrize("ix,pkw,status", [
+    ((0, 64, 128), {}, B.LSA_ERR_INVALID_ARG),
+    ((5, 64, 128), {}, B.LSA_ERR_INVALID_ARG),
+    ((3, 48, 128), {}, B.LSA_ERR_UNSUPPORTED),
+    ((3, 64, 96), {}, B.LSA_ERR_UNSUPPORTED),
+    ((3, 64, 128), dict(n_lookahead=2), B.LSA_ERR_INVALID_ARG),
+])
+def test_recall_validation_rejects(ix, pkw, status):
+    p = good(**pkw)
+    idx = L.Indexer(*ix)
+    lib = L.LIB
+    assert lib.lsa_recall_scores(p.ref, idx.ref, FAKE, FAKE, FAKE, FAKE, None) == status
+    assert lib.lsa_recall_select(p.ref, idx.ref, FAKE, FAKE, FAKE, None) == status
+    assert L.last_error() != ""
+
+
+def test_recall_entry_points_reject_bad_buffers_without_launching():
+    p = good()
+    ws = L.lsa_workspace_size(p)
+    idx = L.Indexer(3, 64, 128)
+    lib = L.LIB
+    assert lib.lsa_recall_scores(p.ref, None, FAKE, FAKE, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_recall_scores(p.ref, idx.ref, FAKE, MISALIGNED, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_recall_select(p.ref, idx.ref, FAKE, None, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_recall_step(p.ref, idx.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None,
+                               FAKE, ws - 1, None) == B.LSA_ERR_WORKSPACE
+    assert lib.lsa_recall_step(p.ref, idx.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, FAKE, None,
+                               FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_recall_step(p.ref, idx.ref, None, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None,
+                               FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
+
+
+def test_recall_presets_validate():
+    import lsa_synth
+    for name in lsa_synth.RECALL_PRESETS:
+        prob = lsa_synth.make_problem(name, 0)
+        p, idx = L.Problem.from_synth(prob), L.Indexer.from_synth(prob)
+        assert L.lsa_validate(p) == 0
+        assert L.LIB.lsa_recall_select(p.ref, idx.ref, None, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
