@@ -46,6 +46,13 @@ WORKLOADS = {
             "head_dim 128, bf16 K/V, int8 indexer dim 256",
     "tiny": "tiny: 4,096 tokens, 64-token chunks (64), keep 8, 8 query / 8 KV heads, head_dim 128, bf16 K/V, "
             "fp32 indexer dim 256",
+    "recall1m": "recall1m: 1,048,576-token context, 64-token chunks (16,384), full Memory Indexer of 3 layers x 64 "
+                "heads x 128-wide bf16 index keys, sigmoid threshold 1/2, OR over layers, K_max 1,638 (10%), "
+                "32 query / 8 KV heads, head_dim 128, bf16 K/V, batch 1",
+    "recall_batch": "recall_batch: 4 sequences x 131,072 tokens, 64-token chunks (2,048 each), Memory Indexer of "
+                    "2 layers x 32 heads x 128, no K_max cut, 32 query / 8 KV heads, head_dim 128, bf16 K/V",
+    "recall_tiny": "recall_tiny: 4,096 tokens, 64-token chunks (64), Memory Indexer of 3 layers x 16 heads x 64, "
+                   "K_max 12, 8 query / 8 KV heads, head_dim 128, bf16 K/V",
 }
 EMB_BYTES = {"f32": 4, "bf16": 2, "i8": 1}
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "attn_kernel_paper1m_traffic.md")
@@ -118,13 +125,20 @@ def main() -> int:
     t_setup = time.time()
     host0 = synth.host_inputs(prob, 0)
     dev = synth.device_inputs(prob, 0, host=host0)
+    recall = prob.idx_layers > 0
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).cuda()
+
     rot = []
     for r in range(args.rotations):
         h = host0 if r == 0 else synth.host_inputs(prob, 1000 + r)
-        qe = torch.from_numpy(np.ascontiguousarray(h["qe"]).view(np.int16)).cuda()
-        q = torch.from_numpy(np.ascontiguousarray(h["q"]).view(np.int16)).cuda()
-        rot.append((qe, q))
+        # the query side changes from step to step; embeddings, index keys and K/V stay
+        rot.append({"qe": up(h["qe"]), "q": up(h["q"]), **({"idx_q": up(h["idx_q"]), "idx_w": up(h["idx_w"])}
+                                                           if recall else {})})
     P = L.Problem.from_synth(prob)
+    ix = L.Indexer.from_synth(prob) if recall else None
     B, Tq, Hq, d = prob.batch, prob.n_qtok, prob.n_q_heads, prob.head_dim
     ws_bytes = L.lsa_workspace_size(P)
     ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
@@ -137,14 +151,17 @@ def main() -> int:
     log(f"[bench] setup {time.time() - t_setup:.1f}s, workspace {ws_bytes / 2**20:.1f} MiB")
 
     def step(i: int) -> None:
-        qe, q = rot[i % len(rot)]
-        L.lsa_decode_step(P, qe, dev["E"], q, dev["k"], dev["v"], 0.0, out, lse, sels[i % len(rot)],
-                          cnts[i % len(rot)], ws, ws_bytes, stream)
+        r = rot[i % len(rot)]
+        if recall:
+            L.lsa_recall_step(P, ix, r["idx_q"], r["idx_w"], dev["idx_k"], r["q"], dev["k"], dev["v"], 0.0, out,
+                              lse, sels[i % len(rot)], cnts[i % len(rot)], ws, ws_bytes, stream)
+        else:
+            L.lsa_decode_step(P, r["qe"], dev["E"], r["q"], dev["k"], dev["v"], 0.0, out, lse, sels[i % len(rot)],
+                              cnts[i % len(rot)], ws, ws_bytes, stream)
 
     def attn(i: int) -> None:
-        _, q = rot[i % len(rot)]
-        L.lsa_sparse_decode_attn(P, q, dev["k"], dev["v"], sels[i % len(rot)], cnts[i % len(rot)], 0.0, out, lse,
-                                 ws, ws_bytes, stream)
+        L.lsa_sparse_decode_attn(P, rot[i % len(rot)]["q"], dev["k"], dev["v"], sels[i % len(rot)],
+                                 cnts[i % len(rot)], 0.0, out, lse, ws, ws_bytes, stream)
 
     # every rotation's kept set exists before any attention-only launch
     for i in range(len(rot)):
@@ -238,7 +255,11 @@ def main() -> int:
     C, Hkv = prob.chunk, prob.n_kv_heads
     kv_bytes = [n * C * Hkv * d * 2 * 2 for n in counts]
     attn_bytes = sum(kv_bytes) / len(kv_bytes) + B * Tq * Hq * d * (2 + 4) + B * Tq * Hq * 4 + max(counts) * 4
-    emb_bytes = (prob.total_chunks + B * prob.n_lookahead) * prob.emb_dim * EMB_BYTES[prob.emb_dtype]
+    if recall:  # index keys of every layer, plus the indexer queries and gates
+        Lay, nh, c = prob.idx_layers, prob.idx_heads, prob.idx_dim
+        emb_bytes = Lay * prob.total_chunks * c * 2 + B * Lay * nh * (c * 2 + 4)
+    else:
+        emb_bytes = (prob.total_chunks + B * prob.n_lookahead) * prob.emb_dim * EMB_BYTES[prob.emb_dtype]
     step_bytes = attn_bytes + emb_bytes
     achieved = attn_bytes / (att_avg_us * 1e-6) / 1e9
     traffic = measured_traffic() if args.workload == "paper1m" else None
@@ -287,15 +308,20 @@ def cpu_baseline(prob, host, budget_s: float):
     import lsa_synth as synth
     import oracle
 
+    def select():
+        if prob.idx_layers > 0:
+            return oracle.recall_for_sequence(prob, host, 0)[1]
+        return oracle.select_for_sequence(prob, host, 0)[2]
+
     t_prep = time.time()
-    _, _, kept = oracle.select_for_sequence(prob, host, 0)
+    kept = select()
     Hkv, G = prob.n_kv_heads, prob.group
     kv = {(w, g): synth.kv_head_sparse(prob, 0, w, 0, g, kept) for g in range(Hkv) for w in ("k", "v")}
     log(f"[bench] cpu baseline inputs prepared in {time.time() - t_prep:.1f}s")
     threads = min(Hkv, os.cpu_count() or 1)
 
     def one_step():
-        _, _, kept_s = oracle.select_for_sequence(prob, host, 0)
+        kept_s = select()
 
         def head(g):
             qr = np.stack([host["q"][0, 0, g * G + j] for j in range(G)])
@@ -314,9 +340,14 @@ def cpu_baseline(prob, host, budget_s: float):
     full = prob.batch == 1 and prob.n_qtok == 1
     what = ("full step(s) of the same workload" if full else
             "step(s) of sequence 0 of the same workload, attention for its first query token only")
+    if prob.idx_layers > 0:
+        sel_what = (f"{prob.idx_layers}-layer x {prob.idx_heads}-head index scores of {prob.n_chunks[0]:,} chunks, "
+                    f"recall bounded by {prob.keep[0]:,}")
+    else:
+        sel_what = f"score {prob.n_chunks[0]:,} chunks, top-{prob.keep[0]:,}"
     return {"value": round(reps / el, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{reps} {what} (score {prob.n_chunks[0]:,} chunks, top-{prob.keep[0]:,}, fp64 attention "
-                      f"for {prob.n_q_heads} query heads) in {el:.1f}s; KV-head groups on {threads} threads"}
+            "sample": f"{reps} {what} ({sel_what}, fp64 attention for {prob.n_q_heads} query heads) in {el:.1f}s; "
+                      f"KV-head groups on {threads} threads"}
 
 
 if __name__ == "__main__":

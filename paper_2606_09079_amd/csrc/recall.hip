@@ -13,9 +13,14 @@
 // the c / 32 steps each lane holds the dot products of 4 heads with one entry,
 // applies ReLU and its gates, and two xor shuffles finish the sum over heads.
 //
-// One workgroup of 4 waves covers 64 entries of one sequence.  Its first act is
-// to issue the loads of all its index keys (every layer), so that they are in
-// flight while the queries and gates of the sequence are staged in LDS.
+// One workgroup of 4 waves covers 64 entries of one sequence.  It first copies
+// the sequence's queries from HBM straight into LDS (global->LDS copies), laid
+// out in MFMA operand order: each 1 KiB block is the A operand of one (layer,
+// 16-head block, k-step), so every operand is one conflict-free 16-byte LDS
+// read per lane.  Then it issues the loads of all its index keys, every layer.
+// Vector loads complete in order, so the barrier after the copy waits only for
+// the queries, and the products of layer l start as soon as layer l's keys are
+// in while later layers' keys are still arriving.
 #include "lsa_internal.h"
 
 namespace lsa {
@@ -25,14 +30,46 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+// s_waitcnt immediates (gfx9 encoding): at most n vector loads of this wave
+// outstanding, or no LDS operation outstanding
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+constexpr int kWaitLds = 0xF | (0x3 << 14) | (0x7 << 4);
+
+// The A operands of kBlocks MFMAs, one 1 KiB staged block each, read as one
+// assembly block that ends with its own LDS wait (the compiler would otherwise
+// make the first read wait for every vector load still in flight, since it
+// cannot tell these reads from the global->LDS copies).
+template <int N>
+__device__ __forceinline__ void read_blocks(const uint4 (*blocks)[64], int first, int lane, bf16x8 (&out)[N]) {
+  static_assert(N == 1 || N == 2 || N == 4, "1, 2 or 4 blocks");
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)&blocks[first][lane];
+  uint4 v[N];
+  if constexpr (N == 1) {
+    asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=&v"(v[0]) : "v"(a) : "memory");
+  } else if constexpr (N == 2) {
+    asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:1024\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&v"(v[0]), "=&v"(v[1]) : "v"(a) : "memory");
+  } else {
+    asm volatile(
+        "ds_read_b128 %0, %4\n\tds_read_b128 %1, %4 offset:1024\n\t"
+        "ds_read_b128 %2, %4 offset:2048\n\tds_read_b128 %3, %4 offset:3072\n\ts_waitcnt lgkmcnt(0)"
+        : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]) : "v"(a) : "memory");
+  }
+#pragma unroll
+  for (int i = 0; i < N; ++i) out[i] = __builtin_bit_cast(bf16x8, v[i]);
+}
 
 template <int NH, int CD, bool KEYS>
 __global__ void __launch_bounds__(kThreads)
 recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
-  constexpr int kPitch = CD / 8 + 1;  // uint4 per staged query row; the pad slot spreads rows over the banks
-  constexpr int kSteps = CD / 32;     // MFMA k-steps
-  constexpr int kBlocks = NH / 16;    // 16-head blocks
-  __shared__ uint4 sq[kMaxIdxLayers * NH * kPitch];
+  constexpr int kSteps = CD / 32;   // MFMA k-steps
+  constexpr int kBlocks = NH / 16;  // 16-head blocks
+  constexpr int kMaxStaged = kMaxIdxLayers * kBlocks * kSteps;
+  // staged block (l, hb, st) at index (l * kSteps + st) * kBlocks + hb: the
+  // kBlocks operands of one k-step are adjacent
+  __shared__ uint4 sq[kMaxStaged][64];
   __shared__ float sw[kMaxIdxLayers * NH];
 
   const int L = r.n_layers;
@@ -40,12 +77,26 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
   int b = 0;
   while (wg >= t.score_wg_off[b + 1]) ++b;
   const int n = t.n[b];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int e0 = (wg - t.score_wg_off[b]) * kRecallRowsPerWg + wave * 16;
   const int hi = lane >> 4;  // this lane's k-slice 8 hi .. 8 hi + 7 of every 32-wide step
 
+  // queries -> LDS in operand order: lane i of block (l, hb, st) holds
+  // q_l[16 hb + i % 16][32 st + 8 (i / 16) .. + 7]
+  const int n_staged = L * kBlocks * kSteps;
+  const uint16_t* qb = r.q + (int64_t)b * L * NH * CD + (lane & 15) * CD + 8 * hi;
+  for (int blk = wave; blk < n_staged; blk += kWaves) {  // wave-uniform
+    const int st = (blk / kBlocks) % kSteps, hb = blk % kBlocks, l = blk / (kBlocks * kSteps);
+    __builtin_amdgcn_global_load_lds((const void*)(qb + (l * NH + 16 * hb) * CD + 32 * st),
+                                     (void __attribute__((address_space(3)))*)&sq[blk][0], 16, 0, 0);
+  }
+  const float gate = r.w[(int64_t)b * L * NH + min(tid, L * NH - 1)];  // L * NH <= kThreads
+
   // B operands: entry e0 + lane % 16 (clamped; its result is not stored), dims
-  // 32 st + 8 hi .. + 7, every layer
+  // 32 st + 8 hi .. + 7, every layer (layers past L re-read layer 0 and are
+  // not used, so that the loads need no branches)
+  constexpr int kKeyLoads = kMaxIdxLayers * kSteps;
   bf16x8 kb[kMaxIdxLayers][kSteps];
   {
     const int ent = min(e0 + (lane & 15), n - 1);
@@ -54,15 +105,17 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
     for (int l = 0; l < kMaxIdxLayers; ++l)
 #pragma unroll
       for (int st = 0; st < kSteps; ++st)
-        kb[l][st] = l < L ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kp + l * r.layer_stride + 32 * st))
-                          : bf16x8{};
+        kb[l][st] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const uint4*>(kp + (l < L ? l : 0) * r.layer_stride + 32 * st));
   }
 
-  // queries [L][NH][CD] and gates [L][NH] of sequence b
-  const uint4* qsrc = reinterpret_cast<const uint4*>(r.q) + (int64_t)b * L * NH * (CD / 8);
-  for (int i = tid; i < L * NH * (CD / 8); i += kThreads) sq[(i / (CD / 8)) * kPitch + i % (CD / 8)] = qsrc[i];
-  for (int i = tid; i < L * NH; i += kThreads) sw[i] = r.w[(int64_t)b * L * NH + i];
-  __syncthreads();
+  // the copies and the gate are in once at most the key loads are outstanding
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(kKeyLoads));
+  if (tid < L * NH) sw[tid] = gate;
+  __builtin_amdgcn_s_waitcnt(kWaitLds);
+  __asm__ volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  __asm__ volatile("" ::: "memory");
   if (e0 >= n) return;
 
   float best = -INFINITY;
@@ -73,13 +126,13 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
 #pragma unroll
     for (int hb = 0; hb < kBlocks; ++hb) acc[hb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int st = 0; st < kSteps; ++st)
+    for (int st = 0; st < kSteps; ++st) {
+      bf16x8 a[kBlocks];  // A operands: heads 16 hb + lane % 16, dims 32 st + 8 hi .. + 7
+      read_blocks<kBlocks>(sq, (l * kSteps + st) * kBlocks, lane, a);
 #pragma unroll
-      for (int hb = 0; hb < kBlocks; ++hb) {
-        // A operand: head 16 hb + lane % 16, dims 32 st + 8 hi .. + 7
-        const uint4 a = sq[(l * NH + 16 * hb + (lane & 15)) * kPitch + 4 * st + hi];
-        acc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), kb[l][st], acc[hb], 0, 0, 0);
-      }
+      for (int hb = 0; hb < kBlocks; ++hb)
+        acc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hb], kb[l][st], acc[hb], 0, 0, 0);
+    }
     // acc[hb][j] = q_l[16 hb + 4 hi + j] . K_l[e0 + lane % 16]
     float x = 0.f;
 #pragma unroll
