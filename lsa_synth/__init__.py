@@ -36,6 +36,7 @@ _DEV_SO = os.path.join(_HERE, "libsynth_dev.so")
 GAMMA = 0x9E3779B97F4A7C15
 STREAM_K, STREAM_V, STREAM_Q, STREAM_E, STREAM_QE, STREAM_LEN, STREAM_QE_NOISE = 1, 2, 3, 4, 5, 6, 7
 STREAM_IDX_Q, STREAM_IDX_K, STREAM_IDX_W = 8, 9, 10
+STREAM_NAT_Q, STREAM_NAT_K, STREAM_NAT_W = 11, 12, 13
 M64 = (1 << 64) - 1
 
 
@@ -146,6 +147,13 @@ class Problem:
     idx_heads: int = 64
     idx_dim: int = 128
     idx_rate: float = 0.05
+    # two-level path: Level-2 budget k2 per sequence (empty = not used), native
+    # indexer heads, the always-resident window in tokens per sequence, and the
+    # fraction of entries the native gates are drawn to favour
+    core_keep: List[int] = field(default_factory=list)
+    nat_heads: int = 64
+    window_tokens: List[int] = field(default_factory=list)
+    nat_rate: float = 0.5
     meta: Dict[str, object] = field(default_factory=dict)
 
     @property
@@ -154,7 +162,22 @@ class Problem:
 
     @property
     def n_chunks(self) -> List[int]:
-        return [L // self.chunk for L in self.ctx_tokens]
+        """Chunks of every sequence, a partial last chunk included."""
+        return [(L + self.chunk - 1) // self.chunk for L in self.ctx_tokens]
+
+    def window_start(self, b: int) -> int:
+        """First chunk of the always-resident window: the chunks holding the last
+        window_tokens[b] tokens, and always the partial last chunk."""
+        W = self.window_tokens[b] if self.window_tokens else 0
+        return min(max(self.ctx_tokens[b] - W, 0) // self.chunk, self.ctx_tokens[b] // self.chunk)
+
+    def history_chunks(self, b: int) -> int:
+        """Complete chunks before the window: what the two levels select from."""
+        return self.window_start(b)
+
+    def tail_tokens(self, b: int) -> int:
+        """Tokens in the last chunk (chunk when it is complete)."""
+        return self.ctx_tokens[b] - (self.n_chunks[b] - 1) * self.chunk
 
     @property
     def chunk_offsets(self) -> List[int]:
@@ -218,11 +241,22 @@ def make_problem(name: str, seed: int = 0) -> Problem:
         n = 1048576 // 64
         return Problem("recall1m", [1048576], 64, [int(0.10 * n)], 32, 8, emb_dtype="bf16", idx_layers=3,
                        idx_heads=64, idx_dim=128, idx_rate=0.05)
+    if name == "twolevel_tiny":
+        return Problem("twolevel_tiny", [4096 + 37], 64, [24], 8, 8, emb_dtype="bf16", idx_layers=3, idx_heads=16,
+                       idx_dim=64, idx_rate=0.1, core_keep=[6], nat_heads=16, window_tokens=[512])
+    if name == "twolevel1m":
+        # a 1M-token context with a partial last chunk: Level 1 recalls at most
+        # 2,048 history chunks, Level 2 keeps 1,024 of them, plus the window of
+        # the last 8,192 tokens (129 chunks with the partial one)
+        return Problem("twolevel1m", [1048576 + 37], 64, [2048], 32, 8, emb_dtype="bf16", idx_layers=3,
+                       idx_heads=64, idx_dim=128, idx_rate=0.05, core_keep=[1024], nat_heads=64,
+                       window_tokens=[8192])
     raise KeyError(name)
 
 
 PRESETS = ("tiny", "int8", "paper1m", "batch32", "lookahead")
 RECALL_PRESETS = ("recall_tiny", "recall_batch", "recall1m")
+TWO_LEVEL_PRESETS = ("twolevel_tiny", "twolevel1m")
 
 
 # ------------------------------------------------------------ host inputs
@@ -275,7 +309,20 @@ def _recall_inputs(prob: Problem, seed: int) -> Dict[str, np.ndarray]:
         for l in range(L):
             sig = np.linalg.norm(qf[b, l], axis=-1) / math.sqrt(c)
             w[b, l] = (g[b, l] - _gate_shift(g[b, l], sig, prob.idx_rate)).astype(np.float32)
-    return {"idx_q": q, "idx_w": w, "idx_k": K.reshape(L, n, c)}
+    out = {"idx_q": q, "idx_w": w, "idx_k": K.reshape(L, n, c)}
+    if prob.core_keep:
+        # native indexer of Level 2: its own queries, gates and index keys
+        Hn = prob.nat_heads
+        nq = normal_bf16(stream_key(seed, STREAM_NAT_Q), 0, B * Hn * c).reshape(B, Hn, c)
+        nK = f64_to_bf16_bits(_unit_rows(normal_f64(stream_key(seed, STREAM_NAT_K), 0, n * c).reshape(n, c)))
+        ng = normal_f64(stream_key(seed, STREAM_NAT_W), 0, B * Hn).reshape(B, Hn)
+        nqf = bf16_bits_to_f64(nq)
+        nw = np.empty((B, Hn), dtype=np.float32)
+        for b in range(B):
+            sig = np.linalg.norm(nqf[b], axis=-1) / math.sqrt(c)
+            nw[b] = (ng[b] - _gate_shift(ng[b], sig, prob.nat_rate)).astype(np.float32)
+        out.update({"nat_q": nq, "nat_w": nw, "nat_k": nK})
+    return out
 
 
 def host_inputs(prob: Problem, seed: int) -> Dict[str, object]:
@@ -362,12 +409,13 @@ def kv_chunks(prob: Problem, seed: int, which: str, b: int, h: int, chunks) -> n
 
 
 def kv_head_sparse(prob: Problem, seed: int, which: str, b: int, h: int, chunks) -> np.ndarray:
-    """Logical token-major K or V of one (sequence, KV head): [ctx_tokens][head_dim].
+    """Logical token-major K or V of one (sequence, KV head): [n_chunks * chunk][head_dim]
+    (the slots past the context end of a partial last chunk hold values too).
 
     Only the listed chunks are filled; every other token is zero.
     """
     C = prob.chunk
-    full = np.zeros((prob.ctx_tokens[b], prob.head_dim), dtype=np.uint16)
+    full = np.zeros((prob.n_chunks[b] * C, prob.head_dim), dtype=np.uint16)
     chunks = np.asarray(chunks, dtype=np.int64)
     if len(chunks):
         vals = kv_chunks(prob, seed, which, b, h, chunks)
@@ -466,7 +514,7 @@ def device_inputs(prob: Problem, seed: int, device: str = "cuda", host: Optional
     fill_kv_device(prob, seed, "k", k.data_ptr(), table.data_ptr(), stream)
     fill_kv_device(prob, seed, "v", v.data_ptr(), table.data_ptr(), stream)
     out = {"qe": up(h["qe"]), "E": up(h["E"]), "q": up(h["q"]), "k": k, "v": v, "table": table, "host": h}
-    for name in ("idx_q", "idx_w", "idx_k"):
+    for name in ("idx_q", "idx_w", "idx_k", "nat_q", "nat_w", "nat_k"):
         if name in h:
             out[name] = up(h[name])
     return out

@@ -66,6 +66,10 @@ def bind(path: str) -> ctypes.CDLL:
     L.oracle_index_score_bf16.restype = None
     L.oracle_recall.argtypes = [_P, _I32, _I64, _I64, _P]
     L.oracle_recall.restype = _I64
+    L.oracle_attention_tokens.argtypes = [_P, _I32, _P, _P, _I64, _I32, _P, _I64, _F64, _P, _P]
+    L.oracle_attention_tokens.restype = ctypes.c_int
+    L.oracle_two_level.argtypes = [_P, _I64, _P, _I64, _I64, _I64, _I64, _P]
+    L.oracle_two_level.restype = _I64
     return L
 
 
@@ -185,6 +189,58 @@ def recall_for_sequence(prob, inputs: Dict[str, object], b: int):
     x = np.stack([index_score(inputs["idx_q"][b, l], inputs["idx_w"][b, l], inputs["idx_k"][l, lo:hi])
                   for l in range(L)])
     return x, recall(x, prob.keep[b])
+
+
+def attention_tokens(q_rows: np.ndarray, Kh: np.ndarray, Vh: np.ndarray, toks: np.ndarray,
+                     scale: Optional[float] = None):
+    """Attention of q_rows [R][d] over the explicit token list ``toks`` of one KV
+    head (Kh, Vh logical token-major bf16 bit patterns).  Returns (out, lse)."""
+    R, d = q_rows.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    q_rows, Kh, Vh = _c(q_rows, np.uint16), _c(Kh, np.uint16), _c(Vh, np.uint16)
+    toks = _c(toks, np.int64)
+    out = np.empty((R, d), dtype=np.float64)
+    lse = np.empty(R, dtype=np.float64)
+    rc = lib().oracle_attention_tokens(q_rows.ctypes.data, R, Kh.ctypes.data, Vh.ctypes.data, Kh.shape[0], d,
+                                       toks.ctypes.data, len(toks), float(scale), out.ctypes.data, lse.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_attention_tokens rejected its input")
+    return out, lse
+
+
+def two_level(recalled: np.ndarray, native: np.ndarray, k2: int, w0: int, n_total: int) -> np.ndarray:
+    """Level 2 (top-k2 of the native score within the recalled history ids) plus
+    the window chunks w0 .. n_total - 1; ascending ids."""
+    recalled, native = _c(recalled, np.int32), _c(native, np.float64)
+    out = np.empty(len(recalled) + max(n_total - w0, 0) + 1, dtype=np.int32)
+    m = lib().oracle_two_level(recalled.ctypes.data, len(recalled), native.ctypes.data, len(native), k2, w0,
+                               n_total, out.ctypes.data)
+    if m < 0:
+        raise ValueError("oracle_two_level rejected its input")
+    return out[:m].copy()
+
+
+def two_level_for_sequence(prob, inputs: Dict[str, object], b: int):
+    """Level 1 (recall over the history before the window), Level 2 and the
+    window for sequence b.  Returns (x [L][n_hist], recalled, native [n_hist],
+    kept ascending chunk ids, token count of the last chunk)."""
+    lo = prob.chunk_offsets[b]
+    n_hist, w0, n_total, tail = prob.history_chunks(b), prob.window_start(b), prob.n_chunks[b], prob.tail_tokens(b)
+    L = prob.idx_layers
+    x = np.stack([index_score(inputs["idx_q"][b, l], inputs["idx_w"][b, l], inputs["idx_k"][l, lo:lo + n_hist])
+                  for l in range(L)]) if n_hist > 0 else np.zeros((L, 0))
+    recalled = recall(x, prob.keep[b]) if n_hist > 0 else np.zeros(0, dtype=np.int32)
+    native = (index_score(inputs["nat_q"][b], inputs["nat_w"][b], inputs["nat_k"][lo:lo + n_hist])
+              if n_hist > 0 else np.zeros(0))
+    kept = two_level(recalled, native, prob.core_keep[b], w0, n_total)
+    return x, recalled, native, kept, tail
+
+
+def kept_tokens(kept: np.ndarray, chunk: int, ctx_tokens: int) -> np.ndarray:
+    """Token list of the kept chunks, ascending, the last chunk cut at the context end."""
+    return np.concatenate([np.arange(c * chunk, min((c + 1) * chunk, ctx_tokens)) for c in kept]) \
+        if len(kept) else np.zeros(0, dtype=np.int64)
 
 
 # ---------------------------------------------------------------- O4 step

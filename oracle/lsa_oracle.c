@@ -25,6 +25,11 @@
  *    softmax(q K^T * scale) V over the tokens of the kept chunks, with query
  *    head h reading KV head floor(h / G).  An empty kept set gives out = 0 and
  *    lse = -inf (the empty sum), which only the recall path below can produce.
+ *  - Two-level selection (Sec. 2.1 after Eq. 5; Sec. 2.5): the history is the
+ *    complete entries before the always-resident window; Level 1 recalls from
+ *    it as below, Level 2 keeps the k2 recalled entries with the largest native
+ *    indexer score (Eq. 6, lower id first on ties), and the kept set is those
+ *    plus every chunk of the window, the last one possibly partial.
  *  - Recall (the full Memory Indexer of Sec. 2.1 Eq. 4, the threshold of Eq. 5,
  *    the OR over indexer layers of Eq. 13 and the K_max bound of Sec. 2.5):
  *    layer l recalls entry s when sigma(x_l(s)) >= 1/2 with
@@ -202,6 +207,50 @@ int oracle_attention(const uint16_t* q, int32_t R, const uint16_t* Kh, const uin
   return 0;
 }
 
+/*
+ * Attention of R query rows over an explicit list of tokens of one KV head
+ * (the token-level form of the function above, for kept sets whose last
+ * chunk is partial).  toks [ntoks] are token indices < n_tok, attended in the
+ * given order.  Returns 0, or -1 on a bad argument or allocation failure.
+ */
+int oracle_attention_tokens(const uint16_t* q, int32_t R, const uint16_t* Kh, const uint16_t* Vh, int64_t n_tok,
+                            int32_t d, const int64_t* toks, int64_t ntoks, double scale, double* out, double* lse) {
+  if (R < 1 || d < 1 || ntoks < 0) return -1;
+  for (int64_t i = 0; i < ntoks; ++i)
+    if (toks[i] < 0 || toks[i] >= n_tok) return -1;
+  if (ntoks == 0) { /* nothing to attend: the empty sum */
+    for (int64_t i = 0; i < (int64_t)R * d; ++i) out[i] = 0.0;
+    for (int32_t r = 0; r < R; ++r) lse[r] = -INFINITY;
+    return 0;
+  }
+  double* w = (double*)malloc((size_t)ntoks * sizeof *w);
+  if (!w) return -1;
+  for (int32_t r = 0; r < R; ++r) {
+    const uint16_t* qr = q + (int64_t)r * d;
+    for (int64_t i = 0; i < ntoks; ++i) {
+      double dot = 0.0;
+      for (int32_t e = 0; e < d; ++e) dot += bf16_to_f64(qr[e]) * bf16_to_f64(Kh[toks[i] * d + e]);
+      w[i] = dot * scale;
+    }
+    double m = w[0];
+    for (int64_t i = 1; i < ntoks; ++i)
+      if (w[i] > m) m = w[i];
+    double Z = 0.0;
+    for (int64_t i = 0; i < ntoks; ++i) {
+      w[i] = exp(w[i] - m);
+      Z += w[i];
+    }
+    for (int32_t e = 0; e < d; ++e) {
+      double acc = 0.0;
+      for (int64_t i = 0; i < ntoks; ++i) acc += w[i] * bf16_to_f64(Vh[toks[i] * d + e]);
+      out[(int64_t)r * d + e] = acc / Z;
+    }
+    lse[r] = m + log(Z);
+  }
+  free(w);
+  return 0;
+}
+
 /* ---------------------------------------------------------------- R recall */
 
 /*
@@ -262,4 +311,39 @@ int64_t oracle_recall(const double* x, int32_t L, int64_t n, int64_t kmax, int32
   free(v);
   qsort(out, (size_t)m, sizeof *out, ascending_i32);
   return m;
+}
+
+/*
+ * Level 2 of the two-level selection and the window (Sec. 2.1 after Eq. 5,
+ * Eq. 6; Sec. 2.5).  recalled [m] are the ascending ids that Level 1 kept from
+ * the history (entries before w0); native [n_hist] is the native indexer's
+ * score of every history entry.  The k2 recalled entries with the largest
+ * native score stay (all of them when m <= k2; lower id first on ties); the
+ * kept set is those plus the window chunks w0 .. n_total - 1.  Writes the kept
+ * ids in ascending order and returns their count, or -1 on a bad argument or
+ * allocation failure.
+ */
+int64_t oracle_two_level(const int32_t* recalled, int64_t m, const double* native, int64_t n_hist, int64_t k2,
+                         int64_t w0, int64_t n_total, int32_t* out) {
+  if (m < 0 || k2 < 1 || n_hist < 0 || w0 < n_hist || w0 > n_total) return -1;
+  for (int64_t j = 0; j < m; ++j)
+    if (recalled[j] < 0 || recalled[j] >= n_hist || (j > 0 && recalled[j] <= recalled[j - 1])) return -1;
+  int64_t core = m;
+  if (m > 0) {
+    scored_f* v = (scored_f*)malloc((size_t)m * sizeof *v);
+    if (!v) return -1;
+    for (int64_t j = 0; j < m; ++j) {
+      v[j].s = native[recalled[j]];
+      v[j].c = recalled[j];
+    }
+    if (m > k2) {
+      qsort(v, (size_t)m, sizeof *v, by_score_desc_f);
+      core = k2;
+    }
+    for (int64_t j = 0; j < core; ++j) out[j] = (int32_t)v[j].c;
+    free(v);
+    qsort(out, (size_t)core, sizeof *out, ascending_i32);
+  }
+  for (int64_t c = w0; c < n_total; ++c) out[core + (c - w0)] = (int32_t)c;
+  return core + (n_total - w0);
 }

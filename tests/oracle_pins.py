@@ -356,6 +356,64 @@ def pin_recall_boundaries():
     assert oracle.recall(x[None, :], 25).tolist() == [], "nothing recalled"
 
 
+# ---------------------------------------------------------------- two-level
+def pin_attention_tokens_reduces_to_chunks():
+    """Token-list attention equals the pinned chunk attention: with whole chunks
+    on the chunk list, and token by token as chunks of one token; a single token
+    returns its V row; the empty list is the empty sum."""
+    rng = np.random.default_rng(18)
+    n_chunks, C, d = 6, 8, 16
+    K, V = _rand_head(rng, n_chunks * C, d)
+    q = _bf16(rng.standard_normal((3, d)))
+    kept = np.array([0, 2, 5])
+    toks = np.concatenate([np.arange(c * C, (c + 1) * C) for c in kept])
+    a, la = oracle.attention_tokens(q, K, V, toks)
+    b, lb = oracle.attention(q, K, V, kept, C)
+    assert np.array_equal(a, b) and np.array_equal(la, lb), "whole chunks"
+    part = np.concatenate([toks, np.arange(3 * C, 3 * C + 5)])  # a partial chunk of 5 tokens
+    a, la = oracle.attention_tokens(q, K, V, part)
+    b, lb = oracle.attention(q, K, V, part.astype(np.int32), 1)
+    assert np.array_equal(a, b) and np.array_equal(la, lb), "token by token"
+    a, _ = oracle.attention_tokens(q, K, V, np.array([11]))
+    assert np.array_equal(a, np.tile(_f64(V)[11], (3, 1))), "single token"
+    a, la = oracle.attention_tokens(q, K, V, np.zeros(0, dtype=np.int64))
+    assert np.array_equal(a, np.zeros((3, d))) and np.all(np.isneginf(la)), "empty list"
+
+
+def pin_two_level_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "two_level_worked.json")))
+    for case in g["cases"]:
+        got = oracle.two_level(np.array(g["recalled"]), np.array(g["native"], dtype=np.float64), case["k2"], g["w0"],
+                               g["n_total"])
+        assert got.tolist() == case["kept"], f"worked two-level, k2={case['k2']}"
+
+
+def pin_two_level_bruteforce():
+    """Level 2 keeps, among all k2-subsets of the recalled ids, the one with the
+    largest native-score sum and, among those, the smallest ascending id list
+    (all recalled ids when there are at most k2); the window chunks are always
+    appended; nothing recalled leaves the window alone."""
+    rng = np.random.default_rng(19)
+    for _ in range(80):
+        n_hist = int(rng.integers(0, 9))
+        n_total = n_hist + int(rng.integers(0, 4))
+        native = rng.integers(-2, 3, size=n_hist).astype(np.float64)
+        rec = sorted(rng.choice(n_hist, size=int(rng.integers(0, n_hist + 1)), replace=False).tolist()) \
+            if n_hist else []
+        k2 = int(rng.integers(1, 6))
+        if len(rec) <= k2:
+            core = rec
+        else:
+            core, best = None, -math.inf
+            for comb in itertools.combinations(rec, k2):
+                tot = native[list(comb)].sum()
+                if tot > best:
+                    core, best = list(comb), tot
+        want = core + list(range(n_hist, n_total))
+        got = oracle.two_level(np.array(rec, dtype=np.int32), native, k2, n_hist, n_total).tolist()
+        assert got == want, f"two-level brute force rec={rec} native={native.tolist()} k2={k2}"
+
+
 ALL_PINS = [
     pin_score_library_matmul, pin_score_int8_exact, pin_score_closed_forms,
     pin_topk_worked_example, pin_topk_bruteforce, pin_topk_library_sort, pin_union_bruteforce,
@@ -363,5 +421,6 @@ ALL_PINS = [
     pin_gqa_mapping, pin_attention_empty_set,
     pin_recall_worked_example, pin_index_score_single_head, pin_index_score_relu_identities,
     pin_index_score_head_permutation, pin_recall_sigmoid_threshold, pin_recall_or_bruteforce,
-    pin_recall_boundaries,
+    pin_recall_boundaries, pin_attention_tokens_reduces_to_chunks, pin_two_level_worked_example,
+    pin_two_level_bruteforce,
 ]

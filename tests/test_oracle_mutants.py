@@ -41,10 +41,24 @@ MUTANTS = {
                            "const int64_t tok = (int64_t)sel[i / C] + i % C;\n        acc"),
     "attn_k_transposed_dims": ("bf16_to_f64(Kh[tok * d + e])", "bf16_to_f64(Kh[tok * d + (d - 1 - e)])"),
     "attn_v_transposed_dims": ("bf16_to_f64(Vh[tok * d + e])", "bf16_to_f64(Vh[tok * d + (d - 1 - e)])"),
-    "attn_lse_dropped_max": ("lse[r] = m + log(Z);", "lse[r] = log(Z);"),
-    "attn_unnormalised": ("out[(int64_t)r * d + e] = acc / Z;", "out[(int64_t)r * d + e] = acc;"),
-    "attn_empty_lse_zero": ("for (int32_t r = 0; r < R; ++r) lse[r] = -INFINITY;",
-                            "for (int32_t r = 0; r < R; ++r) lse[r] = 0.0;"),
+    "attn_lse_dropped_max": ("    lse[r] = m + log(Z);\n  }\n  free(logit);", "    lse[r] = log(Z);\n  }\n  free(logit);"),
+    "attn_unnormalised": ("      out[(int64_t)r * d + e] = acc / Z;\n    }\n    lse[r] = m + log(Z);\n  }\n  free(logit);",
+                          "      out[(int64_t)r * d + e] = acc;\n    }\n    lse[r] = m + log(Z);\n  }\n  free(logit);"),
+    "tokens_lse_dropped_max": ("    lse[r] = m + log(Z);\n  }\n  free(w);", "    lse[r] = log(Z);\n  }\n  free(w);"),
+    "tokens_unnormalised": ("      out[(int64_t)r * d + e] = acc / Z;\n    }\n    lse[r] = m + log(Z);\n  }\n  free(w);",
+                            "      out[(int64_t)r * d + e] = acc;\n    }\n    lse[r] = m + log(Z);\n  }\n  free(w);"),
+    "attn_empty_lse_zero": ("  if (nsel == 0) { /* nothing to attend: the empty sum */\n"
+                            "    for (int64_t i = 0; i < (int64_t)R * d; ++i) out[i] = 0.0;\n"
+                            "    for (int32_t r = 0; r < R; ++r) lse[r] = -INFINITY;",
+                            "  if (nsel == 0) { /* nothing to attend: the empty sum */\n"
+                            "    for (int64_t i = 0; i < (int64_t)R * d; ++i) out[i] = 0.0;\n"
+                            "    for (int32_t r = 0; r < R; ++r) lse[r] = 0.0;"),
+    "tokens_empty_lse_zero": ("  if (ntoks == 0) { /* nothing to attend: the empty sum */\n"
+                              "    for (int64_t i = 0; i < (int64_t)R * d; ++i) out[i] = 0.0;\n"
+                              "    for (int32_t r = 0; r < R; ++r) lse[r] = -INFINITY;",
+                              "  if (ntoks == 0) { /* nothing to attend: the empty sum */\n"
+                              "    for (int64_t i = 0; i < (int64_t)R * d; ++i) out[i] = 0.0;\n"
+                              "    for (int32_t r = 0; r < R; ++r) lse[r] = 0.0;"),
     "idx_dropped_relu": ("const double relu = dot > 0.0 ? dot : 0.0;", "const double relu = dot;"),
     "idx_gate_inside_relu": ("x += (double)w[h] * relu;",
                              "x += (double)w[h] * dot > 0.0 ? (double)w[h] * dot : 0.0;"),
@@ -55,6 +69,12 @@ MUTANTS = {
                                 "for (int32_t l = 0; l < 1; ++l) {\n      const double xl"),
     "recall_ranks_first_layer": ("if (xl > best) best = xl;", "if (xl > best && l < 0) best = xl;"),
     "recall_bound_ignored": ("  if (m > kmax) {", "  if (m > n) {"),
+    "tokens_dropped_scale": ("      w[i] = dot * scale;", "      w[i] = dot;"),
+    "tokens_v_wrong_token": ("acc += w[i] * bf16_to_f64(Vh[toks[i] * d + e]);",
+                             "acc += w[i] * bf16_to_f64(Vh[toks[ntoks - 1 - i] * d + e]);"),
+    "two_level_native_by_position": ("      v[j].s = native[recalled[j]];", "      v[j].s = native[j];"),
+    "two_level_budget_ignored": ("    if (m > k2) {", "    if (m > n_hist) {"),
+    "two_level_window_short": ("  for (int64_t c = w0; c < n_total; ++c)", "  for (int64_t c = w0 + 1; c < n_total; ++c)"),
 }
 
 
