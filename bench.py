@@ -53,6 +53,12 @@ WORKLOADS = {
                     "2 layers x 32 heads x 128, no K_max cut, 32 query / 8 KV heads, head_dim 128, bf16 K/V",
     "recall_tiny": "recall_tiny: 4,096 tokens, 64-token chunks (64), Memory Indexer of 3 layers x 16 heads x 64, "
                    "K_max 12, 8 query / 8 KV heads, head_dim 128, bf16 K/V",
+    "twolevel1m": "twolevel1m: 1,048,613-token context (16,385 64-token chunks, the last one 37 tokens), Level 1: "
+                  "Memory Indexer of 3 layers x 64 heads x 128 over the history, K_max 2,048; Level 2: native "
+                  "indexer of 64 heads keeps 1,024; plus the window of the last 8,192 tokens; 32 query / 8 KV heads, "
+                  "head_dim 128, bf16 K/V, batch 1",
+    "twolevel_tiny": "twolevel_tiny: 4,133 tokens (65 chunks, the last one 37 tokens), Level 1 3 x 16 x 64 with "
+                     "K_max 24, Level 2 keeps 6, window 512 tokens, 8 query / 8 KV heads, head_dim 128, bf16 K/V",
 }
 EMB_BYTES = {"f32": 4, "bf16": 2, "i8": 1}
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "attn_kernel_paper1m_traffic.md")
@@ -126,6 +132,7 @@ def main() -> int:
     host0 = synth.host_inputs(prob, 0)
     dev = synth.device_inputs(prob, 0, host=host0)
     recall = prob.idx_layers > 0
+    two_level = bool(prob.core_keep)
 
     def up(a):
         a = np.ascontiguousarray(a)
@@ -135,16 +142,20 @@ def main() -> int:
     for r in range(args.rotations):
         h = host0 if r == 0 else synth.host_inputs(prob, 1000 + r)
         # the query side changes from step to step; embeddings, index keys and K/V stay
-        rot.append({"qe": up(h["qe"]), "q": up(h["q"]), **({"idx_q": up(h["idx_q"]), "idx_w": up(h["idx_w"])}
-                                                           if recall else {})})
+        rot.append({"qe": up(h["qe"]), "q": up(h["q"]),
+                    **({"idx_q": up(h["idx_q"]), "idx_w": up(h["idx_w"])} if recall else {}),
+                    **({"nat_q": up(h["nat_q"]), "nat_w": up(h["nat_w"])} if two_level else {})})
     P = L.Problem.from_synth(prob)
     ix = L.Indexer.from_synth(prob) if recall else None
+    tl = L.TwoLevel.from_synth(prob) if two_level else None
     B, Tq, Hq, d = prob.batch, prob.n_qtok, prob.n_q_heads, prob.head_dim
-    ws_bytes = L.lsa_workspace_size(P)
+    if two_level:
+        max_sel, ws_bytes = L.lsa_two_level_sizes(P, tl)
+    else:
+        ws_bytes, max_sel = L.lsa_workspace_size(P), L.lsa_max_sel(P)
     ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
     out = torch.empty(B, Tq, Hq, d, dtype=torch.float32, device="cuda")
     lse = torch.empty(B, Tq, Hq, dtype=torch.float32, device="cuda")
-    max_sel = L.lsa_max_sel(P)
     sels = [torch.empty(B, max_sel, dtype=torch.int32, device="cuda") for _ in rot]
     cnts = [torch.empty(B, dtype=torch.int32, device="cuda") for _ in rot]
     torch.cuda.synchronize()
@@ -152,15 +163,24 @@ def main() -> int:
 
     def step(i: int) -> None:
         r = rot[i % len(rot)]
-        if recall:
+        if two_level:
+            L.lsa_two_level_step(P, ix, tl, r["idx_q"], r["idx_w"], dev["idx_k"], r["nat_q"], r["nat_w"],
+                                 dev["nat_k"], r["q"], dev["k"], dev["v"], 0.0, out, lse, sels[i % len(rot)],
+                                 cnts[i % len(rot)], ws, ws_bytes, stream)
+        elif recall:
             L.lsa_recall_step(P, ix, r["idx_q"], r["idx_w"], dev["idx_k"], r["q"], dev["k"], dev["v"], 0.0, out,
                               lse, sels[i % len(rot)], cnts[i % len(rot)], ws, ws_bytes, stream)
         else:
             L.lsa_decode_step(P, r["qe"], dev["E"], r["q"], dev["k"], dev["v"], 0.0, out, lse, sels[i % len(rot)],
                               cnts[i % len(rot)], ws, ws_bytes, stream)
 
+    # attention alone over the kept sets of the steps; the two-level kept sets
+    # have the row pitch of a problem whose keep budget is that pitch
+    PA = L.Problem(prob.ctx_tokens, prob.chunk, [max_sel] * B, prob.n_q_heads, prob.n_kv_heads, prob.head_dim,
+                   prob.emb_dim, prob.n_lookahead, prob.n_qtok, prob.emb_dtype) if two_level else P
+
     def attn(i: int) -> None:
-        L.lsa_sparse_decode_attn(P, rot[i % len(rot)]["q"], dev["k"], dev["v"], sels[i % len(rot)],
+        L.lsa_sparse_decode_attn(PA, rot[i % len(rot)]["q"], dev["k"], dev["v"], sels[i % len(rot)],
                                  cnts[i % len(rot)], 0.0, out, lse, ws, ws_bytes, stream)
 
     # every rotation's kept set exists before any attention-only launch
@@ -255,7 +275,12 @@ def main() -> int:
     C, Hkv = prob.chunk, prob.n_kv_heads
     kv_bytes = [n * C * Hkv * d * 2 * 2 for n in counts]
     attn_bytes = sum(kv_bytes) / len(kv_bytes) + B * Tq * Hq * d * (2 + 4) + B * Tq * Hq * 4 + max(counts) * 4
-    if recall:  # index keys of every layer, plus the indexer queries and gates
+    if two_level:  # Level-1 keys of the history, native keys of (at most) K_max recalled chunks, queries, gates
+        Lay, nh, c = prob.idx_layers, prob.idx_heads, prob.idx_dim
+        hist = sum(prob.history_chunks(b) for b in range(B))
+        rec = sum(min(prob.keep[b], prob.history_chunks(b)) for b in range(B))
+        emb_bytes = (Lay * hist + rec) * c * 2 + B * (Lay * nh + prob.nat_heads) * (c * 2 + 4)
+    elif recall:  # index keys of every layer, plus the indexer queries and gates
         Lay, nh, c = prob.idx_layers, prob.idx_heads, prob.idx_dim
         emb_bytes = Lay * prob.total_chunks * c * 2 + B * Lay * nh * (c * 2 + 4)
     else:
@@ -309,6 +334,8 @@ def cpu_baseline(prob, host, budget_s: float):
     import oracle
 
     def select():
+        if prob.core_keep:
+            return oracle.two_level_for_sequence(prob, host, 0)[3]
         if prob.idx_layers > 0:
             return oracle.recall_for_sequence(prob, host, 0)[1]
         return oracle.select_for_sequence(prob, host, 0)[2]
@@ -323,9 +350,11 @@ def cpu_baseline(prob, host, budget_s: float):
     def one_step():
         kept_s = select()
 
+        toks = oracle.kept_tokens(kept_s, prob.chunk, prob.ctx_tokens[0])
+
         def head(g):
             qr = np.stack([host["q"][0, 0, g * G + j] for j in range(G)])
-            return oracle.attention(qr, kv[("k", g)], kv[("v", g)], kept_s, prob.chunk)
+            return oracle.attention_tokens(qr, kv[("k", g)], kv[("v", g)], toks)
 
         with cf.ThreadPoolExecutor(threads) as ex:
             list(ex.map(head, range(Hkv)))
@@ -340,7 +369,11 @@ def cpu_baseline(prob, host, budget_s: float):
     full = prob.batch == 1 and prob.n_qtok == 1
     what = ("full step(s) of the same workload" if full else
             "step(s) of sequence 0 of the same workload, attention for its first query token only")
-    if prob.idx_layers > 0:
+    if prob.core_keep:
+        sel_what = (f"{prob.idx_layers}-layer x {prob.idx_heads}-head index scores of {prob.history_chunks(0):,} "
+                    f"history chunks, recall bounded by {prob.keep[0]:,}, native top-{prob.core_keep[0]:,}, "
+                    f"window of {prob.n_chunks[0] - prob.window_start(0)} chunks")
+    elif prob.idx_layers > 0:
         sel_what = (f"{prob.idx_layers}-layer x {prob.idx_heads}-head index scores of {prob.n_chunks[0]:,} chunks, "
                     f"recall bounded by {prob.keep[0]:,}")
     else:

@@ -57,6 +57,11 @@
  * steps 1 and 2 -- a gated multi-head score per indexer layer (Eq. 4), the
  * sigmoid threshold 1/2 (Eq. 5), the OR over L indexer layers (Eq. 13) and
  * the bound K_max on the recalled set (Sec. 2.5) -- followed by step 3.
+ *
+ * Two-level path (lsa_two_level_*): that recall over the history before an
+ * always-resident window (Level 1), the native indexer's top-k inside the
+ * recalled set (Level 2, Eq. 6), and the window chunks added (Sec. 2.5); the
+ * context may end inside a chunk, whose missing tokens get no weight.
  */
 #ifndef LSA_H_
 #define LSA_H_
@@ -112,6 +117,15 @@ typedef struct lsa_indexer {
   int32_t reserved;  /* must be 0 */
 } lsa_indexer;
 
+/* Two-level selection.  Host memory only; read during the call. */
+typedef struct lsa_two_level {
+  int32_t native_heads;          /* heads of the native indexer of Level 2: 16, 32 or 64 (key width as the
+                                    lsa_indexer's key_dim) */
+  int32_t reserved;              /* must be 0 */
+  const int32_t* core_keep;      /* HOST [B]: Level-2 budget k2_b >= 1 */
+  const int64_t* window_tokens;  /* HOST [B]: always-resident context tail in tokens, >= 0 */
+} lsa_two_level;
+
 int lsa_abi_version(void);
 const char* lsa_status_string(lsa_status status);
 /* Message of the last failed call on this host thread ("" if none). */
@@ -159,7 +173,11 @@ lsa_status lsa_topk_chunks(const lsa_problem* p, const void* scores, int32_t* se
  * nullable.  Split-K partials live in the workspace and are merged in a fixed
  * order, so results are bitwise reproducible.  Chunk ids must be < n_b and
  * sel_count[b] must be in 0 .. max_sel; an empty kept set (which only the
- * recall path produces) gives out = 0 and lse = -inf.
+ * recall path produces) gives out = 0 and lse = -inf.  Unlike the other
+ * entry points of steps 1 and 2 this one also takes a context that ends
+ * inside a chunk (n_b = ceil(ctx_tokens[b] / chunk_size)); tokens past the
+ * context end get no weight, which needs n_qtok * n_q_heads / n_kv_heads <= 16
+ * (LSA_ERR_UNSUPPORTED otherwise).
  */
 lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const uint16_t* k_cache,
                                   const uint16_t* v_cache, const int32_t* sel_idx,
@@ -212,6 +230,37 @@ lsa_status lsa_recall_step(const lsa_problem* p, const lsa_indexer* ix, const vo
                            const void* idx_k, const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
                            float softmax_scale, float* out, float* lse, int32_t* sel_idx, int32_t* sel_count,
                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Two-level path.  The problem must have n_lookahead == 1; ctx_tokens[b] may be
+ * any positive count: sequence b has n_b = ceil(ctx_tokens[b] / chunk_size)
+ * chunks (every chunk-indexed tensor counts them all), the last one possibly
+ * partial.  keep[b] is the Level-1 bound K_max.  The window is the chunks
+ * w0_b .. n_b - 1 with w0_b = min(floor(max(ctx - window_tokens, 0) / C),
+ * floor(ctx / C)), so it always holds a partial last chunk; the history is
+ * the complete chunks 0 .. w0_b - 1.  Per sequence:
+ *   Level 1  recalled = the recall of lsa_recall_select over the history
+ *            (idx_q, idx_w, idx_k as for lsa_recall_scores)
+ *   Level 2  native[s] = sum_h nat_w[b][h] * ReLU(nat_q[b][h] . nat_k[chunk_off[b] + s])
+ *            for the recalled s; the k2_b recalled chunks with the largest
+ *            native score stay (all of them when there are at most k2_b;
+ *            ties towards the lower id)
+ *   kept     those chunks, ascending, then w0_b .. n_b - 1
+ * then step 3 over the kept chunks; tokens past ctx_tokens[b] in the last
+ * chunk get no weight.  Layouts: nat_q bf16 [B][native_heads][key_dim],
+ * nat_w float32 [B][native_heads], nat_k bf16 [sum_b n_b][key_dim].  A context
+ * that ends inside a chunk needs n_qtok * n_q_heads / n_kv_heads <= 16
+ * (LSA_ERR_UNSUPPORTED otherwise).
+ */
+/* Row pitch of sel_idx and the workspace size of lsa_two_level_step (either
+ * output pointer may be NULL). */
+lsa_status lsa_two_level_sizes(const lsa_problem* p, const lsa_two_level* tl, int32_t* max_sel,
+                               size_t* ws_bytes);
+lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const lsa_two_level* tl,
+                              const void* idx_q, const float* idx_w, const void* idx_k, const void* nat_q,
+                              const float* nat_w, const void* nat_k, const uint16_t* q, const uint16_t* k_cache,
+                              const uint16_t* v_cache, float softmax_scale, float* out, float* lse, int32_t* sel_idx,
+                              int32_t* sel_count, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -8,6 +8,7 @@ kernels behind the C ABI of ``include/lsa.h``.  The Python layer is the thin
 ctypes binding in :mod:`.lsa`; importing it loads ``liblsa.so`` and raises if
 that is not possible.
 """
-from .lsa import (LIB, Indexer, LsaError, Problem, lsa_decode_step, lsa_max_keep, lsa_max_sel,  # noqa: F401
-                  lsa_recall_scores, lsa_recall_select, lsa_recall_step, lsa_score_chunks, lsa_sparse_decode_attn,
-                  lsa_topk_chunks, lsa_validate, lsa_workspace_init, lsa_workspace_size, last_error)
+from .lsa import (LIB, Indexer, LsaError, Problem, TwoLevel, lsa_decode_step, lsa_max_keep,  # noqa: F401
+                  lsa_max_sel, lsa_recall_scores, lsa_recall_select, lsa_recall_step, lsa_score_chunks,
+                  lsa_sparse_decode_attn, lsa_topk_chunks, lsa_two_level_sizes, lsa_two_level_step, lsa_validate,
+                  lsa_workspace_init, lsa_workspace_size, last_error)

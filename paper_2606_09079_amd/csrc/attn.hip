@@ -165,7 +165,9 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
 
   // K and V tiles are 8 KiB each and contiguous in the MFMA-ordered block
   // layout: load instruction q of a tile reads bytes [1024 q, 1024 q + 1024).
-  auto load_tile = [&](int i, bf16x8(&kt)[8], bf16x8(&vt)[8]) {
+  // Returns how many of the tile's tokens exist: 32, or fewer in the last
+  // chunk of a context that ends inside it (and <= 0 for a tile past the end).
+  auto load_tile = [&](int i, bf16x8(&kt)[8], bf16x8(&vt)[8]) -> int {
     const int T = Tb + i;
     const int j = T / TPC - pos0, tt = T % TPC;
     if (j - sel_base >= 64) {  // wave-uniform: next window of chunk ids
@@ -180,9 +182,11 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
     for (int q = 0; q < 8; ++q) kt[q] = load8_stream(kp + q * 512);
 #pragma unroll
     for (int q = 0; q < 8; ++q) vt[q] = load8_stream(vp + q * 512);
+    return c == n_b - 1 ? t.tail[b] - 32 * tt : 32;
   };
 
-  auto compute_tile = [&](const bf16x8(&kt)[8], const bf16x8(&vt)[8]) {
+  auto compute_tile = [&](const bf16x8(&kt)[8], const bf16x8(&vt)[8], int lim) {
+    if (lim <= 0) return;  // wave-uniform: the tile lies past the context end
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
@@ -197,7 +201,15 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
       x[i] *= a.scale_log2e;
       mx = fmaxf(mx, x[i]);
     }
-    mx = col_max(mx);
+    if (lim < 32) {  // the context ends inside this tile: no weight for tokens 8 kg + i >= lim
+      mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        x[i] = 8 * kg + i < lim ? x[i] : -INFINITY;
+        mx = fmaxf(mx, x[i]);
+      }
+    }
+    mx = col_max(mx);  // finite: token 0 of the tile exists
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
     f32x8 p;
@@ -229,13 +241,14 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
 
   // Two tile buffers: the loads of tile i+1 are in flight while tile i computes.
   bf16x8 ka[8], va[8], kb2[8], vb2[8];
-  if (nT > 0) load_tile(0, ka, va);
+  int lim_a = 32, lim_b = 32;
+  if (nT > 0) lim_a = load_tile(0, ka, va);
   for (int i = 0; i < nT; i += 2) {
-    if (i + 1 < nT) load_tile(i + 1, kb2, vb2);
-    compute_tile(ka, va);
+    if (i + 1 < nT) lim_b = load_tile(i + 1, kb2, vb2);
+    compute_tile(ka, va, lim_a);
     if (i + 1 < nT) {
-      if (i + 2 < nT) load_tile(i + 2, ka, va);
-      compute_tile(kb2, vb2);
+      if (i + 2 < nT) lim_a = load_tile(i + 2, ka, va);
+      compute_tile(kb2, vb2, lim_b);
     }
   }
   l_run += __shfl_xor(l_run, 16);

@@ -41,12 +41,21 @@ struct Plan {
   int64_t chunk_stride = 0, head_stride = 0;
   int64_t n_units = 0;
   size_t emb_elem = 0;
+  // two-level path: history chunks (before the window) per sequence, and the
+  // pitches of the recalled list and of the Level-2 positions
+  int32_t n_hist[LSA_MAX_BATCH] = {};
+  int32_t rec_pitch = 0, core_pitch = 0;
   // workspace layout (byte offsets)
   size_t off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0;
+  size_t off_rec = 0, off_rec_cnt = 0, off_nat = 0, off_core = 0, off_core_cnt = 0;
   size_t ws_total = 0;
 };
 
-lsa_status make_plan(const lsa_problem* p, Plan* pl) {
+// tl != NULL plans the two-level path: contexts may end inside a chunk, and
+// the kept set of sequence b is at most min(core_keep, keep, history) chunks
+// plus the window.
+// partial: contexts may end inside a chunk (attention alone).
+lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = nullptr, bool partial = false) {
   if (p == nullptr) return fail(LSA_ERR_INVALID_ARG, "problem is NULL");
   const int B = p->batch;
   if (B < 1 || B > LSA_MAX_BATCH) return fail(LSA_ERR_INVALID_ARG, "batch %d not in [1, %d]", B, LSA_MAX_BATCH);
@@ -68,6 +77,16 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   if (p->reserved != 0) return fail(LSA_ERR_INVALID_ARG, "reserved field must be 0");
   if (p->ctx_tokens == nullptr || p->keep == nullptr)
     return fail(LSA_ERR_INVALID_ARG, "ctx_tokens and keep must be host arrays of batch entries");
+  if (tl != nullptr) {
+    if (tl->native_heads != 16 && tl->native_heads != 32 && tl->native_heads != 64)
+      return fail(LSA_ERR_UNSUPPORTED, "native_heads %d not in {16, 32, 64}", tl->native_heads);
+    if (tl->reserved != 0) return fail(LSA_ERR_INVALID_ARG, "two-level reserved field must be 0");
+    if (tl->core_keep == nullptr || tl->window_tokens == nullptr)
+      return fail(LSA_ERR_INVALID_ARG, "core_keep and window_tokens must be host arrays of batch entries");
+    if (p->n_lookahead != 1)
+      return fail(LSA_ERR_INVALID_ARG, "the two-level path takes one query token: n_lookahead %d != 1",
+                  p->n_lookahead);
+  }
   const int G = p->n_q_heads / p->n_kv_heads;
   const int rows = G * p->n_qtok;
   if (rows > LSA_MAX_ROWS)
@@ -83,29 +102,51 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   P.group = G;
   P.rows = rows;
   P.rows_pad = (rows + 15) / 16 * 16;  // partial rows per unit: whole 16-row MFMA blocks
-  // First pass: shapes and the total kept-chunk bound, which sizes the splits.
-  int64_t sel_total = 0;
-  for (int b = 0; b < B; ++b) {
+  // Kept-chunk bound of sequence b (0 when its shape is invalid; the second
+  // pass reports that).
+  auto kept_bound = [&](int b) -> int64_t {
     const int64_t L = p->ctx_tokens[b];
-    if (L >= C && L % C == 0 && p->keep[b] >= 1)
-      sel_total += std::min<int64_t>((int64_t)p->n_lookahead * p->keep[b], L / C);
-  }
+    if (tl == nullptr) {
+      if (L < 1 || (!partial && (L < C || L % C != 0)) || p->keep[b] < 1) return 0;
+      return std::min<int64_t>((int64_t)p->n_lookahead * p->keep[b], (L + C - 1) / C);
+    }
+    if (L < 1 || p->keep[b] < 1 || tl->core_keep[b] < 1 || tl->window_tokens[b] < 0) return 0;
+    const int64_t n = (L + C - 1) / C, full = L / C;
+    const int64_t w0 = std::min<int64_t>(std::max<int64_t>(L - tl->window_tokens[b], 0) / C, full);
+    return std::min<int64_t>({(int64_t)tl->core_keep[b], (int64_t)p->keep[b], w0}) + (n - w0);
+  };
+  // First pass: the total kept-chunk bound, which sizes the splits.
+  int64_t sel_total = 0;
+  for (int b = 0; b < B; ++b) sel_total += kept_bound(b);
   const int tpc = C / 32;
   int64_t chunk_off = 0, wg_off = 0, swg_off = 0;
   for (int b = 0; b < B; ++b) {
     const int64_t L = p->ctx_tokens[b];
-    if (L < C || L % C != 0)
+    if (tl == nullptr && !partial && (L < C || L % C != 0))
       return fail(LSA_ERR_INVALID_ARG, "ctx_tokens[%d] = %lld is not a positive multiple of chunk_size %d", b,
                   (long long)L, C);
-    const int64_t n = L / C;
+    if (L < 1) return fail(LSA_ERR_INVALID_ARG, "ctx_tokens[%d] = %lld < 1", b, (long long)L);
+    const int64_t n = (L + C - 1) / C;
     if (n > INT32_MAX / 2) return fail(LSA_ERR_UNSUPPORTED, "sequence %d has too many chunks", b);
     if (p->n_lookahead > 1 && n > LSA_MAX_UNION_CHUNKS)
       return fail(LSA_ERR_UNSUPPORTED, "sequence %d: %lld chunks > %d with several lookahead queries", b,
                   (long long)n, LSA_MAX_UNION_CHUNKS);
     const int32_t k = p->keep[b];
-    if (k < 1 || k > n)
+    if (k < 1 || (tl == nullptr && k > n))
       return fail(LSA_ERR_INVALID_ARG, "keep[%d] = %d not in [1, n_b = %lld]", b, k, (long long)n);
-    const int32_t msel = (int32_t)std::min<int64_t>((int64_t)p->n_lookahead * k, n);
+    if (tl != nullptr) {
+      if (tl->core_keep[b] < 1) return fail(LSA_ERR_INVALID_ARG, "core_keep[%d] = %d < 1", b, tl->core_keep[b]);
+      if (tl->window_tokens[b] < 0)
+        return fail(LSA_ERR_INVALID_ARG, "window_tokens[%d] = %lld < 0", b, (long long)tl->window_tokens[b]);
+      const int64_t w0 = std::min<int64_t>(std::max<int64_t>(L - tl->window_tokens[b], 0) / C, L / C);
+      t.w0[b] = (int32_t)w0;
+      P.n_hist[b] = (int32_t)w0;
+      P.rec_pitch = std::max<int32_t>(P.rec_pitch, (int32_t)std::min<int64_t>(k, w0));
+      P.core_pitch = std::max<int32_t>(
+          P.core_pitch, (int32_t)std::min<int64_t>({(int64_t)tl->core_keep[b], (int64_t)k, w0}));
+    }
+    t.tail[b] = (int32_t)(L - (n - 1) * C);
+    const int32_t msel = (int32_t)kept_bound(b);
     // splits of sequence b in proportion to its share of the kept chunks, so the
     // whole grid is about kTargetWorkgroups; at least one 32-token tile per split
     const double share = (double)kTargetWorkgroups * (double)msel /
@@ -159,6 +200,20 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl) {
   off = align_up(off + (size_t)P.n_units * P.rows_pad * 2 * 4);
   P.off_o = off;
   off = align_up(off + (size_t)P.n_units * P.rows_pad * kHeadDim * 4);
+  if (tl != nullptr) {
+    P.rec_pitch = std::max(P.rec_pitch, 1);
+    P.core_pitch = std::max(P.core_pitch, 1);
+    P.off_rec = off;
+    off = align_up(off + (size_t)B * P.rec_pitch * 4);
+    P.off_rec_cnt = off;
+    off = align_up(off + (size_t)B * 4);
+    P.off_nat = off;
+    off = align_up(off + (size_t)B * P.rec_pitch * 4);
+    P.off_core = off;
+    off = align_up(off + (size_t)B * P.core_pitch * 4);
+    P.off_core_cnt = off;
+    off = align_up(off + (size_t)B * 4);
+  }
   P.ws_total = off;
   return LSA_OK;
 }
@@ -231,6 +286,17 @@ lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, cons
   a.rows = P.rows;
   a.rows_pad = P.rows_pad;
   LSA_HIP(launch_attn(P.t, a, p->chunk_size, s), "attention launch");
+  return LSA_OK;
+}
+
+// A context that ends inside a chunk is masked by the attention kernel for at
+// most 16 query rows per KV head.
+lsa_status check_partial_rows(const lsa_problem* p, const Plan& P) {
+  if (P.rows > 16)
+    for (int b = 0; b < p->batch; ++b)
+      if (P.t.tail[b] != p->chunk_size)
+        return fail(LSA_ERR_UNSUPPORTED, "sequence %d ends inside a chunk; that needs at most 16 query rows per "
+                    "KV head (n_qtok * n_q_heads / n_kv_heads = %d)", b, P.rows);
   return LSA_OK;
 }
 
@@ -368,7 +434,8 @@ lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const
                                   float softmax_scale, float* out, float* lse, void* ws, size_t ws_bytes,
                                   void* stream) {
   Plan P;
-  LSA_TRY(make_plan(p, &P));
+  LSA_TRY(make_plan(p, &P, nullptr, true));
+  LSA_TRY(check_partial_rows(p, P));
   LSA_TRY(check_ptr(q, "q"));
   LSA_TRY(check_ptr(k_cache, "k_cache"));
   LSA_TRY(check_ptr(v_cache, "v_cache"));
@@ -479,6 +546,111 @@ lsa_status lsa_recall_step(const lsa_problem* p, const lsa_indexer* ix, const vo
   SelectArgs sa;
   sa.recall = true;
   LSA_HIP(launch_topk(P.t, LSA_F32, true, keys, sel, P.max_sel, 0, cnt, s, sa), "recall select launch");
+  return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
+}
+
+lsa_status lsa_two_level_sizes(const lsa_problem* p, const lsa_two_level* tl, int32_t* max_sel,
+                               size_t* ws_bytes) {
+  if (tl == nullptr) return fail(LSA_ERR_INVALID_ARG, "two-level description is NULL");
+  Plan P;
+  LSA_TRY(make_plan(p, &P, tl));
+  if (max_sel != nullptr) *max_sel = P.max_sel;
+  if (ws_bytes != nullptr) *ws_bytes = P.ws_total;
+  return LSA_OK;
+}
+
+lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const lsa_two_level* tl,
+                              const void* idx_q, const float* idx_w, const void* idx_k, const void* nat_q,
+                              const float* nat_w, const void* nat_k, const uint16_t* q, const uint16_t* k_cache,
+                              const uint16_t* v_cache, float softmax_scale, float* out, float* lse, int32_t* sel_idx,
+                              int32_t* sel_count, void* ws, size_t ws_bytes, void* stream) {
+  if (tl == nullptr) return fail(LSA_ERR_INVALID_ARG, "two-level description is NULL");
+  Plan P;
+  LSA_TRY(make_plan(p, &P, tl));
+  LSA_TRY(check_indexer(p, ix));
+  LSA_TRY(check_recall_inputs(idx_q, idx_w, idx_k));
+  LSA_TRY(check_ptr(nat_q, "nat_q"));
+  LSA_TRY(check_ptr(nat_w, "nat_w"));
+  LSA_TRY(check_ptr(nat_k, "nat_k"));
+  LSA_TRY(check_ptr(q, "q"));
+  LSA_TRY(check_ptr(k_cache, "k_cache"));
+  LSA_TRY(check_ptr(v_cache, "v_cache"));
+  LSA_TRY(check_ptr(out, "out"));
+  if (lse != nullptr && (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(LSA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if ((sel_idx == nullptr) != (sel_count == nullptr))
+    return fail(LSA_ERR_INVALID_ARG, "sel_idx and sel_count must both be given or both be NULL");
+  if (sel_idx != nullptr) {
+    LSA_TRY(check_ptr(sel_idx, "sel_idx"));
+    LSA_TRY(check_ptr(sel_count, "sel_count"));
+  }
+  if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
+  LSA_TRY(check_partial_rows(p, P));
+  LSA_TRY(check_ws(P, ws, ws_bytes));
+  const hipStream_t s = (hipStream_t)stream;
+  const int B = p->batch;
+  void* keys = at(ws, P.off_scores);
+  int32_t* rec = reinterpret_cast<int32_t*>(at(ws, P.off_rec));
+  int32_t* rec_cnt = reinterpret_cast<int32_t*>(at(ws, P.off_rec_cnt));
+  uint32_t* nat = reinterpret_cast<uint32_t*>(at(ws, P.off_nat));
+  int32_t* core = reinterpret_cast<int32_t*>(at(ws, P.off_core));
+  int32_t* core_cnt = reinterpret_cast<int32_t*>(at(ws, P.off_core_cnt));
+  int32_t* sel = sel_idx ? sel_idx : reinterpret_cast<int32_t*>(at(ws, P.off_sel));
+  int32_t* cnt = sel_count ? sel_count : reinterpret_cast<int32_t*>(at(ws, P.off_cnt));
+
+  // Level 1 over the history chunks: scores -> recalled ids (at most K_max)
+  SeqTable th = P.t;
+  for (int b = 0; b < B; ++b) th.n[b] = P.n_hist[b];
+  SeqTable ths = th;
+  {
+    int32_t off = 0;
+    for (int b = 0; b < B; ++b) {
+      ths.score_wg_off[b] = off;
+      off += (th.n[b] + kRecallRowsPerWg - 1) / kRecallRowsPerWg;
+    }
+    ths.score_wg_off[B] = off;
+  }
+  LSA_HIP(launch_recall_score(ths, recall_args(P, ix, idx_q, idx_w, idx_k), keys, true, s), "recall score launch");
+  SelectArgs sa1;
+  sa1.recall = true;
+  LSA_HIP(launch_topk(th, LSA_F32, true, keys, rec, P.rec_pitch, 0, rec_cnt, s, sa1), "recall select launch");
+
+  // Level 2: native scores of the recalled ids, then their top-k2 positions
+  SeqTable tn = P.t;
+  {
+    int32_t off = 0;
+    for (int b = 0; b < B; ++b) {
+      tn.n[b] = std::min(p->keep[b], P.n_hist[b]);  // list capacity
+      tn.score_wg_off[b] = off;
+      off += (tn.n[b] + kRecallRowsPerWg - 1) / kRecallRowsPerWg;
+    }
+    tn.score_wg_off[B] = off;
+  }
+  RecallArgs rn;
+  rn.q = static_cast<const uint16_t*>(nat_q);
+  rn.w = nat_w;
+  rn.k = static_cast<const uint16_t*>(nat_k);
+  rn.total = P.total_chunks;
+  rn.layer_stride = 0;
+  rn.n_layers = 1;
+  rn.n_heads = tl->native_heads;
+  rn.key_dim = ix->key_dim;
+  rn.list = rec;
+  rn.list_count = rec_cnt;
+  rn.list_pitch = P.rec_pitch;
+  LSA_HIP(launch_recall_score(tn, rn, nat, true, s), "native score launch");
+  SeqTable tc = tn;  // the compact [B][rec_pitch] native keys as sequences of capacity tn.n[b]
+  for (int b = 0; b < B; ++b) {
+    tc.keep[b] = tl->core_keep[b];
+    tc.chunk_off[b] = (int64_t)b * P.rec_pitch;
+  }
+  SelectArgs sa2;
+  sa2.dev_n = rec_cnt;
+  LSA_HIP(launch_topk(tc, LSA_F32, true, nat, core, P.core_pitch, 0, core_cnt, s, sa2), "native top-k launch");
+
+  // kept set: Level-2 ids, then the window
+  LSA_HIP(launch_two_level_finish(P.t, rec, P.rec_pitch, core, core_cnt, P.core_pitch, sel, P.max_sel, cnt, s),
+          "two-level finish launch");
   return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
 }
 

@@ -15,7 +15,9 @@ namespace lsa {
 struct SeqTable {
   int32_t batch;
   int32_t n_lookahead;
-  int32_t n[LSA_MAX_BATCH];            // chunks of sequence b
+  int32_t n[LSA_MAX_BATCH];            // chunks of sequence b (a partial last chunk included)
+  int32_t tail[LSA_MAX_BATCH];         // tokens in the last chunk of sequence b (the chunk size when complete)
+  int32_t w0[LSA_MAX_BATCH];           // two-level path: first chunk of the always-resident window
   int32_t keep[LSA_MAX_BATCH];         // keep budget k_b
   int32_t nsplit[LSA_MAX_BATCH];       // attention splits per (b, kv head)
   int32_t wg_off[LSA_MAX_BATCH + 1];   // first attention workgroup of sequence b
@@ -83,10 +85,13 @@ int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim, int32_t n_lookahead);
 // key of +0.0), i.e. the entries whose sigmoid score reaches 1/2, bounded by
 // K_max = keep[b]; n_layers > 1 reads that many score arrays layer_stride
 // elements apart and selects on their per-entry maximum (the OR over layers).
+// dev_n (nullable): per-sequence key counts in device memory, read by the
+// kernel (at most t.n[b]); k_b is then min(keep[b], that count).
 struct SelectArgs {
   bool recall = false;
   int32_t n_layers = 1;
   int64_t layer_stride = 0;
+  const int32_t* dev_n = nullptr;
 };
 
 // keys_ready == true: `scores` holds keys written by launch_score(keys = true)
@@ -109,11 +114,22 @@ struct RecallArgs {
   int64_t layer_stride;  // total * c
   int64_t total;         // sum_b n_b
   int32_t n_layers, n_heads, key_dim;
+  // list mode (nullable list): score only the entries list[b * list_pitch + i],
+  // i < list_count[b], and write the keys to out[b * list_pitch + i]
+  const int32_t* list = nullptr;
+  const int32_t* list_count = nullptr;
+  int64_t list_pitch = 0;
 };
 // t.score_wg_off must count kRecallRowsPerWg entries per workgroup.  keys ==
 // false writes x [L][total] float32; keys == true writes the order key of
 // max_l x_l per entry, [total] (the input of the recall selection).
 hipError_t launch_recall_score(const SeqTable& t, const RecallArgs& r, void* out, bool keys, hipStream_t s);
+
+// Two-level selection, last step: sel[b] = list[b][pos[b][i]] for the count[b]
+// ascending positions, then the window chunks t.w0[b] .. t.n[b] - 1.
+hipError_t launch_two_level_finish(const SeqTable& t, const int32_t* list, int64_t list_pitch, const int32_t* pos,
+                                   const int32_t* pos_count, int64_t pos_pitch, int32_t* sel_idx, int64_t sel_pitch,
+                                   int32_t* sel_count, hipStream_t s);
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 

@@ -61,7 +61,11 @@ __device__ __forceinline__ void read_blocks(const uint4 (*blocks)[64], int first
   for (int i = 0; i < N; ++i) out[i] = __builtin_bit_cast(bf16x8, v[i]);
 }
 
-template <int NH, int CD, bool KEYS>
+// What the kernel writes: every layer's score x_l; the order key of max_l x_l
+// per entry; or, in list mode, that key per listed entry.
+enum RecallOut : int { kOutScores = 0, kOutKeys = 1, kOutListKeys = 2 };
+
+template <int NH, int CD, int OUT>
 __global__ void __launch_bounds__(kThreads)
 recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
   constexpr int kSteps = CD / 32;   // MFMA k-steps
@@ -76,7 +80,10 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
   const int wg = blockIdx.x;
   int b = 0;
   while (wg >= t.score_wg_off[b + 1]) ++b;
-  const int n = t.n[b];
+  // entries of sequence b; in list mode t.n[b] is the list capacity and the
+  // count is on the device
+  const int n = OUT == kOutListKeys ? min(t.n[b], max(r.list_count[b], 0)) : t.n[b];
+  if ((wg - t.score_wg_off[b]) * kRecallRowsPerWg >= n) return;  // the whole workgroup: nothing to score
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int e0 = (wg - t.score_wg_off[b]) * kRecallRowsPerWg + wave * 16;
@@ -99,7 +106,8 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
   constexpr int kKeyLoads = kMaxIdxLayers * kSteps;
   bf16x8 kb[kMaxIdxLayers][kSteps];
   {
-    const int ent = min(e0 + (lane & 15), n - 1);
+    const int pos = min(e0 + (lane & 15), n - 1);
+    const int ent = OUT == kOutListKeys ? r.list[b * r.list_pitch + pos] : pos;
     const uint16_t* kp = r.k + (t.chunk_off[b] + ent) * CD + 8 * hi;
 #pragma unroll
     for (int l = 0; l < kMaxIdxLayers; ++l)
@@ -141,25 +149,28 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
       for (int j = 0; j < 4; ++j) x = fmaf(sw[l * NH + 16 * hb + 4 * hi + j], fmaxf(acc[hb][j], 0.f), x);
     x += __shfl_xor(x, 16);
     x += __shfl_xor(x, 32);
-    if constexpr (!KEYS) {
+    if constexpr (OUT == kOutScores) {
       if (lane < 16 && e0 + lane < n)
         static_cast<float*>(out)[l * r.total + t.chunk_off[b] + e0 + lane] = x;
     }
     best = fmaxf(best, x);
   }
-  if constexpr (KEYS) {
+  if constexpr (OUT != kOutScores) {
+    const int64_t base = OUT == kOutListKeys ? b * r.list_pitch : t.chunk_off[b];
     if (lane < 16 && e0 + lane < n)
-      static_cast<uint32_t*>(out)[t.chunk_off[b] + e0 + lane] = order_key<kKeysFromF32>(__float_as_uint(best));
+      static_cast<uint32_t*>(out)[base + e0 + lane] = order_key<kKeysFromF32>(__float_as_uint(best));
   }
 }
 
 template <int NH, int CD>
 hipError_t launch_nh_cd(const SeqTable& t, const RecallArgs& r, void* out, bool keys, hipStream_t s) {
   const dim3 grid(t.score_wg_off[t.batch]);
-  if (keys)
-    hipLaunchKernelGGL((recall_score_kernel<NH, CD, true>), grid, dim3(kThreads), 0, s, t, r, out);
+  if (r.list != nullptr)
+    hipLaunchKernelGGL((recall_score_kernel<NH, CD, kOutListKeys>), grid, dim3(kThreads), 0, s, t, r, out);
+  else if (keys)
+    hipLaunchKernelGGL((recall_score_kernel<NH, CD, kOutKeys>), grid, dim3(kThreads), 0, s, t, r, out);
   else
-    hipLaunchKernelGGL((recall_score_kernel<NH, CD, false>), grid, dim3(kThreads), 0, s, t, r, out);
+    hipLaunchKernelGGL((recall_score_kernel<NH, CD, kOutScores>), grid, dim3(kThreads), 0, s, t, r, out);
   return hipGetLastError();
 }
 

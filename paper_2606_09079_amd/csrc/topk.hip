@@ -68,11 +68,16 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
 
   const int Q = t.n_lookahead;
   const int b = blockIdx.x / Q, j = blockIdx.x % Q;
-  const int n = t.n[b];
-  int k = t.keep[b];
+  // keys of this (sequence, query): t.n[b], or fewer when the count is on the device
+  const int n = sa.dev_n != nullptr ? min(t.n[b], max(sa.dev_n[b], 0)) : t.n[b];
+  int k = min(t.keep[b], n);
   const int tid = threadIdx.x;
-  const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * n;
+  const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * t.n[b];
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
+  if (k == 0) {  // no keys (uniform across the workgroup)
+    if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+    return;
+  }
   const bool staged = n <= kLdsKeys;
   // key of entry i; for the recall, the largest over the indexer layers
   auto key_at = [&](int i) -> uint32_t {
@@ -266,11 +271,16 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
 
   const int Q = t.n_lookahead;
   const int b = blockIdx.x / Q, j = blockIdx.x % Q;
-  const int n = t.n[b];
-  int k = t.keep[b];
+  // keys of this (sequence, query): t.n[b], or fewer when the count is on the device
+  const int n = sa.dev_n != nullptr ? min(t.n[b], max(sa.dev_n[b], 0)) : t.n[b];
+  int k = min(t.keep[b], n);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane >> 4;
-  const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * n;
+  const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * t.n[b];
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
+  if (k == 0) {  // no keys (uniform across the workgroup)
+    if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+    return;
+  }
 
   // Key i = q * 1024 + tid sits in slot q of thread tid: coalesced buffer loads,
   // all in flight while the histogram is cleared.  Slots past the end hold key
@@ -474,6 +484,22 @@ union_kernel(SeqTable t, const int32_t* __restrict__ per_query, int32_t k_pitch,
   if (tid == kThreads - 1) sel_count[b] = (int32_t)pos;
 }
 
+// Two-level selection, last step: kept ids of Level 2 (positions into the
+// recalled list, ascending, so the ids come out ascending too), then the
+// window chunks, which lie above every history chunk.
+__global__ void __launch_bounds__(kThreads)
+two_level_finish_kernel(SeqTable t, const int32_t* __restrict__ list, int64_t list_pitch,
+                        const int32_t* __restrict__ pos, const int32_t* __restrict__ pos_count, int64_t pos_pitch,
+                        int32_t* __restrict__ sel, int64_t sel_pitch, int32_t* __restrict__ sel_count) {
+  const int b = blockIdx.x;
+  const int m = max(pos_count[b], 0);
+  const int w0 = t.w0[b], nw = max(t.n[b] - w0, 0);
+  int32_t* out = sel + (int64_t)b * sel_pitch;
+  for (int i = threadIdx.x; i < m; i += kThreads) out[i] = list[(int64_t)b * list_pitch + pos[(int64_t)b * pos_pitch + i]];
+  for (int i = threadIdx.x; i < nw; i += kThreads) out[m + i] = w0 + i;
+  if (threadIdx.x == 0) sel_count[b] = m + nw;
+}
+
 __global__ void zero_kernel(uint4* p, size_t n16, uint8_t* tail, size_t ntail) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
@@ -522,6 +548,14 @@ hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_p
                         int32_t* sel_idx, int32_t sel_pitch, int32_t* sel_count, hipStream_t s) {
   hipLaunchKernelGGL(union_kernel, dim3(t.batch), dim3(kThreads), 0, s, t, per_query, k_pitch, sel_idx,
                      sel_pitch, sel_count);
+  return hipGetLastError();
+}
+
+hipError_t launch_two_level_finish(const SeqTable& t, const int32_t* list, int64_t list_pitch, const int32_t* pos,
+                                   const int32_t* pos_count, int64_t pos_pitch, int32_t* sel_idx, int64_t sel_pitch,
+                                   int32_t* sel_count, hipStream_t s) {
+  hipLaunchKernelGGL(two_level_finish_kernel, dim3(t.batch), dim3(kThreads), 0, s, t, list, list_pitch, pos,
+                     pos_count, pos_pitch, sel_idx, sel_pitch, sel_count);
   return hipGetLastError();
 }
 

@@ -31,7 +31,7 @@ DTYPES = {"f32": 0, "bf16": 1, "i8": 2}
 EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_validate", "lsa_max_sel",
            "lsa_max_keep", "lsa_workspace_size", "lsa_workspace_init", "lsa_score_chunks", "lsa_topk_chunks",
            "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
-           "lsa_recall_step")
+           "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step")
 
 
 class lsa_problem(ctypes.Structure):
@@ -48,6 +48,11 @@ class lsa_problem(ctypes.Structure):
 class lsa_indexer(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("key_dim", ctypes.c_int32),
                 ("reserved", ctypes.c_int32)]
+
+
+class lsa_two_level(ctypes.Structure):
+    _fields_ = [("native_heads", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("core_keep", ctypes.POINTER(ctypes.c_int32)), ("window_tokens", ctypes.POINTER(ctypes.c_int64))]
 
 
 def _load() -> ctypes.CDLL:
@@ -79,6 +84,10 @@ def _load() -> ctypes.CDLL:
     lib.lsa_recall_select.argtypes = [pp, ip, _P, _P, _P, _P]
     lib.lsa_recall_step.argtypes = [pp, ip, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P,
                                     ctypes.c_size_t, _P]
+    tp = ctypes.POINTER(lsa_two_level)
+    lib.lsa_two_level_sizes.argtypes = [pp, tp, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
+    lib.lsa_two_level_step.argtypes = [pp, ip, tp, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P,
+                                       _P, _P, ctypes.c_size_t, _P]
     for name in EXPORTS[3:]:
         getattr(lib, name).restype = ctypes.c_int
     if lib.lsa_abi_version() != 1:
@@ -123,6 +132,24 @@ class Indexer:
     @classmethod
     def from_synth(cls, prob) -> "Indexer":
         return cls(prob.idx_layers, prob.idx_heads, prob.idx_dim)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+class TwoLevel:
+    """Two-level selection (mirrors ``lsa_two_level``; keeps its host arrays alive)."""
+
+    def __init__(self, native_heads: int, core_keep: Sequence[int], window_tokens: Sequence[int]):
+        self._core = (ctypes.c_int32 * max(len(core_keep), 1))(*core_keep)
+        self._win = (ctypes.c_int64 * max(len(window_tokens), 1))(*window_tokens)
+        self.c = lsa_two_level(native_heads, 0, ctypes.cast(self._core, ctypes.POINTER(ctypes.c_int32)),
+                               ctypes.cast(self._win, ctypes.POINTER(ctypes.c_int64)))
+
+    @classmethod
+    def from_synth(cls, prob) -> "TwoLevel":
+        return cls(prob.nat_heads, prob.core_keep, prob.window_tokens)
 
     @property
     def ref(self):
@@ -221,3 +248,19 @@ def lsa_recall_step(p: Problem, ix: Indexer, idx_q, idx_w, idx_k, q, k_cache, v_
     _check(LIB.lsa_recall_step(p.ref, ix.ref, _ptr(idx_q), _ptr(idx_w), _ptr(idx_k), _ptr(q), _ptr(k_cache),
                                _ptr(v_cache), float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx),
                                _ptr(sel_count), _ptr(ws), ws_bytes, _stream(stream)), "lsa_recall_step")
+
+
+def lsa_two_level_sizes(p: Problem, tl: TwoLevel):
+    """(row pitch of sel_idx, workspace bytes) of lsa_two_level_step."""
+    m, w = ctypes.c_int32(), ctypes.c_size_t()
+    _check(LIB.lsa_two_level_sizes(p.ref, tl.ref, ctypes.byref(m), ctypes.byref(w)), "lsa_two_level_sizes")
+    return m.value, w.value
+
+
+def lsa_two_level_step(p: Problem, ix: Indexer, tl: TwoLevel, idx_q, idx_w, idx_k, nat_q, nat_w, nat_k, q, k_cache,
+                       v_cache, softmax_scale: float, out, lse=None, sel_idx=None, sel_count=None, ws=None,
+                       ws_bytes: int = 0, stream=None) -> None:
+    _check(LIB.lsa_two_level_step(p.ref, ix.ref, tl.ref, _ptr(idx_q), _ptr(idx_w), _ptr(idx_k), _ptr(nat_q),
+                                  _ptr(nat_w), _ptr(nat_k), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                  float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx), _ptr(sel_count), _ptr(ws),
+                                  ws_bytes, _stream(stream)), "lsa_two_level_step")

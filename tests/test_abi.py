@@ -155,3 +155,38 @@ def test_recall_presets_validate():
         p, idx = L.Problem.from_synth(prob), L.Indexer.from_synth(prob)
         assert L.lsa_validate(p) == 0
         assert L.LIB.lsa_recall_select(p.ref, idx.ref, None, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+
+
+def test_two_level_sizes_and_validation():
+    ix = L.Indexer(2, 32, 128)
+    p = L.Problem([64 * 100 + 13, 64 * 50], 64, [30, 10], 8, 2)     # contexts may end inside a chunk here
+    tl = L.TwoLevel(32, [8, 4], [640, 0])
+    max_sel, ws = L.lsa_two_level_sizes(p, tl)
+    # sequence 0: 101 chunks, window 90 .. 100 (11 chunks), core <= 8; sequence 1: no window, core <= 4
+    assert max_sel == 8 + 11 and ws > 0
+    assert L.lsa_validate(p) == B.LSA_ERR_INVALID_ARG                # the other paths need whole chunks
+    lib = L.LIB
+    bad = [L.TwoLevel(48, [8, 4], [640, 0]), L.TwoLevel(32, [0, 4], [640, 0]), L.TwoLevel(32, [8, 4], [-1, 0])]
+    for t in bad:
+        assert lib.lsa_two_level_sizes(p.ref, t.ref, None, None) != 0
+    assert lib.lsa_two_level_sizes(p.ref, None, None, None) == B.LSA_ERR_INVALID_ARG
+    q = L.Problem([64 * 100], 64, [30], 8, 2, n_lookahead=2)
+    assert lib.lsa_two_level_sizes(q.ref, L.TwoLevel(32, [8], [0]).ref, None, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_two_level_step(p.ref, ix.ref, tl.ref, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0,
+                                  FAKE, None, None, None, FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_two_level_step(p.ref, ix.ref, tl.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0,
+                                  FAKE, None, None, None, FAKE, ws - 1, None) == B.LSA_ERR_WORKSPACE
+    rows32 = L.Problem([64 * 40 + 3], 64, [10], 16, 2, n_qtok=4)
+    t1 = L.TwoLevel(32, [4], [256])
+    _, ws32 = L.lsa_two_level_sizes(rows32, t1)
+    assert lib.lsa_two_level_step(rows32.ref, ix.ref, t1.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                  0.0, FAKE, None, None, None, FAKE, ws32, None) == B.LSA_ERR_UNSUPPORTED
+
+
+def test_two_level_presets_size():
+    import lsa_synth
+    for name in lsa_synth.TWO_LEVEL_PRESETS:
+        prob = lsa_synth.make_problem(name, 0)
+        ms, ws = L.lsa_two_level_sizes(L.Problem.from_synth(prob), L.TwoLevel.from_synth(prob))
+        assert ms == max(min(prob.core_keep[b], prob.keep[b], prob.history_chunks(b)) + prob.n_chunks[b]
+                         - prob.window_start(b) for b in range(prob.batch))

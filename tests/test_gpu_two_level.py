@@ -1,0 +1,121 @@
+"""Parity of the two-level path (Level-1 recall over the history, Level-2
+native top-k inside the recalled set, always-resident window, partial last
+chunk, attention) with the CPU oracle, on the GPU, through the C ABI."""
+import numpy as np
+import pytest
+
+import lsa_synth as synth
+from gpu_case import log
+from two_level_case import run_two_level_case
+
+pytestmark = pytest.mark.gpu
+
+
+def T(name, ctx, kmax, k2, window, hq=8, hkv=2, layers=2, heads=32, native=32, dim=128, rate=0.1, Tq=1, chunk=64):
+    return synth.Problem(name, list(ctx), chunk, list(kmax), hq, hkv, n_qtok=Tq, idx_layers=layers, idx_heads=heads,
+                         idx_dim=dim, idx_rate=rate, core_keep=list(k2), nat_heads=native, window_tokens=list(window))
+
+
+SMALL = [
+    T("partial_tail", [64 * 100 + 13], [30], [8], [640]),
+    T("tail_one_token", [64 * 80 + 1], [20], [5], [100], layers=3, heads=16, native=16, dim=64),
+    T("no_window_full_chunks", [64 * 120], [25], [7], [0], layers=1, heads=64, native=64),
+    T("no_window_partial", [64 * 90 + 40], [25], [7], [0]),
+    T("window_covers_all", [64 * 10 + 5], [4], [2], [100000]),
+    T("k2_above_recall", [64 * 70 + 9], [40], [500], [256], rate=0.05),
+    T("kmax_cuts", [64 * 300 + 50], [10], [6], [1000], rate=0.2),
+    T("ragged_batch", [64 * 50 + 3, 64 * 200, 7, 64 * 33 + 63], [10, 30, 1, 8], [4, 9, 1, 8], [200, 0, 64, 5000],
+      layers=4, heads=16, native=64, dim=64),
+    T("c128_partial", [128 * 60 + 100], [12], [5], [512], chunk=128, hq=16, hkv=4, Tq=4),
+    T("history_beyond_lds", [64 * 20000 + 17], [1800], [600], [8192], layers=2, heads=16, native=16, dim=64,
+      rate=0.05),
+]
+
+
+@pytest.mark.parametrize("prob", SMALL, ids=lambda p: p.name)
+def test_two_level_small(prob):
+    r = run_two_level_case(prob, seed=31)
+    assert r["worst_attn"] <= 2e-3
+
+
+def test_two_level_nothing_recalled_no_window():
+    """Nothing recalled and no window over full chunks: the kept set is empty and
+    the attention is out = 0, lse = -inf."""
+    prob = T("empty", [64 * 40, 64 * 30], [10, 10], [4, 4], [0, 0], layers=1, heads=16, native=16, dim=64)
+    host = synth.host_inputs(prob, 6)
+    q = host["idx_q"]
+    q[:, :, 1::2, :] = q[:, :, 0::2, :] ^ np.uint16(0x8000)
+    host["idx_w"][:] = -1.0
+    r = run_two_level_case(prob, seed=6, host=host)
+    assert r["cnt"].tolist() == [0, 0]
+
+
+def test_two_level_rows_above_16_need_full_chunks():
+    """More than 16 query rows per KV head run with full chunks (the many-rows
+    attention kernel) and are rejected when a context ends inside a chunk."""
+    import torch
+    import paper_2606_09079_amd as L
+    ok = T("rows32_full", [64 * 40], [10], [4], [256], hq=16, hkv=2, Tq=4)
+    run_two_level_case(ok, seed=7)
+    bad = T("rows32_partial", [64 * 40 + 3], [10], [4], [256], hq=16, hkv=2, Tq=4)
+    dev = synth.device_inputs(bad, 7)
+    P, ix, tl = L.Problem.from_synth(bad), L.Indexer.from_synth(bad), L.TwoLevel.from_synth(bad)
+    max_sel, ws_bytes = L.lsa_two_level_sizes(P, tl)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty(1, 4, 16, 128, device="cuda")
+    with pytest.raises(L.LsaError) as e:
+        L.lsa_two_level_step(P, ix, tl, dev["idx_q"], dev["idx_w"], dev["idx_k"], dev["nat_q"], dev["nat_w"],
+                             dev["nat_k"], dev["q"], dev["k"], dev["v"], 0.0, out, None, None, None, ws, ws_bytes)
+    assert e.value.status == 2
+
+
+def _sample_rows(prob, n_rows):
+    rng = np.random.default_rng(7)
+    allr = [(t, h) for t in range(prob.n_qtok) for h in range(prob.n_q_heads)]
+    idx = rng.choice(len(allr), size=min(n_rows, len(allr)), replace=False)
+    return [allr[i] for i in sorted(idx)]
+
+
+def test_preset_two_level_tiny():
+    for seed in range(4):
+        run_two_level_case(synth.make_problem("twolevel_tiny", seed), seed)
+
+
+def test_preset_two_level_1m():
+    """The 1M-token two-level workload in the benchmark's launch configuration."""
+    prob = synth.make_problem("twolevel1m", 0)
+    r = run_two_level_case(prob, 0, rows=_sample_rows(prob, 6))
+    log(f"[twolevel1m] kept {r['cnt'].tolist()} chunks of {prob.n_chunks[0]}")
+
+
+@pytest.mark.parametrize("tail", [1, 31, 32, 33, 63])
+def test_attention_alone_partial_context(tail):
+    """lsa_sparse_decode_attn on a context that ends inside its last chunk:
+    tokens past the end get no weight (compared token by token)."""
+    import torch
+    import oracle
+    import parity
+    import paper_2606_09079_amd as L
+    prob = synth.Problem("partial_attn", [64 * 30 + tail], 64, [8], 8, 2)
+    host = synth.host_inputs(prob, 8)
+    dev = synth.device_inputs(prob, 8, host=host)
+    P = L.Problem.from_synth(prob)
+    n = prob.n_chunks[0]
+    kept = np.array([0, 3, 11, 20, n - 2, n - 1], dtype=np.int32)
+    P = L.Problem(prob.ctx_tokens, 64, [len(kept)], 8, 2)
+    ws_bytes = L.lsa_workspace_size(L.Problem([64 * n], 64, [len(kept)], 8, 2))
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    sel = torch.from_numpy(kept[None, :].copy()).cuda()
+    cnt = torch.tensor([len(kept)], dtype=torch.int32, device="cuda")
+    out = torch.empty(1, 1, 8, 128, device="cuda")
+    lse = torch.empty(1, 1, 8, device="cuda")
+    L.lsa_sparse_decode_attn(P, dev["q"], dev["k"], dev["v"], sel, cnt, 0.0, out, lse, ws, ws_bytes)
+    torch.cuda.synchronize()
+    toks = oracle.kept_tokens(kept, 64, prob.ctx_tokens[0])
+    for g in range(2):
+        Kh = synth.kv_head_sparse(prob, 8, "k", 0, g, kept)
+        Vh = synth.kv_head_sparse(prob, 8, "v", 0, g, kept)
+        qr = np.stack([host["q"][0, 0, 4 * g + j] for j in range(4)])
+        r_out, r_lse = oracle.attention_tokens(qr, Kh, Vh, toks)
+        parity.check_attention(out.cpu().numpy()[0, 0, 4 * g:4 * g + 4], lse.cpu().numpy()[0, 0, 4 * g:4 * g + 4],
+                               r_out, r_lse, f"partial context, tail {tail}, KV head {g}")
