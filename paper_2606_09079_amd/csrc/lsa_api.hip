@@ -42,12 +42,12 @@ struct Plan {
   int64_t n_units = 0;
   size_t emb_elem = 0;
   // two-level path: history chunks (before the window) per sequence, and the
-  // pitches of the recalled list and of the Level-2 positions
+  // pitch of the recalled list
   int32_t n_hist[LSA_MAX_BATCH] = {};
-  int32_t rec_pitch = 0, core_pitch = 0;
+  int32_t rec_pitch = 0;
   // workspace layout (byte offsets)
   size_t off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0;
-  size_t off_rec = 0, off_rec_cnt = 0, off_nat = 0, off_core = 0, off_core_cnt = 0;
+  size_t off_rec = 0, off_rec_cnt = 0, off_nat = 0;
   size_t ws_total = 0;
 };
 
@@ -140,10 +140,9 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = n
         return fail(LSA_ERR_INVALID_ARG, "window_tokens[%d] = %lld < 0", b, (long long)tl->window_tokens[b]);
       const int64_t w0 = std::min<int64_t>(std::max<int64_t>(L - tl->window_tokens[b], 0) / C, L / C);
       t.w0[b] = (int32_t)w0;
+      t.win[b] = (int32_t)(n - w0);
       P.n_hist[b] = (int32_t)w0;
       P.rec_pitch = std::max<int32_t>(P.rec_pitch, (int32_t)std::min<int64_t>(k, w0));
-      P.core_pitch = std::max<int32_t>(
-          P.core_pitch, (int32_t)std::min<int64_t>({(int64_t)tl->core_keep[b], (int64_t)k, w0}));
     }
     t.tail[b] = (int32_t)(L - (n - 1) * C);
     const int32_t msel = (int32_t)kept_bound(b);
@@ -202,17 +201,12 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = n
   off = align_up(off + (size_t)P.n_units * P.rows_pad * kHeadDim * 4);
   if (tl != nullptr) {
     P.rec_pitch = std::max(P.rec_pitch, 1);
-    P.core_pitch = std::max(P.core_pitch, 1);
     P.off_rec = off;
     off = align_up(off + (size_t)B * P.rec_pitch * 4);
     P.off_rec_cnt = off;
     off = align_up(off + (size_t)B * 4);
     P.off_nat = off;
     off = align_up(off + (size_t)B * P.rec_pitch * 4);
-    P.off_core = off;
-    off = align_up(off + (size_t)B * P.core_pitch * 4);
-    P.off_core_cnt = off;
-    off = align_up(off + (size_t)B * 4);
   }
   P.ws_total = off;
   return LSA_OK;
@@ -593,8 +587,6 @@ lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const
   int32_t* rec = reinterpret_cast<int32_t*>(at(ws, P.off_rec));
   int32_t* rec_cnt = reinterpret_cast<int32_t*>(at(ws, P.off_rec_cnt));
   uint32_t* nat = reinterpret_cast<uint32_t*>(at(ws, P.off_nat));
-  int32_t* core = reinterpret_cast<int32_t*>(at(ws, P.off_core));
-  int32_t* core_cnt = reinterpret_cast<int32_t*>(at(ws, P.off_core_cnt));
   int32_t* sel = sel_idx ? sel_idx : reinterpret_cast<int32_t*>(at(ws, P.off_sel));
   int32_t* cnt = sel_count ? sel_count : reinterpret_cast<int32_t*>(at(ws, P.off_cnt));
 
@@ -639,18 +631,18 @@ lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const
   rn.list_count = rec_cnt;
   rn.list_pitch = P.rec_pitch;
   LSA_HIP(launch_recall_score(tn, rn, nat, true, s), "native score launch");
-  SeqTable tc = tn;  // the compact [B][rec_pitch] native keys as sequences of capacity tn.n[b]
+  // the compact [B][rec_pitch] native keys as sequences of capacity tn.n[b];
+  // the selection writes the recalled ids it keeps, then the window chunks
+  SeqTable tc = tn;
   for (int b = 0; b < B; ++b) {
     tc.keep[b] = tl->core_keep[b];
     tc.chunk_off[b] = (int64_t)b * P.rec_pitch;
   }
   SelectArgs sa2;
   sa2.dev_n = rec_cnt;
-  LSA_HIP(launch_topk(tc, LSA_F32, true, nat, core, P.core_pitch, 0, core_cnt, s, sa2), "native top-k launch");
-
-  // kept set: Level-2 ids, then the window
-  LSA_HIP(launch_two_level_finish(P.t, rec, P.rec_pitch, core, core_cnt, P.core_pitch, sel, P.max_sel, cnt, s),
-          "two-level finish launch");
+  sa2.map = rec;
+  sa2.map_pitch = P.rec_pitch;
+  LSA_HIP(launch_topk(tc, LSA_F32, true, nat, sel, P.max_sel, 0, cnt, s, sa2), "native top-k launch");
   return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
 }
 

@@ -18,6 +18,7 @@ struct SeqTable {
   int32_t n[LSA_MAX_BATCH];            // chunks of sequence b (a partial last chunk included)
   int32_t tail[LSA_MAX_BATCH];         // tokens in the last chunk of sequence b (the chunk size when complete)
   int32_t w0[LSA_MAX_BATCH];           // two-level path: first chunk of the always-resident window
+  int32_t win[LSA_MAX_BATCH];          // two-level path: chunks in that window
   int32_t keep[LSA_MAX_BATCH];         // keep budget k_b
   int32_t nsplit[LSA_MAX_BATCH];       // attention splits per (b, kv head)
   int32_t wg_off[LSA_MAX_BATCH + 1];   // first attention workgroup of sequence b
@@ -87,11 +88,16 @@ int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim, int32_t n_lookahead);
 // elements apart and selects on their per-entry maximum (the OR over layers).
 // dev_n (nullable): per-sequence key counts in device memory, read by the
 // kernel (at most t.n[b]); k_b is then min(keep[b], that count).
+// map (nullable): write map[b * map_pitch + i] for each selected key i instead
+// of i, then append the window chunks t.w0[b] .. t.w0[b] + t.win[b] - 1, and
+// count them in sel_count (the two-level path's Level 2).
 struct SelectArgs {
   bool recall = false;
   int32_t n_layers = 1;
   int64_t layer_stride = 0;
   const int32_t* dev_n = nullptr;
+  const int32_t* map = nullptr;
+  int64_t map_pitch = 0;
 };
 
 // keys_ready == true: `scores` holds keys written by launch_score(keys = true)
@@ -125,11 +131,6 @@ struct RecallArgs {
 // max_l x_l per entry, [total] (the input of the recall selection).
 hipError_t launch_recall_score(const SeqTable& t, const RecallArgs& r, void* out, bool keys, hipStream_t s);
 
-// Two-level selection, last step: sel[b] = list[b][pos[b][i]] for the count[b]
-// ascending positions, then the window chunks t.w0[b] .. t.n[b] - 1.
-hipError_t launch_two_level_finish(const SeqTable& t, const int32_t* list, int64_t list_pitch, const int32_t* pos,
-                                   const int32_t* pos_count, int64_t pos_pitch, int32_t* sel_idx, int64_t sel_pitch,
-                                   int32_t* sel_count, hipStream_t s);
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 

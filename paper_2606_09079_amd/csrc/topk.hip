@@ -57,6 +57,24 @@ __device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t* w
   return incl - v + wave_tot[wave];
 }
 
+// Selected key i as written: i itself, or its mapped id (two-level Level 2).
+__device__ __forceinline__ int32_t emitted(const SelectArgs& sa, int b, int i) {
+  return sa.map != nullptr ? sa.map[b * sa.map_pitch + i] : i;
+}
+
+// Count of the selection of sequence b, after the window chunks that follow
+// the k selected ones in mapped mode (all threads of the workgroup call it).
+__device__ __forceinline__ void finish_count(const SeqTable& t, const SelectArgs& sa, int b, int k, int32_t* out,
+                                             int32_t* sel_count, int tid, int nthreads) {
+  int total = k;
+  if (sa.map != nullptr) {
+    const int w0 = t.w0[b], nw = t.win[b];
+    for (int i = tid; i < nw; i += nthreads) out[k + i] = w0 + i;
+    total += nw;
+  }
+  if (sel_count != nullptr && tid == 0) sel_count[b] = total;
+}
+
 template <int MODE, bool RECALL>
 __global__ void __launch_bounds__(kThreads)
 topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict__ out_idx,
@@ -75,7 +93,7 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
   const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * t.n[b];
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
   if (k == 0) {  // no keys (uniform across the workgroup)
-    if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+    finish_count(t, sa, b, 0, out, sel_count, tid, kThreads);
     return;
   }
   const bool staged = n <= kLdsKeys;
@@ -139,7 +157,7 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
       if (shift == 24) {
         k = (int)sh_k;
         if (k == 0) {  // nothing recalled (uniform across the workgroup)
-          if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+          finish_count(t, sa, b, 0, out, sel_count, tid, kThreads);
           return;
         }
       }
@@ -165,14 +183,14 @@ topk_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict
     const uint32_t key = key_at(i);
     if (key > T) {
       const uint32_t pos = pgt + min(peq, krem);
-      if (pos < (uint32_t)k) out[pos] = i;
+      if (pos < (uint32_t)k) out[pos] = emitted(sa, b, i);
       ++pgt;
     } else if (key == T) {
-      if (peq < krem && pgt + peq < (uint32_t)k) out[pgt + peq] = i;
+      if (peq < krem && pgt + peq < (uint32_t)k) out[pgt + peq] = emitted(sa, b, i);
       ++peq;
     }
   }
-  if (sel_count != nullptr && tid == 0) sel_count[b] = k;
+  finish_count(t, sa, b, k, out, sel_count, tid, kThreads);
 }
 
 // ---------------------------------------------------------------------------
@@ -278,20 +296,29 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * t.n[b];
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
   if (k == 0) {  // no keys (uniform across the workgroup)
-    if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+    finish_count(t, sa, b, 0, out, sel_count, tid, kSelThreads);
     return;
   }
 
   // Key i = q * 1024 + tid sits in slot q of thread tid: coalesced buffer loads,
   // all in flight while the histogram is cleared.  Slots past the end hold key
-  // 0, the smallest key.  They are counted in bin 0 like real keys, which
-  // changes neither the threshold nor the tie quota (k <= n real keys all lie
-  // at or above them), and the emission drops their chunk ids.
+  // 0, which no finite score maps to.  They stay out of the histogram (with
+  // few real keys they would all land in bin 0 and serialise its atomics),
+  // never fall in the threshold bin, and the emission drops their chunk ids.
   const __amdgpu_buffer_rsrc_t src = raw_buffer(s, (uint32_t)n * 4u);
   uint32_t kk[kSelKPT];
 #pragma unroll
   for (int q = 0; q < kSelKPT; ++q)
     kk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
+  // mapped mode: the ids that the keys stand for, loaded with them and staged
+  // in LDS (in the histogram's space, once it is free) for the emission
+  uint32_t mp[kSelKPT];
+  if (sa.map != nullptr) {
+    const __amdgpu_buffer_rsrc_t msrc = raw_buffer(sa.map + b * sa.map_pitch, (uint32_t)n * 4u);
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q)
+      mp[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(msrc, tid * 4, q * kSelThreads * 4, 0);
+  }
   if constexpr (RECALL) {
     // keys of the first layer, then the largest over the other indexer layers
 #pragma unroll
@@ -318,7 +345,7 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   for (int q = 0; q < kSelKPT; ++q) {
     if constexpr (MODE != kKeysReady && !RECALL) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
     bin[q] = kk[q] >> 20;
-    rk[q] = atomicAdd(&hist[bin[q] * kSelSub + sub], 1u);
+    rk[q] = q * kSelThreads + tid < n ? atomicAdd(&hist[bin[q] * kSelSub + sub], 1u) : 0u;
   }
   if constexpr (RECALL) {
     uint32_t nn = 0;
@@ -332,7 +359,7 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
     const uint32_t c = lane < kSelWaves ? nonneg[lane] : 0u;
     k = min(k, (int)lane_bcast(wave_scan_incl(c), 63));
     if (k == 0) {  // nothing recalled (uniform across the workgroup)
-      if (sel_count != nullptr && tid == 0) sel_count[b] = 0;
+      finish_count(t, sa, b, 0, out, sel_count, tid, kSelThreads);
       return;
     }
   }
@@ -405,6 +432,11 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   // start, only where it is not empty).
   const uint32_t T = sh[0];
   krem = sh[1];
+  uint32_t* map_lds = hist;  // free from here on
+  if (sa.map != nullptr) {
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) map_lds[q * kSelThreads + tid] = mp[q];
+  }
   uint64_t* gdst = reinterpret_cast<uint64_t*>(bm_gt) + wave;
   uint64_t* edst = reinterpret_cast<uint64_t*>(bm_eq) + wave;
 #pragma unroll
@@ -442,11 +474,12 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
     }
     uint32_t pos = gb + min(eb, krem);
     while (kept != 0u) {
-      out[pos++] = 32 * tid + __builtin_ctz(kept);
+      const int i = 32 * tid + __builtin_ctz(kept);
+      out[pos++] = sa.map != nullptr ? (int32_t)map_lds[i] : i;
       kept &= kept - 1u;
     }
   }
-  if (sel_count != nullptr && tid == 0) sel_count[b] = k;
+  finish_count(t, sa, b, k, out, sel_count, tid, kSelThreads);
 }
 
 // Ascending union of the Q per-query lists of each sequence via an LDS bitmap.
@@ -482,22 +515,6 @@ union_kernel(SeqTable t, const int32_t* __restrict__ per_query, int32_t k_pitch,
     }
   }
   if (tid == kThreads - 1) sel_count[b] = (int32_t)pos;
-}
-
-// Two-level selection, last step: kept ids of Level 2 (positions into the
-// recalled list, ascending, so the ids come out ascending too), then the
-// window chunks, which lie above every history chunk.
-__global__ void __launch_bounds__(kThreads)
-two_level_finish_kernel(SeqTable t, const int32_t* __restrict__ list, int64_t list_pitch,
-                        const int32_t* __restrict__ pos, const int32_t* __restrict__ pos_count, int64_t pos_pitch,
-                        int32_t* __restrict__ sel, int64_t sel_pitch, int32_t* __restrict__ sel_count) {
-  const int b = blockIdx.x;
-  const int m = max(pos_count[b], 0);
-  const int w0 = t.w0[b], nw = max(t.n[b] - w0, 0);
-  int32_t* out = sel + (int64_t)b * sel_pitch;
-  for (int i = threadIdx.x; i < m; i += kThreads) out[i] = list[(int64_t)b * list_pitch + pos[(int64_t)b * pos_pitch + i]];
-  for (int i = threadIdx.x; i < nw; i += kThreads) out[m + i] = w0 + i;
-  if (threadIdx.x == 0) sel_count[b] = m + nw;
 }
 
 __global__ void zero_kernel(uint4* p, size_t n16, uint8_t* tail, size_t ntail) {
@@ -548,14 +565,6 @@ hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_p
                         int32_t* sel_idx, int32_t sel_pitch, int32_t* sel_count, hipStream_t s) {
   hipLaunchKernelGGL(union_kernel, dim3(t.batch), dim3(kThreads), 0, s, t, per_query, k_pitch, sel_idx,
                      sel_pitch, sel_count);
-  return hipGetLastError();
-}
-
-hipError_t launch_two_level_finish(const SeqTable& t, const int32_t* list, int64_t list_pitch, const int32_t* pos,
-                                   const int32_t* pos_count, int64_t pos_pitch, int32_t* sel_idx, int64_t sel_pitch,
-                                   int32_t* sel_count, hipStream_t s) {
-  hipLaunchKernelGGL(two_level_finish_kernel, dim3(t.batch), dim3(kThreads), 0, s, t, list, list_pitch, pos,
-                     pos_count, pos_pitch, sel_idx, sel_pitch, sel_count);
   return hipGetLastError();
 }
 
