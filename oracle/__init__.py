@@ -243,6 +243,37 @@ def kept_tokens(kept: np.ndarray, chunk: int, ctx_tokens: int) -> np.ndarray:
         if len(kept) else np.zeros(0, dtype=np.int64)
 
 
+# ------------------------------------------------------------- host tier
+def tier_plan(owner: Sequence[int], old_slots: Sequence[int], kept: Sequence[int]):
+    """Residency plan of one sequence's GPU reserve (Sec. 2.5: the recalled set
+    is materialised from the host cold mirror into a GPU reserve of slots).
+
+    owner[s] is the chunk slot s holds (-1: empty); old_slots are the slots the
+    previous kept set is read from (they must survive this step, so that the
+    previous set stays readable while the new one is copied in); kept are the
+    new kept chunk ids, ascending.  A kept chunk that some slot already holds
+    keeps that slot; the others take the free slots -- neither protected by
+    old_slots nor holding a kept chunk -- in ascending order.  Returns
+    (new_owner, slot of every kept chunk in kept order, [(chunk, slot)] to copy
+    in), or raises when the slots do not suffice."""
+    owner = list(owner)
+    where = {}
+    for s, c in enumerate(owner):
+        if c >= 0:
+            where[c] = s
+    protected = set(old_slots) | {where[c] for c in kept if c in where}
+    free = [s for s in range(len(owner)) if s not in protected]
+    missing = [c for c in kept if c not in where]
+    if len(missing) > len(free):
+        raise ValueError("reserve too small")
+    fetch = list(zip(missing, free))
+    for c, s in fetch:
+        owner[s] = c
+    slot_of = {c: where[c] for c in kept if c in where}
+    slot_of.update({c: s for c, s in fetch})
+    return owner, [slot_of[c] for c in kept], fetch
+
+
 # ---------------------------------------------------------------- O4 step
 def select_for_sequence(prob, inputs: Dict[str, object], b: int):
     """O1 then O2 for sequence b.

@@ -414,6 +414,44 @@ def pin_two_level_bruteforce():
         assert got == want, f"two-level brute force rec={rec} native={native.tolist()} k2={k2}"
 
 
+# ---------------------------------------------------------------- host tier
+def pin_tier_plan_invariants():
+    """What the reserve must guarantee, checked on random firings: every kept
+    chunk ends up in exactly one slot; a chunk already resident is not copied
+    again; no slot the previous kept set reads is given to another chunk; the
+    copies are exactly the kept chunks that were not resident; an empty reserve
+    fills its slots in ascending order."""
+    rng = np.random.default_rng(20)
+    for trial in range(60):
+        n, kmax = int(rng.integers(1, 40)), int(rng.integers(1, 8))
+        n_slots = 2 * min(kmax, n) + int(rng.integers(0, 3))
+        owner = [-1] * n_slots
+        old = []
+        for firing in range(6):
+            kept = sorted(rng.choice(n, size=int(rng.integers(0, min(kmax, n) + 1)), replace=False).tolist())
+            before = list(owner)
+            owner, slots, fetch = oracle.tier_plan(owner, old, kept)
+            assert len(slots) == len(kept) and len(set(slots)) == len(slots), "one slot per kept chunk"
+            assert all(owner[s] == c for c, s in zip(kept, slots)), "the slot holds its chunk"
+            assert sorted(c for c in owner if c >= 0) == sorted(set(c for c in owner if c >= 0)), "no chunk twice"
+            resident = {c for c in before if c >= 0}
+            assert [c for c, _ in fetch] == [c for c in kept if c not in resident], "copies = kept, not resident"
+            for s in old:
+                assert owner[s] == before[s], "a slot the previous set reads was reassigned"
+            for c, s in zip(kept, slots):
+                if c in resident:
+                    assert before[s] == c, "a resident chunk moved"
+            if firing == 0 and trial % 2 == 0:
+                assert slots == list(range(len(kept))), "empty reserve fills from slot 0"
+            old = slots
+    # too small a reserve is an error
+    try:
+        oracle.tier_plan([-1], [0], [3])
+        raise AssertionError("no free slot must raise")
+    except ValueError:
+        pass
+
+
 ALL_PINS = [
     pin_score_library_matmul, pin_score_int8_exact, pin_score_closed_forms,
     pin_topk_worked_example, pin_topk_bruteforce, pin_topk_library_sort, pin_union_bruteforce,
@@ -422,5 +460,5 @@ ALL_PINS = [
     pin_recall_worked_example, pin_index_score_single_head, pin_index_score_relu_identities,
     pin_index_score_head_permutation, pin_recall_sigmoid_threshold, pin_recall_or_bruteforce,
     pin_recall_boundaries, pin_attention_tokens_reduces_to_chunks, pin_two_level_worked_example,
-    pin_two_level_bruteforce,
+    pin_two_level_bruteforce, pin_tier_plan_invariants,
 ]
