@@ -62,6 +62,12 @@
  * always-resident window (Level 1), the native indexer's top-k inside the
  * recalled set (Level 2, Eq. 6), and the window chunks added (Sec. 2.5); the
  * context may end inside a chunk, whose missing tokens get no weight.
+ *
+ * Host tier (lsa_tier_*): the decode-side offload of Sec. 2.5 -- the whole
+ * cache stays in a pinned host mirror, each sequence has a GPU reserve of
+ * chunk slots, a residency plan maps the recalled chunks to slots, the missing
+ * ones are copied in from the mirror (a side-band step that can overlap
+ * decode), and attention runs over the reserve.
  */
 #ifndef LSA_H_
 #define LSA_H_
@@ -80,6 +86,8 @@ extern "C" {
 #define LSA_MAX_ROWS 128           /* n_qtok * n_q_heads / n_kv_heads */
 #define LSA_MAX_UNION_CHUNKS 262144 /* n_b limit when n_lookahead > 1 */
 #define LSA_MAX_IDX_LAYERS 4       /* indexer layers OR-ed by the recall path */
+#define LSA_MAX_TIER_CHUNKS 131072 /* n_b limit of the host tier's residency plan */
+#define LSA_MAX_TIER_SLOTS 65536   /* reserve slots per sequence */
 
 typedef enum {
   LSA_OK = 0,
@@ -116,6 +124,13 @@ typedef struct lsa_indexer {
   int32_t key_dim;   /* c, width of the indexer queries and compressed index keys: 64 or 128 */
   int32_t reserved;  /* must be 0 */
 } lsa_indexer;
+
+/* Host tier.  Host memory only; read during the call. */
+typedef struct lsa_tier {
+  const int32_t* slots;  /* HOST [B]: reserve slots of sequence b, 2 * keep[b] .. LSA_MAX_TIER_SLOTS */
+  int32_t reserved;      /* must be 0 */
+  int32_t reserved2;     /* must be 0 */
+} lsa_tier;
 
 /* Two-level selection.  Host memory only; read during the call. */
 typedef struct lsa_two_level {
@@ -261,6 +276,71 @@ lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const
                               const float* nat_w, const void* nat_k, const uint16_t* q, const uint16_t* k_cache,
                               const uint16_t* v_cache, float softmax_scale, float* out, float* lse, int32_t* sel_idx,
                               int32_t* sel_count, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Host tier (Sec. 2.5, decode-side offload and asynchronous recall).  The
+ * problem is the one of the full context (ctx_tokens[b] a multiple of
+ * chunk_size, n_b <= LSA_MAX_TIER_CHUNKS, n_lookahead == 1) with keep[b] the
+ * bound K_max on the kept set.  Sequence b owns slots[b] reserve slots; slot
+ * ids are local to the sequence and reserve slot s of sequence b is global
+ * slot slot_off[b] + s, slot_off the exclusive prefix sum of slots.
+ *   owner    device int32 [sum_b slots[b]]: the chunk id each slot holds, -1
+ *            when it holds none (the residency table; the library keeps it up
+ *            to date, the caller allocates it and resets it once)
+ *   res_k, res_v   device bf16 reserve, [sum_b slots[b]][n_kv_heads][C x 128]:
+ *            global slot j and KV head g start at element (j * n_kv_heads + g)
+ *            * C * 128 and hold that chunk-head block exactly as the cache
+ *            stores it (the MFMA operand order above)
+ *   host_k, host_v  the mirror: pinned host memory (hipHostMalloc, or a pinned
+ *            torch tensor) laid out as the cache, with the problem's strides
+ * Kept lists, slot lists and copy lists are [B][pitch] with pitch = lsa_max_sel()
+ * (copy lists [B][pitch][2] of (chunk id, local slot id)).
+ */
+/* Pitch of the lists, slots in the reserve, and the workspace of
+ * lsa_tier_attend (any output pointer may be NULL). */
+lsa_status lsa_tier_sizes(const lsa_problem* p, const lsa_tier* tr, int32_t* pitch, int64_t* total_slots,
+                          size_t* ws_bytes);
+/* owner[0 .. sum_b slots[b]) = -1: an empty reserve (a fill kernel on stream). */
+lsa_status lsa_tier_reset(const lsa_problem* p, const lsa_tier* tr, int32_t* owner, void* stream);
+/*
+ * Residency plan of one firing.  kept_idx[b][0 .. kept_count[b]) are distinct
+ * chunk ids < n_b in ascending order (as the selections write them);
+ * prev_slots[b][0 .. prev_count[b]) are the slots the previous kept set reads
+ * (the previous call's slot_idx; both NULL at the first firing).  Per sequence:
+ *  - a kept chunk that a slot already holds keeps that slot;
+ *  - the other kept chunks, in ascending order, take the free slots in
+ *    ascending order, a free slot being one that holds no kept chunk and that
+ *    the previous set does not read (so decode may go on reading the previous
+ *    set until the copies are done);
+ *  - slot_idx[b][i] = slot of kept_idx[b][i]; fetch[b][f] = (chunk, slot) for
+ *    f < fetch_count[b], ascending in both; owner is updated.
+ * slots[b] >= 2 * keep[b] guarantees enough free slots.  Should that fail
+ * anyway, fetch_count[b] = -1 and owner is left as it was.  A kept id
+ * outside 0 .. n_b - 1 gets slot -1 and no copy.
+ */
+lsa_status lsa_tier_plan(const lsa_problem* p, const lsa_tier* tr, const int32_t* kept_idx,
+                         const int32_t* kept_count, const int32_t* prev_slots, const int32_t* prev_count,
+                         int32_t* owner, int32_t* slot_idx, int32_t* fetch, int32_t* fetch_count, void* stream);
+/*
+ * Copy the chunks of a plan's copy list from the mirror into the reserve: for
+ * f < fetch_count[b], the K and V blocks of every KV head of chunk fetch[b][f][0]
+ * into slot fetch[b][f][1].  The GPU reads the mirror over PCIe (no host
+ * synchronisation; the copy list stays on the device).  LSA_ERR_INVALID_ARG
+ * when host_k or host_v is not pinned, device-visible host memory.
+ */
+lsa_status lsa_tier_fetch(const lsa_problem* p, const lsa_tier* tr, const uint16_t* host_k,
+                          const uint16_t* host_v, const int32_t* fetch, const int32_t* fetch_count,
+                          uint16_t* res_k, uint16_t* res_v, void* stream);
+/*
+ * Step 3 over the reserve: the attention of lsa_sparse_decode_attn for the
+ * chunks held in slots slot_idx[b][0 .. slot_count[b]) (the remapped kept
+ * set), reading res_k / res_v only.  The kept chunks in the same order give
+ * the same result, bit for bit, as lsa_sparse_decode_attn on the full cache
+ * with sel_idx = the kept ids.
+ */
+lsa_status lsa_tier_attend(const lsa_problem* p, const lsa_tier* tr, const uint16_t* q, const uint16_t* res_k,
+                           const uint16_t* res_v, const int32_t* slot_idx, const int32_t* slot_count,
+                           float softmax_scale, float* out, float* lse, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

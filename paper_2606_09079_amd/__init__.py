@@ -3,12 +3,16 @@
 score every compressed chunk (Memory Indexer dot product) -> keep the top-k
 chunks -> sparse decode attention over the kept chunks, and the recall path
 (full gated multi-head Memory Indexer, sigmoid threshold, OR over indexer
-layers, K_max bound) in front of the same attention, as hand-written HIP
+layers, K_max bound) in front of the same attention, the two-level selection
+(recall, native top-k inside it, always-resident window) and the host tier
+(pinned host mirror, GPU reserve of chunk slots, residency plan, copies,
+attention over the reserve), as hand-written HIP
 kernels behind the C ABI of ``include/lsa.h``.  The Python layer is the thin
 ctypes binding in :mod:`.lsa`; importing it loads ``liblsa.so`` and raises if
 that is not possible.
 """
-from .lsa import (LIB, Indexer, LsaError, Problem, TwoLevel, lsa_decode_step, lsa_max_keep,  # noqa: F401
+from .lsa import (LIB, Indexer, LsaError, Problem, Tier, TwoLevel, lsa_decode_step, lsa_max_keep,  # noqa: F401
                   lsa_max_sel, lsa_recall_scores, lsa_recall_select, lsa_recall_step, lsa_score_chunks,
-                  lsa_sparse_decode_attn, lsa_topk_chunks, lsa_two_level_sizes, lsa_two_level_step, lsa_validate,
+                  lsa_sparse_decode_attn, lsa_tier_attend, lsa_tier_fetch, lsa_tier_plan, lsa_tier_reset,
+                  lsa_tier_sizes, lsa_topk_chunks, lsa_two_level_sizes, lsa_two_level_step, lsa_validate,
                   lsa_workspace_init, lsa_workspace_size, last_error)

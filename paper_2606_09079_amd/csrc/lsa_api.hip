@@ -341,6 +341,50 @@ lsa_status check_recall_inputs(const void* idx_q, const float* idx_w, const void
   return LSA_OK;
 }
 
+// The host tier's plans: P for the full context (its kept lists and copies),
+// R for the reserve, a problem whose sequence b has slots[b] chunks, so that
+// the attention over slot ids is the attention over chunk ids with the
+// reserve as the cache.  Both have the same kept bound min(keep[b], n) =
+// keep[b], hence the same split-K plan.
+struct TierPlan {
+  Plan P, R;
+  int32_t slot_off[LSA_MAX_BATCH + 1] = {};
+  int64_t total_slots = 0;
+};
+
+lsa_status make_tier_plan(const lsa_problem* p, const lsa_tier* tr, TierPlan* tp) {
+  LSA_TRY(make_plan(p, &tp->P));
+  if (tr == nullptr) return fail(LSA_ERR_INVALID_ARG, "tier is NULL");
+  if (tr->reserved != 0 || tr->reserved2 != 0) return fail(LSA_ERR_INVALID_ARG, "tier reserved fields must be 0");
+  if (tr->slots == nullptr) return fail(LSA_ERR_INVALID_ARG, "tier slots must be a host array of batch entries");
+  if (p->n_lookahead != 1)
+    return fail(LSA_ERR_INVALID_ARG, "the host tier takes one query token: n_lookahead %d != 1", p->n_lookahead);
+  const int B = p->batch;
+  int64_t rctx[LSA_MAX_BATCH];
+  int64_t off = 0;
+  for (int b = 0; b < B; ++b) {
+    const int32_t n = tp->P.t.n[b], k = p->keep[b], S = tr->slots[b];
+    if (n > LSA_MAX_TIER_CHUNKS)
+      return fail(LSA_ERR_UNSUPPORTED, "sequence %d: %d chunks > %d in the host tier", b, n, LSA_MAX_TIER_CHUNKS);
+    if (S < 2 * (int64_t)k || S > LSA_MAX_TIER_SLOTS)
+      return fail(LSA_ERR_INVALID_ARG, "slots[%d] = %d not in [2 * keep = %lld, %d]", b, S, 2 * (long long)k,
+                  LSA_MAX_TIER_SLOTS);
+    tp->slot_off[b] = (int32_t)off;
+    off += S;
+    rctx[b] = (int64_t)S * p->chunk_size;
+  }
+  tp->slot_off[B] = (int32_t)off;
+  tp->total_slots = off;
+  lsa_problem r = *p;
+  r.ctx_tokens = rctx;
+  r.kv_chunk_stride = 0;
+  r.kv_head_stride = 0;
+  LSA_TRY(make_plan(&r, &tp->R));
+  if (tp->R.max_sel != tp->P.max_sel || tp->R.n_units != tp->P.n_units)
+    return fail(LSA_ERR_INVALID_ARG, "reserve plan differs from the context plan");
+  return LSA_OK;
+}
+
 }  // namespace
 }  // namespace lsa
 
@@ -644,6 +688,124 @@ lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const
   sa2.map_pitch = P.rec_pitch;
   LSA_HIP(launch_topk(tc, LSA_F32, true, nat, sel, P.max_sel, 0, cnt, s, sa2), "native top-k launch");
   return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
+}
+
+lsa_status lsa_tier_sizes(const lsa_problem* p, const lsa_tier* tr, int32_t* pitch, int64_t* total_slots,
+                          size_t* ws_bytes) {
+  TierPlan T;
+  LSA_TRY(make_tier_plan(p, tr, &T));
+  if (pitch != nullptr) *pitch = T.P.max_sel;
+  if (total_slots != nullptr) *total_slots = T.total_slots;
+  if (ws_bytes != nullptr) *ws_bytes = T.R.ws_total;
+  return LSA_OK;
+}
+
+lsa_status lsa_tier_reset(const lsa_problem* p, const lsa_tier* tr, int32_t* owner, void* stream) {
+  TierPlan T;
+  LSA_TRY(make_tier_plan(p, tr, &T));
+  LSA_TRY(check_ptr(owner, "owner"));
+  LSA_HIP(launch_tier_reset(owner, T.total_slots, (hipStream_t)stream), "tier reset launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_tier_plan(const lsa_problem* p, const lsa_tier* tr, const int32_t* kept_idx,
+                         const int32_t* kept_count, const int32_t* prev_slots, const int32_t* prev_count,
+                         int32_t* owner, int32_t* slot_idx, int32_t* fetch, int32_t* fetch_count, void* stream) {
+  TierPlan T;
+  LSA_TRY(make_tier_plan(p, tr, &T));
+  LSA_TRY(check_ptr(kept_idx, "kept_idx"));
+  LSA_TRY(check_ptr(kept_count, "kept_count"));
+  if ((prev_slots == nullptr) != (prev_count == nullptr))
+    return fail(LSA_ERR_INVALID_ARG, "prev_slots and prev_count must both be given or both be NULL");
+  if (prev_slots != nullptr) {
+    LSA_TRY(check_ptr(prev_slots, "prev_slots"));
+    LSA_TRY(check_ptr(prev_count, "prev_count"));
+  }
+  LSA_TRY(check_ptr(owner, "owner"));
+  LSA_TRY(check_ptr(slot_idx, "slot_idx"));
+  LSA_TRY(check_ptr(fetch, "fetch"));
+  LSA_TRY(check_ptr(fetch_count, "fetch_count"));
+  if (slot_idx == kept_idx || slot_idx == prev_slots)
+    return fail(LSA_ERR_INVALID_ARG, "slot_idx must not alias kept_idx or prev_slots");
+  TierArgs a;
+  a.kept = kept_idx;
+  a.kept_count = kept_count;
+  a.prev_slots = prev_slots;
+  a.prev_count = prev_count;
+  a.owner = owner;
+  a.slot_idx = slot_idx;
+  a.fetch = fetch;
+  a.fetch_count = fetch_count;
+  a.pitch = T.P.max_sel;
+  for (int b = 0; b < p->batch; ++b) a.slots[b] = tr->slots[b];
+  memcpy(a.slot_off, T.slot_off, sizeof a.slot_off);
+  LSA_HIP(launch_tier_plan(T.P.t, a, (hipStream_t)stream), "tier plan launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_tier_fetch(const lsa_problem* p, const lsa_tier* tr, const uint16_t* host_k,
+                          const uint16_t* host_v, const int32_t* fetch, const int32_t* fetch_count,
+                          uint16_t* res_k, uint16_t* res_v, void* stream) {
+  TierPlan T;
+  LSA_TRY(make_tier_plan(p, tr, &T));
+  LSA_TRY(check_ptr(host_k, "host_k"));
+  LSA_TRY(check_ptr(host_v, "host_v"));
+  LSA_TRY(check_ptr(fetch, "fetch"));
+  LSA_TRY(check_ptr(fetch_count, "fetch_count"));
+  LSA_TRY(check_ptr(res_k, "res_k"));
+  LSA_TRY(check_ptr(res_v, "res_v"));
+  const Plan& P = T.P;
+  // last element of the mirror: the final block of the last chunk and head
+  const int64_t last = (P.total_chunks - 1) * P.chunk_stride + (int64_t)(p->n_kv_heads - 1) * P.head_stride +
+                       (int64_t)p->chunk_size * kHeadDim - 1;
+  const uint16_t* host[2] = {host_k, host_v};
+  const uint16_t* dev[2] = {nullptr, nullptr};
+  for (int i = 0; i < 2; ++i) {
+    void* d0 = nullptr;
+    void* d1 = nullptr;
+    if (hipHostGetDevicePointer(&d0, const_cast<uint16_t*>(host[i]), 0) != hipSuccess || d0 == nullptr ||
+        hipHostGetDevicePointer(&d1, const_cast<uint16_t*>(host[i] + last), 0) != hipSuccess ||
+        static_cast<uint16_t*>(d1) != static_cast<uint16_t*>(d0) + last) {
+      (void)hipGetLastError();  // clear the error the failed lookup recorded
+      return fail(LSA_ERR_INVALID_ARG, "%s is not pinned host memory mapped for the device over the whole mirror",
+                  i ? "host_v" : "host_k");
+    }
+    dev[i] = static_cast<const uint16_t*>(d0);
+  }
+  TierFetchArgs a;
+  a.host_k = dev[0];
+  a.host_v = dev[1];
+  a.res_k = res_k;
+  a.res_v = res_v;
+  a.fetch = fetch;
+  a.fetch_count = fetch_count;
+  a.chunk_stride = P.chunk_stride;
+  a.head_stride = P.head_stride;
+  a.res_slot_stride = (int64_t)p->n_kv_heads * p->chunk_size * kHeadDim;
+  a.pitch = P.max_sel;
+  a.n_kv_heads = p->n_kv_heads;
+  for (int b = 0; b < p->batch; ++b) a.slots[b] = tr->slots[b];
+  memcpy(a.slot_off, T.slot_off, sizeof a.slot_off);
+  LSA_HIP(launch_tier_fetch(P.t, a, p->chunk_size, (hipStream_t)stream), "tier fetch launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_tier_attend(const lsa_problem* p, const lsa_tier* tr, const uint16_t* q, const uint16_t* res_k,
+                           const uint16_t* res_v, const int32_t* slot_idx, const int32_t* slot_count,
+                           float softmax_scale, float* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  TierPlan T;
+  LSA_TRY(make_tier_plan(p, tr, &T));
+  LSA_TRY(check_ptr(q, "q"));
+  LSA_TRY(check_ptr(res_k, "res_k"));
+  LSA_TRY(check_ptr(res_v, "res_v"));
+  LSA_TRY(check_ptr(slot_idx, "slot_idx"));
+  LSA_TRY(check_ptr(slot_count, "slot_count"));
+  LSA_TRY(check_ptr(out, "out"));
+  if (lse != nullptr && (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(LSA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
+  LSA_TRY(check_ws(T.R, ws, ws_bytes));
+  return run_attn(p, T.R, q, res_k, res_v, slot_idx, slot_count, softmax_scale, out, lse, ws, (hipStream_t)stream);
 }
 
 }  // extern "C"

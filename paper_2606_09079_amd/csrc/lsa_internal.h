@@ -132,6 +132,43 @@ struct RecallArgs {
 hipError_t launch_recall_score(const SeqTable& t, const RecallArgs& r, void* out, bool keys, hipStream_t s);
 
 
+// Host tier: residency plan and copies between a pinned host mirror of the
+// cache and a GPU reserve of chunk slots.  Sequence b owns reserve slots
+// slot_off[b] .. slot_off[b] + slots[b] - 1; slot ids in the lists are local
+// to the sequence.
+constexpr int kMaxTierChunks = LSA_MAX_TIER_CHUNKS;
+constexpr int kMaxTierSlots = LSA_MAX_TIER_SLOTS;
+struct TierArgs {
+  const int32_t* kept;        // [B][pitch] ascending chunk ids
+  const int32_t* kept_count;  // [B]
+  const int32_t* prev_slots;  // nullable [B][pitch]: slots the previous kept set reads
+  const int32_t* prev_count;  // [B]
+  int32_t* owner;             // [sum_b slots[b]] chunk held by each slot, -1 when none
+  int32_t* slot_idx;          // [B][pitch] slot of each kept chunk
+  int32_t* fetch;             // [B][pitch][2] (chunk, slot) copies
+  int32_t* fetch_count;       // [B]
+  int32_t pitch;
+  int32_t slots[LSA_MAX_BATCH];
+  int32_t slot_off[LSA_MAX_BATCH + 1];
+};
+struct TierFetchArgs {
+  const uint16_t* host_k;     // device-visible addresses of the pinned mirror
+  const uint16_t* host_v;
+  uint16_t* res_k;
+  uint16_t* res_v;
+  const int32_t* fetch;
+  const int32_t* fetch_count;
+  int64_t chunk_stride, head_stride;  // mirror strides (the cache's)
+  int64_t res_slot_stride;            // n_kv_heads * C * 128
+  int32_t pitch;
+  int32_t n_kv_heads;
+  int32_t slots[LSA_MAX_BATCH];
+  int32_t slot_off[LSA_MAX_BATCH + 1];
+};
+hipError_t launch_tier_plan(const SeqTable& t, const TierArgs& a, hipStream_t s);
+hipError_t launch_tier_fetch(const SeqTable& t, const TierFetchArgs& a, int32_t chunk_size, hipStream_t s);
+hipError_t launch_tier_reset(int32_t* owner, int64_t n, hipStream_t s);
+
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 
 }  // namespace lsa

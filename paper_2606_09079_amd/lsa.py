@@ -31,7 +31,8 @@ DTYPES = {"f32": 0, "bf16": 1, "i8": 2}
 EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_validate", "lsa_max_sel",
            "lsa_max_keep", "lsa_workspace_size", "lsa_workspace_init", "lsa_score_chunks", "lsa_topk_chunks",
            "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
-           "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step")
+           "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step", "lsa_tier_sizes", "lsa_tier_reset",
+           "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_attend")
 
 
 class lsa_problem(ctypes.Structure):
@@ -53,6 +54,11 @@ class lsa_indexer(ctypes.Structure):
 class lsa_two_level(ctypes.Structure):
     _fields_ = [("native_heads", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("core_keep", ctypes.POINTER(ctypes.c_int32)), ("window_tokens", ctypes.POINTER(ctypes.c_int64))]
+
+
+class lsa_tier(ctypes.Structure):
+    _fields_ = [("slots", ctypes.POINTER(ctypes.c_int32)), ("reserved", ctypes.c_int32),
+                ("reserved2", ctypes.c_int32)]
 
 
 def _load() -> ctypes.CDLL:
@@ -88,6 +94,13 @@ def _load() -> ctypes.CDLL:
     lib.lsa_two_level_sizes.argtypes = [pp, tp, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
     lib.lsa_two_level_step.argtypes = [pp, ip, tp, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P,
                                        _P, _P, ctypes.c_size_t, _P]
+    rp = ctypes.POINTER(lsa_tier)
+    lib.lsa_tier_sizes.argtypes = [pp, rp, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int64),
+                                   ctypes.POINTER(ctypes.c_size_t)]
+    lib.lsa_tier_reset.argtypes = [pp, rp, _P, _P]
+    lib.lsa_tier_plan.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.lsa_tier_fetch.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P]
+    lib.lsa_tier_attend.argtypes = [pp, rp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
     for name in EXPORTS[3:]:
         getattr(lib, name).restype = ctypes.c_int
     if lib.lsa_abi_version() != 1:
@@ -150,6 +163,18 @@ class TwoLevel:
     @classmethod
     def from_synth(cls, prob) -> "TwoLevel":
         return cls(prob.nat_heads, prob.core_keep, prob.window_tokens)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+class Tier:
+    """Host tier: reserve slots per sequence (mirrors ``lsa_tier``; keeps its host array alive)."""
+
+    def __init__(self, slots: Sequence[int]):
+        self._slots = (ctypes.c_int32 * max(len(slots), 1))(*slots)
+        self.c = lsa_tier(ctypes.cast(self._slots, ctypes.POINTER(ctypes.c_int32)), 0, 0)
 
     @property
     def ref(self):
@@ -264,3 +289,33 @@ def lsa_two_level_step(p: Problem, ix: Indexer, tl: TwoLevel, idx_q, idx_w, idx_
                                   _ptr(nat_w), _ptr(nat_k), _ptr(q), _ptr(k_cache), _ptr(v_cache),
                                   float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx), _ptr(sel_count), _ptr(ws),
                                   ws_bytes, _stream(stream)), "lsa_two_level_step")
+
+
+def lsa_tier_sizes(p: Problem, tr: Tier):
+    """(pitch of the kept, slot and copy lists, reserve slots in total, workspace bytes of lsa_tier_attend)."""
+    m, n, w = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_size_t()
+    _check(LIB.lsa_tier_sizes(p.ref, tr.ref, ctypes.byref(m), ctypes.byref(n), ctypes.byref(w)), "lsa_tier_sizes")
+    return m.value, n.value, w.value
+
+
+def lsa_tier_reset(p: Problem, tr: Tier, owner, stream=None) -> None:
+    _check(LIB.lsa_tier_reset(p.ref, tr.ref, _ptr(owner), _stream(stream)), "lsa_tier_reset")
+
+
+def lsa_tier_plan(p: Problem, tr: Tier, kept_idx, kept_count, prev_slots, prev_count, owner, slot_idx, fetch,
+                  fetch_count, stream=None) -> None:
+    _check(LIB.lsa_tier_plan(p.ref, tr.ref, _ptr(kept_idx), _ptr(kept_count), _ptr(prev_slots), _ptr(prev_count),
+                             _ptr(owner), _ptr(slot_idx), _ptr(fetch), _ptr(fetch_count), _stream(stream)),
+           "lsa_tier_plan")
+
+
+def lsa_tier_fetch(p: Problem, tr: Tier, host_k, host_v, fetch, fetch_count, res_k, res_v, stream=None) -> None:
+    _check(LIB.lsa_tier_fetch(p.ref, tr.ref, _ptr(host_k), _ptr(host_v), _ptr(fetch), _ptr(fetch_count),
+                              _ptr(res_k), _ptr(res_v), _stream(stream)), "lsa_tier_fetch")
+
+
+def lsa_tier_attend(p: Problem, tr: Tier, q, res_k, res_v, slot_idx, slot_count, softmax_scale: float, out, lse=None,
+                    ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(LIB.lsa_tier_attend(p.ref, tr.ref, _ptr(q), _ptr(res_k), _ptr(res_v), _ptr(slot_idx), _ptr(slot_count),
+                               float(softmax_scale), _ptr(out), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)),
+           "lsa_tier_attend")

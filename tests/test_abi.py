@@ -190,3 +190,51 @@ def test_two_level_presets_size():
         ms, ws = L.lsa_two_level_sizes(L.Problem.from_synth(prob), L.TwoLevel.from_synth(prob))
         assert ms == max(min(prob.core_keep[b], prob.keep[b], prob.history_chunks(b)) + prob.n_chunks[b]
                          - prob.window_start(b) for b in range(prob.batch))
+
+
+def test_tier_sizes_and_validation():
+    p = L.Problem([64 * 300, 64 * 1000], 64, [40, 100], 8, 2)
+    T = L.Tier([80, 200])
+    pitch, total, ws = L.lsa_tier_sizes(p, T)
+    assert (pitch, total) == (100, 280) and ws > 0
+    # the reserve plan has the context plan's split-K layout, so its workspace
+    # differs from the context's only in the per-chunk score region
+    assert ws <= L.lsa_workspace_size(p)
+    lib = L.LIB
+    for slots in ([79, 200], [80, 199], [80, 65537]):
+        assert lib.lsa_tier_sizes(p.ref, L.Tier(slots).ref, None, None, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_sizes(p.ref, None, None, None, None) == B.LSA_ERR_INVALID_ARG
+    bad = L.Tier([80, 200])
+    bad.c.reserved = 1
+    assert lib.lsa_tier_sizes(p.ref, bad.ref, None, None, None) == B.LSA_ERR_INVALID_ARG
+    la = L.Problem([64 * 300], 64, [40], 8, 2, n_lookahead=2)
+    assert lib.lsa_tier_sizes(la.ref, L.Tier([80]).ref, None, None, None) == B.LSA_ERR_INVALID_ARG
+    part = L.Problem([64 * 300 + 5], 64, [40], 8, 2)
+    assert lib.lsa_tier_sizes(part.ref, L.Tier([80]).ref, None, None, None) == B.LSA_ERR_INVALID_ARG
+    big = L.Problem([64 * (131072 + 1)], 64, [40], 8, 2)
+    assert lib.lsa_tier_sizes(big.ref, L.Tier([80]).ref, None, None, None) == B.LSA_ERR_UNSUPPORTED
+    ok = L.Problem([64 * 131072], 64, [40], 8, 2)
+    assert lib.lsa_tier_sizes(ok.ref, L.Tier([80]).ref, None, None, None) == 0
+
+
+def test_tier_entry_points_reject_bad_buffers_without_launching():
+    p = L.Problem([64 * 300, 64 * 1000], 64, [40, 100], 8, 2)
+    T = L.Tier([80, 200])
+    _, _, ws = L.lsa_tier_sizes(p, T)
+    lib = L.LIB
+    F2 = FAKE + 4096
+    assert lib.lsa_tier_reset(p.ref, T.ref, None, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_plan(p.ref, T.ref, None, FAKE, None, None, FAKE, F2, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_plan(p.ref, T.ref, FAKE, FAKE, FAKE, None, FAKE, F2, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_plan(p.ref, T.ref, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, FAKE, None) \
+        == B.LSA_ERR_INVALID_ARG  # slot_idx aliases kept_idx
+    assert lib.lsa_tier_plan(p.ref, T.ref, FAKE + 1, FAKE, None, None, FAKE, F2, FAKE, FAKE, None) \
+        == B.LSA_ERR_INVALID_ARG  # misaligned
+    assert lib.lsa_tier_fetch(p.ref, T.ref, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_fetch(p.ref, T.ref, FAKE, FAKE, FAKE, FAKE, None, FAKE, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_attend(p.ref, T.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, FAKE, ws - 1, None) \
+        == B.LSA_ERR_WORKSPACE
+    assert lib.lsa_tier_attend(p.ref, T.ref, FAKE, FAKE, FAKE, FAKE, FAKE, float("nan"), FAKE, None, FAKE, ws,
+                               None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_attend(p.ref, T.ref, FAKE, None, FAKE, FAKE, FAKE, 0.0, FAKE, None, FAKE, ws, None) \
+        == B.LSA_ERR_INVALID_ARG

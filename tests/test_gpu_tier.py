@@ -1,0 +1,322 @@
+"""The host tier on the GPU, through the C ABI: residency plan, copies from a
+pinned host mirror into the GPU reserve, and attention over the reserve.
+
+- The plan (slot of every kept chunk, copy list, slot owners) equals the
+  oracle's plan exactly, firing after firing, from a cold reserve on.
+- After the copies every kept chunk's reserve blocks equal its mirror blocks
+  byte for byte, and slots that received no copy are untouched.
+- Attention over the reserve equals the attention over the full cache for the
+  same kept chunks bit for bit, and the oracle's attention within tolerance.
+- Asynchronous recall: the plan and copies of firing t run on a second stream
+  while decode reads the previous kept set on the first; every decode output
+  equals the full-cache attention over the set it read.
+- The attention over the reserve replays from a captured graph with new slot
+  lists between replays, each replay equal to the eager call.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import lsa_synth as synth
+import oracle
+import parity
+from gpu_case import log
+
+pytestmark = pytest.mark.gpu
+
+
+def _kept_sets(n, keep, firings, rng):
+    """Ascending kept sets of one sequence for consecutive firings: a cold set,
+    the same set again, small and large churn, a smaller set, an empty one and
+    a full one."""
+    def pick(k, base=None, churn=1.0):
+        if base is None or len(base) == 0:
+            return np.sort(rng.choice(n, size=k, replace=False))
+        keep_n = min(len(base), int(round(k * (1.0 - churn))))
+        kept = rng.choice(base, size=keep_n, replace=False) if keep_n else np.zeros(0, np.int64)
+        rest = np.setdiff1d(np.arange(n), kept)
+        new = rng.choice(rest, size=k - keep_n, replace=False)
+        return np.sort(np.concatenate([kept, new]))
+    out = [pick(keep)]
+    patterns = [(keep, 0.0), (keep, 0.1), (keep, 1.0), (max(keep // 2, 1), 0.3), (0, 1.0), (keep, 0.5)]
+    for i in range(firings - 1):
+        k, churn = patterns[i % len(patterns)]
+        out.append(pick(k, out[-1], churn) if k else np.zeros(0, np.int64))
+    return out
+
+
+class TierCase:
+    """Device state of one host-tier problem: pinned mirror, reserve, owner table."""
+
+    def __init__(self, prob, seed, slots):
+        import torch
+        import paper_2606_09079_amd as L
+        self.prob, self.seed = prob, seed
+        self.dev = synth.device_inputs(prob, seed)
+        self.host_k = torch.empty(self.dev["k"].shape, dtype=torch.int16, pin_memory=True)
+        self.host_v = torch.empty(self.dev["v"].shape, dtype=torch.int16, pin_memory=True)
+        self.host_k.copy_(self.dev["k"])
+        self.host_v.copy_(self.dev["v"])
+        self.P, self.T = L.Problem.from_synth(prob), L.Tier(slots)
+        self.pitch, self.total, self.ws_bytes = L.lsa_tier_sizes(self.P, self.T)
+        self.slots = list(slots)
+        self.slot_off = np.concatenate([[0], np.cumsum(slots)]).astype(np.int64)
+        blk = prob.n_kv_heads * prob.chunk * prob.head_dim
+        self.res_k = torch.full((self.total * blk,), 0x5A5A, dtype=torch.int16, device="cuda")
+        self.res_v = torch.full((self.total * blk,), 0x3C3C, dtype=torch.int16, device="cuda")
+        self.owner = torch.empty(self.total, dtype=torch.int32, device="cuda")
+        L.lsa_tier_reset(self.P, self.T, self.owner)
+        self.ws = torch.zeros(max(self.ws_bytes, 256), dtype=torch.uint8, device="cuda")
+        B = prob.batch
+        self.fetch = torch.full((B, self.pitch, 2), -7, dtype=torch.int32, device="cuda")
+        self.fetch_count = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+
+    def kept_tensors(self, sets):
+        import torch
+        B = self.prob.batch
+        kept = np.full((B, self.pitch), -1, dtype=np.int32)
+        cnt = np.zeros(B, dtype=np.int32)
+        for b, s in enumerate(sets):
+            kept[b, :len(s)] = s
+            cnt[b] = len(s)
+        return torch.from_numpy(kept).cuda(), torch.from_numpy(cnt).cuda()
+
+    def blocks(self, t, ids):
+        """[len(ids)][Hkv][C * 128] blocks of a chunk-paged buffer at global ids."""
+        import torch
+        v = t.view(-1, self.prob.n_kv_heads, self.prob.chunk * self.prob.head_dim)
+        return v[torch.as_tensor(np.asarray(ids, dtype=np.int64), device=t.device)]
+
+
+def _plan_and_check(tc, L, sets, prev, oracle_state, stream=None):
+    """One firing: plan on the GPU, compare with the oracle, return the slot list tensor."""
+    import torch
+    prob = tc.prob
+    kept, cnt = tc.kept_tensors(sets)
+    slot_idx = torch.full((prob.batch, tc.pitch), -9, dtype=torch.int32, device="cuda")
+    prev_slots, prev_cnt = prev if prev is not None else (None, None)
+    L.lsa_tier_plan(tc.P, tc.T, kept, cnt, prev_slots, prev_cnt, tc.owner, slot_idx, tc.fetch, tc.fetch_count,
+                    stream)
+    torch.cuda.synchronize()
+    g_owner, g_slots = tc.owner.cpu().numpy(), slot_idx.cpu().numpy()
+    g_fetch, g_fc = tc.fetch.cpu().numpy(), tc.fetch_count.cpu().numpy()
+    copies = []
+    for b, s in enumerate(sets):
+        o_owner, o_old = oracle_state[b]
+        new_owner, new_slots, fetch = oracle.tier_plan(o_owner, o_old, [int(c) for c in s])
+        lo, hi = tc.slot_off[b], tc.slot_off[b + 1]
+        assert g_owner[lo:hi].tolist() == new_owner, f"seq {b}: owner table differs from the oracle"
+        assert g_slots[b, :len(s)].tolist() == new_slots, f"seq {b}: slots differ from the oracle"
+        assert int(g_fc[b]) == len(fetch), f"seq {b}: {g_fc[b]} copies, oracle {len(fetch)}"
+        assert [tuple(x) for x in g_fetch[b, :len(fetch)].tolist()] == fetch, f"seq {b}: copy list differs"
+        oracle_state[b] = (new_owner, new_slots)
+        copies.append(fetch)
+    return kept, cnt, slot_idx, copies
+
+
+def _check_reserve(tc, sets, slot_lists):
+    """Every kept chunk's reserve blocks equal its mirror blocks."""
+    for b, s in enumerate(sets):
+        if len(s) == 0:
+            continue
+        glob_c = np.asarray(s, dtype=np.int64) + tc.prob.chunk_offsets[b]
+        glob_s = np.asarray(slot_lists[b], dtype=np.int64) + tc.slot_off[b]
+        for which, res in (("k", tc.res_k), ("v", tc.res_v)):
+            got = tc.blocks(res, glob_s)
+            want = tc.blocks(tc.dev[which], glob_c)
+            assert bool((got == want).all()), f"seq {b}: reserve {which} blocks differ from the mirror"
+
+
+def _direct_attention(tc, L, kept, cnt):
+    import torch
+    prob = tc.prob
+    P = L.Problem.from_synth(prob)
+    ws_bytes = L.lsa_workspace_size(P)
+    ws = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    shp = (prob.batch, prob.n_qtok, prob.n_q_heads, prob.head_dim)
+    out = torch.empty(shp, dtype=torch.float32, device="cuda")
+    lse = torch.empty(shp[:3], dtype=torch.float32, device="cuda")
+    L.lsa_sparse_decode_attn(P, tc.dev["q"], tc.dev["k"], tc.dev["v"], kept, cnt, 0.0, out, lse, ws, ws_bytes)
+    return out, lse
+
+
+def _tier_attention(tc, L, slot_idx, cnt, stream=None):
+    import torch
+    prob = tc.prob
+    shp = (prob.batch, prob.n_qtok, prob.n_q_heads, prob.head_dim)
+    out = torch.full(shp, float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.full(shp[:3], float("nan"), dtype=torch.float32, device="cuda")
+    L.lsa_tier_attend(tc.P, tc.T, tc.dev["q"], tc.res_k, tc.res_v, slot_idx, cnt, 0.0, out, lse, tc.ws, tc.ws_bytes,
+                      stream)
+    return out, lse
+
+
+def _oracle_rows(tc, b, kept, out, lse, rows):
+    prob, host = tc.prob, tc.dev["host"]
+    toks = oracle.kept_tokens(kept, prob.chunk, prob.ctx_tokens[b])
+    by_g = {}
+    for (t, h) in rows:
+        by_g.setdefault(h // prob.group, []).append((t, h))
+    for g, rs in sorted(by_g.items()):
+        Kh = synth.kv_head_sparse(prob, tc.seed, "k", b, g, kept)
+        Vh = synth.kv_head_sparse(prob, tc.seed, "v", b, g, kept)
+        qr = np.stack([host["q"][b, t, h] for (t, h) in rs])
+        r_out, r_lse = oracle.attention_tokens(qr, Kh, Vh, toks)
+        parity.check_attention(np.stack([out[b, t, h] for (t, h) in rs]), [lse[b, t, h] for (t, h) in rs], r_out,
+                               r_lse, f"tier seq {b} g {g}")
+
+
+CASES = [
+    ("ragged3", [64 * 300, 64 * 1000, 64 * 77], 64, [40, 100, 77], [80, 250, 154], 8, 2),
+    ("c128_one", [128 * 500], 128, [60], [121], 16, 4),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: c[0])
+def test_tier_firings_match_oracle(case):
+    import torch
+    import paper_2606_09079_amd as L
+    name, ctx, C, keep, slots, hq, hkv = case
+    prob = synth.Problem(f"tier_{name}", ctx, C, keep, hq, hkv)
+    log(f"[tier] {name} ctx={ctx} C={C} keep={keep} slots={slots}")
+    tc = TierCase(prob, 11, slots)
+    rng = np.random.default_rng(5)
+    per_seq = [_kept_sets(prob.n_chunks[b], keep[b], 7, rng) for b in range(prob.batch)]
+    state = [([-1] * slots[b], []) for b in range(prob.batch)]
+    prev = None
+    for f in range(7):
+        sets = [per_seq[b][f] for b in range(prob.batch)]
+        kept, cnt, slot_idx, copies = _plan_and_check(tc, L, sets, prev, state)
+        L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+        torch.cuda.synchronize()
+        if f == 0:  # cold start: every kept chunk is copied; untouched slots keep their fill
+            for b in range(prob.batch):
+                assert len(copies[b]) == len(sets[b])
+                unused = np.setdiff1d(np.arange(slots[b]), [s for _, s in copies[b]]) + tc.slot_off[b]
+                if len(unused):
+                    assert bool((tc.blocks(tc.res_k, unused) == 0x5A5A).all())
+        _check_reserve(tc, sets, [state[b][1] for b in range(prob.batch)])
+        t_out, t_lse = _tier_attention(tc, L, slot_idx, cnt)
+        d_out, d_lse = _direct_attention(tc, L, kept, cnt)
+        torch.cuda.synchronize()
+        assert torch.equal(t_out, d_out) and torch.equal(t_lse, d_lse), \
+            f"firing {f}: reserve attention differs from the full-cache attention"
+        if f in (0, 2):
+            rows = [(0, h) for h in range(0, prob.n_q_heads, max(prob.group // 2, 1))]
+            o, s = t_out.cpu().numpy(), t_lse.cpu().numpy()
+            for b in range(prob.batch):
+                if len(sets[b]):
+                    _oracle_rows(tc, b, sets[b], o, s, rows)
+        prev = (slot_idx, cnt)
+        log(f"[tier] firing {f}: kept {[len(s) for s in sets]}, copies {[len(c) for c in copies]}")
+
+
+def test_tier_async_recall_two_streams():
+    """Firing t plans and copies on a side stream while decode reads the set of
+    firing t - 1 on the main stream; decode t + 1 reads the new set."""
+    import torch
+    import paper_2606_09079_amd as L
+    prob = synth.Problem("tier_async", [64 * 2000, 64 * 600], 64, [200, 60], 8, 2)
+    slots = [400, 130]
+    tc = TierCase(prob, 12, slots)
+    rng = np.random.default_rng(9)
+    F = 8
+    per_seq = [_kept_sets(prob.n_chunks[b], prob.keep[b], F, rng) for b in range(prob.batch)]
+    firings = [tc.kept_tensors([per_seq[b][f] for b in range(prob.batch)]) for f in range(F)]
+    slot_buf = [torch.full((prob.batch, tc.pitch), -1, dtype=torch.int32, device="cuda") for _ in range(2)]
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    L.lsa_tier_plan(tc.P, tc.T, firings[0][0], firings[0][1], None, None, tc.owner, slot_buf[0], tc.fetch,
+                    tc.fetch_count)
+    L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+    outs = []
+    for t in range(1, F):
+        cur, nxt = (t - 1) % 2, t % 2
+        side.wait_stream(main)  # decode t - 1 has finished reading slot_buf[nxt]
+        L.lsa_tier_plan(tc.P, tc.T, firings[t][0], firings[t][1], slot_buf[cur], firings[t - 1][1], tc.owner,
+                        slot_buf[nxt], tc.fetch, tc.fetch_count, side)
+        L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v, side)
+        outs.append(_tier_attention(tc, L, slot_buf[cur], firings[t - 1][1], main))
+        main.wait_stream(side)
+    outs.append(_tier_attention(tc, L, slot_buf[(F - 1) % 2], firings[F - 1][1], main))
+    torch.cuda.synchronize()
+    for t in range(F):
+        d_out, d_lse = _direct_attention(tc, L, *firings[t])
+        torch.cuda.synchronize()
+        assert torch.equal(outs[t][0], d_out) and torch.equal(outs[t][1], d_lse), \
+            f"decode over the set of firing {t} differs from the full-cache attention"
+    log(f"[tier] async: {F} firings, kept {[int(x) for x in firings[-1][1].cpu()]}")
+
+
+def test_tier_attention_graph_replay():
+    """The attention over the reserve captured once, replayed with new slot lists."""
+    import torch
+    import paper_2606_09079_amd as L
+    prob = synth.Problem("tier_graph", [64 * 900], 64, [90], 32, 8)
+    tc = TierCase(prob, 13, [180])
+    rng = np.random.default_rng(4)
+    sets = _kept_sets(prob.n_chunks[0], 90, 5, rng)
+    state = [([-1] * 180, [])]
+    slot_g = torch.full((1, tc.pitch), 0, dtype=torch.int32, device="cuda")
+    cnt_g = torch.zeros(1, dtype=torch.int32, device="cuda")
+    shp = (1, 1, prob.n_q_heads, prob.head_dim)
+    out_g = torch.empty(shp, dtype=torch.float32, device="cuda")
+    lse_g = torch.empty(shp[:3], dtype=torch.float32, device="cuda")
+
+    def attend():
+        L.lsa_tier_attend(tc.P, tc.T, tc.dev["q"], tc.res_k, tc.res_v, slot_g, cnt_g, 0.0, out_g, lse_g, tc.ws,
+                          tc.ws_bytes)
+
+    prev = None
+    kept, cnt, slot_idx, _ = _plan_and_check(tc, L, [sets[0]], prev, state)
+    L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+    slot_g.copy_(slot_idx)
+    cnt_g.copy_(cnt)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        attend()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        attend()
+    torch.cuda.synchronize()
+    prev = (slot_idx, cnt)
+    for f in range(1, 5):
+        kept, cnt, slot_idx, _ = _plan_and_check(tc, L, [sets[f]], prev, state)
+        L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+        slot_g.copy_(slot_idx)
+        cnt_g.copy_(cnt)
+        for rep in range(2):
+            out_g.fill_(float("nan"))
+            g.replay()
+            torch.cuda.synchronize()
+            e_out, e_lse = _tier_attention(tc, L, slot_idx, cnt)
+            torch.cuda.synchronize()
+            assert torch.equal(out_g, e_out) and torch.equal(lse_g, e_lse), f"firing {f} replay {rep} differs"
+        prev = (slot_idx, cnt)
+    log("[tier] graph replays match the eager calls")
+
+
+def test_tier_fetch_rejects_pageable_mirror():
+    """A mirror in ordinary (pageable) host memory is refused before any launch."""
+    import torch
+    import paper_2606_09079_amd as L
+    prob = synth.Problem("tier_pageable", [64 * 40], 64, [8], 8, 2)
+    P, T = L.Problem.from_synth(prob), L.Tier([16])
+    pitch, total, _ = L.lsa_tier_sizes(P, T)
+    n = prob.kv_elems()
+    pageable = np.zeros(n + 8, dtype=np.int16)
+    base = pageable.ctypes.data
+    aligned = base + (-base % 16)
+    fetch = torch.zeros((1, pitch, 2), dtype=torch.int32, device="cuda")
+    fc = torch.zeros(1, dtype=torch.int32, device="cuda")
+    res = torch.zeros(total * 2 * 64 * 128, dtype=torch.int16, device="cuda")
+    with pytest.raises(L.LsaError) as e:
+        L.lsa_tier_fetch(P, T, aligned, aligned, fetch, fc, res, res)
+    assert e.value.status == 1
+    pinned = torch.empty(n, dtype=torch.int16, pin_memory=True)
+    L.lsa_tier_fetch(P, T, pinned, pinned, fetch, fc, res, res)  # no copies (count 0), accepted
+    torch.cuda.synchronize()
