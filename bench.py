@@ -57,6 +57,10 @@ WORKLOADS = {
                   "Memory Indexer of 3 layers x 64 heads x 128 over the history, K_max 2,048; Level 2: native "
                   "indexer of 64 heads keeps 1,024; plus the window of the last 8,192 tokens; 32 query / 8 KV heads, "
                   "head_dim 128, bf16 K/V, batch 1",
+    "tier1m": "tier1m: the recall1m context and Memory Indexer with the host tier: K/V in a pinned host mirror, a "
+              "GPU reserve of 2 x K_max chunk slots; every 64 decode steps the indexer fires (recall, residency plan, "
+              "copies of the missing chunks) on a second stream, the new set is read 16 steps later; each "
+              "decode step attends over the reserve",
     "twolevel_tiny": "twolevel_tiny: 4,133 tokens (65 chunks, the last one 37 tokens), Level 1 3 x 16 x 64 with "
                      "K_max 24, Level 2 keeps 6, window 512 tokens, 8 query / 8 KV heads, head_dim 128, bf16 K/V",
 }
@@ -110,6 +114,8 @@ def main() -> int:
                     help="untimed streaming read between the per-step samples of the step-time distribution, "
                          "so that the 256 MB Infinity Cache cannot serve a previous step's bytes "
                          "(a multiple of 32; default: 1024 for workloads below 1 GB per step, else 0)")
+    ap.add_argument("--tier-lag", type=int, default=16,
+                    help="tier1m: decode steps from a firing until its kept set is read (1 .. 63)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="profiling aid: also run one plain copy of this many MiB (known bytes)")
     args = ap.parse_args()
@@ -126,6 +132,8 @@ def main() -> int:
     import paper_2606_09079_amd as L
 
     torch.cuda.set_device(0)
+    if args.workload == "tier1m":
+        return bench_tier(args)
     stream = torch.cuda.current_stream()
     prob = synth.make_problem(args.workload, 0)
     t_setup = time.time()
@@ -320,6 +328,233 @@ def main() -> int:
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(prob, host0, args.cpu_seconds)
 
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+TIER_TAU = 64        # decode steps between firings of the indexer
+TIER_RHO = 0.99      # correlation of the indexer queries of consecutive firings
+
+
+def bench_tier(args) -> int:
+    """Decode over the host tier at 1M context (see the tier1m workload line).
+
+    Firings: the indexer queries of firing f are bf16(sqrt(rho) q_{f-1} +
+    sqrt(1 - rho) g_f) with fresh N(0, 1) draws g_f and the gates of firing 0,
+    so that consecutive kept sets overlap as a slowly moving decode state would
+    (about 11% of the set changes per firing at rho = 0.99).  A step is one
+    decode step: the attention over the reserve, plus 1/64 of a firing (index
+    scores of 3 layers over the full history, recall selection, residency plan
+    and the copies of the missing chunks over PCIe) run on a second stream."""
+    import numpy as np
+    import torch
+
+    import lsa_synth as synth
+    import paper_2606_09079_amd as L
+
+    if not 1 <= args.tier_lag < TIER_TAU:
+        raise SystemExit(f"--tier-lag must be in 1 .. {TIER_TAU - 1}")
+    if args.warmup % TIER_TAU:
+        args.warmup += TIER_TAU - args.warmup % TIER_TAU  # the timed region starts at a firing
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()  # default priority
+    prob = synth.make_problem("recall1m", 0)
+    t_setup = time.time()
+    host0 = synth.host_inputs(prob, 0)
+    dev = synth.device_inputs(prob, 0, host=host0)
+    host_k = torch.empty(dev["k"].shape, dtype=torch.int16, pin_memory=True)
+    host_v = torch.empty(dev["v"].shape, dtype=torch.int16, pin_memory=True)
+    host_k.copy_(dev["k"])
+    host_v.copy_(dev["v"])
+    cache_bytes = 2 * dev["k"].numel() * 2
+    del dev["k"], dev["v"]  # from here on the GPU holds the reserve only
+    torch.cuda.empty_cache()
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).cuda()
+
+    n_fire = 2 * ((args.warmup + args.steps) // TIER_TAU + 1) + 2
+    rng = np.random.default_rng(2024)
+    qf = synth.bf16_bits_to_f64(host0["idx_q"])
+    idx_q = []
+    for f in range(n_fire):
+        if f > 0:
+            qf = math.sqrt(TIER_RHO) * qf + math.sqrt(1.0 - TIER_RHO) * rng.standard_normal(qf.shape)
+        idx_q.append(up(synth.f64_to_bf16_bits(qf)))
+    fresh_q = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))  # an unrelated query: a full change
+    qs = [dev["q"]] + [up(synth.host_inputs(prob, 1000 + r)["q"]) for r in range(1, 4)]
+
+    B, K, C, Hkv, d = prob.batch, prob.keep[0], prob.chunk, prob.n_kv_heads, prob.head_dim
+    P, ix, T = L.Problem.from_synth(prob), L.Indexer.from_synth(prob), L.Tier([2 * K] * B)
+    pitch, total, ws_bytes = L.lsa_tier_sizes(P, T)
+    slot_bytes = Hkv * C * d * 2
+    res_k = torch.empty(total * slot_bytes // 2, dtype=torch.int16, device="cuda")
+    res_v = torch.empty_like(res_k)
+    owner = torch.empty(total, dtype=torch.int32, device="cuda")
+    L.lsa_tier_reset(P, T, owner)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    scores = torch.empty(prob.idx_layers * prob.total_chunks, dtype=torch.float32, device="cuda")
+    kept = [torch.empty(B, pitch, dtype=torch.int32, device="cuda") for _ in range(2)]
+    cnt = [torch.zeros(B, dtype=torch.int32, device="cuda") for _ in range(2)]
+    slots = [torch.empty(B, pitch, dtype=torch.int32, device="cuda") for _ in range(2)]
+    fetch = torch.empty(B, pitch, 2, dtype=torch.int32, device="cuda")
+    fcount = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = torch.empty(B, 1, prob.n_q_heads, d, dtype=torch.float32, device="cuda")
+    lse = torch.empty(B, 1, prob.n_q_heads, dtype=torch.float32, device="cuda")
+    copies = []
+
+    def select_and_plan(q_idx, prev, new, s):
+        L.lsa_recall_scores(P, ix, q_idx, dev["idx_w"], dev["idx_k"], scores, s)
+        L.lsa_recall_select(P, ix, scores, kept[new], cnt[new], s)
+        L.lsa_tier_plan(P, T, kept[new], cnt[new], slots[prev] if prev is not None else None,
+                        cnt[prev] if prev is not None else None, owner, slots[new], fetch, fcount, s)
+
+    def fire(q_idx, prev, new, s):
+        select_and_plan(q_idx, prev, new, s)
+        L.lsa_tier_fetch(P, T, host_k, host_v, fetch, fcount, res_k, res_v, s)
+
+    def decode(buf, i, s):
+        L.lsa_tier_attend(P, T, qs[i % len(qs)], res_k, res_v, slots[buf], cnt[buf], 0.0, out, lse, ws, ws_bytes, s)
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    # ---- cold start: everything kept is copied in
+    e = [ev() for _ in range(3)]
+    e[0].record(main)
+    select_and_plan(idx_q[0], None, 0, main)
+    e[1].record(main)
+    L.lsa_tier_fetch(P, T, host_k, host_v, fetch, fcount, res_k, res_v, main)
+    e[2].record(main)
+    torch.cuda.synchronize()
+    cold_n = int(fcount.cpu()[0])
+    cold_ms = e[1].elapsed_time(e[2])
+    log(f"[tier] setup {time.time() - t_setup:.1f}s; cold fetch of {cold_n} chunks in {cold_ms:.2f} ms "
+        f"({cold_n * 2 * slot_bytes / (cold_ms * 1e-3) / 1e9:.1f} GB/s); select+plan {e[0].elapsed_time(e[1]):.3f} ms")
+
+    # ---- decode alone (HIP events per launch on the launch stream)
+    n_dec = 50
+    for i in range(20):
+        decode(0, i, main)
+    de = [(ev(), ev()) for _ in range(n_dec)]
+    for i in range(n_dec):
+        de[i][0].record(main)
+        decode(0, i, main)
+        de[i][1].record(main)
+    torch.cuda.synchronize()
+    dec_us = 1e3 * sum(a.elapsed_time(b) for a, b in de) / n_dec
+
+    # ---- a full change of the kept set, copied on the side stream while decode
+    # goes on over the old set
+    fe = [ev(), ev()]
+    side.wait_stream(main)
+    fe[0].record(side)
+    fire(fresh_q, 0, 1, side)
+    fe[1].record(side)
+    dd = [(ev(), ev()) for _ in range(n_dec)]
+    for i in range(n_dec):
+        dd[i][0].record(main)
+        decode(0, i, main)
+        dd[i][1].record(main)
+    torch.cuda.synchronize()
+    full_n = int(fcount.cpu()[0])
+    full_ms = fe[0].elapsed_time(fe[1])
+    during = [1e3 * a.elapsed_time(b) for a, b in dd if fe[0].elapsed_time(b) <= full_ms]
+    dec_during_us = sum(during) / len(during) if during else None
+    log(f"[tier] full change: {full_n} copies in {full_ms:.2f} ms on the side stream; decode {dec_us:.1f} us alone, "
+        f"{dec_during_us} us during the copies ({len(during)} steps)")
+    # back to the firing-0 set as the starting point of the steady state
+    side.wait_stream(main)
+    fire(idx_q[0], 1, 0, side)
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+
+    # ---- steady state: a firing every TIER_TAU steps on the side stream; steps
+    # t .. t + lag - 1 read the previous set, steps from t + lag on the new one
+    state = {"cur": 0, "f": 1}
+
+    def steady(lag):
+        cur, f = state["cur"], state["f"]
+        fire_ev, copies, new = [], [], None
+        e0, e1 = ev(), ev()
+        t0 = 0.0
+        for i in range(args.warmup + args.steps):
+            if i == args.warmup:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                e0.record(main)
+            if i % TIER_TAU == 0:
+                new = 1 - cur
+                side.wait_stream(main)
+                a_, b_ = ev(), ev()
+                a_.record(side)
+                fire(idx_q[f], cur, new, side)
+                b_.record(side)
+                fire_ev.append((a_, b_, i >= args.warmup))
+                f += 1
+            if i % TIER_TAU == lag:
+                main.wait_stream(side)
+                cur = new
+                copies.append(fcount.clone())
+            decode(cur, i, main)
+        main.wait_stream(side)
+        e1.record(main)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        state["cur"], state["f"] = (new if new is not None else cur), f
+        ms = e0.elapsed_time(e1) / args.steps
+        fire_ms = [a.elapsed_time(b) for a, b, timed in fire_ev if timed]
+        n_copies = [int(c.cpu()[0]) for c in copies]
+        log(f"[tier] lag {lag}: {args.steps} steps, {ms * 1e3:.2f} us/step (wall {wall:.3f}s); firings "
+            f"{[round(x, 3) for x in fire_ms]} ms; copies {n_copies}")
+        return ms, fire_ms, n_copies[-len(fire_ms):] if fire_ms else []
+
+    ms_lag1, fire_lag1, _ = steady(1)
+    ms_per_step, fire_ms, n_copies = steady(args.tier_lag)
+    cur = state["cur"]
+
+    kept_n = int(cnt[cur].cpu()[0])
+    attn_bytes = kept_n * 2 * slot_bytes + B * prob.n_q_heads * d * (2 + 4) + B * prob.n_q_heads * 4 + kept_n * 4
+    achieved = attn_bytes / (dec_us * 1e-6) / 1e9
+    reserve_bytes = 2 * total * slot_bytes
+    result = {
+        "metric": METRIC,
+        "value": round(1e3 / ms_per_step, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS["tier1m"], "global_batch": B, "seq_len": prob.ctx_tokens[0],
+                   "parallelism": "single GPU", "tau": TIER_TAU, "query_correlation_per_firing": TIER_RHO,
+                   "k_max": K, "reserve_slots": total},
+        "tier": {
+            "cache_bytes": cache_bytes, "reserve_bytes": reserve_bytes,
+            "cold_fetch": {"chunks": cold_n, "ms": round(cold_ms, 3),
+                           "pcie_gbs": round(cold_n * 2 * slot_bytes / (cold_ms * 1e-3) / 1e9, 2)},
+            "decode_us_alone": round(dec_us, 2),
+            "full_change": {"copies": full_n, "ms": round(full_ms, 3),
+                            "decode_us_during_copies": round(dec_during_us, 2) if dec_during_us else None,
+                            "decode_steps_during_copies": len(during)},
+            "steady_state": {"lag_steps": args.tier_lag, "firings_timed": len(fire_ms),
+                             "firing_ms": round(sum(fire_ms) / len(fire_ms), 3) if fire_ms else None,
+                             "copies_per_firing": n_copies, "kept_chunks": kept_n,
+                             "us_per_step_lag1": round(ms_lag1 * 1e3, 2),
+                             "firing_ms_lag1": round(sum(fire_lag1) / len(fire_lag1), 3) if fire_lag1 else None},
+        },
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "attn_kernel (lsa_tier_attend)", "avg_launch_us": round(dec_us, 2),
+                     "algorithmic_bytes_per_launch": int(attn_bytes)},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(prob, host0, args.cpu_seconds)
     print(json.dumps(result), flush=True)
     return 0
 

@@ -332,6 +332,22 @@ lsa_status lsa_tier_fetch(const lsa_problem* p, const lsa_tier* tr, const uint16
                           const uint16_t* host_v, const int32_t* fetch, const int32_t* fetch_count,
                           uint16_t* res_k, uint16_t* res_v, void* stream);
 /*
+ * The copies of lsa_tier_fetch made by the GPU's DMA engines and issued from
+ * the host: h_fetch [B][pitch][2] and h_fetch_count [B] are HOST copies of a
+ * plan's copy list (the caller brings them over once the plan has run, in a
+ * side band off the decode path).  One asynchronous host-to-device copy per
+ * chunk and K/V (per chunk and KV head plane for a mirror whose heads of a
+ * chunk are not adjacent), copies of adjacent chunks into adjacent slots
+ * merged.  The DMA engines take no compute units, so a decode running at the
+ * same time is hardly slowed, but they move fewer bytes per second than
+ * lsa_tier_fetch.  Every entry is validated before the first copy is issued
+ * (chunk < n_b, slot < slots[b], 0 <= count <= pitch); a copy that fails to
+ * issue returns LSA_ERR_HIP with the earlier copies already queued.
+ */
+lsa_status lsa_tier_fetch_dma(const lsa_problem* p, const lsa_tier* tr, const uint16_t* host_k,
+                              const uint16_t* host_v, const int32_t* h_fetch, const int32_t* h_fetch_count,
+                              uint16_t* res_k, uint16_t* res_v, void* stream);
+/*
  * Step 3 over the reserve: the attention of lsa_sparse_decode_attn for the
  * chunks held in slots slot_idx[b][0 .. slot_count[b]) (the remapped kept
  * set), reading res_k / res_v only.  The kept chunks in the same order give

@@ -385,6 +385,29 @@ lsa_status make_tier_plan(const lsa_problem* p, const lsa_tier* tr, TierPlan* tp
   return LSA_OK;
 }
 
+// Device-visible addresses of the pinned host mirror; fails unless both ends
+// of each mirror lie in one pinned allocation mapped for the device.
+lsa_status mirror_device_ptrs(const lsa_problem* p, const Plan& P, const uint16_t* host_k, const uint16_t* host_v,
+                              const uint16_t* dev[2]) {
+  // last element of the mirror: the final block of the last chunk and head
+  const int64_t last = (P.total_chunks - 1) * P.chunk_stride + (int64_t)(p->n_kv_heads - 1) * P.head_stride +
+                       (int64_t)p->chunk_size * kHeadDim - 1;
+  const uint16_t* host[2] = {host_k, host_v};
+  for (int i = 0; i < 2; ++i) {
+    void* d0 = nullptr;
+    void* d1 = nullptr;
+    if (hipHostGetDevicePointer(&d0, const_cast<uint16_t*>(host[i]), 0) != hipSuccess || d0 == nullptr ||
+        hipHostGetDevicePointer(&d1, const_cast<uint16_t*>(host[i] + last), 0) != hipSuccess ||
+        static_cast<uint16_t*>(d1) != static_cast<uint16_t*>(d0) + last) {
+      (void)hipGetLastError();  // clear the error the failed lookup recorded
+      return fail(LSA_ERR_INVALID_ARG, "%s is not pinned host memory mapped for the device over the whole mirror",
+                  i ? "host_v" : "host_k");
+    }
+    dev[i] = static_cast<const uint16_t*>(d0);
+  }
+  return LSA_OK;
+}
+
 }  // namespace
 }  // namespace lsa
 
@@ -754,24 +777,9 @@ lsa_status lsa_tier_fetch(const lsa_problem* p, const lsa_tier* tr, const uint16
   LSA_TRY(check_ptr(fetch_count, "fetch_count"));
   LSA_TRY(check_ptr(res_k, "res_k"));
   LSA_TRY(check_ptr(res_v, "res_v"));
-  const Plan& P = T.P;
-  // last element of the mirror: the final block of the last chunk and head
-  const int64_t last = (P.total_chunks - 1) * P.chunk_stride + (int64_t)(p->n_kv_heads - 1) * P.head_stride +
-                       (int64_t)p->chunk_size * kHeadDim - 1;
-  const uint16_t* host[2] = {host_k, host_v};
   const uint16_t* dev[2] = {nullptr, nullptr};
-  for (int i = 0; i < 2; ++i) {
-    void* d0 = nullptr;
-    void* d1 = nullptr;
-    if (hipHostGetDevicePointer(&d0, const_cast<uint16_t*>(host[i]), 0) != hipSuccess || d0 == nullptr ||
-        hipHostGetDevicePointer(&d1, const_cast<uint16_t*>(host[i] + last), 0) != hipSuccess ||
-        static_cast<uint16_t*>(d1) != static_cast<uint16_t*>(d0) + last) {
-      (void)hipGetLastError();  // clear the error the failed lookup recorded
-      return fail(LSA_ERR_INVALID_ARG, "%s is not pinned host memory mapped for the device over the whole mirror",
-                  i ? "host_v" : "host_k");
-    }
-    dev[i] = static_cast<const uint16_t*>(d0);
-  }
+  LSA_TRY(mirror_device_ptrs(p, T.P, host_k, host_v, dev));
+  const Plan& P = T.P;
   TierFetchArgs a;
   a.host_k = dev[0];
   a.host_v = dev[1];
@@ -787,6 +795,58 @@ lsa_status lsa_tier_fetch(const lsa_problem* p, const lsa_tier* tr, const uint16
   for (int b = 0; b < p->batch; ++b) a.slots[b] = tr->slots[b];
   memcpy(a.slot_off, T.slot_off, sizeof a.slot_off);
   LSA_HIP(launch_tier_fetch(P.t, a, p->chunk_size, (hipStream_t)stream), "tier fetch launch");
+  return LSA_OK;
+}
+
+lsa_status lsa_tier_fetch_dma(const lsa_problem* p, const lsa_tier* tr, const uint16_t* host_k,
+                              const uint16_t* host_v, const int32_t* h_fetch, const int32_t* h_fetch_count,
+                              uint16_t* res_k, uint16_t* res_v, void* stream) {
+  TierPlan T;
+  LSA_TRY(make_tier_plan(p, tr, &T));
+  LSA_TRY(check_ptr(host_k, "host_k"));
+  LSA_TRY(check_ptr(host_v, "host_v"));
+  LSA_TRY(check_ptr(res_k, "res_k"));
+  LSA_TRY(check_ptr(res_v, "res_v"));
+  if (h_fetch == nullptr || h_fetch_count == nullptr)
+    return fail(LSA_ERR_INVALID_ARG, "h_fetch and h_fetch_count must be host arrays");
+  const Plan& P = T.P;
+  const int32_t pitch = P.max_sel;
+  for (int b = 0; b < p->batch; ++b) {
+    const int32_t nf = h_fetch_count[b];
+    if (nf < 0 || nf > pitch)
+      return fail(LSA_ERR_INVALID_ARG, "h_fetch_count[%d] = %d not in [0, %d]", b, nf, pitch);
+    for (int f = 0; f < nf; ++f) {
+      const int32_t c = h_fetch[((int64_t)b * pitch + f) * 2], s = h_fetch[((int64_t)b * pitch + f) * 2 + 1];
+      if (c < 0 || c >= P.t.n[b] || s < 0 || s >= tr->slots[b])
+        return fail(LSA_ERR_INVALID_ARG, "copy %d of sequence %d: chunk %d / slot %d out of range", f, b, c, s);
+    }
+  }
+  const uint16_t* dev[2] = {nullptr, nullptr};
+  LSA_TRY(mirror_device_ptrs(p, P, host_k, host_v, dev));
+  const hipStream_t st = (hipStream_t)stream;
+  const int64_t blk = (int64_t)p->chunk_size * kHeadDim;     // elements of one chunk-head block
+  const int64_t slot = (int64_t)p->n_kv_heads * blk;          // elements of one reserve slot
+  const bool packed = P.head_stride == blk && P.chunk_stride == slot;  // a chunk's heads adjacent in the mirror
+  for (int b = 0; b < p->batch; ++b) {
+    const int32_t* fl = h_fetch + (int64_t)b * pitch * 2;
+    for (int f = 0; f < h_fetch_count[b];) {
+      const int32_t c = fl[2 * f], s = fl[2 * f + 1];
+      int r = 1;  // adjacent chunks into adjacent slots
+      while (packed && f + r < h_fetch_count[b] && fl[2 * (f + r)] == c + r && fl[2 * (f + r) + 1] == s + r) ++r;
+      for (int kv = 0; kv < 2; ++kv) {
+        const uint16_t* src = (kv ? host_v : host_k) + (P.t.chunk_off[b] + c) * P.chunk_stride;
+        uint16_t* dst = (kv ? res_v : res_k) + ((int64_t)T.slot_off[b] + s) * slot;
+        if (packed) {
+          LSA_HIP(hipMemcpyAsync(dst, src, (size_t)r * slot * 2, hipMemcpyHostToDevice, st), "tier DMA copy");
+        } else {
+          LSA_HIP(hipMemcpy2DAsync(dst, (size_t)blk * 2, src, (size_t)P.head_stride * 2, (size_t)blk * 2,
+                                   (size_t)p->n_kv_heads, hipMemcpyHostToDevice, st),
+                  "tier DMA copy");
+        }
+      }
+      f += r;
+    }
+  }
   return LSA_OK;
 }
 

@@ -14,8 +14,8 @@
 //           plus a popcount) is its position in the ascending kept list
 //     mbit  kept chunks that no slot holds (the copies to make)
 //     pbit  protected slots (held by a kept chunk or read by the previous set)
-// tier_fetch_kernel -- one workgroup per (copy, KV head, K or V) moves one
-//   chunk-head block from the host mirror into its reserve slot.  The reads
+// tier_fetch_kernel -- a few workgroups per sequence move the chunk-head
+//   blocks of the copy list from the host mirror into their slots.  The reads
 //   cross PCIe: the mirror is pinned host memory mapped into the GPU's address
 //   space, so the copy list never has to go back to the host.
 #include "lsa_internal.h"
@@ -27,6 +27,7 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kChunkWords = kMaxTierChunks / 32;
 constexpr int kSlotWords = kMaxTierSlots / 32;
+constexpr int kFetchWorkgroups = 32;  // copy workgroups per launch (at least one per sequence)
 
 // Exclusive prefix sum over the workgroup (one value per thread); *total
 // receives the sum of all values.
@@ -163,32 +164,35 @@ tier_plan_kernel(SeqTable t, TierArgs a) {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// blockIdx.x = (f * Hkv + g) * 2 + kv for copy f of sequence blockIdx.y;
-// 256 threads move the C x 128 bf16 block of (chunk, head g) of K (kv = 0) or
-// V (kv = 1), 16 bytes per thread per round, every load of the block issued
-// before its stores.
+// Copy block j of sequence blockIdx.y is (copy f, KV head g, K or V) with j =
+// (f * Hkv + g) * 2 + kv; a few workgroups per sequence loop over the blocks,
+// so that a copy that overlaps decode leaves the compute units to the
+// attention (the PCIe link, not the number of workgroups, bounds the copy).
+// 256 threads move one C x 128 bf16 block, 16 bytes per thread per round,
+// every load of the block issued before its stores.
 template <int C>
 __global__ void __launch_bounds__(256)
 tier_fetch_kernel(SeqTable t, TierFetchArgs a) {
   constexpr int kRounds = C * kHeadDim * 2 / 16 / 256;
   const int b = blockIdx.y;
-  const int kv = blockIdx.x & 1;
-  const int g = (blockIdx.x >> 1) % a.n_kv_heads, f = (blockIdx.x >> 1) / a.n_kv_heads;
   const int nf = min(max(a.fetch_count[b], 0), a.pitch);
-  if (f >= nf) return;
-  const int32_t* fe = a.fetch + ((int64_t)b * a.pitch + f) * 2;
-  const int c = min(max(fe[0], 0), t.n[b] - 1);
-  const int s = min(max(fe[1], 0), a.slots[b] - 1);
-  const u32x4* src = reinterpret_cast<const u32x4*>((kv ? a.host_v : a.host_k) +
-                                                    (t.chunk_off[b] + c) * a.chunk_stride + g * a.head_stride);
-  u32x4* dst = reinterpret_cast<u32x4*>((kv ? a.res_v : a.res_k) +
-                                        ((int64_t)a.slot_off[b] + s) * a.res_slot_stride +
-                                        (int64_t)g * C * kHeadDim);
-  u32x4 v[kRounds];
+  const int n_blocks = nf * a.n_kv_heads * 2;
+  for (int j = blockIdx.x; j < n_blocks; j += gridDim.x) {
+    const int kv = j & 1, g = (j >> 1) % a.n_kv_heads, f = (j >> 1) / a.n_kv_heads;
+    const int32_t* fe = a.fetch + ((int64_t)b * a.pitch + f) * 2;
+    const int c = min(max(fe[0], 0), t.n[b] - 1);
+    const int s = min(max(fe[1], 0), a.slots[b] - 1);
+    const u32x4* src = reinterpret_cast<const u32x4*>((kv ? a.host_v : a.host_k) +
+                                                      (t.chunk_off[b] + c) * a.chunk_stride + g * a.head_stride);
+    u32x4* dst = reinterpret_cast<u32x4*>((kv ? a.res_v : a.res_k) +
+                                          ((int64_t)a.slot_off[b] + s) * a.res_slot_stride +
+                                          (int64_t)g * C * kHeadDim);
+    u32x4 v[kRounds];
 #pragma unroll
-  for (int j = 0; j < kRounds; ++j) v[j] = __builtin_nontemporal_load(src + j * 256 + threadIdx.x);
+    for (int r = 0; r < kRounds; ++r) v[r] = __builtin_nontemporal_load(src + r * 256 + threadIdx.x);
 #pragma unroll
-  for (int j = 0; j < kRounds; ++j) dst[j * 256 + threadIdx.x] = v[j];
+    for (int r = 0; r < kRounds; ++r) dst[r * 256 + threadIdx.x] = v[r];
+  }
 }
 
 __global__ void __launch_bounds__(256) tier_reset_kernel(int32_t* owner, int64_t n) {
@@ -203,9 +207,10 @@ hipError_t launch_tier_plan(const SeqTable& t, const TierArgs& a, hipStream_t s)
 }
 
 hipError_t launch_tier_fetch(const SeqTable& t, const TierFetchArgs& a, int32_t chunk_size, hipStream_t s) {
-  const int64_t gx = (int64_t)a.pitch * a.n_kv_heads * 2;
-  if (gx == 0) return hipSuccess;
-  const dim3 grid((unsigned)gx, (unsigned)t.batch);
+  const int64_t blocks = (int64_t)a.pitch * a.n_kv_heads * 2;
+  if (blocks == 0) return hipSuccess;
+  const int64_t per_seq = std::min<int64_t>(blocks, std::max(1, kFetchWorkgroups / t.batch));
+  const dim3 grid((unsigned)per_seq, (unsigned)t.batch);
   if (chunk_size == 64)
     hipLaunchKernelGGL(tier_fetch_kernel<64>, grid, dim3(256), 0, s, t, a);
   else

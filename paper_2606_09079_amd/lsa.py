@@ -32,7 +32,7 @@ EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_valida
            "lsa_max_keep", "lsa_workspace_size", "lsa_workspace_init", "lsa_score_chunks", "lsa_topk_chunks",
            "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
            "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step", "lsa_tier_sizes", "lsa_tier_reset",
-           "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_attend")
+           "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_fetch_dma", "lsa_tier_attend")
 
 
 class lsa_problem(ctypes.Structure):
@@ -100,6 +100,7 @@ def _load() -> ctypes.CDLL:
     lib.lsa_tier_reset.argtypes = [pp, rp, _P, _P]
     lib.lsa_tier_plan.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.lsa_tier_fetch.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P]
+    lib.lsa_tier_fetch_dma.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P]
     lib.lsa_tier_attend.argtypes = [pp, rp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
     for name in EXPORTS[3:]:
         getattr(lib, name).restype = ctypes.c_int
@@ -186,6 +187,17 @@ def _ptr(x) -> Optional[int]:
         return None
     if isinstance(x, int):
         return x
+    return x.data_ptr()
+
+
+def _host_ptr(x) -> Optional[int]:
+    """Address of a host buffer: a numpy array (C-contiguous), a CPU tensor or an integer."""
+    if x is None or isinstance(x, int):
+        return x
+    if hasattr(x, "ctypes"):
+        if not x.flags["C_CONTIGUOUS"]:
+            raise ValueError("host array must be C-contiguous")
+        return x.ctypes.data
     return x.data_ptr()
 
 
@@ -312,6 +324,14 @@ def lsa_tier_plan(p: Problem, tr: Tier, kept_idx, kept_count, prev_slots, prev_c
 def lsa_tier_fetch(p: Problem, tr: Tier, host_k, host_v, fetch, fetch_count, res_k, res_v, stream=None) -> None:
     _check(LIB.lsa_tier_fetch(p.ref, tr.ref, _ptr(host_k), _ptr(host_v), _ptr(fetch), _ptr(fetch_count),
                               _ptr(res_k), _ptr(res_v), _stream(stream)), "lsa_tier_fetch")
+
+
+def lsa_tier_fetch_dma(p: Problem, tr: Tier, host_k, host_v, h_fetch, h_fetch_count, res_k, res_v,
+                       stream=None) -> None:
+    """h_fetch / h_fetch_count: host int32 buffers (numpy arrays or CPU tensors) holding a plan's copy list."""
+    _check(LIB.lsa_tier_fetch_dma(p.ref, tr.ref, _ptr(host_k), _ptr(host_v), _host_ptr(h_fetch),
+                                  _host_ptr(h_fetch_count), _ptr(res_k), _ptr(res_v), _stream(stream)),
+           "lsa_tier_fetch_dma")
 
 
 def lsa_tier_attend(p: Problem, tr: Tier, q, res_k, res_v, slot_idx, slot_count, softmax_scale: float, out, lse=None,

@@ -238,3 +238,25 @@ def test_tier_entry_points_reject_bad_buffers_without_launching():
                                None) == B.LSA_ERR_INVALID_ARG
     assert lib.lsa_tier_attend(p.ref, T.ref, FAKE, None, FAKE, FAKE, FAKE, 0.0, FAKE, None, FAKE, ws, None) \
         == B.LSA_ERR_INVALID_ARG
+
+
+def test_tier_dma_validates_the_host_copy_list_before_copying():
+    import numpy as np
+    p = L.Problem([64 * 300, 64 * 1000], 64, [40, 100], 8, 2)
+    T = L.Tier([80, 200])
+    pitch, _, _ = L.lsa_tier_sizes(p, T)
+    lib = L.LIB
+    fl = np.zeros((2, pitch, 2), dtype=np.int32)
+    for counts, entry, what in (([-1, 0], None, "negative count"), ([0, pitch + 1], None, "count above pitch"),
+                                ([1, 0], (0, 0, 300, 0), "chunk beyond n_b"), ([1, 0], (0, 0, 5, 80), "slot beyond slots"),
+                                ([0, 2], (1, 1, -1, 3), "negative chunk")):
+        f = fl.copy()
+        if entry is not None:
+            b, i, c, s = entry
+            f[b, i] = (c, s)
+        cnt = np.asarray(counts, dtype=np.int32)
+        rc = lib.lsa_tier_fetch_dma(p.ref, T.ref, FAKE, FAKE, f.ctypes.data, cnt.ctypes.data, FAKE, FAKE, None)
+        assert rc == B.LSA_ERR_INVALID_ARG, what
+    cnt = np.zeros(2, dtype=np.int32)
+    assert lib.lsa_tier_fetch_dma(p.ref, T.ref, FAKE, FAKE, None, cnt.ctypes.data, FAKE, FAKE, None) \
+        == B.LSA_ERR_INVALID_ARG

@@ -12,6 +12,8 @@ pinned host mirror into the GPU reserve, and attention over the reserve.
   equals the full-cache attention over the set it read.
 - The attention over the reserve replays from a captured graph with new slot
   lists between replays, each replay equal to the eager call.
+- The DMA-engine copies from a host copy of the list (packed and padded mirror
+  layouts, merged runs of adjacent chunks) fill the reserve the same way.
 """
 from __future__ import annotations
 
@@ -320,3 +322,87 @@ def test_tier_fetch_rejects_pageable_mirror():
     pinned = torch.empty(n, dtype=torch.int16, pin_memory=True)
     L.lsa_tier_fetch(P, T, pinned, pinned, fetch, fc, res, res)  # no copies (count 0), accepted
     torch.cuda.synchronize()
+
+
+def _strided_cache(prob, seed, cs, hs):
+    """K and V of prob in a device cache with chunk stride cs and head stride hs (elements)."""
+    import torch
+    n = (prob.total_chunks - 1) * cs + (prob.n_kv_heads - 1) * hs + prob.chunk * prob.head_dim
+    table = torch.from_numpy(synth.normal_table_bf16().view(np.int16)).cuda()
+    out = []
+    for which in ("k", "v"):
+        t = torch.zeros(n, dtype=torch.int16, device="cuda")
+        synth.fill_kv_device(prob, seed, which, t.data_ptr(), table.data_ptr(),
+                             torch.cuda.current_stream().cuda_stream, chunk_stride=cs, head_stride=hs)
+        out.append(t)
+    return out
+
+
+@pytest.mark.parametrize("layout", ["packed", "padded_heads"])
+def test_tier_dma_copies(layout):
+    """lsa_tier_fetch_dma from the host copy of a plan's list: the reserve holds
+    the mirror's blocks, and attention over it equals the full-cache attention."""
+    import torch
+    import paper_2606_09079_amd as L
+    prob = synth.Problem(f"tier_dma_{layout}", [64 * 700, 64 * 90], 64, [70, 30], 16, 4)
+    C, d, H = prob.chunk, prob.head_dim, prob.n_kv_heads
+    hs = C * d if layout == "packed" else C * d + 64
+    cs = H * hs
+    k_dev, v_dev = _strided_cache(prob, 14, cs, hs)
+    host_k = torch.empty(k_dev.shape, dtype=torch.int16, pin_memory=True)
+    host_v = torch.empty(v_dev.shape, dtype=torch.int16, pin_memory=True)
+    host_k.copy_(k_dev)
+    host_v.copy_(v_dev)
+    P = L.Problem.from_synth(prob, kv_chunk_stride=cs, kv_head_stride=hs)
+    T = L.Tier([140, 60])
+    pitch, total, ws_bytes = L.lsa_tier_sizes(P, T)
+    slot_off = [0, 140]
+    res_k = torch.full((total * H * C * d,), 0x1111, dtype=torch.int16, device="cuda")
+    res_v = torch.full_like(res_k, 0x2222)
+    owner = torch.empty(total, dtype=torch.int32, device="cuda")
+    L.lsa_tier_reset(P, T, owner)
+    rng = np.random.default_rng(2)
+    # firing 0: a run of adjacent chunks (merged copies) plus scattered ones; then churn
+    sets0 = [np.sort(np.concatenate([np.arange(100, 140), rng.choice(np.arange(200, 700), 30, replace=False)])),
+             np.arange(0, 30)]
+    sets1 = [np.sort(np.concatenate([sets0[0][::2], rng.choice(np.setdiff1d(np.arange(700), sets0[0]), 35,
+                                                                replace=False)])),
+             np.sort(rng.choice(90, 30, replace=False))]
+    side = torch.cuda.Stream()
+    prev = None
+    ws = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    q = torch.from_numpy(synth.host_inputs(prob, 14)["q"].view(np.int16)).cuda()
+    for f, sets in enumerate((sets0, sets1)):
+        kept = np.full((2, pitch), -1, dtype=np.int32)
+        cnt = np.zeros(2, dtype=np.int32)
+        for b, s in enumerate(sets):
+            kept[b, :len(s)] = s
+            cnt[b] = len(s)
+        kept_d, cnt_d = torch.from_numpy(kept).cuda(), torch.from_numpy(cnt).cuda()
+        slot_idx = torch.empty(2, pitch, dtype=torch.int32, device="cuda")
+        fetch = torch.empty(2, pitch, 2, dtype=torch.int32, device="cuda")
+        fc = torch.empty(2, dtype=torch.int32, device="cuda")
+        L.lsa_tier_plan(P, T, kept_d, cnt_d, prev[0] if prev else None, prev[1] if prev else None, owner, slot_idx,
+                        fetch, fc)
+        torch.cuda.synchronize()
+        h_fetch, h_fc = fetch.cpu().numpy(), fc.cpu().numpy()
+        L.lsa_tier_fetch_dma(P, T, host_k, host_v, h_fetch, h_fc, res_k, res_v, side)
+        torch.cuda.synchronize()
+        slots = slot_idx.cpu().numpy()
+        for b, s in enumerate(sets):
+            for which, dev_t, res in (("k", k_dev, res_k), ("v", v_dev, res_v)):
+                for i, c in enumerate(s):
+                    g_off = (prob.chunk_offsets[b] + int(c)) * cs
+                    want = torch.as_strided(dev_t, (H, C * d), (hs, 1), g_off)
+                    got = res.view(-1, H, C * d)[slot_off[b] + int(slots[b, i])]
+                    assert torch.equal(got, want), f"firing {f} seq {b} chunk {c} {which}: reserve != mirror"
+        shp = (2, 1, 16, d)
+        t_out, t_lse = torch.empty(shp, device="cuda"), torch.empty(shp[:3], device="cuda")
+        L.lsa_tier_attend(P, T, q, res_k, res_v, slot_idx, cnt_d, 0.0, t_out, t_lse, ws, ws_bytes)
+        d_ws = torch.zeros(max(L.lsa_workspace_size(P), 256), dtype=torch.uint8, device="cuda")
+        d_out, d_lse = torch.empty(shp, device="cuda"), torch.empty(shp[:3], device="cuda")
+        L.lsa_sparse_decode_attn(P, q, k_dev, v_dev, kept_d, cnt_d, 0.0, d_out, d_lse, d_ws, d_ws.numel())
+        torch.cuda.synchronize()
+        assert torch.equal(t_out, d_out) and torch.equal(t_lse, d_lse)
+        prev = (slot_idx, cnt_d)
+        log(f"[tier] DMA {layout} firing {f}: copies {h_fc.tolist()}")
