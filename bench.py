@@ -59,8 +59,8 @@ WORKLOADS = {
                   "head_dim 128, bf16 K/V, batch 1",
     "tier1m": "tier1m: the recall1m context and Memory Indexer with the host tier: K/V in a pinned host mirror, a "
               "GPU reserve of 2 x K_max chunk slots; every 64 decode steps the indexer fires (recall, residency plan, "
-              "copies of the missing chunks) on a second stream, the new set is read 16 steps later; each "
-              "decode step attends over the reserve",
+              "copies of the missing chunks) on a second stream, copied by the DMA engines, and the new set is read "
+              "48 steps later; each decode step attends over the reserve",
     "twolevel_tiny": "twolevel_tiny: 4,133 tokens (65 chunks, the last one 37 tokens), Level 1 3 x 16 x 64 with "
                      "K_max 24, Level 2 keeps 6, window 512 tokens, 8 query / 8 KV heads, head_dim 128, bf16 K/V",
 }
@@ -114,7 +114,7 @@ def main() -> int:
                     help="untimed streaming read between the per-step samples of the step-time distribution, "
                          "so that the 256 MB Infinity Cache cannot serve a previous step's bytes "
                          "(a multiple of 32; default: 1024 for workloads below 1 GB per step, else 0)")
-    ap.add_argument("--tier-lag", type=int, default=16,
+    ap.add_argument("--tier-lag", type=int, default=48,
                     help="tier1m: decode steps from a firing until its kept set is read (1 .. 63)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="profiling aid: also run one plain copy of this many MiB (known bytes)")
@@ -337,7 +337,7 @@ TIER_RHO = 0.99      # correlation of the indexer queries of consecutive firings
 
 
 def bench_tier(args) -> int:
-    """Decode over the host tier at 1M context (see the tier1m workload line).
+    """Decode over the host tier at 1M context (the tier1m workload).
 
     Firings: the indexer queries of firing f are bf16(sqrt(rho) q_{f-1} +
     sqrt(1 - rho) g_f) with fresh N(0, 1) draws g_f and the gates of firing 0,
@@ -345,7 +345,11 @@ def bench_tier(args) -> int:
     (about 11% of the set changes per firing at rho = 0.99).  A step is one
     decode step: the attention over the reserve, plus 1/64 of a firing (index
     scores of 3 layers over the full history, recall selection, residency plan
-    and the copies of the missing chunks over PCIe) run on a second stream."""
+    and the copies of the missing chunks over PCIe) run on a second stream.
+    The reported value is the DMA side band: the copy list comes to the host,
+    which issues DMA-engine copies, and the new set is read --tier-lag steps
+    after the firing.  For comparison the same loop runs with the copy kernel
+    (the list stays on the GPU) and the new set read 1 and 16 steps later."""
     import numpy as np
     import torch
 
@@ -374,7 +378,7 @@ def bench_tier(args) -> int:
         a = np.ascontiguousarray(a)
         return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).cuda()
 
-    n_fire = 2 * ((args.warmup + args.steps) // TIER_TAU + 1) + 2
+    n_fire = 3 * ((args.warmup + args.steps) // TIER_TAU + 1) + 2  # three steady-state runs
     rng = np.random.default_rng(2024)
     qf = synth.bf16_bits_to_f64(host0["idx_q"])
     idx_q = []
@@ -382,7 +386,9 @@ def bench_tier(args) -> int:
         if f > 0:
             qf = math.sqrt(TIER_RHO) * qf + math.sqrt(1.0 - TIER_RHO) * rng.standard_normal(qf.shape)
         idx_q.append(up(synth.f64_to_bf16_bits(qf)))
-    fresh_q = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))  # an unrelated query: a full change
+    # unrelated queries: a full change of the kept set
+    fresh_q = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))
+    fresh_q2 = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))
     qs = [dev["q"]] + [up(synth.host_inputs(prob, 1000 + r)["q"]) for r in range(1, 4)]
 
     B, K, C, Hkv, d = prob.batch, prob.keep[0], prob.chunk, prob.n_kv_heads, prob.head_dim
@@ -445,38 +451,61 @@ def bench_tier(args) -> int:
     torch.cuda.synchronize()
     dec_us = 1e3 * sum(a.elapsed_time(b) for a, b in de) / n_dec
 
+    # the copy list on the host, for the DMA engines
+    h_fetch = torch.empty(B, pitch, 2, dtype=torch.int32, pin_memory=True)
+    h_fcount = torch.empty(B, dtype=torch.int32, pin_memory=True)
+
+    def fire_dma(q_idx, prev, new, s):
+        select_and_plan(q_idx, prev, new, s)
+        h_fetch.copy_(fetch, non_blocking=True)
+        h_fcount.copy_(fcount, non_blocking=True)
+        listed = ev()
+        listed.record(s)
+        listed.synchronize()  # the side band waits for the list on the host
+        L.lsa_tier_fetch_dma(P, T, host_k, host_v, h_fetch, h_fcount, res_k, res_v, s)
+
     # ---- a full change of the kept set, copied on the side stream while decode
-    # goes on over the old set
-    fe = [ev(), ev()]
-    side.wait_stream(main)
-    fe[0].record(side)
-    fire(fresh_q, 0, 1, side)
-    fe[1].record(side)
-    dd = [(ev(), ev()) for _ in range(n_dec)]
-    for i in range(n_dec):
-        dd[i][0].record(main)
-        decode(0, i, main)
-        dd[i][1].record(main)
-    torch.cuda.synchronize()
-    full_n = int(fcount.cpu()[0])
-    full_ms = fe[0].elapsed_time(fe[1])
-    during = [1e3 * a.elapsed_time(b) for a, b in dd if fe[0].elapsed_time(b) <= full_ms]
-    dec_during_us = sum(during) / len(during) if during else None
-    log(f"[tier] full change: {full_n} copies in {full_ms:.2f} ms on the side stream; decode {dec_us:.1f} us alone, "
-        f"{dec_during_us} us during the copies ({len(during)} steps)")
-    # back to the firing-0 set as the starting point of the steady state
-    side.wait_stream(main)
-    fire(idx_q[0], 1, 0, side)
-    main.wait_stream(side)
-    torch.cuda.synchronize()
+    # goes on over the old set, by the copy kernel and by the DMA engines
+    full = {}
+    for mode, q_full in (("kernel", fresh_q), ("dma", fresh_q2)):
+        fe = [ev(), ev()]
+        side.wait_stream(main)
+        fe[0].record(side)
+        (fire if mode == "kernel" else fire_dma)(q_full, 0, 1, side)
+        fe[1].record(side)
+        n_during = 400 if mode == "dma" else 120
+        dd = [(ev(), ev()) for _ in range(n_during)]
+        for i in range(n_during):
+            dd[i][0].record(main)
+            decode(0, i, main)
+            dd[i][1].record(main)
+        torch.cuda.synchronize()
+        n_full = int(fcount.cpu()[0])
+        ms_full = fe[0].elapsed_time(fe[1])
+        during = [1e3 * a_.elapsed_time(b_) for a_, b_ in dd
+                  if fe[0].elapsed_time(a_) >= 0 and fe[0].elapsed_time(b_) <= ms_full]
+        full[mode] = {"copies": n_full, "ms": round(ms_full, 3),
+                      "gbs": round(n_full * 2 * slot_bytes / (ms_full * 1e-3) / 1e9, 2),
+                      "decode_us_during_copies": round(float(np.median(during)), 2) if during else None,
+                      "decode_steps_during_copies": len(during)}
+        log(f"[tier] full change by {mode}: {full[mode]}")
+        # back to the firing-0 set
+        side.wait_stream(main)
+        fire(idx_q[0], 1, 0, side)
+        main.wait_stream(side)
+        torch.cuda.synchronize()
 
     # ---- steady state: a firing every TIER_TAU steps on the side stream; steps
-    # t .. t + lag - 1 read the previous set, steps from t + lag on the new one
+    # t .. t + lag - 1 read the previous set, steps from t + lag on the new one.
+    # The side band waits only for the switch to the previous set (the decodes
+    # of the set before it have finished then), never for the latest decode.
     state = {"cur": 0, "f": 1}
 
-    def steady(lag):
+    def steady(mode, lag):
         cur, f = state["cur"], state["f"]
         fire_ev, copies, new = [], [], None
+        switched = ev()
+        switched.record(main)
         e0, e1 = ev(), ev()
         t0 = 0.0
         for i in range(args.warmup + args.steps):
@@ -486,16 +515,18 @@ def bench_tier(args) -> int:
                 e0.record(main)
             if i % TIER_TAU == 0:
                 new = 1 - cur
-                side.wait_stream(main)
+                side.wait_event(switched)
                 a_, b_ = ev(), ev()
                 a_.record(side)
-                fire(idx_q[f], cur, new, side)
+                (fire if mode == "kernel" else fire_dma)(idx_q[f], cur, new, side)
                 b_.record(side)
                 fire_ev.append((a_, b_, i >= args.warmup))
                 f += 1
             if i % TIER_TAU == lag:
                 main.wait_stream(side)
                 cur = new
+                switched = ev()
+                switched.record(main)
                 copies.append(fcount.clone())
             decode(cur, i, main)
         main.wait_stream(side)
@@ -506,12 +537,15 @@ def bench_tier(args) -> int:
         ms = e0.elapsed_time(e1) / args.steps
         fire_ms = [a.elapsed_time(b) for a, b, timed in fire_ev if timed]
         n_copies = [int(c.cpu()[0]) for c in copies]
-        log(f"[tier] lag {lag}: {args.steps} steps, {ms * 1e3:.2f} us/step (wall {wall:.3f}s); firings "
-            f"{[round(x, 3) for x in fire_ms]} ms; copies {n_copies}")
-        return ms, fire_ms, n_copies[-len(fire_ms):] if fire_ms else []
+        log(f"[tier] {mode} copies, lag {lag}: {args.steps} steps, {ms * 1e3:.2f} us/step (wall {wall:.3f}s); "
+            f"firings {[round(x, 3) for x in fire_ms]} ms; copies {n_copies}")
+        return {"us_per_step": round(ms * 1e3, 2), "lag_steps": lag, "firings_timed": len(fire_ms),
+                "firing_ms": round(sum(fire_ms) / len(fire_ms), 3) if fire_ms else None,
+                "copies_per_firing": n_copies[-len(fire_ms):] if fire_ms else []}
 
-    ms_lag1, fire_lag1, _ = steady(1)
-    ms_per_step, fire_ms, n_copies = steady(args.tier_lag)
+    runs = {"kernel_lag1": steady("kernel", 1), "kernel_lag16": steady("kernel", 16),
+            "dma": steady("dma", args.tier_lag)}
+    ms_per_step = runs["dma"]["us_per_step"] * 1e-3
     cur = state["cur"]
 
     kept_n = int(cnt[cur].cpu()[0])
@@ -539,14 +573,9 @@ def bench_tier(args) -> int:
             "cold_fetch": {"chunks": cold_n, "ms": round(cold_ms, 3),
                            "pcie_gbs": round(cold_n * 2 * slot_bytes / (cold_ms * 1e-3) / 1e9, 2)},
             "decode_us_alone": round(dec_us, 2),
-            "full_change": {"copies": full_n, "ms": round(full_ms, 3),
-                            "decode_us_during_copies": round(dec_during_us, 2) if dec_during_us else None,
-                            "decode_steps_during_copies": len(during)},
-            "steady_state": {"lag_steps": args.tier_lag, "firings_timed": len(fire_ms),
-                             "firing_ms": round(sum(fire_ms) / len(fire_ms), 3) if fire_ms else None,
-                             "copies_per_firing": n_copies, "kept_chunks": kept_n,
-                             "us_per_step_lag1": round(ms_lag1 * 1e3, 2),
-                             "firing_ms_lag1": round(sum(fire_lag1) / len(fire_lag1), 3) if fire_lag1 else None},
+            "full_change": full,
+            "steady_state": runs,
+            "kept_chunks": kept_n,
         },
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
