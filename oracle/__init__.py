@@ -13,7 +13,9 @@ step:
 * O3 attend -- softmax(q K^T * scale) V over the tokens of the kept chunks
   (an empty kept set gives out = 0, lse = -inf).
 
-and, for the recall path, the full Memory Indexer in the paper's order:
+and the golden-label pipeline of Sec. 2.2 (softmax, top-p set, vote over
+layers, golden set, union over the window; Eqs. 7-11), and, for the recall
+path, the full Memory Indexer in the paper's order:
 
 * R1 index score -- x = sum_h w_h ReLU(q_h . K_s) per indexer layer (the
   argument of the sigmoid of Sec. 2.1 Eq. 4);
@@ -70,6 +72,12 @@ def bind(path: str) -> ctypes.CDLL:
     L.oracle_attention_tokens.restype = ctypes.c_int
     L.oracle_two_level.argtypes = [_P, _I64, _P, _I64, _I64, _I64, _I64, _P]
     L.oracle_two_level.restype = _I64
+    L.oracle_exp_fixed.argtypes = [_F64]
+    L.oracle_exp_fixed.restype = _F64
+    L.oracle_top_p.argtypes = [_P, _I64, _I64, _I64, _P]
+    L.oracle_top_p.restype = _I64
+    L.oracle_golden_labels.argtypes = [_P, _I32, _I32, _I64, _I64, _I64, _I32, _P, _P, _P]
+    L.oracle_golden_labels.restype = _I64
     return L
 
 
@@ -275,6 +283,36 @@ def tier_plan(owner: Sequence[int], old_slots: Sequence[int], kept: Sequence[int
 
 
 # ---------------------------------------------------------------- O4 step
+def exp_fixed(x: float) -> float:
+    """exp(x) for x <= 0 by the oracle's fixed float64 method (Cody-Waite reduction, degree-13 Taylor series)."""
+    return float(lib().oracle_exp_fixed(float(x)))
+
+
+def top_p(S: np.ndarray, p_num: int, p_den: int):
+    """Top-p set of one row of float32 logits (Eqs. 7-8): (0/1 marks [n], set size)."""
+    S = _c(S, np.float32)
+    mark = np.zeros(len(S), dtype=np.uint8)
+    size = lib().oracle_top_p(S.ctypes.data, len(S), p_num, p_den, mark.ctypes.data)
+    if size < 0:
+        raise ValueError("oracle_top_p rejected its arguments")
+    return mark, int(size)
+
+
+def golden_labels(logits: np.ndarray, p_num: int, p_den: int, theta: int):
+    """Label set of one window (Eqs. 7-11) from float32 logits [tau][L][n]:
+    (ascending entry ids of Y, top-p set sizes [tau][L], golden-set sizes [tau])."""
+    logits = _c(logits, np.float32)
+    tau, L, n = logits.shape
+    label = np.zeros(n, dtype=np.uint8)
+    sizes = np.zeros((tau, L), dtype=np.int32)
+    golden = np.zeros(tau, dtype=np.int32)
+    cnt = lib().oracle_golden_labels(logits.ctypes.data, tau, L, n, p_num, p_den, theta, label.ctypes.data,
+                                     sizes.ctypes.data, golden.ctypes.data)
+    if cnt < 0:
+        raise ValueError("oracle_golden_labels rejected its arguments")
+    return np.nonzero(label)[0].astype(np.int32), sizes, golden
+
+
 def select_for_sequence(prob, inputs: Dict[str, object], b: int):
     """O1 then O2 for sequence b.
 

@@ -36,6 +36,14 @@
  *    x_l(s) = sum_h w_h ReLU(q_h . K_s); the recalled set is the OR over the
  *    layers; when it holds more than K_max entries, the K_max with the largest
  *    max_l x_l(s) are kept (lower id first on ties).
+ *  - Golden labels (Sec. 2.2, Eqs. 7-11): the top-p set of Eq. 8 is read as
+ *    the text states it, the smallest set of the most probable entries whose
+ *    probability mass reaches p (entries ordered by probability, then by lower
+ *    index); Eq. 8 as printed (cumulative mass <= p) would leave the set empty
+ *    whenever the most probable entry alone exceeds p.  Probabilities are held
+ *    as whole multiples of 2^-40 of the largest one, with the exponential
+ *    evaluated by one fixed float64 method (below), so that which entries
+ *    reach the mass is an exact integer decision.
  */
 #include <math.h>
 #include <stdint.h>
@@ -346,4 +354,124 @@ int64_t oracle_two_level(const int32_t* recalled, int64_t m, const double* nativ
   }
   for (int64_t c = w0; c < n_total; ++c) out[core + (c - w0)] = (int32_t)c;
   return core + (n_total - w0);
+}
+
+/* ------------------------------------------------------------ golden labels */
+
+/*
+ * exp(x) for x <= 0 by a fixed float64 method, so that the result is one
+ * determined double: Cody and Waite's reduction x = k ln2 + r with k the
+ * nearest integer to x / ln2 and ln2 split into a high part with trailing zero
+ * bits and a low part (the split fdlibm uses), the Taylor series of e^r to
+ * degree 13 (|r| <= ln2 / 2, truncation below 4e-18) in Horner form with
+ * fused multiply-adds, and an exact scaling by 2^k.  Below -64 the result is
+ * 0 (its weight would be far below 2^-40 anyway).
+ */
+double oracle_exp_fixed(double x) {
+  if (x > 0.0) x = 0.0;
+  if (x < -64.0) return 0.0;
+  const double log2e = 1.4426950408889634;
+  const double ln2_hi = 6.93147180369123816490e-01;
+  const double ln2_lo = 1.90821492927058770002e-10;
+  const double k = rint(x * log2e);
+  double r = fma(-k, ln2_hi, x);
+  r = fma(-k, ln2_lo, r);
+  /* 1 / j! for j = 13 down to 0 */
+  const double inv_fact[14] = {1.0 / 6227020800.0, 1.0 / 479001600.0, 1.0 / 39916800.0, 1.0 / 3628800.0,
+                               1.0 / 362880.0,     1.0 / 40320.0,     1.0 / 5040.0,      1.0 / 720.0,
+                               1.0 / 120.0,        1.0 / 24.0,        1.0 / 6.0,         1.0 / 2.0,
+                               1.0,                1.0};
+  double p = inv_fact[0];
+  for (int j = 1; j < 14; ++j) p = fma(p, r, inv_fact[j]);
+  return ldexp(p, (int)k);
+}
+
+typedef struct { float s; int64_t c; } logit_entry;
+
+/* Larger logit first (so larger probability first); equal logits, -0.0 and
+ * +0.0 included: lower entry index first. */
+static int by_logit_desc(const void* a, const void* b) {
+  const logit_entry* x = (const logit_entry*)a;
+  const logit_entry* y = (const logit_entry*)b;
+  if (x->s > y->s) return -1;
+  if (x->s < y->s) return 1;
+  return (x->c > y->c) - (x->c < y->c);
+}
+
+/*
+ * Top-p set of one row of logits (Eq. 7 softmax, Eq. 8 nucleus): mark[s] = 1
+ * for the entries of the smallest prefix, in (probability desc, index asc)
+ * order, whose mass reaches p_num / p_den.  Returns the size of the set, or -1
+ * on a bad argument or allocation failure.  Logits must be finite.
+ */
+int64_t oracle_top_p(const float* S, int64_t n, int64_t p_num, int64_t p_den, uint8_t* mark) {
+  if (n < 1 || p_num < 1 || p_den < p_num) return -1;
+  float m = S[0];
+  for (int64_t s = 1; s < n; ++s)
+    if (S[s] > m) m = S[s];
+  uint64_t* q = (uint64_t*)malloc((size_t)n * sizeof *q);
+  logit_entry* v = (logit_entry*)malloc((size_t)n * sizeof *v);
+  if (!q || !v) { free(q); free(v); return -1; }
+  uint64_t Z = 0;
+  for (int64_t s = 0; s < n; ++s) {
+    const double w = oracle_exp_fixed((double)S[s] - (double)m);
+    q[s] = (uint64_t)(w * 1099511627776.0); /* floor(w * 2^40) */
+    Z += q[s];
+    v[s].s = S[s];
+    v[s].c = s;
+  }
+  qsort(v, (size_t)n, sizeof *v, by_logit_desc);
+  memset(mark, 0, (size_t)n);
+  const unsigned __int128 need = (unsigned __int128)Z * (uint64_t)p_num;
+  uint64_t cum = 0;
+  int64_t size = 0;
+  for (int64_t j = 0; j < n; ++j) {
+    cum += q[v[j].c];
+    mark[v[j].c] = 1;
+    ++size;
+    if ((unsigned __int128)cum * (uint64_t)p_den >= need) break;
+  }
+  free(q);
+  free(v);
+  return size;
+}
+
+/*
+ * The label pipeline of one window: logits [tau][L][n] (row (i, l) holds
+ * S_{i,l,.}).  For each step i the top-p set of every layer, the vote count
+ * V_{i,s} = number of layers whose set holds s (Eq. 9), the golden set
+ * A_i = {s : V_{i,s} >= theta} (Eq. 10), and the label set Y = the union of
+ * the A_i over the window (Eq. 11).  Writes label[s] = 1 for s in Y,
+ * nucleus_size[i * L + l] = size of the top-p set of row (i, l) and
+ * golden_count[i] = |A_i| (both nullable), and returns |Y| (-1 on a bad
+ * argument or allocation failure).
+ */
+int64_t oracle_golden_labels(const float* logits, int32_t tau, int32_t L, int64_t n, int64_t p_num, int64_t p_den,
+                             int32_t theta, uint8_t* label, int32_t* nucleus_size, int32_t* golden_count) {
+  if (tau < 1 || L < 1 || n < 1 || theta < 1) return -1;
+  uint8_t* mark = (uint8_t*)malloc((size_t)n);
+  int32_t* votes = (int32_t*)malloc((size_t)n * sizeof *votes);
+  if (!mark || !votes) { free(mark); free(votes); return -1; }
+  memset(label, 0, (size_t)n);
+  for (int32_t i = 0; i < tau; ++i) {
+    memset(votes, 0, (size_t)n * sizeof *votes);
+    for (int32_t l = 0; l < L; ++l) {
+      const int64_t size = oracle_top_p(logits + ((int64_t)i * L + l) * n, n, p_num, p_den, mark);
+      if (size < 0) { free(mark); free(votes); return -1; }
+      if (nucleus_size) nucleus_size[(int64_t)i * L + l] = (int32_t)size;
+      for (int64_t s = 0; s < n; ++s) votes[s] += mark[s];
+    }
+    int32_t golden = 0;
+    for (int64_t s = 0; s < n; ++s)
+      if (votes[s] >= theta) {
+        ++golden;
+        label[s] = 1;
+      }
+    if (golden_count) golden_count[i] = golden;
+  }
+  int64_t count = 0;
+  for (int64_t s = 0; s < n; ++s) count += label[s];
+  free(mark);
+  free(votes);
+  return count;
 }

@@ -452,6 +452,141 @@ def pin_tier_plan_invariants():
         pass
 
 
+# ------------------------------------------------------------ golden labels
+def _golden_logits(weights) -> np.ndarray:
+    return np.log(np.asarray(weights, dtype=np.float64)).astype(np.float32)
+
+
+def pin_golden_worked_example():
+    """The hand-worked window of tests/golden/golden_labels_worked.json."""
+    g = json.load(open(os.path.join(GOLDEN, "golden_labels_worked.json")))
+    logits = _golden_logits(g["weights"])
+    for case in g["cases"]:
+        labels, sizes, golden = oracle.golden_labels(logits, g["p_num"], g["p_den"], case["theta"])
+        assert labels.tolist() == case["labels"], (case, labels)
+        assert sizes.tolist() == g["nucleus_size"], sizes
+        assert golden.tolist() == case["golden_count"], golden
+
+
+def pin_exp_fixed_accuracy():
+    """The oracle's fixed exponential against numpy's exp: within 2^-50 relative
+    on [-64, 0], exactly 1 at 0, exactly 2^-j at -j ln 2 rounded, 0 below -64."""
+    xs = np.concatenate([-np.linspace(0.0, 64.0, 4001), -np.logspace(-300, 1.8, 400), [-0.34657359, -0.34657360]])
+    for x in xs:
+        got, want = oracle.exp_fixed(float(x)), math.exp(float(x))
+        assert abs(got - want) <= 2.0 ** -50 * want, (x, got, want)
+    assert oracle.exp_fixed(0.0) == 1.0
+    assert oracle.exp_fixed(-64.5) == 0.0 and oracle.exp_fixed(-1000.0) == 0.0
+
+
+def _numpy_nucleus(S: np.ndarray, p: float):
+    """Top-p set from numpy: float64 softmax, stable sort by (logit desc, index
+    asc), cumulative mass; returns (set, cumulative masses in that order)."""
+    P = scipy.special.softmax(S.astype(np.float64))
+    order = np.lexsort((np.arange(len(S)), -S.astype(np.float64)))
+    cum = np.cumsum(P[order])
+    size = int(np.searchsorted(cum, p - 0.0, side="left")) + 1
+    size = min(size, len(S))
+    return set(order[:size].tolist()), cum
+
+
+def pin_top_p_library_softmax():
+    """Random rows against numpy's softmax, sort and cumulative sum.  The two
+    may differ only where numpy's cumulative mass sits within 1e-9 of p at the
+    cut (the oracle holds masses in units of 2^-40 of the largest)."""
+    rng = np.random.default_rng(41)
+    for trial in range(300):
+        n = int(rng.integers(1, 3000))
+        scale = float(rng.choice([0.05, 0.5, 1.0, 3.0, 10.0, 30.0]))
+        S = (rng.standard_normal(n) * scale).astype(np.float32)
+        if trial % 5 == 0:  # many exact ties
+            S = np.round(S * 2.0).astype(np.float32) / np.float32(2.0)
+        num, den = [(3, 5), (1, 2), (9, 10), (1, 100), (99, 100), (1, 1)][trial % 6]
+        mark, size = oracle.top_p(S, num, den)
+        want, cum = _numpy_nucleus(S, num / den)
+        got = set(np.nonzero(mark)[0].tolist())
+        assert size == len(got)
+        if got != want:
+            k = len(want)
+            near = abs(cum[k - 1] - num / den) <= 1e-9 or (k >= 2 and abs(cum[k - 2] - num / den) <= 1e-9) \
+                or (num == den and S.max() - S.min() > 27.0)
+            assert near, (trial, n, scale, len(got), len(want))
+
+
+def pin_top_p_bruteforce():
+    """Tiny rows with integer weights: over all subsets whose probability mass
+    reaches p, the smallest ones; among those the most probable; among equals
+    the lexicographically smallest index list -- the top-p set by its own
+    definition, with exact fractions."""
+    from fractions import Fraction
+    rng = np.random.default_rng(43)
+    checked = 0
+    for trial in range(400):
+        n = int(rng.integers(1, 8))
+        wts = [int(x) for x in rng.integers(1, 6, size=n)]
+        num, den = [(3, 5), (1, 2), (2, 3), (1, 7), (6, 7)][trial % 5]
+        p, tot = Fraction(num, den), sum(wts)
+        best = None
+        for mask in range(1, 1 << n):
+            idx = [s for s in range(n) if mask >> s & 1]
+            mass = Fraction(sum(wts[s] for s in idx), tot)
+            if mass < p:
+                continue
+            key = (len(idx), -mass, idx)
+            if best is None or key < best[0]:
+                best = (key, idx)
+        # skip rows where some subset's mass lies within float rounding of p
+        masses = {Fraction(sum(wts[s] for s in range(n) if m >> s & 1), tot) for m in range(1 << n)}
+        if any(0 < abs(float(x - p)) < 1e-6 for x in masses):
+            continue
+        mark, size = oracle.top_p(_golden_logits(wts), num, den)
+        assert np.nonzero(mark)[0].tolist() == best[1], (wts, num, den, best[1])
+        checked += 1
+    assert checked > 200
+
+
+def pin_top_p_boundaries():
+    """Equal logits make every mass exact: a set that reaches p exactly is
+    enough (3 of 5 equal entries at p = 3/5, the lower indices); the most
+    probable entry alone when it exceeds p; the whole support at p = 1; the
+    first maximum alone for a tiny p."""
+    mark, size = oracle.top_p(np.zeros(5, np.float32), 3, 5)
+    assert mark.tolist() == [1, 1, 1, 0, 0] and size == 3
+    mark, size = oracle.top_p(np.zeros(5, np.float32), 61, 100)
+    assert size == 4
+    mark, size = oracle.top_p(np.array([0.0, 5.0, 1.0], np.float32), 3, 5)
+    assert mark.tolist() == [0, 1, 0]
+    S = np.array([0.0, -40.0, -1.0, 0.0], np.float32)
+    mark, size = oracle.top_p(S, 1, 1)  # weights below 2^-40 of the largest hold no mass
+    assert mark.tolist() == [1, 0, 1, 1]
+    mark, size = oracle.top_p(np.array([2.0, 3.0, 3.0, -0.0, 0.0], np.float32), 1, 1 << 30)
+    assert mark.tolist() == [0, 1, 0, 0, 0]
+
+
+def pin_golden_votes_and_union():
+    """Eqs. 9-11 as indicator-matrix arithmetic over the oracle's own top-p sets
+    (themselves pinned above): votes are column sums over layers, the golden
+    set is votes >= theta, the label set the OR over steps; theta = 1 gives the
+    union of every set, theta > L the empty set."""
+    rng = np.random.default_rng(47)
+    for trial in range(40):
+        tau, L, n = int(rng.integers(1, 5)), int(rng.integers(1, 7)), int(rng.integers(1, 300))
+        logits = (rng.standard_normal((tau, L, n)) * rng.choice([0.5, 2.0, 6.0])).astype(np.float32)
+        num, den = (3, 5) if trial % 2 else (1, 3)
+        M = np.stack([np.stack([oracle.top_p(logits[i, l], num, den)[0] for l in range(L)]) for i in range(tau)])
+        votes = M.astype(np.int64).sum(axis=1)                      # [tau][n]
+        for theta in (1, 2, 3, L, L + 1):
+            labels, sizes, golden = oracle.golden_labels(logits, num, den, theta)
+            A = votes >= theta
+            assert labels.tolist() == np.nonzero(A.any(axis=0))[0].tolist()
+            assert golden.tolist() == A.sum(axis=1).tolist()
+            assert sizes.tolist() == M.sum(axis=2).tolist()
+            if theta == 1:
+                assert labels.tolist() == np.nonzero(M.any(axis=(0, 1)))[0].tolist()
+            if theta > L:
+                assert len(labels) == 0
+
+
 ALL_PINS = [
     pin_score_library_matmul, pin_score_int8_exact, pin_score_closed_forms,
     pin_topk_worked_example, pin_topk_bruteforce, pin_topk_library_sort, pin_union_bruteforce,
@@ -461,4 +596,6 @@ ALL_PINS = [
     pin_index_score_head_permutation, pin_recall_sigmoid_threshold, pin_recall_or_bruteforce,
     pin_recall_boundaries, pin_attention_tokens_reduces_to_chunks, pin_two_level_worked_example,
     pin_two_level_bruteforce, pin_tier_plan_invariants,
+    pin_golden_worked_example, pin_exp_fixed_accuracy, pin_top_p_library_softmax, pin_top_p_bruteforce,
+    pin_top_p_boundaries, pin_golden_votes_and_union,
 ]

@@ -18,6 +18,21 @@ import oracle_pins as P
 SRC = os.path.join(os.path.dirname(oracle.__file__), "lsa_oracle.c")
 
 MUTANTS = {
+    "top_p_strict_mass": ("if ((unsigned __int128)cum * (uint64_t)p_den >= need) break;",
+                          "if ((unsigned __int128)cum * (uint64_t)p_den > need) break;"),
+    "top_p_tie_reversed": ("  return (x->c > y->c) - (x->c < y->c);\n}\n\n/*\n * Top-p set",
+                           "  return (x->c < y->c) - (x->c > y->c);\n}\n\n/*\n * Top-p set"),
+    "top_p_least_probable_first": ("  if (x->s > y->s) return -1;\n  if (x->s < y->s) return 1;\n"
+                                   "  return (x->c > y->c) - (x->c < y->c);\n}\n\n/*\n * Top-p set",
+                                   "  if (x->s > y->s) return 1;\n  if (x->s < y->s) return -1;\n"
+                                   "  return (x->c > y->c) - (x->c < y->c);\n}\n\n/*\n * Top-p set"),
+    "top_p_mass_not_summed": ("    Z += q[s];\n", "    Z = q[s];\n"),
+    "exp_fixed_no_low_part": ("  r = fma(-k, ln2_lo, r);\n", ""),
+    "exp_fixed_short_series": ("for (int j = 1; j < 14; ++j) p = fma(p, r, inv_fact[j]);",
+                               "for (int j = 1; j < 13; ++j) p = fma(p, r, inv_fact[j]);"),
+    "golden_vote_strict": ("if (votes[s] >= theta) {", "if (votes[s] > theta) {"),
+    "golden_union_last_step": ("    memset(votes, 0, (size_t)n * sizeof *votes);\n",
+                               "    memset(votes, 0, (size_t)n * sizeof *votes);\n    memset(label, 0, (size_t)n);\n"),
     "tie_break_reversed_f": ("  return (x->c > y->c) - (x->c < y->c);\n}\n\nstatic int by_score_desc_i",
                              "  return (x->c < y->c) - (x->c > y->c);\n}\n\nstatic int by_score_desc_i"),
     "tie_break_reversed_i": ("  return (x->c > y->c) - (x->c < y->c);\n}\n\nstatic int ascending_i32",
