@@ -68,6 +68,10 @@
  * chunk slots, a residency plan maps the recalled chunks to slots, the missing
  * ones are copied in from the mirror (a side-band step that can overlap
  * decode), and attention runs over the reserve.
+ *
+ * Golden labels (lsa_golden_*): the offline label pipeline of Sec. 2.2 over
+ * raw indexer logits -- softmax, top-p set, votes across layers, golden set,
+ * union over the look-ahead window.
  */
 #ifndef LSA_H_
 #define LSA_H_
@@ -88,6 +92,8 @@ extern "C" {
 #define LSA_MAX_IDX_LAYERS 4       /* indexer layers OR-ed by the recall path */
 #define LSA_MAX_TIER_CHUNKS 131072 /* n_b limit of the host tier's residency plan */
 #define LSA_MAX_TIER_SLOTS 65536   /* reserve slots per sequence */
+#define LSA_MAX_GOLDEN_ENTRIES 4194304 /* entries per sequence of the golden-label pipeline */
+#define LSA_MAX_GOLDEN_LAYERS 63   /* layers voting in the golden-label pipeline */
 
 typedef enum {
   LSA_OK = 0,
@@ -131,6 +137,16 @@ typedef struct lsa_tier {
   int32_t reserved;      /* must be 0 */
   int32_t reserved2;     /* must be 0 */
 } lsa_tier;
+
+/* Golden-label pipeline.  Host memory only; read during the call. */
+typedef struct lsa_golden {
+  int32_t batch;              /* B, 1 .. LSA_MAX_BATCH windows (one per sequence) */
+  int32_t n_steps;            /* tau, decoding steps of a window, >= 1 */
+  int32_t n_layers;           /* L, layers that vote, 1 .. LSA_MAX_GOLDEN_LAYERS */
+  int32_t theta;              /* votes an entry needs, 1 .. 64 (above L no entry qualifies) */
+  int32_t p_num, p_den;       /* top-p mass p = p_num / p_den, 1 <= p_num <= p_den <= 2^30 */
+  const int64_t* n_entries;   /* HOST [B]: entries of each sequence, 1 .. LSA_MAX_GOLDEN_ENTRIES */
+} lsa_golden;
 
 /* Two-level selection.  Host memory only; read during the call. */
 typedef struct lsa_two_level {
@@ -357,6 +373,32 @@ lsa_status lsa_tier_fetch_dma(const lsa_problem* p, const lsa_tier* tr, const ui
 lsa_status lsa_tier_attend(const lsa_problem* p, const lsa_tier* tr, const uint16_t* q, const uint16_t* res_k,
                            const uint16_t* res_v, const int32_t* slot_idx, const int32_t* slot_count,
                            float softmax_scale, float* out, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Golden labels (Sec. 2.2, Eqs. 7-11).  logits: device float32, sequence b's
+ * block [tau][L][n_b] at element tau * L * entry_off[b] (entry_off the
+ * exclusive prefix sum of n_entries); row (i, l) holds the raw indexer logits
+ * S_{i,l,s} of decoding step i and layer l over the n_b entries.  Per row:
+ * P = softmax(S) (Eq. 7) and its top-p set (Eq. 8), the smallest set of the
+ * most probable entries whose probability mass reaches p, more probable first
+ * and lower index first among equal logits (-0.0 equal to +0.0).  Per step:
+ * V_s = the number of layers whose set holds s (Eq. 9) and the golden set
+ * {s : V_s >= theta} (Eq. 10).  Per sequence: the label set, the union of the
+ * golden sets of the tau steps (Eq. 11).
+ * The decision is exact: weights exp(S - max S) come from one fixed float64
+ * method (Cody-Waite reduction, Taylor series of degree 13 with fused
+ * multiply-adds) as integers floor(w * 2^40), and a set reaches p when
+ * (its mass) * p_den >= p_num * (total mass) in integers.  Logits must be
+ * finite.
+ * Outputs (device): labels [sum_b n_b] int32, sequence b's label ids ascending
+ * from element entry_off[b], label_count [B] their number; nucleus_size
+ * [B][tau][L] int32 the size of every top-p set and golden_count [B][tau] the
+ * size of every golden set (both nullable).  The workspace holds the
+ * membership bitmaps of every row.
+ */
+lsa_status lsa_golden_sizes(const lsa_golden* g, size_t* ws_bytes);
+lsa_status lsa_golden_labels(const lsa_golden* g, const float* logits, int32_t* labels, int32_t* label_count,
+                             int32_t* nucleus_size, int32_t* golden_count, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -25,7 +25,7 @@ import os
 import statistics
 import subprocess
 from dataclasses import dataclass, field
-from typing import Dict, List, Optional
+from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
@@ -37,6 +37,7 @@ GAMMA = 0x9E3779B97F4A7C15
 STREAM_K, STREAM_V, STREAM_Q, STREAM_E, STREAM_QE, STREAM_LEN, STREAM_QE_NOISE = 1, 2, 3, 4, 5, 6, 7
 STREAM_IDX_Q, STREAM_IDX_K, STREAM_IDX_W = 8, 9, 10
 STREAM_NAT_Q, STREAM_NAT_K, STREAM_NAT_W = 11, 12, 13
+STREAM_GOLD_NOISE, STREAM_GOLD_REL, STREAM_GOLD_BOOST = 14, 15, 16
 M64 = (1 << 64) - 1
 
 
@@ -388,6 +389,11 @@ def host_lib() -> ctypes.CDLL:
                                         ctypes.c_void_p]
         lib.synth_kv_chunks.restype = None
         lib.synth_draws.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p]
+        lib.synth_golden_logits.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p,
+                                            ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                            ctypes.c_float, ctypes.c_float, ctypes.c_uint32, ctypes.c_uint32,
+                                            ctypes.c_void_p]
+        lib.synth_golden_logits.restype = None
         lib.synth_stream_key.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         lib.synth_stream_key.restype = ctypes.c_uint64
         _host_lib = lib
@@ -441,6 +447,11 @@ def dev_lib() -> ctypes.CDLL:
         lib.synth_read_device.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         lib.synth_read_device.restype = ctypes.c_int
         lib.synth_read_sink_words.restype = ctypes.c_int
+        lib.synth_fill_golden_device.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p,
+                                                 ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                                 ctypes.c_float, ctypes.c_float, ctypes.c_uint32, ctypes.c_uint32,
+                                                 ctypes.c_void_p, ctypes.c_void_p]
+        lib.synth_fill_golden_device.restype = ctypes.c_int
         _dev_lib = lib
     return _dev_lib
 
@@ -517,6 +528,107 @@ def device_inputs(prob: Problem, seed: int, device: str = "cuda", host: Optional
     for name in ("idx_q", "idx_w", "idx_k", "nat_q", "nat_w", "nat_k"):
         if name in h:
             out[name] = up(h[name])
+    return out
+
+
+# ------------------------------------------------------ golden-label inputs
+@dataclass
+class GoldenProblem:
+    """One window of the golden-label pipeline per sequence: tau decoding steps x
+    L layers x n_b entries of raw indexer logits.  The logits are N(0, 1)
+    noise scaled by 2^sigma_log2; a fraction rel_rate of each sequence's
+    entries is relevant, and a relevant entry gets +beta in a fraction
+    boost_rate of the (step, layer) rows."""
+    name: str
+    n_entries: List[int]
+    tau: int
+    layers: int
+    p_num: int = 3
+    p_den: int = 5
+    theta: int = 3
+    sigma_log2: int = 0
+    beta: float = 8.5
+    rel_rate: float = 1.0 / 256.0
+    boost_rate: float = 0.5
+
+    @property
+    def batch(self) -> int:
+        return len(self.n_entries)
+
+    @property
+    def entry_offsets(self) -> List[int]:
+        out, acc = [], 0
+        for n in self.n_entries:
+            out.append(acc)
+            acc += n
+        return out + [acc]
+
+    def logit_offset(self, b: int) -> int:
+        """First element of sequence b's block [tau][L][n_b] in the packed logits."""
+        return self.tau * self.layers * self.entry_offsets[b]
+
+    @property
+    def total_logits(self) -> int:
+        return self.tau * self.layers * self.entry_offsets[-1]
+
+
+def make_golden_problem(name: str) -> GoldenProblem:
+    """Golden-label presets.  Entries are compressed KV entries (4 tokens each):
+    the paper's training documents run from 16K to 512K tokens, so 4,096 to
+    131,072 entries, with tau = 64 steps and the 21 layers of its backbone."""
+    if name == "golden_tiny":
+        return GoldenProblem("golden_tiny", [1000], 4, 5, rel_rate=1.0 / 16.0, beta=5.0)
+    if name == "golden512k":
+        return GoldenProblem("golden512k", [131072], 64, 21)
+    if name == "golden_batch":
+        u = uniform53(stream_key(0, STREAM_LEN), 100, 8)
+        lo, hi = math.log(4096.0), math.log(131072.0)
+        return GoldenProblem("golden_batch", [int(math.exp(lo + (hi - lo) * float(x))) for x in u], 64, 21)
+    raise KeyError(name)
+
+
+GOLDEN_PRESETS = ("golden_tiny", "golden512k", "golden_batch")
+
+
+def _golden_args(gp: GoldenProblem, seed: int, b: int):
+    return (stream_key(seed, STREAM_GOLD_NOISE), stream_key(seed, STREAM_GOLD_REL), stream_key(seed, STREAM_GOLD_BOOST),
+            float(2.0 ** gp.sigma_log2), float(np.float32(gp.beta)), min(int(gp.rel_rate * 2 ** 32), 2 ** 32 - 1),
+            min(int(gp.boost_rate * 2 ** 32), 2 ** 32 - 1))
+
+
+def golden_table_f32() -> np.ndarray:
+    return np.ascontiguousarray(normal_table_f64().astype(np.float32))
+
+
+def golden_logits(gp: GoldenProblem, seed: int, b: int, steps: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Host logits of sequence b, [len(steps)][L][n_b] float32 (all tau steps by default)."""
+    kn, kr, kb, sigma, beta, rel, boost = _golden_args(gp, seed, b)
+    n, L = gp.n_entries[b], gp.layers
+    steps = list(range(gp.tau)) if steps is None else list(steps)
+    tab = golden_table_f32()
+    out = np.empty((len(steps), L, n), dtype=np.float32)
+    for j, i in enumerate(steps):
+        start = gp.logit_offset(b) + i * L * n
+        host_lib().synth_golden_logits(kn, kr, kb, tab.ctypes.data, start, L, n, b, sigma, beta, rel, boost,
+                                       out[j].ctypes.data)
+    return out
+
+
+def golden_logits_device(gp: GoldenProblem, seed: int, device: str = "cuda"):
+    """All logits of the problem on the device, packed [B]{[tau][L][n_b]} float32."""
+    import torch
+    tab = torch.from_numpy(golden_table_f32()).to(device)
+    out = torch.empty(gp.total_logits, dtype=torch.float32, device=device)
+    stream = torch.cuda.current_stream(device).cuda_stream
+    for b in range(gp.batch):
+        kn, kr, kb, sigma, beta, rel, boost = _golden_args(gp, seed, b)
+        off = gp.logit_offset(b)
+        rc = dev_lib().synth_fill_golden_device(kn, kr, kb, tab.data_ptr(), off, gp.tau * gp.layers,
+                                                gp.n_entries[b], b, sigma, beta, rel, boost,
+                                                out.data_ptr() + 4 * off, stream)
+        if rc != 0:
+            raise RuntimeError(f"synth_fill_golden_device failed with code {rc}")
+    torch.cuda.synchronize()
     return out
 
 

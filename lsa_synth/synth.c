@@ -54,3 +54,29 @@ void synth_kv_chunks(uint64_t key, const uint16_t* table, int32_t hkv, int32_t h
 void synth_draws(uint64_t key, uint64_t start, int64_t n, uint64_t* out) {
   for (int64_t i = 0; i < n; ++i) out[i] = synth_draw(key, start + (uint64_t)i);
 }
+
+/*
+ * Logits of the golden-label workload, rows x n entries starting at counter
+ * start (row r, entry s at counter start + r * n + s).  Every value is built
+ * from exact or single correctly rounded float32 operations, so the device
+ * fill produces the same bytes:
+ *   z    = table[draw >> 48] + ((draw >> 32) & 0xFFFF) * 2^-26
+ *   v    = z * sigma                          (sigma a power of two: exact)
+ *   v   += beta   when entry s of sequence b is relevant (a per-sequence draw
+ *                 below rel_thr) and boosted in this row (a per-element draw
+ *                 below boost_thr)
+ */
+void synth_golden_logits(uint64_t key_noise, uint64_t key_rel, uint64_t key_boost, const float* table,
+                         uint64_t start, int64_t rows, int64_t n, int32_t b, float sigma, float beta,
+                         uint32_t rel_thr, uint32_t boost_thr, float* out) {
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t s = 0; s < n; ++s) {
+      const uint64_t c = start + (uint64_t)(r * n + s);
+      const uint64_t d = synth_draw(key_noise, c);
+      const float z = table[d >> 48] + (float)((d >> 32) & 0xFFFFu) * 0x1p-26f;
+      float v = z * sigma;
+      const int relevant = (uint32_t)(synth_draw(key_rel, ((uint64_t)b << 32) | (uint64_t)s) >> 32) < rel_thr;
+      if (relevant && (uint32_t)(synth_draw(key_boost, c) >> 32) < boost_thr) v = v + beta;
+      out[r * n + s] = v;
+    }
+}

@@ -125,6 +125,37 @@ extern "C" int synth_copy_device(const void* src, void* dst, int64_t bytes, void
   return hipGetLastError() == hipSuccess ? 0 : 2;
 }
 
+// Golden-label logits: the same function as synth_golden_logits on the host,
+// one element per thread iteration.
+__global__ void __launch_bounds__(256)
+fill_golden(uint64_t key_noise, uint64_t key_rel, uint64_t key_boost, const float* __restrict__ table,
+            uint64_t start, int64_t total, int64_t n, int32_t b, float sigma, float beta, uint32_t rel_thr,
+            uint32_t boost_thr, float* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t c = start + (uint64_t)i;
+    const uint64_t d = mix64(key_noise + (c + 1ULL) * kGamma);
+    const float z = __fadd_rn(table[d >> 48], (float)((d >> 32) & 0xFFFFu) * 0x1p-26f);
+    float v = __fmul_rn(z, sigma);
+    const int64_t s = i % n;
+    const uint64_t rc = ((uint64_t)b << 32) | (uint64_t)s;
+    const bool relevant = (uint32_t)(mix64(key_rel + (rc + 1ULL) * kGamma) >> 32) < rel_thr;
+    if (relevant && (uint32_t)(mix64(key_boost + (c + 1ULL) * kGamma) >> 32) < boost_thr) v = __fadd_rn(v, beta);
+    out[i] = v;
+  }
+}
+
+extern "C" int synth_fill_golden_device(uint64_t key_noise, uint64_t key_rel, uint64_t key_boost, const float* table,
+                                        uint64_t start, int64_t rows, int64_t n, int32_t b, float sigma, float beta,
+                                        uint32_t rel_thr, uint32_t boost_thr, float* out, void* stream) {
+  if (!table || !out || rows <= 0 || n <= 0) return 1;
+  const int64_t total = rows * n;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(fill_golden, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, key_noise, key_rel,
+                     key_boost, table, start, total, n, b, sigma, beta, rel_thr, boost_thr, out);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
+
 // Returns 0 on success, 1 on a bad argument, 2 on a HIP launch error.
 extern "C" int synth_fill_kv_device(uint64_t key, const uint16_t* table, uint16_t* out,
                                     int64_t total_chunks, int32_t hkv, int32_t chunk,

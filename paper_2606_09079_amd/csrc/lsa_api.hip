@@ -408,6 +408,56 @@ lsa_status mirror_device_ptrs(const lsa_problem* p, const Plan& P, const uint16_
   return LSA_OK;
 }
 
+// The golden-label pipeline's geometry and workspace layout.
+struct GoldenPlan {
+  GoldenTable t;
+  int64_t row_words = 0;    // words of all row bitmaps
+  int64_t label_words = 0;  // words of the label bitmaps
+  size_t off_bits = 0, off_labels = 0, ws_total = 0;
+};
+
+lsa_status make_golden_plan(const lsa_golden* g, GoldenPlan* gp) {
+  if (g == nullptr) return fail(LSA_ERR_INVALID_ARG, "golden problem is NULL");
+  if (g->batch < 1 || g->batch > LSA_MAX_BATCH)
+    return fail(LSA_ERR_INVALID_ARG, "batch %d not in [1, %d]", g->batch, LSA_MAX_BATCH);
+  if (g->n_steps < 1) return fail(LSA_ERR_INVALID_ARG, "n_steps %d < 1", g->n_steps);
+  if (g->n_layers < 1 || g->n_layers > LSA_MAX_GOLDEN_LAYERS)
+    return fail(LSA_ERR_INVALID_ARG, "n_layers %d not in [1, %d]", g->n_layers, LSA_MAX_GOLDEN_LAYERS);
+  if (g->theta < 1 || g->theta > 64) return fail(LSA_ERR_INVALID_ARG, "theta %d not in [1, 64]", g->theta);
+  if (g->p_num < 1 || g->p_den < g->p_num || g->p_den > (1 << 30))
+    return fail(LSA_ERR_INVALID_ARG, "top-p %d / %d is not a fraction in (0, 1] with denominator <= 2^30",
+                g->p_num, g->p_den);
+  if (g->n_entries == nullptr) return fail(LSA_ERR_INVALID_ARG, "n_entries must be a host array of batch entries");
+  if ((int64_t)g->batch * g->n_steps * g->n_layers > INT32_MAX)
+    return fail(LSA_ERR_UNSUPPORTED, "too many rows for one launch");
+  GoldenTable& t = gp->t;
+  memset(&t, 0, sizeof t);
+  t.batch = g->batch;
+  const int64_t rows = (int64_t)g->n_steps * g->n_layers;
+  int64_t entries = 0, bits = 0, labels = 0;
+  for (int b = 0; b < g->batch; ++b) {
+    const int64_t n = g->n_entries[b];
+    if (n < 1 || n > LSA_MAX_GOLDEN_ENTRIES)
+      return fail(LSA_ERR_INVALID_ARG, "n_entries[%d] = %lld not in [1, %d]", b, (long long)n,
+                  LSA_MAX_GOLDEN_ENTRIES);
+    t.n[b] = (int32_t)n;
+    t.words[b] = (int32_t)((n + 31) / 32);
+    t.entry_off[b] = entries;
+    t.logit_off[b] = rows * entries;
+    t.bit_off[b] = bits;
+    t.label_word_off[b] = labels;
+    entries += n;
+    bits += rows * t.words[b];
+    labels += t.words[b];
+  }
+  gp->row_words = bits;
+  gp->label_words = labels;
+  gp->off_bits = 0;
+  gp->off_labels = align_up((size_t)bits * 4);
+  gp->ws_total = align_up(gp->off_labels + (size_t)labels * 4);
+  return LSA_OK;
+}
+
 }  // namespace
 }  // namespace lsa
 
@@ -866,6 +916,40 @@ lsa_status lsa_tier_attend(const lsa_problem* p, const lsa_tier* tr, const uint1
   if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
   LSA_TRY(check_ws(T.R, ws, ws_bytes));
   return run_attn(p, T.R, q, res_k, res_v, slot_idx, slot_count, softmax_scale, out, lse, ws, (hipStream_t)stream);
+}
+
+lsa_status lsa_golden_sizes(const lsa_golden* g, size_t* ws_bytes) {
+  GoldenPlan G;
+  LSA_TRY(make_golden_plan(g, &G));
+  if (ws_bytes != nullptr) *ws_bytes = G.ws_total;
+  return LSA_OK;
+}
+
+lsa_status lsa_golden_labels(const lsa_golden* g, const float* logits, int32_t* labels, int32_t* label_count,
+                             int32_t* nucleus_size, int32_t* golden_count, void* ws, size_t ws_bytes, void* stream) {
+  GoldenPlan G;
+  LSA_TRY(make_golden_plan(g, &G));
+  LSA_TRY(check_ptr(logits, "logits"));
+  LSA_TRY(check_ptr(labels, "labels"));
+  LSA_TRY(check_ptr(label_count, "label_count"));
+  if (nucleus_size != nullptr) LSA_TRY(check_ptr(nucleus_size, "nucleus_size"));
+  if (golden_count != nullptr) LSA_TRY(check_ptr(golden_count, "golden_count"));
+  if (ws_bytes < G.ws_total)
+    return fail(LSA_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, G.ws_total);
+  if (ws == nullptr || !aligned16(ws)) return fail(LSA_ERR_WORKSPACE, "workspace is NULL or not 16-byte aligned");
+  GoldenArgs a;
+  a.logits = logits;
+  a.bits = reinterpret_cast<uint32_t*>(at(ws, G.off_bits));
+  a.nucleus_size = nucleus_size;
+  a.p_num = g->p_num;
+  a.p_den = g->p_den;
+  a.tau = g->n_steps;
+  a.layers = g->n_layers;
+  a.theta = g->theta;
+  LSA_HIP(launch_golden(G.t, a, reinterpret_cast<uint32_t*>(at(ws, G.off_labels)), G.label_words, labels,
+                        label_count, golden_count, (hipStream_t)stream),
+          "golden-label launch");
+  return LSA_OK;
 }
 
 }  // extern "C"

@@ -169,6 +169,26 @@ hipError_t launch_tier_plan(const SeqTable& t, const TierArgs& a, hipStream_t s)
 hipError_t launch_tier_fetch(const SeqTable& t, const TierFetchArgs& a, int32_t chunk_size, hipStream_t s);
 hipError_t launch_tier_reset(int32_t* owner, int64_t n, hipStream_t s);
 
+// Golden-label pipeline: per-sequence geometry (by value) and launch arguments.
+struct GoldenTable {
+  int32_t batch;
+  int32_t n[LSA_MAX_BATCH];                // entries n_b
+  int32_t words[LSA_MAX_BATCH];            // 32-bit bitmap words per row, ceil(n_b / 32)
+  int64_t entry_off[LSA_MAX_BATCH];        // first entry of sequence b (labels)
+  int64_t logit_off[LSA_MAX_BATCH];        // first logit of sequence b, tau * L * entry_off[b]
+  int64_t bit_off[LSA_MAX_BATCH];          // first word of sequence b's row bitmaps
+  int64_t label_word_off[LSA_MAX_BATCH];   // first word of sequence b's label bitmap
+};
+struct GoldenArgs {
+  const float* logits;
+  uint32_t* bits;          // [sum_b tau * L * words_b] top-p membership per row
+  int32_t* nucleus_size;   // nullable [B][tau][L]
+  int64_t p_num, p_den;
+  int32_t tau, layers, theta;
+};
+hipError_t launch_golden(const GoldenTable& gt, const GoldenArgs& a, uint32_t* label_bits, int64_t label_words,
+                         int32_t* labels, int32_t* label_count, int32_t* golden_count, hipStream_t s);
+
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 
 }  // namespace lsa

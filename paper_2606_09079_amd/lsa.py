@@ -32,7 +32,8 @@ EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_valida
            "lsa_max_keep", "lsa_workspace_size", "lsa_workspace_init", "lsa_score_chunks", "lsa_topk_chunks",
            "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
            "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step", "lsa_tier_sizes", "lsa_tier_reset",
-           "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_fetch_dma", "lsa_tier_attend")
+           "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_fetch_dma", "lsa_tier_attend",
+           "lsa_golden_sizes", "lsa_golden_labels")
 
 
 class lsa_problem(ctypes.Structure):
@@ -59,6 +60,12 @@ class lsa_two_level(ctypes.Structure):
 class lsa_tier(ctypes.Structure):
     _fields_ = [("slots", ctypes.POINTER(ctypes.c_int32)), ("reserved", ctypes.c_int32),
                 ("reserved2", ctypes.c_int32)]
+
+
+class lsa_golden(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_steps", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("theta", ctypes.c_int32), ("p_num", ctypes.c_int32), ("p_den", ctypes.c_int32),
+                ("n_entries", ctypes.POINTER(ctypes.c_int64))]
 
 
 def _load() -> ctypes.CDLL:
@@ -102,6 +109,9 @@ def _load() -> ctypes.CDLL:
     lib.lsa_tier_fetch.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P]
     lib.lsa_tier_fetch_dma.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P]
     lib.lsa_tier_attend.argtypes = [pp, rp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
+    gp = ctypes.POINTER(lsa_golden)
+    lib.lsa_golden_sizes.argtypes = [gp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.lsa_golden_labels.argtypes = [gp, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
     for name in EXPORTS[3:]:
         getattr(lib, name).restype = ctypes.c_int
     if lib.lsa_abi_version() != 1:
@@ -176,6 +186,26 @@ class Tier:
     def __init__(self, slots: Sequence[int]):
         self._slots = (ctypes.c_int32 * max(len(slots), 1))(*slots)
         self.c = lsa_tier(ctypes.cast(self._slots, ctypes.POINTER(ctypes.c_int32)), 0, 0)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+class Golden:
+    """Golden-label pipeline shape (mirrors ``lsa_golden``; keeps its host array alive)."""
+
+    def __init__(self, n_entries: Sequence[int], n_steps: int, n_layers: int, theta: int = 3, p_num: int = 3,
+                 p_den: int = 5):
+        self._n = (ctypes.c_int64 * max(len(n_entries), 1))(*n_entries)
+        self.c = lsa_golden(len(n_entries), n_steps, n_layers, theta, p_num, p_den,
+                            ctypes.cast(self._n, ctypes.POINTER(ctypes.c_int64)))
+
+    @classmethod
+    def from_synth(cls, gp, **kw) -> "Golden":
+        args = dict(theta=gp.theta, p_num=gp.p_num, p_den=gp.p_den)
+        args.update(kw)
+        return cls(gp.n_entries, gp.tau, gp.layers, **args)
 
     @property
     def ref(self):
@@ -339,3 +369,16 @@ def lsa_tier_attend(p: Problem, tr: Tier, q, res_k, res_v, slot_idx, slot_count,
     _check(LIB.lsa_tier_attend(p.ref, tr.ref, _ptr(q), _ptr(res_k), _ptr(res_v), _ptr(slot_idx), _ptr(slot_count),
                                float(softmax_scale), _ptr(out), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)),
            "lsa_tier_attend")
+
+
+def lsa_golden_sizes(g: Golden) -> int:
+    """Workspace bytes of lsa_golden_labels."""
+    w = ctypes.c_size_t()
+    _check(LIB.lsa_golden_sizes(g.ref, ctypes.byref(w)), "lsa_golden_sizes")
+    return w.value
+
+
+def lsa_golden_labels(g: Golden, logits, labels, label_count, nucleus_size=None, golden_count=None, ws=None,
+                      ws_bytes: int = 0, stream=None) -> None:
+    _check(LIB.lsa_golden_labels(g.ref, _ptr(logits), _ptr(labels), _ptr(label_count), _ptr(nucleus_size),
+                                 _ptr(golden_count), _ptr(ws), ws_bytes, _stream(stream)), "lsa_golden_labels")

@@ -260,3 +260,28 @@ def test_tier_dma_validates_the_host_copy_list_before_copying():
     cnt = np.zeros(2, dtype=np.int32)
     assert lib.lsa_tier_fetch_dma(p.ref, T.ref, FAKE, FAKE, None, cnt.ctypes.data, FAKE, FAKE, None) \
         == B.LSA_ERR_INVALID_ARG
+
+
+def test_golden_sizes_and_validation():
+    g = L.Golden([1000, 70], 4, 21)
+    ws = L.lsa_golden_sizes(g)
+    rows = 4 * 21
+    bits = rows * (32 + 3) * 4
+    assert ws == (bits + 255) // 256 * 256 + ((32 + 3) * 4 + 255) // 256 * 256
+    lib = L.LIB
+    bad = [dict(n_entries=[0], n_steps=4, n_layers=21), dict(n_entries=[4194305], n_steps=4, n_layers=21),
+           dict(n_entries=[10], n_steps=0, n_layers=21), dict(n_entries=[10], n_steps=4, n_layers=0),
+           dict(n_entries=[10], n_steps=4, n_layers=64), dict(n_entries=[10], n_steps=4, n_layers=21, theta=0),
+           dict(n_entries=[10], n_steps=4, n_layers=21, theta=65),
+           dict(n_entries=[10], n_steps=4, n_layers=21, p_num=0, p_den=5),
+           dict(n_entries=[10], n_steps=4, n_layers=21, p_num=6, p_den=5),
+           dict(n_entries=[10], n_steps=4, n_layers=21, p_num=1, p_den=(1 << 30) + 1),
+           dict(n_entries=[], n_steps=4, n_layers=21)]
+    for kw in bad:
+        gb = L.Golden(**kw)
+        assert lib.lsa_golden_sizes(gb.ref, None) == B.LSA_ERR_INVALID_ARG, kw
+    assert lib.lsa_golden_sizes(None, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_golden_labels(g.ref, None, FAKE, FAKE, None, None, FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_golden_labels(g.ref, FAKE, FAKE, FAKE, FAKE + 4, None, FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_golden_labels(g.ref, FAKE, FAKE, FAKE, None, None, FAKE, ws - 1, None) == B.LSA_ERR_WORKSPACE
+    assert lib.lsa_golden_labels(g.ref, FAKE, FAKE, FAKE, None, None, None, ws, None) == B.LSA_ERR_WORKSPACE
