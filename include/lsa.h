@@ -385,9 +385,10 @@ lsa_status lsa_tier_attend(const lsa_problem* p, const lsa_tier* tr, const uint1
  * V_s = the number of layers whose set holds s (Eq. 9) and the golden set
  * {s : V_s >= theta} (Eq. 10).  Per sequence: the label set, the union of the
  * golden sets of the tau steps (Eq. 11).
- * The decision is exact: weights exp(S - max S) come from one fixed float64
- * method (Cody-Waite reduction, Taylor series of degree 13 with fused
- * multiply-adds) as integers floor(w * 2^40), and a set reaches p when
+ * The decision is exact: weights exp(S - max S) come from one fixed float32
+ * method (S - max S rounded to float32, Cody-Waite reduction, Taylor series
+ * of degree 7 with fused multiply-adds) as integers floor(w * 2^40), and a set
+ * reaches p when
  * (its mass) * p_den >= p_num * (total mass) in integers.  Logits must be
  * finite.
  * Outputs (device): labels [sum_b n_b] int32, sequence b's label ids ascending

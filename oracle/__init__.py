@@ -72,8 +72,8 @@ def bind(path: str) -> ctypes.CDLL:
     L.oracle_attention_tokens.restype = ctypes.c_int
     L.oracle_two_level.argtypes = [_P, _I64, _P, _I64, _I64, _I64, _I64, _P]
     L.oracle_two_level.restype = _I64
-    L.oracle_exp_fixed.argtypes = [_F64]
-    L.oracle_exp_fixed.restype = _F64
+    L.oracle_exp_fixed.argtypes = [ctypes.c_float]
+    L.oracle_exp_fixed.restype = ctypes.c_float
     L.oracle_top_p.argtypes = [_P, _I64, _I64, _I64, _P]
     L.oracle_top_p.restype = _I64
     L.oracle_golden_labels.argtypes = [_P, _I32, _I32, _I64, _I64, _I64, _I32, _P, _P, _P]
@@ -284,8 +284,8 @@ def tier_plan(owner: Sequence[int], old_slots: Sequence[int], kept: Sequence[int
 
 # ---------------------------------------------------------------- O4 step
 def exp_fixed(x: float) -> float:
-    """exp(x) for x <= 0 by the oracle's fixed float64 method (Cody-Waite reduction, degree-13 Taylor series)."""
-    return float(lib().oracle_exp_fixed(float(x)))
+    """exp(x) for x <= 0 by the oracle's fixed float32 method (Cody-Waite reduction, degree-7 Taylor series)."""
+    return float(lib().oracle_exp_fixed(float(np.float32(x))))
 
 
 def top_p(S: np.ndarray, p_num: int, p_den: int):

@@ -42,7 +42,7 @@
  *    index); Eq. 8 as printed (cumulative mass <= p) would leave the set empty
  *    whenever the most probable entry alone exceeds p.  Probabilities are held
  *    as whole multiples of 2^-40 of the largest one, with the exponential
- *    evaluated by one fixed float64 method (below), so that which entries
+ *    evaluated by one fixed float32 method (below), so that which entries
  *    reach the mass is an exact integer decision.
  */
 #include <math.h>
@@ -359,31 +359,31 @@ int64_t oracle_two_level(const int32_t* recalled, int64_t m, const double* nativ
 /* ------------------------------------------------------------ golden labels */
 
 /*
- * exp(x) for x <= 0 by a fixed float64 method, so that the result is one
- * determined double: Cody and Waite's reduction x = k ln2 + r with k the
- * nearest integer to x / ln2 and ln2 split into a high part with trailing zero
- * bits and a low part (the split fdlibm uses), the Taylor series of e^r to
- * degree 13 (|r| <= ln2 / 2, truncation below 4e-18) in Horner form with
- * fused multiply-adds, and an exact scaling by 2^k.  Below -64 the result is
- * 0 (its weight would be far below 2^-40 anyway).
+ * exp(x) for x <= 0 by a fixed float32 method, so that the result is one
+ * determined float on any IEEE machine: Cody and Waite's reduction
+ * x = k ln2 + r with k the nearest integer to x / ln2 and ln2 split into a
+ * high part with trailing zero bits and a low part (the split fdlibm's expf
+ * uses), the Taylor series of e^r to degree 7 (|r| <= ln2 / 2, truncation
+ * below 6e-9 relative) in Horner form with fused multiply-adds, and an exact
+ * scaling by 2^k.  Below -64 the result is 0 (its weight would be far below
+ * 2^-40 anyway).  float32 is the precision in which the GPU takes the same
+ * decision.
  */
-double oracle_exp_fixed(double x) {
-  if (x > 0.0) x = 0.0;
-  if (x < -64.0) return 0.0;
-  const double log2e = 1.4426950408889634;
-  const double ln2_hi = 6.93147180369123816490e-01;
-  const double ln2_lo = 1.90821492927058770002e-10;
-  const double k = rint(x * log2e);
-  double r = fma(-k, ln2_hi, x);
-  r = fma(-k, ln2_lo, r);
-  /* 1 / j! for j = 13 down to 0 */
-  const double inv_fact[14] = {1.0 / 6227020800.0, 1.0 / 479001600.0, 1.0 / 39916800.0, 1.0 / 3628800.0,
-                               1.0 / 362880.0,     1.0 / 40320.0,     1.0 / 5040.0,      1.0 / 720.0,
-                               1.0 / 120.0,        1.0 / 24.0,        1.0 / 6.0,         1.0 / 2.0,
-                               1.0,                1.0};
-  double p = inv_fact[0];
-  for (int j = 1; j < 14; ++j) p = fma(p, r, inv_fact[j]);
-  return ldexp(p, (int)k);
+float oracle_exp_fixed(float x) {
+  if (x > 0.0f) x = 0.0f;
+  if (x < -64.0f) return 0.0f;
+  const float log2e = 1.44269502e+00f;
+  const float ln2_hi = 6.9314575195e-01f;
+  const float ln2_lo = 1.4286067653e-06f;
+  const float k = rintf(x * log2e);
+  float r = fmaf(-k, ln2_hi, x);
+  r = fmaf(-k, ln2_lo, r);
+  /* 1 / j! for j = 7 down to 0 */
+  const float inv_fact[8] = {1.0f / 5040.0f, 1.0f / 720.0f, 1.0f / 120.0f, 1.0f / 24.0f,
+                             1.0f / 6.0f,    1.0f / 2.0f,   1.0f,          1.0f};
+  float p = inv_fact[0];
+  for (int j = 1; j < 8; ++j) p = fmaf(p, r, inv_fact[j]);
+  return ldexpf(p, (int)k);
 }
 
 typedef struct { float s; int64_t c; } logit_entry;
@@ -414,8 +414,8 @@ int64_t oracle_top_p(const float* S, int64_t n, int64_t p_num, int64_t p_den, ui
   if (!q || !v) { free(q); free(v); return -1; }
   uint64_t Z = 0;
   for (int64_t s = 0; s < n; ++s) {
-    const double w = oracle_exp_fixed((double)S[s] - (double)m);
-    q[s] = (uint64_t)(w * 1099511627776.0); /* floor(w * 2^40) */
+    const float w = oracle_exp_fixed(S[s] - m);
+    q[s] = (uint64_t)((double)w * 1099511627776.0); /* floor(w * 2^40) */
     Z += q[s];
     v[s].s = S[s];
     v[s].c = s;

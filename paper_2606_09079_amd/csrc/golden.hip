@@ -7,13 +7,13 @@
 // the union of the golden sets over the window (Eq. 11).
 //
 // The top-p decision is exact: a weight is exp(S - max S) evaluated by one
-// fixed float64 method (Cody-Waite reduction with the fdlibm split of ln 2,
-// Taylor series of degree 13 in Horner form with fused multiply-adds), held
-// as the integer q = floor(w * 2^40); masses are integer sums, so their order
+// fixed float32 method (Cody-Waite reduction with the fdlibm split of ln 2,
+// Taylor series of degree 7 in Horner form with fused multiply-adds), held as
+// the integer q = floor(w * 2^40); masses are integer sums, so their order
 // does not matter, and a set reaches p = num / den when
 // (its mass) * den >= num * Z in 128-bit integers.
 //
-// golden_row_kernel -- one 1024-thread workgroup per (step, layer) row, three
+// golden_row_kernel -- one 512-thread workgroup per (step, layer) row, three
 //   passes over the row: (1) the maximum; (2) a 4096-bin LDS histogram of the
 //   masses by the top 12 bits of each logit's order key, whose descending
 //   scan finds the bin where the cumulative mass reaches p; (3) the row's
@@ -32,12 +32,14 @@
 namespace lsa {
 namespace {
 
-constexpr int kThreads = 1024;
+constexpr int kThreads = 512;   // three rows per compute unit at a time
 constexpr int kWaves = kThreads / 64;
 constexpr int kBins = 4096;     // first digit: top 12 bits of the order key
 constexpr int kSubBins = 1024;  // two more digits of 10 bits
-constexpr int kCand = 4096;     // entries of the threshold bin staged in LDS
-constexpr int kUnroll = 8;      // 64-entry groups per wavefront per round
+constexpr int kBinsPerThread = kBins / kThreads;
+constexpr int kSubPerThread = kSubBins / kThreads;
+constexpr int kCand = 1024;     // entries of the threshold bin staged in LDS
+constexpr int kUnroll = 16;     // 64-entry groups per wavefront per round
 
 struct u128 {
   uint64_t hi, lo;
@@ -46,36 +48,36 @@ struct u128 {
 __device__ __forceinline__ u128 mul64(uint64_t a, uint64_t b) { return {__umul64hi(a, b), a * b}; }
 __device__ __forceinline__ bool ge128(u128 a, u128 b) { return a.hi > b.hi || (a.hi == b.hi && a.lo >= b.lo); }
 
-// exp(x) for x <= 0 by the fixed float64 method described above.
-__device__ __forceinline__ double exp_fixed(double x) {
-  x = x > 0.0 ? 0.0 : x;
-  if (x < -64.0) return 0.0;
-  const double log2e = 1.4426950408889634;
-  const double ln2_hi = 6.93147180369123816490e-01;
-  const double ln2_lo = 1.90821492927058770002e-10;
-  const double k = __builtin_rint(x * log2e);
-  double r = __builtin_fma(-k, ln2_hi, x);
-  r = __builtin_fma(-k, ln2_lo, r);
-  double p = 1.0 / 6227020800.0;
-  p = __builtin_fma(p, r, 1.0 / 479001600.0);
-  p = __builtin_fma(p, r, 1.0 / 39916800.0);
-  p = __builtin_fma(p, r, 1.0 / 3628800.0);
-  p = __builtin_fma(p, r, 1.0 / 362880.0);
-  p = __builtin_fma(p, r, 1.0 / 40320.0);
-  p = __builtin_fma(p, r, 1.0 / 5040.0);
-  p = __builtin_fma(p, r, 1.0 / 720.0);
-  p = __builtin_fma(p, r, 1.0 / 120.0);
-  p = __builtin_fma(p, r, 1.0 / 24.0);
-  p = __builtin_fma(p, r, 1.0 / 6.0);
-  p = __builtin_fma(p, r, 1.0 / 2.0);
-  p = __builtin_fma(p, r, 1.0);
-  p = __builtin_fma(p, r, 1.0);
-  return __builtin_ldexp(p, (int)k);
+// exp(x) for x <= 0 by the fixed float32 method described above.
+__device__ __forceinline__ float exp_fixed(float x) {
+  x = x > 0.0f ? 0.0f : x;
+  if (x < -64.0f) return 0.0f;
+  const float log2e = 1.44269502e+00f;
+  const float ln2_hi = 6.9314575195e-01f;
+  const float ln2_lo = 1.4286067653e-06f;
+  const float k = __builtin_rintf(x * log2e);
+  float r = __builtin_fmaf(-k, ln2_hi, x);
+  r = __builtin_fmaf(-k, ln2_lo, r);
+  float p = 1.0f / 5040.0f;
+  p = __builtin_fmaf(p, r, 1.0f / 720.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 120.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 24.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 6.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 2.0f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  return __builtin_ldexpf(p, (int)k);
 }
 
-// Weight of a logit in units of 2^-40 of the largest weight.
+// Weight of a logit in units of 2^-40 of the largest weight: floor(w * 2^40)
+// taken exactly from w's bits, w = M 2^(E - 23) with a 24-bit mantissa M and
+// -93 <= E <= 0 (w is 0 or normal), so that floor(w 2^40) = M shifted by E + 17.
 __device__ __forceinline__ uint64_t mass_of(float s, float m) {
-  return (uint64_t)(exp_fixed((double)s - (double)m) * 1099511627776.0);
+  const uint32_t bits = __float_as_uint(exp_fixed(__fsub_rn(s, m)));
+  if (bits == 0u) return 0ull;
+  const int sh = (int)(bits >> 23) - 127 + 17;
+  const uint64_t M = (uint64_t)((bits & 0x7FFFFFu) | 0x800000u);
+  return sh >= 0 ? M << sh : (sh > -24 ? M >> -sh : 0ull);
 }
 
 __device__ __forceinline__ uint32_t key_of(float f) { return order_key<kKeysFromF32>(__float_as_uint(f)); }
@@ -176,11 +178,12 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
   }
   __syncthreads();
 
-  // descending scan of the bins: thread t owns bins 4095 - 4t .. 4092 - 4t
-  uint64_t own[4], own_sum = 0;
+  // descending scan of the bins: thread t owns the kBinsPerThread bins below
+  // kBins - 1 - kBinsPerThread * t
+  uint64_t own[kBinsPerThread], own_sum = 0;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    own[j] = hist[kBins - 1 - 4 * tid - j];
+  for (int j = 0; j < kBinsPerThread; ++j) {
+    own[j] = hist[kBins - 1 - kBinsPerThread * tid - j];
     own_sum += own[j];
   }
   uint64_t Z;
@@ -188,9 +191,9 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
   const u128 need = mul64(Z, (uint64_t)a.p_num);
   const uint64_t den = (uint64_t)a.p_den;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < kBinsPerThread; ++j) {
     if (!ge128(mul64(before, den), need) && ge128(mul64(before + own[j], den), need)) {
-      sh_digit = (uint32_t)(kBins - 1 - 4 * tid - j);
+      sh_digit = (uint32_t)(kBins - 1 - kBinsPerThread * tid - j);
       sh_above = before;
     }
     before += own[j];
@@ -208,6 +211,9 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
       const int e = entry(base, u);
       v[u] = e < n ? S[e] : -INFINITY;
     }
+    // the wavefront's kUnroll groups are 2 * kUnroll consecutive bitmap
+    // words; lane j < 2 * kUnroll collects word j and stores it
+    uint32_t word = 0u;
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int e = entry(base, u);
@@ -215,9 +221,7 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
       const bool valid = e < n;
       const uint64_t in = __ballot(valid && (key >> 20) > bstar);
       const uint64_t cnd = __ballot(valid && (key >> 20) == bstar);
-      const int g = (base >> 6) + wave * kUnroll + u;  // 64-entry group
-      if (lane == 0 && 2 * g < words) bm[2 * g] = (uint32_t)in;
-      if (lane == 1 && 2 * g + 1 < words) bm[2 * g + 1] = (uint32_t)(in >> 32);
+      word = (lane == 2 * u) ? (uint32_t)in : (lane == 2 * u + 1) ? (uint32_t)(in >> 32) : word;
       n_in += lane == 0 ? (uint32_t)__popcll(in) : 0u;
       if (cnd) {
         uint32_t first = 0;
@@ -232,6 +236,8 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
         }
       }
     }
+    const int w0 = (base >> 5) + wave * 2 * kUnroll;  // first word of this wavefront's groups
+    if (lane < 2 * kUnroll && w0 + lane < words) bm[w0 + lane] = word;
   }
   n_in = wave_reduce(n_in, [](uint32_t x, uint32_t y) { return x + y; });
   if (lane == 0) wave_tot[wave] = n_in;
@@ -273,12 +279,23 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
       atomicAdd(&sub_cnt[d], 1u);
     });
     __syncthreads();
-    const uint64_t mine = hist[kSubBins - 1 - tid];  // descending: thread t owns digit 1023 - t
+    // descending: thread t owns the kSubPerThread digits below 1023 - kSubPerThread * t
+    uint64_t mine[kSubPerThread], mine_sum = 0;
+#pragma unroll
+    for (int j = 0; j < kSubPerThread; ++j) {
+      mine[j] = hist[kSubBins - 1 - kSubPerThread * tid - j];
+      mine_sum += mine[j];
+    }
     uint64_t tot;
-    const uint64_t ex = above + block_scan_u64(mine, wave_tot, &tot);
-    if (sub_cnt[kSubBins - 1 - tid] != 0u && !ge128(mul64(ex, den), need) && ge128(mul64(ex + mine, den), need)) {
-      sh_digit = (uint32_t)(kSubBins - 1 - tid);
-      sh_above = ex;
+    uint64_t ex = above + block_scan_u64(mine_sum, wave_tot, &tot);
+#pragma unroll
+    for (int j = 0; j < kSubPerThread; ++j) {
+      const int d = kSubBins - 1 - kSubPerThread * tid - j;
+      if (sub_cnt[d] != 0u && !ge128(mul64(ex, den), need) && ge128(mul64(ex + mine[j], den), need)) {
+        sh_digit = (uint32_t)d;
+        sh_above = ex;
+      }
+      ex += mine[j];
     }
     __syncthreads();
     prefix = (prefix << 10) | sh_digit;

@@ -469,12 +469,13 @@ def pin_golden_worked_example():
 
 
 def pin_exp_fixed_accuracy():
-    """The oracle's fixed exponential against numpy's exp: within 2^-50 relative
-    on [-64, 0], exactly 1 at 0, exactly 2^-j at -j ln 2 rounded, 0 below -64."""
-    xs = np.concatenate([-np.linspace(0.0, 64.0, 4001), -np.logspace(-300, 1.8, 400), [-0.34657359, -0.34657360]])
-    for x in xs:
+    """The oracle's fixed float32 exponential against the float64 exp of the
+    same float32 argument: within 3 * 2^-24 relative (a few float32 rounding
+    steps) on [-64, 0], exactly 1 at 0, 0 below -64."""
+    xs = np.concatenate([-np.linspace(0.0, 64.0, 4001), -np.logspace(-40, 1.8, 400), [-0.34657359, -0.34657360]])
+    for x in xs.astype(np.float32):
         got, want = oracle.exp_fixed(float(x)), math.exp(float(x))
-        assert abs(got - want) <= 2.0 ** -50 * want, (x, got, want)
+        assert abs(got - want) <= 3.0 * 2.0 ** -24 * want, (x, got, want)
     assert oracle.exp_fixed(0.0) == 1.0
     assert oracle.exp_fixed(-64.5) == 0.0 and oracle.exp_fixed(-1000.0) == 0.0
 
@@ -492,8 +493,9 @@ def _numpy_nucleus(S: np.ndarray, p: float):
 
 def pin_top_p_library_softmax():
     """Random rows against numpy's softmax, sort and cumulative sum.  The two
-    may differ only where numpy's cumulative mass sits within 1e-9 of p at the
-    cut (the oracle holds masses in units of 2^-40 of the largest)."""
+    may differ only where numpy's cumulative mass sits within 1e-6 of p at the
+    cut (the oracle's weights are float32, held in units of 2^-40 of the
+    largest)."""
     rng = np.random.default_rng(41)
     for trial in range(300):
         n = int(rng.integers(1, 3000))
@@ -508,7 +510,7 @@ def pin_top_p_library_softmax():
         assert size == len(got)
         if got != want:
             k = len(want)
-            near = abs(cum[k - 1] - num / den) <= 1e-9 or (k >= 2 and abs(cum[k - 2] - num / den) <= 1e-9) \
+            near = abs(cum[k - 1] - num / den) <= 1e-6 or (k >= 2 and abs(cum[k - 2] - num / den) <= 1e-6) \
                 or (num == den and S.max() - S.min() > 27.0)
             assert near, (trial, n, scale, len(got), len(want))
 
@@ -535,14 +537,16 @@ def pin_top_p_bruteforce():
             key = (len(idx), -mass, idx)
             if best is None or key < best[0]:
                 best = (key, idx)
-        # skip rows where some subset's mass lies within float rounding of p
+        # skip rows where some subset's mass lies within float rounding of p,
+        # exactly on it included: logits ln(w) round, so such a mass can land on
+        # either side (equal logits, whose masses are exact, are pinned below)
         masses = {Fraction(sum(wts[s] for s in range(n) if m >> s & 1), tot) for m in range(1 << n)}
-        if any(0 < abs(float(x - p)) < 1e-6 for x in masses):
+        if any(abs(float(x - p)) < 1e-6 for x in masses):
             continue
         mark, size = oracle.top_p(_golden_logits(wts), num, den)
         assert np.nonzero(mark)[0].tolist() == best[1], (wts, num, den, best[1])
         checked += 1
-    assert checked > 200
+    assert checked > 150
 
 
 def pin_top_p_boundaries():

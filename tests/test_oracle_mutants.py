@@ -27,9 +27,9 @@ MUTANTS = {
                                    "  if (x->s > y->s) return 1;\n  if (x->s < y->s) return -1;\n"
                                    "  return (x->c > y->c) - (x->c < y->c);\n}\n\n/*\n * Top-p set"),
     "top_p_mass_not_summed": ("    Z += q[s];\n", "    Z = q[s];\n"),
-    "exp_fixed_no_low_part": ("  r = fma(-k, ln2_lo, r);\n", ""),
-    "exp_fixed_short_series": ("for (int j = 1; j < 14; ++j) p = fma(p, r, inv_fact[j]);",
-                               "for (int j = 1; j < 13; ++j) p = fma(p, r, inv_fact[j]);"),
+    "exp_fixed_no_low_part": ("  r = fmaf(-k, ln2_lo, r);\n", ""),
+    "exp_fixed_short_series": ("for (int j = 1; j < 8; ++j) p = fmaf(p, r, inv_fact[j]);",
+                               "for (int j = 1; j < 7; ++j) p = fmaf(p, r, inv_fact[j]);"),
     "golden_vote_strict": ("if (votes[s] >= theta) {", "if (votes[s] > theta) {"),
     "golden_union_last_step": ("    memset(votes, 0, (size_t)n * sizeof *votes);\n",
                                "    memset(votes, 0, (size_t)n * sizeof *votes);\n    memset(label, 0, (size_t)n);\n"),
