@@ -128,6 +128,11 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
   __shared__ uint64_t sh_above;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (blockIdx.x == 0) {  // the label bitmap and golden-set sizes start at zero (the vote kernel runs after)
+    for (int64_t i = tid; i < a.label_words; i += kThreads) a.label_bits[i] = 0u;
+    if (a.golden_count != nullptr)
+      for (int64_t i = tid; i < (int64_t)gt.batch * a.tau; i += kThreads) a.golden_count[i] = 0;
+  }
   const int rows_per_seq = a.tau * a.layers;
   const int b = blockIdx.x / rows_per_seq, row = blockIdx.x % rows_per_seq;
   const int n = gt.n[b], words = gt.words[b];
@@ -358,13 +363,20 @@ golden_vote_kernel(GoldenTable gt, GoldenArgs a, uint32_t* __restrict__ label_bi
   if (w < words) {
     uint32_t c[kCountBits] = {};
     const uint32_t* src = a.bits + gt.bit_off[b] + (int64_t)i * a.layers * words + w;
-    for (int l = 0; l < a.layers; ++l) {
-      uint32_t carry = src[(int64_t)l * words];
+    // the layers' words eight at a time, every load of a batch in flight at once
+    for (int l0 = 0; l0 < a.layers; l0 += 8) {
+      uint32_t x[8];
 #pragma unroll
-      for (int k = 0; k < kCountBits; ++k) {
-        const uint32_t t = c[k] & carry;
-        c[k] ^= carry;
-        carry = t;
+      for (int j = 0; j < 8; ++j) x[j] = l0 + j < a.layers ? src[(int64_t)(l0 + j) * words] : 0u;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        uint32_t carry = x[j];
+#pragma unroll
+        for (int k = 0; k < kCountBits; ++k) {
+          const uint32_t t = c[k] & carry;
+          c[k] ^= carry;
+          carry = t;
+        }
       }
     }
     // count >= theta, bit-sliced, from the most significant bit down
@@ -413,20 +425,15 @@ golden_compact_kernel(GoldenTable gt, const uint32_t* __restrict__ label_bits, i
   if (tid == 0) label_count[b] = (int32_t)total;
 }
 
-__global__ void __launch_bounds__(256) golden_zero_kernel(uint32_t* p, int64_t n, int32_t* q, int64_t nq) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0u;
-  if (q != nullptr)
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nq; i += (int64_t)gridDim.x * 256) q[i] = 0;
-}
-
 }  // namespace
 
 hipError_t launch_golden(const GoldenTable& gt, const GoldenArgs& a, uint32_t* label_bits, int64_t label_words,
                          int32_t* labels, int32_t* label_count, int32_t* golden_count, hipStream_t s) {
-  const int64_t zero_blocks = std::min<int64_t>(std::max<int64_t>((label_words + 255) / 256, 1), 1024);
-  hipLaunchKernelGGL(golden_zero_kernel, dim3((unsigned)zero_blocks), dim3(256), 0, s, label_bits, label_words,
-                     golden_count, (int64_t)gt.batch * a.tau);
-  hipLaunchKernelGGL(golden_row_kernel, dim3((unsigned)(gt.batch * a.tau * a.layers)), dim3(kThreads), 0, s, gt, a);
+  GoldenArgs ra = a;
+  ra.label_bits = label_bits;
+  ra.label_words = label_words;
+  ra.golden_count = golden_count;
+  hipLaunchKernelGGL(golden_row_kernel, dim3((unsigned)(gt.batch * a.tau * a.layers)), dim3(kThreads), 0, s, gt, ra);
   int max_words = 0;
   for (int b = 0; b < gt.batch; ++b) max_words = std::max(max_words, gt.words[b]);
   hipLaunchKernelGGL(golden_vote_kernel, dim3((unsigned)((max_words + 255) / 256), (unsigned)a.tau, (unsigned)gt.batch),

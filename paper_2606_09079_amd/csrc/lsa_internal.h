@@ -183,6 +183,9 @@ struct GoldenArgs {
   const float* logits;
   uint32_t* bits;          // [sum_b tau * L * words_b] top-p membership per row
   int32_t* nucleus_size;   // nullable [B][tau][L]
+  uint32_t* label_bits = nullptr;    // [label_words] zeroed by the row kernel's first workgroup
+  int64_t label_words = 0;
+  int32_t* golden_count = nullptr;   // nullable [B][tau], zeroed likewise
   int64_t p_num, p_den;
   int32_t tau, layers, theta;
 };
