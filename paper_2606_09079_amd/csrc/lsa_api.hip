@@ -47,7 +47,7 @@ struct Plan {
   int32_t rec_pitch = 0;
   // workspace layout (byte offsets)
   size_t off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0;
-  size_t off_rec = 0, off_rec_cnt = 0, off_nat = 0;
+  size_t off_rec = 0, off_rec_cnt = 0, off_nat = 0, off_nat_all = 0;
   size_t ws_total = 0;
 };
 
@@ -207,6 +207,8 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = n
     off = align_up(off + (size_t)B * 4);
     P.off_nat = off;
     off = align_up(off + (size_t)B * P.rec_pitch * 4);
+    P.off_nat_all = off;  // native keys of every chunk (the fused selection)
+    off = align_up(off + (size_t)P.total_chunks * 4);
   }
   P.ws_total = off;
   return LSA_OK;
@@ -719,6 +721,31 @@ lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const
     }
     ths.score_wg_off[B] = off;
   }
+  // Fused form: one scoring pass for both indexers (the native one as an extra
+  // layer of the same head count), then both selections and the window in one
+  // workgroup per sequence.
+  int max_hist = 0;
+  for (int b = 0; b < B; ++b) max_hist = std::max(max_hist, P.n_hist[b]);
+  if (tl->native_heads == ix->n_heads && ix->n_layers + 1 <= kMaxIdxLayers &&
+      (ix->n_layers + 1) * ix->n_heads <= kRecallThreads && max_hist <= kTwoLevelSelMaxN) {
+    uint32_t* nat_all = reinterpret_cast<uint32_t*>(at(ws, P.off_nat_all));
+    RecallArgs r = recall_args(P, ix, idx_q, idx_w, idx_k);
+    r.nat_q = static_cast<const uint16_t*>(nat_q);
+    r.nat_w = nat_w;
+    r.nat_k = static_cast<const uint16_t*>(nat_k);
+    r.nat_out = nat_all;
+    LSA_HIP(launch_recall_score(ths, r, keys, true, s), "recall score launch");
+    TwoLevelSelArgs a;
+    a.l1 = static_cast<const uint32_t*>(keys);
+    a.l2 = nat_all;
+    a.out = sel;
+    a.pitch = P.max_sel;
+    a.count = cnt;
+    for (int b = 0; b < B; ++b) a.keep2[b] = tl->core_keep[b];
+    LSA_HIP(launch_two_level_select(th, a, s), "two-level select launch");
+    return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
+  }
+
   LSA_HIP(launch_recall_score(ths, recall_args(P, ix, idx_q, idx_w, idx_k), keys, true, s), "recall score launch");
   SelectArgs sa1;
   sa1.recall = true;

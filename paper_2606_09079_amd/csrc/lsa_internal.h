@@ -113,6 +113,7 @@ hipError_t launch_attn(const SeqTable& t, const AttnArgs& a, int32_t chunk_size,
 // Recall path: the full Memory Indexer score of L layers.
 constexpr int kMaxIdxLayers = LSA_MAX_IDX_LAYERS;
 constexpr int kRecallRowsPerWg = 64;  // entries per scoring workgroup (4 waves x 16)
+constexpr int kRecallThreads = 256;   // threads per scoring workgroup
 struct RecallArgs {
   const uint16_t* q;     // bf16 [B][L][n_h][c]
   const float* w;        // [B][L][n_h]
@@ -125,11 +126,33 @@ struct RecallArgs {
   const int32_t* list = nullptr;
   const int32_t* list_count = nullptr;
   int64_t list_pitch = 0;
+  // keys mode, optional: a second indexer of the same head count scored in
+  // the same pass (one more staged layer, outside the max over layers), whose
+  // order keys go to nat_out[total] (the two-level path's native indexer)
+  const uint16_t* nat_q = nullptr;  // bf16 [B][n_h][c]
+  const float* nat_w = nullptr;     // [B][n_h]
+  const uint16_t* nat_k = nullptr;  // bf16 [total][c]
+  uint32_t* nat_out = nullptr;
 };
 // t.score_wg_off must count kRecallRowsPerWg entries per workgroup.  keys ==
 // false writes x [L][total] float32; keys == true writes the order key of
 // max_l x_l per entry, [total] (the input of the recall selection).
 hipError_t launch_recall_score(const SeqTable& t, const RecallArgs& r, void* out, bool keys, hipStream_t s);
+
+// Two-level selection in one kernel: the recall over the Level-1 keys (order
+// keys of max_l x, ready), then the top-k2 of the native keys (order keys)
+// among the recalled chunks, then the window chunks.  t.n[b] is the history
+// length (at most 16384), t.keep[b] K_max, t.w0 / t.win the window.
+struct TwoLevelSelArgs {
+  const uint32_t* l1;     // [total] indexed by chunk_off[b] + s
+  const uint32_t* l2;     // [total] likewise
+  int32_t* out;           // [B][pitch]
+  int64_t pitch;
+  int32_t* count;         // [B]
+  int32_t keep2[LSA_MAX_BATCH];
+};
+constexpr int kTwoLevelSelMaxN = 16384;
+hipError_t launch_two_level_select(const SeqTable& t, const TwoLevelSelArgs& a, hipStream_t s);
 
 
 // Host tier: residency plan and copies between a pinned host mirror of the

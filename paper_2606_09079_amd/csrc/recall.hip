@@ -29,7 +29,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
+constexpr int kThreads = kRecallThreads;
 constexpr int kWaves = kThreads / 64;
 
 // s_waitcnt immediates (gfx9 encoding): at most n vector loads of this wave
@@ -77,6 +77,9 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
   __shared__ float sw[kMaxIdxLayers * NH];
 
   const int L = r.n_layers;
+  // keys mode with a native indexer: one more layer, scored but not max-ed
+  const int NAT = (OUT == kOutKeys && r.nat_out != nullptr) ? 1 : 0;
+  const int LT = L + NAT;
   const int wg = blockIdx.x;
   int b = 0;
   while (wg >= t.score_wg_off[b + 1]) ++b;
@@ -91,14 +94,19 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
 
   // queries -> LDS in operand order: lane i of block (l, hb, st) holds
   // q_l[16 hb + i % 16][32 st + 8 (i / 16) .. + 7]
-  const int n_staged = L * kBlocks * kSteps;
+  const int n_staged = LT * kBlocks * kSteps;
   const uint16_t* qb = r.q + (int64_t)b * L * NH * CD + (lane & 15) * CD + 8 * hi;
+  const uint16_t* qn = NAT ? r.nat_q + (int64_t)b * NH * CD + (lane & 15) * CD + 8 * hi : qb;
   for (int blk = wave; blk < n_staged; blk += kWaves) {  // wave-uniform
     const int st = (blk / kBlocks) % kSteps, hb = blk % kBlocks, l = blk / (kBlocks * kSteps);
-    __builtin_amdgcn_global_load_lds((const void*)(qb + (l * NH + 16 * hb) * CD + 32 * st),
-                                     (void __attribute__((address_space(3)))*)&sq[blk][0], 16, 0, 0);
+    const uint16_t* src = l < L ? qb + (l * NH + 16 * hb) * CD + 32 * st : qn + (16 * hb) * CD + 32 * st;
+    __builtin_amdgcn_global_load_lds((const void*)src, (void __attribute__((address_space(3)))*)&sq[blk][0], 16, 0,
+                                     0);
   }
-  const float gate = r.w[(int64_t)b * L * NH + min(tid, L * NH - 1)];  // L * NH <= kThreads
+  // LT * NH <= kThreads
+  const float gate = tid < L * NH ? r.w[(int64_t)b * L * NH + tid]
+                     : NAT ? r.nat_w[(int64_t)b * NH + min(tid - L * NH, NH - 1)]
+                           : r.w[(int64_t)b * L * NH + L * NH - 1];
 
   // B operands: entry e0 + lane % 16 (clamped; its result is not stored), dims
   // 32 st + 8 hi .. + 7, every layer (layers past L re-read layer 0 and are
@@ -109,27 +117,29 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
     const int pos = min(e0 + (lane & 15), n - 1);
     const int ent = OUT == kOutListKeys ? r.list[b * r.list_pitch + pos] : pos;
     const uint16_t* kp = r.k + (t.chunk_off[b] + ent) * CD + 8 * hi;
+    const uint16_t* kn = NAT ? r.nat_k + (t.chunk_off[b] + ent) * CD + 8 * hi : kp;
 #pragma unroll
-    for (int l = 0; l < kMaxIdxLayers; ++l)
+    for (int l = 0; l < kMaxIdxLayers; ++l) {
+      const uint16_t* kl = l < L ? kp + l * r.layer_stride : l == L ? kn : kp;
 #pragma unroll
       for (int st = 0; st < kSteps; ++st)
-        kb[l][st] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const uint4*>(kp + (l < L ? l : 0) * r.layer_stride + 32 * st));
+        kb[l][st] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kl + 32 * st));
+    }
   }
 
   // the copies and the gate are in once at most the key loads are outstanding
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(kKeyLoads));
-  if (tid < L * NH) sw[tid] = gate;
+  if (tid < LT * NH) sw[tid] = gate;
   __builtin_amdgcn_s_waitcnt(kWaitLds);
   __asm__ volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   __asm__ volatile("" ::: "memory");
   if (e0 >= n) return;
 
-  float best = -INFINITY;
+  float best = -INFINITY, native = 0.f;
 #pragma unroll
   for (int l = 0; l < kMaxIdxLayers; ++l) {
-    if (l >= L) break;
+    if (l >= LT) break;
     f32x4 acc[kBlocks];
 #pragma unroll
     for (int hb = 0; hb < kBlocks; ++hb) acc[hb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -153,12 +163,15 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
       if (lane < 16 && e0 + lane < n)
         static_cast<float*>(out)[l * r.total + t.chunk_off[b] + e0 + lane] = x;
     }
-    best = fmaxf(best, x);
+    if (l < L) best = fmaxf(best, x);
+    else native = x;
   }
   if constexpr (OUT != kOutScores) {
     const int64_t base = OUT == kOutListKeys ? b * r.list_pitch : t.chunk_off[b];
     if (lane < 16 && e0 + lane < n)
       static_cast<uint32_t*>(out)[base + e0 + lane] = order_key<kKeysFromF32>(__float_as_uint(best));
+    if (NAT && lane < 16 && e0 + lane < n)
+      r.nat_out[t.chunk_off[b] + e0 + lane] = order_key<kKeysFromF32>(__float_as_uint(native));
   }
 }
 

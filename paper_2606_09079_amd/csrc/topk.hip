@@ -517,6 +517,208 @@ union_kernel(SeqTable t, const int32_t* __restrict__ per_query, int32_t k_pitch,
   if (tid == kThreads - 1) sel_count[b] = (int32_t)pos;
 }
 
+// ---------------------------------------------------------------------------
+// Two-level selection in one workgroup per sequence (up to 16384 history
+// chunks): the recall (keys >= the key of +0.0, at most K_max, the largest
+// first) and the Level-2 top-k2 of the native keys among the recalled chunks,
+// each as one LDS radix pass of the kind above, then the window chunks.
+
+// Shared arrays of one selection pass.
+struct SelLds {
+  uint32_t* hist;   // [4096 * kSelSub]
+  uint32_t* cand;   // [kSelCand + 512]
+  uint32_t* keys;   // [kSelMaxN]
+  uint32_t* tot;    // [kSelWaves]
+  uint32_t* bm_gt;  // [kSelMaxN / 32]
+  uint32_t* bm_eq;  // [kSelMaxN / 32]
+  uint32_t* sh;     // [4]
+};
+
+// The k largest nonzero keys of kk (key q * 1024 + tid in slot q), 1 <= k <=
+// the number of nonzero keys: afterwards bm_gt marks the keys above the k-th
+// largest key T and bm_eq the keys equal to T; returns how many of the keys
+// equal to T are kept (those first in position order).
+__device__ __forceinline__ uint32_t select_pass(const uint32_t (&kk)[kSelKPT], uint32_t k, const SelLds& S) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane >> 4;
+#pragma unroll
+  for (int q = 0; q < kSelSub; ++q)
+    reinterpret_cast<uint4*>(S.hist)[q * kSelThreads + tid] = make_uint4(0u, 0u, 0u, 0u);
+  if (tid < kSelMaxN / 128) reinterpret_cast<uint4*>(S.bm_eq)[tid] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  uint32_t bin[kSelKPT], rk[kSelKPT];
+#pragma unroll
+  for (int q = 0; q < kSelKPT; ++q) {
+    bin[q] = kk[q] >> 20;
+    rk[q] = kk[q] != 0u ? atomicAdd(&S.hist[bin[q] * kSelSub + sub], 1u) : 0u;
+  }
+  __syncthreads();
+  {
+    const uint4* h4 = reinterpret_cast<const uint4*>(S.hist) + 4 * tid;
+    uint32_t c[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint4 x = h4[q];
+      c[q] = x.x + x.y + x.z + x.w;
+    }
+    const uint32_t mine = c[0] + c[1] + c[2] + c[3];
+    const uint32_t incl = wave_scan_incl(mine);
+    if (lane == 63) S.tot[wave] = incl;
+    __syncthreads();
+    const uint32_t wt = lane < kSelWaves ? S.tot[lane] : 0u;
+    const uint32_t after = lane_bcast(wave_scan_incl(lane > wave ? wt : 0u), 63);
+    uint32_t cum = after + lane_bcast(incl, 63) - incl;
+#pragma unroll
+    for (int q = 3; q >= 0; --q) {
+      if (cum < k && cum + c[q] >= k) {
+        S.sh[0] = 4u * tid + q;
+        S.sh[1] = k - cum;
+        S.sh[2] = c[q];
+      }
+      cum += c[q];
+    }
+  }
+  __syncthreads();
+  const uint32_t B0 = S.sh[0], m = S.sh[2];
+  const bool packed = m <= (uint32_t)kSelCand;
+  if (packed) {
+    const uint4 bc = reinterpret_cast<const uint4*>(S.hist)[B0];
+    const uint32_t off = (sub > 0 ? bc.x : 0u) + (sub > 1 ? bc.y : 0u) + (sub > 2 ? bc.z : 0u);
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q)
+      if (kk[q] != 0u && bin[q] == B0) S.cand[off + rk[q]] = kk[q];
+  } else {
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) S.keys[q * kSelThreads + tid] = kk[q];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    uint32_t prefix = B0 << 20, kr = S.sh[1];
+    const uint32_t* cs = packed ? S.cand : S.keys;
+    const int lim = packed ? (int)m : kSelMaxN;
+    prefix |= wave_digit(cs, lim, prefix, 0xFFF00000u, 10, kr, S.hist) << 10;
+    prefix |= wave_digit(cs, lim, prefix, 0xFFFFFC00u, 0, kr, S.hist);
+    if (lane == 0) {
+      S.sh[0] = prefix;
+      S.sh[1] = kr;
+    }
+  }
+  __syncthreads();
+  const uint32_t T = S.sh[0], krem = S.sh[1];
+  uint64_t* gdst = reinterpret_cast<uint64_t*>(S.bm_gt) + wave;
+  uint64_t* edst = reinterpret_cast<uint64_t*>(S.bm_eq) + wave;
+#pragma unroll
+  for (int q = 0; q < kSelKPT; ++q) {
+    const uint64_t g = __ballot(kk[q] > T);
+    const uint64_t e = __ballot(kk[q] == T);
+    if (lane == 0) {
+      gdst[q * kSelWaves] = g;
+      if (e != 0ull) edst[q * kSelWaves] = e;
+    }
+  }
+  __syncthreads();
+  return krem;
+}
+
+// For thread v < 512 (chunks 32v .. 32v+31 of n): the kept chunks of the last
+// pass -- every chunk above T and the first krem equal to T -- as a bit word,
+// and its exclusive prefix count in *before.
+__device__ __forceinline__ uint32_t kept_word(const SelLds& S, int n, uint32_t krem, uint32_t* before) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bool mine = tid < kSelMaxN / 32;
+  uint32_t g = 0, e = 0;
+  if (mine) {
+    const int valid = n - 32 * tid;
+    const uint32_t live = valid >= 32 ? 0xFFFFFFFFu : valid > 0 ? (1u << valid) - 1u : 0u;
+    g = S.bm_gt[tid] & live;
+    e = S.bm_eq[tid] & live;
+  }
+  const uint32_t cnt = ((uint32_t)__popc(g) << 16) | (uint32_t)__popc(e);
+  const uint32_t incl = wave_scan_incl(cnt);
+  if (lane == 63) S.tot[wave] = incl;
+  __syncthreads();
+  const uint32_t wt = lane < kSelWaves ? S.tot[lane] : 0u;
+  const uint32_t excl = lane_bcast(wave_scan_incl(lane < wave ? wt : 0u), 63) + incl - cnt;
+  const uint32_t gb = excl >> 16, eb = excl & 0xFFFFu;
+  uint32_t kept = g;
+  for (uint32_t r = eb < krem ? krem - eb : 0u; e != 0u && r != 0u; --r) {
+    kept |= e & (0u - e);
+    e &= e - 1u;
+  }
+  *before = gb + min(eb, krem);
+  __syncthreads();  // S.tot is reused by the next pass
+  return mine ? kept : 0u;
+}
+
+__global__ void __launch_bounds__(kSelThreads)
+two_level_select_kernel(SeqTable t, TwoLevelSelArgs a) {
+  __shared__ __align__(16) uint32_t hist[4096 * kSelSub];
+  __shared__ uint32_t cand[kSelCand + 512];
+  __shared__ uint32_t keys[kSelMaxN];
+  __shared__ __align__(16) uint32_t tot[kSelWaves];
+  __shared__ __align__(16) uint32_t bm_gt[kSelMaxN / 32];
+  __shared__ __align__(16) uint32_t bm_eq[kSelMaxN / 32];
+  __shared__ uint32_t rec[kSelMaxN / 32];
+  __shared__ uint32_t sh[4];
+  __shared__ uint32_t nonneg[kSelWaves];
+  const SelLds S{hist, cand, keys, tot, bm_gt, bm_eq, sh};
+
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = min(t.n[b], kSelMaxN);
+  int32_t* out = a.out + b * a.pitch;
+
+  // Level-1 keys; slots past n read 0 (buffer loads past the end)
+  uint32_t kk[kSelKPT];
+  {
+    const __amdgpu_buffer_rsrc_t src = raw_buffer(a.l1 + t.chunk_off[b], (uint32_t)n * 4u);
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q)
+      kk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
+  }
+  // the native keys are loaded now too, and masked once the recall is known
+  uint32_t nk[kSelKPT];
+  {
+    const __amdgpu_buffer_rsrc_t src = raw_buffer(a.l2 + t.chunk_off[b], (uint32_t)n * 4u);
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q)
+      nk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
+  }
+  uint32_t nn = 0;
+#pragma unroll
+  for (int q = 0; q < kSelKPT; ++q) nn += (uint32_t)__popcll(__ballot(kk[q] >= 0x80000000u));
+  if (lane == 0) nonneg[wave] = nn;
+  __syncthreads();
+  const uint32_t recalled = lane_bcast(wave_scan_incl(lane < kSelWaves ? nonneg[lane] : 0u), 63);
+  const uint32_t k1 = min((uint32_t)max(t.keep[b], 0), recalled);
+  uint32_t k2 = 0;
+  if (k1 > 0u) {  // uniform
+    // Level 1: keys below the key of +0.0 (not recalled) leave the selection
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) kk[q] = kk[q] >= 0x80000000u ? kk[q] : 0u;
+    const uint32_t krem1 = select_pass(kk, k1, S);
+    uint32_t unused;
+    const uint32_t rw = kept_word(S, n, krem1, &unused);
+    if (tid < kSelMaxN / 32) rec[tid] = rw;
+    __syncthreads();
+    // Level 2 over the recalled chunks
+#pragma unroll
+    for (int q = 0; q < kSelKPT; ++q) {
+      const int pos = q * kSelThreads + tid;
+      nk[q] = pos < n && ((rec[pos >> 5] >> (pos & 31)) & 1u) ? nk[q] : 0u;
+    }
+    k2 = min((uint32_t)max(a.keep2[b], 1), k1);
+    const uint32_t krem2 = select_pass(nk, k2, S);
+    uint32_t pos;
+    uint32_t kept = kept_word(S, n, krem2, &pos);
+    while (kept != 0u) {
+      out[pos++] = 32 * tid + __builtin_ctz(kept);
+      kept &= kept - 1u;
+    }
+  }
+  const int w0 = t.w0[b], nw = t.win[b];
+  for (int i = tid; i < nw; i += kSelThreads) out[k2 + i] = w0 + i;
+  if (tid == 0) a.count[b] = (int32_t)k2 + nw;
+}
+
 __global__ void zero_kernel(uint4* p, size_t n16, uint8_t* tail, size_t ntail) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
@@ -559,6 +761,13 @@ hipError_t launch_topk(const SeqTable& t, int32_t emb_dtype, bool keys_ready, co
   if (emb_dtype == LSA_I8)
     return launch_topk_keys<kKeysFromI32, false>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, sa, s);
   return launch_topk_keys<kKeysFromF32, false>(t, sc, out_idx, out_pitch_seq, out_pitch_query, sel_count, sa, s);
+}
+
+hipError_t launch_two_level_select(const SeqTable& t, const TwoLevelSelArgs& a, hipStream_t s) {
+  for (int b = 0; b < t.batch; ++b)
+    if (t.n[b] > kSelMaxN) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(two_level_select_kernel, dim3(t.batch), dim3(kSelThreads), 0, s, t, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_pitch,
