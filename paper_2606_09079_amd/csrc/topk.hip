@@ -340,18 +340,26 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
 
   // First digit (top 12 bits).  The atomic returns the key's rank among the
   // keys of its bin and quarter, which later places it in the candidate list.
-  uint32_t bin[kSelKPT], rk[kSelKPT];
-#pragma unroll
-  for (int q = 0; q < kSelKPT; ++q) {
-    if constexpr (MODE != kKeysReady && !RECALL) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
-    bin[q] = kk[q] >> 20;
-    rk[q] = q * kSelThreads + tid < n ? atomicAdd(&hist[bin[q] * kSelSub + sub], 1u) : 0u;
-  }
+  // Slots past n are padding and stay out.  In the recall the keys below the
+  // key of +0.0 cannot be kept (k is at most the number of the others): they
+  // are set to 0, which no kept key equals there, and stay out too.
   if constexpr (RECALL) {
     uint32_t nn = 0;
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q) nn += (uint32_t)__popcll(__ballot(kk[q] >= 0x80000000u));
+    for (int q = 0; q < kSelKPT; ++q) {
+      nn += (uint32_t)__popcll(__ballot(kk[q] >= 0x80000000u));
+      kk[q] = kk[q] >= 0x80000000u ? kk[q] : 0u;
+    }
     if (lane == 0) nonneg[wave] = nn;
+  }
+  uint32_t bin[kSelKPT], rk[kSelKPT];
+  bool in[kSelKPT];
+#pragma unroll
+  for (int q = 0; q < kSelKPT; ++q) {
+    if constexpr (MODE != kKeysReady && !RECALL) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
+    in[q] = RECALL ? kk[q] != 0u : q * kSelThreads + tid < n;
+    bin[q] = kk[q] >> 20;
+    rk[q] = in[q] ? atomicAdd(&hist[bin[q] * kSelSub + sub], 1u) : 0u;
   }
   __syncthreads();
   if constexpr (RECALL) {
@@ -403,7 +411,7 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
     const uint32_t off = (sub > 0 ? bc.x : 0u) + (sub > 1 ? bc.y : 0u) + (sub > 2 ? bc.z : 0u);
 #pragma unroll
     for (int q = 0; q < kSelKPT; ++q)
-      if (bin[q] == B0) cand[off + rk[q]] = kk[q];
+      if (in[q] && bin[q] == B0) cand[off + rk[q]] = kk[q];
   } else {
 #pragma unroll
     for (int q = 0; q < kSelKPT; ++q) keys[q * kSelThreads + tid] = kk[q];
@@ -411,11 +419,12 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   __syncthreads();
 
   // Last 20 bits: two 10-bit digits resolved by wave 0 alone, over the packed
-  // candidates (or over all keys when the bin was too large to pack).
+  // candidates (or over the n keys in position order when the bin was too
+  // large to pack; keys set to 0 by the recall never match its prefix).
   if (wave == 0) {
     uint32_t prefix = B0 << 20, kr = krem;
     const uint32_t* cs = packed ? cand : keys;
-    const int lim = packed ? (int)m : kSelMaxN;
+    const int lim = packed ? (int)m : n;
     prefix |= wave_digit(cs, lim, prefix, 0xFFF00000u, 10, kr, hist) << 10;
     prefix |= wave_digit(cs, lim, prefix, 0xFFFFFC00u, 0, kr, hist);
     if (lane == 0) {

@@ -113,6 +113,26 @@ def test_int_scores_extremes():
         assert np.array_equal(sel.cpu().numpy()[0], oracle.topk(s.astype(np.int64), k)), f"k={k}"
 
 
+def test_int_scores_all_in_the_lowest_bin():
+    """Every int32 score within 2^20 of INT32_MIN (order keys below 2^20, the
+    first-digit bin 0) and more of them than the candidate list holds, with
+    padding slots present: the last digits come from the keys themselves."""
+    import torch
+    import oracle
+    L = _lib()
+    rng = np.random.default_rng(17)
+    for n, k in ((10000, 5000), (10000, 1), (9000, 8999), (5000, 4097)):
+        s = (np.int64(-2**31) + rng.integers(0, 2**20, size=n)).astype(np.int32)
+        s[::7] = np.int32(-2**31)  # ties at the very bottom too
+        prob = L.Problem([64 * n], 64, [k], 4, 4, emb_dtype="i8")
+        sc = torch.from_numpy(s).cuda()
+        sel = torch.full((1, k), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+        L.lsa_topk_chunks(prob, sc, sel, cnt)
+        torch.cuda.synchronize()
+        assert np.array_equal(sel.cpu().numpy()[0], oracle.topk(s.astype(np.int64), k)), f"n={n} k={k}"
+
+
 def test_step_is_deterministic_and_workspace_reusable():
     """Repeated fused steps give bitwise-equal results, also when the same
     workspace serves a different problem in between (no call depends on what
