@@ -6,8 +6,9 @@
 // 16-byte pieces; L consecutive lanes read one row (one 16-byte load each), so a
 // wavefront load instruction covers 1 KiB of contiguous embeddings.  Each
 // workgroup owns a contiguous block of rows of one sequence, issues all of its
-// row loads up front (8 per lane) and then reuses the registers for every
-// lookahead query of that sequence, so E is read exactly once.  Partial dot
+// row loads up front (2 per lane: many small workgroups beat fewer with more
+// loads each) and then reuses the registers for every lookahead query of that
+// sequence, so E is read exactly once.  Partial dot
 // products are reduced across the L lanes of a row with xor shuffles.
 //   F32 : fp32 FMA accumulation
 //   BF16: bf16 widened to fp32 (exact), fp32 FMA accumulation
@@ -20,7 +21,7 @@ namespace lsa {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kPasses = 8;  // row loads in flight per lane
+constexpr int kPasses = 2;  // row loads per lane: small workgroups, many of them (measured fastest)
 
 template <int DT> struct Elem;
 template <> struct Elem<LSA_F32> { static constexpr int size = 4; };
