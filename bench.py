@@ -321,6 +321,7 @@ def main() -> int:
         "step_roofline_frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "step_us": {"p10": pct(0.10), "median": pct(0.50), "p90": pct(0.90), "samples": n_dist,
                     "flush_mib_between_samples": flush_mib},
+        "step_gbs_at_median": round(step_bytes / (pct(0.50) * 1e-6) / 1e9, 1),
         "read_ceiling_gbs": round(read_gbs, 1) if read_gbs else None,
         "step_frac_of_read_ceiling": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / read_gbs, 4) if read_gbs else None,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -738,6 +739,14 @@ def cpu_baseline(prob, host, budget_s: float):
         el = time.perf_counter() - t0
         if el >= budget_s or el / reps * (reps + 1) > 3 * budget_s:
             break
+    # the same step on one thread (KV-head groups in turn), once
+    t1 = time.perf_counter()
+    kept_1 = select()
+    toks_1 = oracle.kept_tokens(kept_1, prob.chunk, prob.ctx_tokens[0])
+    for g in range(Hkv):
+        qr = np.stack([host["q"][0, 0, g * G + j] for j in range(G)])
+        oracle.attention_tokens(qr, kv[("k", g)], kv[("v", g)], toks_1)
+    one_thread_s = time.perf_counter() - t1
     full = prob.batch == 1 and prob.n_qtok == 1
     what = ("full step(s) of the same workload" if full else
             "step(s) of sequence 0 of the same workload, attention for its first query token only")
@@ -752,7 +761,10 @@ def cpu_baseline(prob, host, budget_s: float):
         sel_what = f"score {prob.n_chunks[0]:,} chunks, top-{prob.keep[0]:,}"
     return {"value": round(reps / el, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} {what} ({sel_what}, fp64 attention for {prob.n_q_heads} query heads) in {el:.1f}s; "
-                      f"KV-head groups on {threads} threads"}
+                      f"KV-head groups on {threads} threads (os.cpu_count() = {os.cpu_count()}, OMP_NUM_THREADS = "
+                      f"{os.environ.get('OMP_NUM_THREADS', 'unset')})",
+            "one_thread": {"value": round(1.0 / one_thread_s, 4), "unit": "steps/s",
+                           "sample": "one more step with the KV-head groups in turn on one thread"}}
 
 
 if __name__ == "__main__":
