@@ -313,7 +313,7 @@ lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const
  * (copy lists [B][pitch][2] of (chunk id, local slot id)).
  */
 /* Pitch of the lists, slots in the reserve, and the workspace of
- * lsa_tier_attend (any output pointer may be NULL). */
+ * lsa_tier_attend and lsa_tier_step (any output pointer may be NULL). */
 lsa_status lsa_tier_sizes(const lsa_problem* p, const lsa_tier* tr, int32_t* pitch, int64_t* total_slots,
                           size_t* ws_bytes);
 /* owner[0 .. sum_b slots[b]) = -1: an empty reserve (a fill kernel on stream). */
@@ -363,6 +363,32 @@ lsa_status lsa_tier_fetch(const lsa_problem* p, const lsa_tier* tr, const uint16
 lsa_status lsa_tier_fetch_dma(const lsa_problem* p, const lsa_tier* tr, const uint16_t* host_k,
                               const uint16_t* host_v, const int32_t* h_fetch, const int32_t* h_fetch_count,
                               uint16_t* res_k, uint16_t* res_v, void* stream);
+/*
+ * One decode step over the resident set (Sec. 2.5, the fixed-shape part that
+ * runs every step between firings): Level 2 of the two-level selection
+ * (Sec. 2.1 after Eq. 5, Eq. 6) over the chunks that the last firing made
+ * resident, then step 3 over their reserve slots.  kept_idx / kept_count are
+ * that firing's kept list (as given to lsa_tier_plan) and slot_idx the slots
+ * lsa_tier_plan assigned to it.  nat describes the native indexer (n_layers
+ * must be 1); nat_q bf16 [B][n_h][c], nat_w float32 [B][n_h], nat_k bf16
+ * [total chunks][c], all device memory.  Per sequence:
+ *   native[i] = sum_h nat_w[b][h] * ReLU(nat_q[b][h] . nat_k[chunk_off[b] + kept_idx[b][i]]),
+ * the core_keep[b] (HOST [B], >= 1) kept chunks with the largest native score
+ * stay (all when there are fewer; equal scores by the lower position in the
+ * kept list, which is ascending); sel_slots[b] (device, row pitch as
+ * lsa_tier_sizes) receives their reserve slots in ascending chunk order and
+ * sel_count[b] their number; out / lse are the attention over those slots
+ * (layouts as lsa_tier_attend); sel_slots must not be kept_idx or slot_idx.
+ * No window is added: chunks that must always
+ * be attended belong in the kept list.  Kept ids outside 0 .. n_b - 1 give
+ * unspecified but in-bounds results.  The workspace is the one lsa_tier_sizes
+ * reports; the call only enqueues work on `stream`.
+ */
+lsa_status lsa_tier_step(const lsa_problem* p, const lsa_tier* tr, const lsa_indexer* nat, const int32_t* core_keep,
+                         const void* nat_q, const float* nat_w, const void* nat_k, const int32_t* kept_idx,
+                         const int32_t* kept_count, const int32_t* slot_idx, const uint16_t* q,
+                         const uint16_t* res_k, const uint16_t* res_v, float softmax_scale, float* out, float* lse,
+                         int32_t* sel_slots, int32_t* sel_count, void* ws, size_t ws_bytes, void* stream);
 /*
  * Step 3 over the reserve: the attention of lsa_sparse_decode_attn for the
  * chunks held in slots slot_idx[b][0 .. slot_count[b]) (the remapped kept

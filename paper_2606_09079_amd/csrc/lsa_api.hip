@@ -352,6 +352,8 @@ struct TierPlan {
   Plan P, R;
   int32_t slot_off[LSA_MAX_BATCH + 1] = {};
   int64_t total_slots = 0;
+  size_t off_keys = 0;  // lsa_tier_step: native order keys of the resident recalled chunks, [B][pitch]
+  size_t ws_total = 0;
 };
 
 lsa_status make_tier_plan(const lsa_problem* p, const lsa_tier* tr, TierPlan* tp) {
@@ -384,6 +386,8 @@ lsa_status make_tier_plan(const lsa_problem* p, const lsa_tier* tr, TierPlan* tp
   LSA_TRY(make_plan(&r, &tp->R));
   if (tp->R.max_sel != tp->P.max_sel || tp->R.n_units != tp->P.n_units)
     return fail(LSA_ERR_INVALID_ARG, "reserve plan differs from the context plan");
+  tp->off_keys = align_up(tp->R.ws_total);
+  tp->ws_total = align_up(tp->off_keys + (size_t)B * tp->P.max_sel * 4);
   return LSA_OK;
 }
 
@@ -796,7 +800,7 @@ lsa_status lsa_tier_sizes(const lsa_problem* p, const lsa_tier* tr, int32_t* pit
   LSA_TRY(make_tier_plan(p, tr, &T));
   if (pitch != nullptr) *pitch = T.P.max_sel;
   if (total_slots != nullptr) *total_slots = T.total_slots;
-  if (ws_bytes != nullptr) *ws_bytes = T.R.ws_total;
+  if (ws_bytes != nullptr) *ws_bytes = T.ws_total;
   return LSA_OK;
 }
 
@@ -927,6 +931,82 @@ lsa_status lsa_tier_fetch_dma(const lsa_problem* p, const lsa_tier* tr, const ui
   return LSA_OK;
 }
 
+lsa_status lsa_tier_step(const lsa_problem* p, const lsa_tier* tr, const lsa_indexer* nat, const int32_t* core_keep,
+                         const void* nat_q, const float* nat_w, const void* nat_k, const int32_t* kept_idx,
+                         const int32_t* kept_count, const int32_t* slot_idx, const uint16_t* q,
+                         const uint16_t* res_k, const uint16_t* res_v, float softmax_scale, float* out, float* lse,
+                         int32_t* sel_slots, int32_t* sel_count, void* ws, size_t ws_bytes, void* stream) {
+  TierPlan T;
+  LSA_TRY(make_tier_plan(p, tr, &T));
+  LSA_TRY(check_indexer(p, nat));
+  if (nat->n_layers != 1) return fail(LSA_ERR_INVALID_ARG, "native indexer n_layers %d != 1", nat->n_layers);
+  if (core_keep == nullptr) return fail(LSA_ERR_INVALID_ARG, "core_keep must be a host array of batch entries");
+  for (int b = 0; b < p->batch; ++b)
+    if (core_keep[b] < 1) return fail(LSA_ERR_INVALID_ARG, "core_keep[%d] = %d < 1", b, core_keep[b]);
+  LSA_TRY(check_ptr(nat_q, "nat_q"));
+  LSA_TRY(check_ptr(nat_w, "nat_w"));
+  LSA_TRY(check_ptr(nat_k, "nat_k"));
+  LSA_TRY(check_ptr(kept_idx, "kept_idx"));
+  LSA_TRY(check_ptr(kept_count, "kept_count"));
+  LSA_TRY(check_ptr(slot_idx, "slot_idx"));
+  LSA_TRY(check_ptr(q, "q"));
+  LSA_TRY(check_ptr(res_k, "res_k"));
+  LSA_TRY(check_ptr(res_v, "res_v"));
+  LSA_TRY(check_ptr(out, "out"));
+  LSA_TRY(check_ptr(sel_slots, "sel_slots"));
+  LSA_TRY(check_ptr(sel_count, "sel_count"));
+  if (sel_slots == slot_idx || sel_slots == kept_idx)
+    return fail(LSA_ERR_INVALID_ARG, "sel_slots aliases kept_idx or slot_idx");
+  if (lse != nullptr && (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(LSA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
+  if (ws_bytes < T.ws_total)
+    return fail(LSA_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, T.ws_total);
+  LSA_TRY(check_ws(T.R, ws, ws_bytes));
+  const hipStream_t s = (hipStream_t)stream;
+  const int B = p->batch;
+  const int32_t pitch = T.P.max_sel;
+  uint32_t* keys = reinterpret_cast<uint32_t*>(at(ws, T.off_keys));
+
+  // native scores of the resident recalled chunks (list mode over kept_idx)
+  SeqTable tn = T.P.t;
+  {
+    int32_t off = 0;
+    for (int b = 0; b < B; ++b) {
+      tn.n[b] = std::min(pitch, T.P.t.n[b]);  // list capacity
+      tn.score_wg_off[b] = off;
+      off += (tn.n[b] + kRecallRowsPerWg - 1) / kRecallRowsPerWg;
+    }
+    tn.score_wg_off[B] = off;
+  }
+  RecallArgs rn;
+  rn.q = static_cast<const uint16_t*>(nat_q);
+  rn.w = nat_w;
+  rn.k = static_cast<const uint16_t*>(nat_k);
+  rn.total = T.P.total_chunks;
+  rn.layer_stride = 0;
+  rn.n_layers = 1;
+  rn.n_heads = nat->n_heads;
+  rn.key_dim = nat->key_dim;
+  rn.list = kept_idx;
+  rn.list_count = kept_count;
+  rn.list_pitch = pitch;
+  LSA_HIP(launch_recall_score(tn, rn, keys, true, s), "native score launch");
+  // the k2 largest of them, mapped to their reserve slots, in chunk order
+  SeqTable tc = tn;
+  for (int b = 0; b < B; ++b) {
+    tc.keep[b] = core_keep[b];
+    tc.chunk_off[b] = (int64_t)b * pitch;
+    tc.win[b] = 0;
+  }
+  SelectArgs sa;
+  sa.dev_n = kept_count;
+  sa.map = slot_idx;
+  sa.map_pitch = pitch;
+  LSA_HIP(launch_topk(tc, LSA_F32, true, keys, sel_slots, pitch, 0, sel_count, s, sa), "native top-k launch");
+  return run_attn(p, T.R, q, res_k, res_v, sel_slots, sel_count, softmax_scale, out, lse, ws, s);
+}
+
 lsa_status lsa_tier_attend(const lsa_problem* p, const lsa_tier* tr, const uint16_t* q, const uint16_t* res_k,
                            const uint16_t* res_v, const int32_t* slot_idx, const int32_t* slot_count,
                            float softmax_scale, float* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
@@ -941,6 +1021,8 @@ lsa_status lsa_tier_attend(const lsa_problem* p, const lsa_tier* tr, const uint1
   if (lse != nullptr && (reinterpret_cast<uintptr_t>(lse) & 3u))
     return fail(LSA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
   if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
+  if (ws_bytes < T.ws_total)
+    return fail(LSA_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, T.ws_total);
   LSA_TRY(check_ws(T.R, ws, ws_bytes));
   return run_attn(p, T.R, q, res_k, res_v, slot_idx, slot_count, softmax_scale, out, lse, ws, (hipStream_t)stream);
 }

@@ -115,7 +115,10 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
   bf16x8 kb[kMaxIdxLayers][kSteps];
   {
     const int pos = min(e0 + (lane & 15), n - 1);
-    const int ent = OUT == kOutListKeys ? r.list[b * r.list_pitch + pos] : pos;
+    // a list id is clamped into the key array (its score is then meaningless)
+    const int ent = OUT == kOutListKeys
+                        ? min(max(r.list[b * r.list_pitch + pos], 0), (int)(r.total - 1 - t.chunk_off[b]))
+                        : pos;
     const uint16_t* kp = r.k + (t.chunk_off[b] + ent) * CD + 8 * hi;
     const uint16_t* kn = NAT ? r.nat_k + (t.chunk_off[b] + ent) * CD + 8 * hi : kp;
 #pragma unroll

@@ -32,7 +32,7 @@ EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_valida
            "lsa_max_keep", "lsa_workspace_size", "lsa_workspace_init", "lsa_score_chunks", "lsa_topk_chunks",
            "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
            "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step", "lsa_tier_sizes", "lsa_tier_reset",
-           "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_fetch_dma", "lsa_tier_attend",
+           "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_fetch_dma", "lsa_tier_attend", "lsa_tier_step",
            "lsa_golden_sizes", "lsa_golden_labels")
 
 
@@ -108,6 +108,8 @@ def _load() -> ctypes.CDLL:
     lib.lsa_tier_plan.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.lsa_tier_fetch.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P]
     lib.lsa_tier_fetch_dma.argtypes = [pp, rp, _P, _P, _P, _P, _P, _P, _P]
+    lib.lsa_tier_step.argtypes = [pp, rp, ip, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P,
+                                  _P, _P, ctypes.c_size_t, _P]
     lib.lsa_tier_attend.argtypes = [pp, rp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
     gp = ctypes.POINTER(lsa_golden)
     lib.lsa_golden_sizes.argtypes = [gp, ctypes.POINTER(ctypes.c_size_t)]
@@ -362,6 +364,16 @@ def lsa_tier_fetch_dma(p: Problem, tr: Tier, host_k, host_v, h_fetch, h_fetch_co
     _check(LIB.lsa_tier_fetch_dma(p.ref, tr.ref, _ptr(host_k), _ptr(host_v), _host_ptr(h_fetch),
                                   _host_ptr(h_fetch_count), _ptr(res_k), _ptr(res_v), _stream(stream)),
            "lsa_tier_fetch_dma")
+
+
+def lsa_tier_step(p: Problem, tr: Tier, nat: Indexer, core_keep, nat_q, nat_w, nat_k, kept_idx, kept_count, slot_idx,
+                  q, res_k, res_v, softmax_scale: float, out, lse, sel_slots, sel_count, ws=None, ws_bytes: int = 0,
+                  stream=None) -> None:
+    ck = (ctypes.c_int32 * len(core_keep))(*[int(x) for x in core_keep])
+    _check(LIB.lsa_tier_step(p.ref, tr.ref, nat.ref, ctypes.cast(ck, ctypes.c_void_p), _ptr(nat_q), _ptr(nat_w),
+                             _ptr(nat_k), _ptr(kept_idx), _ptr(kept_count), _ptr(slot_idx), _ptr(q), _ptr(res_k),
+                             _ptr(res_v), float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_slots), _ptr(sel_count),
+                             _ptr(ws), ws_bytes, _stream(stream)), "lsa_tier_step")
 
 
 def lsa_tier_attend(p: Problem, tr: Tier, q, res_k, res_v, slot_idx, slot_count, softmax_scale: float, out, lse=None,

@@ -240,6 +240,41 @@ def test_tier_entry_points_reject_bad_buffers_without_launching():
         == B.LSA_ERR_INVALID_ARG
 
 
+def test_tier_step_rejects_bad_arguments_without_launching():
+    import ctypes
+    p = L.Problem([64 * 300, 64 * 1000], 64, [40, 100], 8, 2)
+    T = L.Tier([80, 200])
+    _, _, ws = L.lsa_tier_sizes(p, T)
+    lib = L.LIB
+    k2 = (ctypes.c_int32 * 2)(10, 20)
+    k2_bad = (ctypes.c_int32 * 2)(10, 0)
+    nat = L.Indexer(1, 32, 128)
+
+    def call(nat_=nat, core=k2, ptrs=(FAKE,) * 10, scale=0.0, ws_bytes=ws, ws_ptr=FAKE):
+        return lib.lsa_tier_step(p.ref, T.ref, nat_.ref if nat_ is not None else None,
+                                 ctypes.cast(core, ctypes.c_void_p) if core is not None else None, *ptrs[:3],
+                                 *ptrs[3:6], *ptrs[6:9], scale, ptrs[9], None, FAKE + 12288, FAKE + 4096, ws_ptr, ws_bytes,
+                                 None)
+
+    assert call(nat_=None) == B.LSA_ERR_INVALID_ARG
+    assert call(nat_=L.Indexer(2, 32, 128)) == B.LSA_ERR_INVALID_ARG   # one native layer
+    assert call(nat_=L.Indexer(1, 48, 128)) == B.LSA_ERR_UNSUPPORTED   # head count
+    assert call(nat_=L.Indexer(1, 32, 96)) == B.LSA_ERR_UNSUPPORTED    # key width
+    assert call(core=None) == B.LSA_ERR_INVALID_ARG
+    assert call(core=k2_bad) == B.LSA_ERR_INVALID_ARG                  # k2 >= 1
+    assert call(ptrs=(FAKE,) * 3 + (None,) + (FAKE,) * 6) == B.LSA_ERR_INVALID_ARG
+    assert call(scale=float("inf")) == B.LSA_ERR_INVALID_ARG
+    assert lib.lsa_tier_step(p.ref, T.ref, nat.ref, ctypes.cast(k2, ctypes.c_void_p), *(FAKE,) * 5, F2 := FAKE + 8192,
+                             *(FAKE,) * 3, 0.0, FAKE, None, F2, FAKE + 4096, FAKE, ws, None) \
+        == B.LSA_ERR_INVALID_ARG  # sel_slots aliases slot_idx
+    assert call(ws_bytes=ws - 1) == B.LSA_ERR_WORKSPACE
+    assert call(ws_ptr=FAKE + 8) == B.LSA_ERR_WORKSPACE
+    assert call(ws_ptr=None) == B.LSA_ERR_WORKSPACE
+    la = L.Problem([64 * 300], 64, [40], 8, 2, n_lookahead=2)
+    assert lib.lsa_tier_step(la.ref, L.Tier([80]).ref, nat.ref, ctypes.cast(k2, ctypes.c_void_p), *(FAKE,) * 9,
+                             0.0, FAKE, None, FAKE + 12288, FAKE + 4096, FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
+
+
 def test_tier_dma_validates_the_host_copy_list_before_copying():
     import numpy as np
     p = L.Problem([64 * 300, 64 * 1000], 64, [40, 100], 8, 2)

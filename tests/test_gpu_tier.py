@@ -14,6 +14,9 @@ pinned host mirror into the GPU reserve, and attention over the reserve.
   lists between replays, each replay equal to the eager call.
 - The DMA-engine copies from a host copy of the list (packed and padded mirror
   layouts, merged runs of adjacent chunks) fill the reserve the same way.
+- lsa_tier_step (Level 2 over the resident set, then attention over the chosen
+  slots) chooses the oracle's chunks, up to the float32 band of the k2-th
+  native score, and attends over them bit for bit like the full-cache path.
 """
 from __future__ import annotations
 
@@ -406,3 +409,88 @@ def test_tier_dma_copies(layout):
         assert torch.equal(t_out, d_out) and torch.equal(t_lse, d_lse)
         prev = (slot_idx, cnt_d)
         log(f"[tier] DMA {layout} firing {f}: copies {h_fc.tolist()}")
+
+
+STEP_CASES = [
+    # name, ctx tokens, C, K_max, slots, core_keep (k2), native heads, key width
+    ("ragged3", [64 * 900, 64 * 400, 64 * 130], 64, [120, 60, 40], [240, 125, 80], [30, 100, 1], 32, 128),
+    ("c128_n16_c64", [128 * 700], 128, [90], [180], [25], 16, 64),
+]
+
+
+@pytest.mark.parametrize("case", STEP_CASES, ids=lambda c: c[0])
+def test_tier_step_matches_oracle(case):
+    """lsa_tier_step after every firing: the chunks behind its slot list equal
+    the oracle's Level-2 top-k2 of the native score inside the kept set (or
+    differ only inside the float32 band of the k2-th score), and its attention
+    equals lsa_tier_attend over the same slots and the full-cache attention over
+    the same chunks bit for bit, and the oracle's attention within tolerance."""
+    import torch
+    import paper_2606_09079_amd as L
+    name, ctx, C, keep, slots, k2, nat_heads, dim = case
+    prob = synth.Problem(f"tier_step_{name}", ctx, C, keep, 8, 2, idx_layers=1, idx_dim=dim, core_keep=list(k2),
+                         nat_heads=nat_heads)
+    log(f"[tier-step] {name} ctx={ctx} C={C} keep={keep} slots={slots} k2={k2} native={nat_heads}x{dim}")
+    tc = TierCase(prob, 21, slots)
+    host, dev = tc.dev["host"], tc.dev
+    nat = L.Indexer(1, nat_heads, dim)
+    rng = np.random.default_rng(8)
+    F = 7
+    per_seq = [_kept_sets(prob.n_chunks[b], keep[b], F, rng) for b in range(prob.batch)]
+    state = [([-1] * slots[b], []) for b in range(prob.batch)]
+    native = [oracle.index_score(host["nat_q"][b], host["nat_w"][b],
+                                 host["nat_k"][prob.chunk_offsets[b]:prob.chunk_offsets[b + 1]])
+              for b in range(prob.batch)]
+    tol = [parity.index_score_tolerance(host["nat_q"][b], host["nat_w"][b],
+                                        host["nat_k"][prob.chunk_offsets[b]:prob.chunk_offsets[b + 1]])
+           for b in range(prob.batch)]
+    shp = (prob.batch, 1, prob.n_q_heads, prob.head_dim)
+    prev = None
+    modes = set()
+    for f in range(F):
+        sets = [per_seq[b][f] for b in range(prob.batch)]
+        kept, cnt, slot_idx, _ = _plan_and_check(tc, L, sets, prev, state)
+        L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+        sel = torch.full((prob.batch, tc.pitch), -5, dtype=torch.int32, device="cuda")
+        sc = torch.full((prob.batch,), -5, dtype=torch.int32, device="cuda")
+        out = torch.full(shp, float("nan"), dtype=torch.float32, device="cuda")
+        lse = torch.full(shp[:3], float("nan"), dtype=torch.float32, device="cuda")
+        L.lsa_tier_step(tc.P, tc.T, nat, k2, dev["nat_q"], dev["nat_w"], dev["nat_k"], kept, cnt, slot_idx,
+                        dev["q"], tc.res_k, tc.res_v, 0.0, out, lse, sel, sc, tc.ws, tc.ws_bytes)
+        torch.cuda.synchronize()
+        g_sel, g_cnt, g_slot = sel.cpu().numpy(), sc.cpu().numpy(), slot_idx.cpu().numpy()
+        chosen_all = np.full((prob.batch, tc.pitch), -1, dtype=np.int32)
+        for b, s in enumerate(sets):
+            c = int(g_cnt[b])
+            assert c == min(len(s), k2[b]), f"firing {f} seq {b}: {c} slots selected"
+            slot_to_chunk = {int(g_slot[b, i]): int(s[i]) for i in range(len(s))}
+            chosen = np.array([slot_to_chunk[int(x)] for x in g_sel[b, :c]], dtype=np.int64)
+            assert np.all(np.diff(chosen) > 0), f"firing {f} seq {b}: slots not in ascending chunk order"
+            ref = oracle.two_level(np.asarray(s, dtype=np.int32), native[b], k2[b], prob.n_chunks[b],
+                                   prob.n_chunks[b])
+            if np.array_equal(chosen, ref):
+                modes.add("exact")
+            else:
+                ns = np.sort(native[b][np.asarray(s, dtype=np.int64)])[::-1]
+                kth = ns[k2[b] - 1]
+                diff = sorted(set(chosen.tolist()) ^ set(ref.tolist()))
+                assert all(abs(native[b][d] - kth) <= 2 * tol[b][d] for d in diff), \
+                    f"firing {f} seq {b}: Level-2 set differs outside the band at {diff[:10]}"
+                modes.add("band")
+            chosen_all[b, :c] = chosen
+        a_out, a_lse = _tier_attention(tc, L, sel, sc)
+        d_out, d_lse = _direct_attention(tc, L, torch.from_numpy(chosen_all).cuda(), sc)
+        torch.cuda.synchronize()
+        assert torch.equal(out, a_out) and torch.equal(lse, a_lse), f"firing {f}: step != attend over its slots"
+        assert torch.equal(out, d_out) and torch.equal(lse, d_lse), f"firing {f}: step != full-cache attention"
+        o, s_ = out.cpu().numpy(), lse.cpu().numpy()
+        for b in range(prob.batch):
+            c = int(g_cnt[b])
+            if c == 0:
+                assert np.all(o[b] == 0.0) and np.all(np.isneginf(s_[b])), f"firing {f} seq {b}: empty set"
+            elif f in (0, 2):
+                rows = [(0, h) for h in range(0, prob.n_q_heads, 3)]
+                _oracle_rows(tc, b, chosen_all[b, :c], o, s_, rows)
+        prev = (slot_idx, cnt)
+        log(f"[tier-step] firing {f}: kept {[len(s) for s in sets]} -> {g_cnt.tolist()}")
+    log(f"[tier-step] {name}: Level-2 sets {sorted(modes)}")
