@@ -494,3 +494,72 @@ def test_tier_step_matches_oracle(case):
         prev = (slot_idx, cnt)
         log(f"[tier-step] firing {f}: kept {[len(s) for s in sets]} -> {g_cnt.tolist()}")
     log(f"[tier-step] {name}: Level-2 sets {sorted(modes)}")
+
+
+def test_tier_step_graph_replay():
+    """lsa_tier_step captured once and replayed after every firing with the new
+    kept list and slots copied into its buffers; every replay equals the eager
+    call."""
+    import torch
+    import paper_2606_09079_amd as L
+    prob = synth.Problem("tier_step_graph", [64 * 800, 64 * 300], 64, [80, 40], 32, 8, idx_layers=1, idx_dim=128,
+                         core_keep=[20, 12], nat_heads=64)
+    slots = [160, 90]
+    tc = TierCase(prob, 23, slots)
+    dev = tc.dev
+    nat = L.Indexer(1, 64, 128)
+    k2 = [20, 12]
+    rng = np.random.default_rng(6)
+    per_seq = [_kept_sets(prob.n_chunks[b], prob.keep[b], 5, rng) for b in range(prob.batch)]
+    state = [([-1] * slots[b], []) for b in range(prob.batch)]
+    B, shp = prob.batch, (prob.batch, 1, prob.n_q_heads, prob.head_dim)
+    kept_g = torch.zeros((B, tc.pitch), dtype=torch.int32, device="cuda")
+    cnt_g = torch.zeros(B, dtype=torch.int32, device="cuda")
+    slot_g = torch.zeros((B, tc.pitch), dtype=torch.int32, device="cuda")
+    sel_g = torch.zeros((B, tc.pitch), dtype=torch.int32, device="cuda")
+    sc_g = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out_g = torch.empty(shp, dtype=torch.float32, device="cuda")
+    lse_g = torch.empty(shp[:3], dtype=torch.float32, device="cuda")
+
+    def step(kept, cnt, slot_idx, sel, sc, out, lse):
+        L.lsa_tier_step(tc.P, tc.T, nat, k2, dev["nat_q"], dev["nat_w"], dev["nat_k"], kept, cnt, slot_idx,
+                        dev["q"], tc.res_k, tc.res_v, 0.0, out, lse, sel, sc, tc.ws, tc.ws_bytes)
+
+    prev = None
+    kept, cnt, slot_idx, _ = _plan_and_check(tc, L, [per_seq[b][0] for b in range(B)], prev, state)
+    L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+    for dst, src in ((kept_g, kept), (cnt_g, cnt), (slot_g, slot_idx)):
+        dst.copy_(src)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(kept_g, cnt_g, slot_g, sel_g, sc_g, out_g, lse_g)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(kept_g, cnt_g, slot_g, sel_g, sc_g, out_g, lse_g)
+    torch.cuda.synchronize()
+    prev = (slot_idx, cnt)
+    for f in range(1, 5):
+        kept, cnt, slot_idx, _ = _plan_and_check(tc, L, [per_seq[b][f] for b in range(B)], prev, state)
+        L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+        for dst, src in ((kept_g, kept), (cnt_g, cnt), (slot_g, slot_idx)):
+            dst.copy_(src)
+        sel_e = torch.full_like(sel_g, -3)
+        sc_e = torch.full_like(sc_g, -3)
+        out_e, lse_e = torch.empty_like(out_g), torch.empty_like(lse_g)
+        step(kept, cnt, slot_idx, sel_e, sc_e, out_e, lse_e)
+        torch.cuda.synchronize()
+        for rep in range(2):
+            out_g.fill_(float("nan"))
+            sc_g.fill_(-1)
+            g.replay()
+            torch.cuda.synchronize()
+            c = sc_e.cpu().numpy()
+            assert torch.equal(sc_g, sc_e), f"firing {f} replay {rep}: counts differ"
+            for b in range(B):
+                assert torch.equal(sel_g[b, :int(c[b])], sel_e[b, :int(c[b])]), f"firing {f} replay {rep}: slots"
+            assert torch.equal(out_g, out_e) and torch.equal(lse_g, lse_e), f"firing {f} replay {rep}: attention"
+        prev = (slot_idx, cnt)
+    log("[tier-step] graph replays match the eager calls")
