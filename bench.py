@@ -59,8 +59,11 @@ WORKLOADS = {
                   "head_dim 128, bf16 K/V, batch 1",
     "tier1m": "tier1m: the recall1m context and Memory Indexer with the host tier: K/V in a pinned host mirror, a "
               "GPU reserve of 2 x K_max chunk slots; every 64 decode steps the indexer fires (recall, residency plan, "
-              "copies of the missing chunks) on a second stream, copied by the DMA engines, and the new set is read "
-              "48 steps later; each decode step attends over the reserve",
+              "copies of the missing chunks by a copy kernel reading the mirror over PCIe) on a second stream, and "
+              "the new set is read from the next step on; each decode step attends over the reserve",
+    "tier2l1m": "tier2l1m: tier1m with Level 2 inside the resident set: every decode step scores the resident kept "
+                "chunks with a native indexer of 64 heads x 128, keeps the 1,024 best and attends over their reserve "
+                "slots (lsa_tier_step); firings and copies as tier1m",
     "golden512k": "golden512k: golden-label window of a 512K-token context, 131,072 compressed entries x 64 decoding "
                   "steps x 21 layers of float32 indexer logits (704 MB), top-p 0.6, votes >= 3, union over the window",
     "golden_batch": "golden_batch: 8 golden-label windows of 4,096-131,072 entries (log-uniform), 64 steps x 21 layers",
@@ -135,7 +138,7 @@ def main() -> int:
     import paper_2606_09079_amd as L
 
     torch.cuda.set_device(0)
-    if args.workload == "tier1m":
+    if args.workload in ("tier1m", "tier2l1m"):
         return bench_tier(args)
     if args.workload.startswith("golden"):
         return bench_golden(args)
@@ -340,10 +343,12 @@ def main() -> int:
 
 TIER_TAU = 64        # decode steps between firings of the indexer
 TIER_RHO = 0.99      # correlation of the indexer queries of consecutive firings
+TIER_K2 = 1024       # tier2l1m: chunks Level 2 keeps out of the resident kept set
+TIER_AHEAD = 24      # decode steps the host may enqueue ahead of the GPU
 
 
 def bench_tier(args) -> int:
-    """Decode over the host tier at 1M context (the tier1m workload).
+    """Decode over the host tier at 1M context (the tier1m and tier2l1m workloads).
 
     Firings: the indexer queries of firing f are bf16(sqrt(rho) q_{f-1} +
     sqrt(1 - rho) g_f) with fresh N(0, 1) draws g_f and the gates of firing 0,
@@ -352,10 +357,19 @@ def bench_tier(args) -> int:
     decode step: the attention over the reserve, plus 1/64 of a firing (index
     scores of 3 layers over the full history, recall selection, residency plan
     and the copies of the missing chunks over PCIe) run on a second stream.
-    The reported value is the DMA side band: the copy list comes to the host,
-    which issues DMA-engine copies, and the new set is read --tier-lag steps
-    after the firing.  For comparison the same loop runs with the copy kernel
-    (the list stays on the GPU) and the new set read 1 and 16 steps later."""
+    The reported value is the copy kernel's side band with the new set read
+    at the next step (the materialisation at t + 1): the copy list never
+    leaves the GPU.  For comparison the same loop runs with the new set read 16
+    steps later, and with DMA-engine copies issued by the host from a host copy
+    of the list, the new set read --tier-lag steps after the firing.  The host
+    stays at most TIER_AHEAD steps ahead of the GPU.  Decode steps are
+    launched directly: replaying them from a HIP graph measured about 5 us
+    slower per step here.
+    tier2l1m adds Level 2 to every decode step: lsa_tier_step scores the
+    resident kept chunks with the native indexer, keeps TIER_K2 of them and
+    attends over their slots."""
+    import dataclasses
+
     import numpy as np
     import torch
 
@@ -368,7 +382,10 @@ def bench_tier(args) -> int:
         args.warmup += TIER_TAU - args.warmup % TIER_TAU  # the timed region starts at a firing
     main = torch.cuda.current_stream()
     side = torch.cuda.Stream()  # default priority
+    level2 = args.workload == "tier2l1m"
     prob = synth.make_problem("recall1m", 0)
+    if level2:
+        prob = dataclasses.replace(prob, name="tier2l1m", core_keep=[TIER_K2], nat_heads=64)
     t_setup = time.time()
     host0 = synth.host_inputs(prob, 0)
     dev = synth.device_inputs(prob, 0, host=host0)
@@ -395,7 +412,10 @@ def bench_tier(args) -> int:
     # unrelated queries: a full change of the kept set
     fresh_q = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))
     fresh_q2 = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))
-    qs = [dev["q"]] + [up(synth.host_inputs(prob, 1000 + r)["q"]) for r in range(1, 4)]
+    rot = [synth.host_inputs(prob, 1000 + r) for r in range(1, 4)]
+    qs = [dev["q"]] + [up(h["q"]) for h in rot]
+    nat_qs = [dev["nat_q"]] + [up(h["nat_q"]) for h in rot] if level2 else []
+    del rot
 
     B, K, C, Hkv, d = prob.batch, prob.keep[0], prob.chunk, prob.n_kv_heads, prob.head_dim
     P, ix, T = L.Problem.from_synth(prob), L.Indexer.from_synth(prob), L.Tier([2 * K] * B)
@@ -414,7 +434,9 @@ def bench_tier(args) -> int:
     fcount = torch.zeros(B, dtype=torch.int32, device="cuda")
     out = torch.empty(B, 1, prob.n_q_heads, d, dtype=torch.float32, device="cuda")
     lse = torch.empty(B, 1, prob.n_q_heads, dtype=torch.float32, device="cuda")
-    copies = []
+    sel = torch.empty(B, pitch, dtype=torch.int32, device="cuda")
+    sel_cnt = torch.zeros(B, dtype=torch.int32, device="cuda")
+    nat = L.Indexer(1, prob.nat_heads, prob.idx_dim)
 
     def select_and_plan(q_idx, prev, new, s):
         L.lsa_recall_scores(P, ix, q_idx, dev["idx_w"], dev["idx_k"], scores, s)
@@ -427,10 +449,32 @@ def bench_tier(args) -> int:
         L.lsa_tier_fetch(P, T, host_k, host_v, fetch, fcount, res_k, res_v, s)
 
     def decode(buf, i, s):
-        L.lsa_tier_attend(P, T, qs[i % len(qs)], res_k, res_v, slots[buf], cnt[buf], 0.0, out, lse, ws, ws_bytes, s)
+        if level2:
+            L.lsa_tier_step(P, T, nat, prob.core_keep, nat_qs[i % len(nat_qs)], dev["nat_w"], dev["nat_k"],
+                            kept[buf], cnt[buf], slots[buf], qs[i % len(qs)], res_k, res_v, 0.0, out, lse, sel,
+                            sel_cnt, ws, ws_bytes, s)
+        else:
+            L.lsa_tier_attend(P, T, qs[i % len(qs)], res_k, res_v, slots[buf], cnt[buf], 0.0, out, lse, ws, ws_bytes,
+                              s)
 
     def ev():
         return torch.cuda.Event(enable_timing=True)
+
+    # The host enqueues at most TIER_AHEAD decode steps ahead of the GPU, as a
+    # serving loop would: an unbounded lead fills the device queue, and the
+    # side band's copies then wait behind launches that cannot be queued.  The
+    # wait polls a ring of reused events rather than blocking in the runtime,
+    # which the side-band thread's copy calls would otherwise queue behind.
+    ring = [torch.cuda.Event() for _ in range(TIER_AHEAD)]
+    n_paced = [0]
+
+    def pace():
+        e_ = ring[n_paced[0] % TIER_AHEAD]
+        if n_paced[0] >= TIER_AHEAD:
+            while not e_.query():
+                time.sleep(0)
+        e_.record(main)
+        n_paced[0] += 1
 
     # ---- cold start: everything kept is copied in
     e = [ev() for _ in range(3)]
@@ -456,19 +500,35 @@ def bench_tier(args) -> int:
         de[i][1].record(main)
     torch.cuda.synchronize()
     dec_us = 1e3 * sum(a.elapsed_time(b) for a, b in de) / n_dec
+    # host cost of enqueueing one decode step (binding, validation, launches)
+    th = time.perf_counter()
+    for i in range(n_dec):
+        decode(0, i, main)
+    host_us = (time.perf_counter() - th) / n_dec * 1e6
+    torch.cuda.synchronize()
 
     # the copy list on the host, for the DMA engines
     h_fetch = torch.empty(B, pitch, 2, dtype=torch.int32, pin_memory=True)
     h_fcount = torch.empty(B, dtype=torch.int32, pin_memory=True)
 
+
     def fire_dma(q_idx, prev, new, s):
+        """Selection, plan and the copy of the list to the host on stream s;
+        then the DMA copies from the host copy of the list, also on s."""
         select_and_plan(q_idx, prev, new, s)
-        h_fetch.copy_(fetch, non_blocking=True)
-        h_fcount.copy_(fcount, non_blocking=True)
+        with torch.cuda.stream(s):
+            h_fetch.copy_(fetch, non_blocking=True)
+            h_fcount.copy_(fcount, non_blocking=True)
         listed = ev()
         listed.record(s)
-        listed.synchronize()  # the side band waits for the list on the host
+        t_sub = time.perf_counter()
+        # the host waits for the list here, while the GPU works through the
+        # decode steps already queued (at most TIER_AHEAD of them)
+        listed.synchronize()
+        t_list = time.perf_counter()
         L.lsa_tier_fetch_dma(P, T, host_k, host_v, h_fetch, h_fcount, res_k, res_v, s)
+        # host ms from the firing: list on the host, copies issued
+        return round(1e3 * (t_list - t_sub), 3), round(1e3 * (time.perf_counter() - t_sub), 3)
 
     # ---- a full change of the kept set, copied on the side stream while decode
     # goes on over the old set, by the copy kernel and by the DMA engines
@@ -485,6 +545,7 @@ def bench_tier(args) -> int:
             dd[i][0].record(main)
             decode(0, i, main)
             dd[i][1].record(main)
+            pace()
         torch.cuda.synchronize()
         n_full = int(fcount.cpu()[0])
         ms_full = fe[0].elapsed_time(fe[1])
@@ -510,6 +571,7 @@ def bench_tier(args) -> int:
     def steady(mode, lag):
         cur, f = state["cur"], state["f"]
         fire_ev, copies, new = [], [], None
+        side_host = []
         switched = ev()
         switched.record(main)
         e0, e1 = ev(), ev()
@@ -524,8 +586,10 @@ def bench_tier(args) -> int:
                 side.wait_event(switched)
                 a_, b_ = ev(), ev()
                 a_.record(side)
-                (fire if mode == "kernel" else fire_dma)(idx_q[f], cur, new, side)
+                h = (fire if mode == "kernel" else fire_dma)(idx_q[f], cur, new, side)
                 b_.record(side)
+                if h is not None:
+                    side_host.append(h)
                 fire_ev.append((a_, b_, i >= args.warmup))
                 f += 1
             if i % TIER_TAU == lag:
@@ -535,6 +599,7 @@ def bench_tier(args) -> int:
                 switched.record(main)
                 copies.append(fcount.clone())
             decode(cur, i, main)
+            pace()
         main.wait_stream(side)
         e1.record(main)
         torch.cuda.synchronize()
@@ -544,10 +609,11 @@ def bench_tier(args) -> int:
         fire_ms = [a.elapsed_time(b) for a, b, timed in fire_ev if timed]
         n_copies = [int(c.cpu()[0]) for c in copies]
         log(f"[tier] {mode} copies, lag {lag}: {args.steps} steps, {ms * 1e3:.2f} us/step (wall {wall:.3f}s); "
-            f"firings {[round(x, 3) for x in fire_ms]} ms; copies {n_copies}")
+            f"firings {[round(x, 3) for x in fire_ms]} ms; copies {n_copies}; side-band host ms {side_host[-4:]}")
         return {"us_per_step": round(ms * 1e3, 2), "lag_steps": lag, "firings_timed": len(fire_ms),
                 "firing_ms": round(sum(fire_ms) / len(fire_ms), 3) if fire_ms else None,
-                "copies_per_firing": n_copies[-len(fire_ms):] if fire_ms else []}
+                "copies_per_firing": n_copies[-len(fire_ms):] if fire_ms else [],
+                "side_band_host_ms": side_host[-len(fire_ms):] if side_host and fire_ms else None}
 
     runs = {"kernel_lag1": steady("kernel", 1), "kernel_lag16": steady("kernel", 16),
             "dma": steady("dma", args.tier_lag)}
@@ -555,8 +621,32 @@ def bench_tier(args) -> int:
     cur = state["cur"]
 
     kept_n = int(cnt[cur].cpu()[0])
-    attn_bytes = kept_n * 2 * slot_bytes + B * prob.n_q_heads * d * (2 + 4) + B * prob.n_q_heads * 4 + kept_n * 4
-    achieved = attn_bytes / (dec_us * 1e-6) / 1e9
+    attn_n, attn_us = kept_n, dec_us
+    level2_info = None
+    if level2:
+        # the dominant kernel alone: attention over the slots Level 2 chose
+        decode(cur, 0, main)
+        torch.cuda.synchronize()
+        attn_n = int(sel_cnt.cpu()[0])
+
+        def attend(i):
+            L.lsa_tier_attend(P, T, qs[i % len(qs)], res_k, res_v, sel, sel_cnt, 0.0, out, lse, ws, ws_bytes, main)
+
+        for i in range(20):
+            attend(i)
+        ae = [(ev(), ev()) for _ in range(n_dec)]
+        for i in range(n_dec):
+            ae[i][0].record(main)
+            attend(i)
+            ae[i][1].record(main)
+        torch.cuda.synchronize()
+        attn_us = 1e3 * sum(a.elapsed_time(b) for a, b in ae) / n_dec
+        nat_bytes = kept_n * (prob.idx_dim * 2 + 4 + 4) + B * prob.nat_heads * (prob.idx_dim * 2 + 4)
+        level2_info = {"core_keep": TIER_K2, "native_heads": prob.nat_heads, "resident_kept": kept_n,
+                       "attended_chunks": attn_n, "native_score_bytes": nat_bytes,
+                       "attention_us_alone": round(attn_us, 2), "level2_us": round(dec_us - attn_us, 2)}
+    attn_bytes = attn_n * 2 * slot_bytes + B * prob.n_q_heads * d * (2 + 4) + B * prob.n_q_heads * 4 + attn_n * 4
+    achieved = attn_bytes / (attn_us * 1e-6) / 1e9
     reserve_bytes = 2 * total * slot_bytes
     result = {
         "metric": METRIC,
@@ -571,7 +661,7 @@ def bench_tier(args) -> int:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": WORKLOADS["tier1m"], "global_batch": B, "seq_len": prob.ctx_tokens[0],
+        "config": {"workload": WORKLOADS[args.workload], "global_batch": B, "seq_len": prob.ctx_tokens[0],
                    "parallelism": "single GPU", "tau": TIER_TAU, "query_correlation_per_firing": TIER_RHO,
                    "k_max": K, "reserve_slots": total},
         "tier": {
@@ -579,13 +669,15 @@ def bench_tier(args) -> int:
             "cold_fetch": {"chunks": cold_n, "ms": round(cold_ms, 3),
                            "pcie_gbs": round(cold_n * 2 * slot_bytes / (cold_ms * 1e-3) / 1e9, 2)},
             "decode_us_alone": round(dec_us, 2),
+            "host_us_per_decode_enqueue": round(host_us, 2),
             "full_change": full,
             "steady_state": runs,
             "kept_chunks": kept_n,
+            "level2": level2_info,
         },
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "attn_kernel (lsa_tier_attend)", "avg_launch_us": round(dec_us, 2),
+                     "kernel": "attn_kernel (lsa_tier_attend)", "avg_launch_us": round(attn_us, 2),
                      "algorithmic_bytes_per_launch": int(attn_bytes)},
     }
     if not args.no_cpu_baseline:
