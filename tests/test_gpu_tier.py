@@ -563,3 +563,40 @@ def test_tier_step_graph_replay():
             assert torch.equal(out_g, out_e) and torch.equal(lse_g, lse_e), f"firing {f} replay {rep}: attention"
         prev = (slot_idx, cnt)
     log("[tier-step] graph replays match the eager calls")
+
+
+def test_tier_step_ties_go_to_the_lower_chunk():
+    """Native index keys repeated so that many resident chunks score exactly
+    alike: the chunks Level 2 keeps at the cut are the lowest ids among the
+    equal ones, as in the oracle (no band: equal keys give equal scores on both
+    sides)."""
+    import torch
+    import paper_2606_09079_amd as L
+    prob = synth.Problem("tier_step_ties", [64 * 600], 64, [100], 8, 2, idx_layers=1, idx_dim=128, core_keep=[37],
+                         nat_heads=32)
+    tc = TierCase(prob, 31, [200])
+    host = tc.dev["host"]
+    nat_k = host["nat_k"].copy()
+    nat_k[:] = nat_k[np.arange(prob.total_chunks) % 5]  # five distinct keys
+    nat_k_d = torch.from_numpy(nat_k.view(np.int16)).cuda()
+    native = oracle.index_score(host["nat_q"][0], host["nat_w"][0], nat_k)
+    assert len(np.unique(native)) <= 5
+    rng = np.random.default_rng(12)
+    kept_set = np.sort(rng.choice(prob.n_chunks[0], 100, replace=False))
+    state = [([-1] * 200, [])]
+    kept, cnt, slot_idx, _ = _plan_and_check(tc, L, [kept_set], None, state)
+    L.lsa_tier_fetch(tc.P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+    sel = torch.full((1, tc.pitch), -5, dtype=torch.int32, device="cuda")
+    sc = torch.full((1,), -5, dtype=torch.int32, device="cuda")
+    out = torch.empty((1, 1, prob.n_q_heads, prob.head_dim), dtype=torch.float32, device="cuda")
+    for k2 in (1, 37, 99, 100, 150):
+        L.lsa_tier_step(tc.P, tc.T, L.Indexer(1, 32, 128), [k2], tc.dev["nat_q"], tc.dev["nat_w"], nat_k_d, kept, cnt,
+                        slot_idx, tc.dev["q"], tc.res_k, tc.res_v, 0.0, out, None, sel, sc, tc.ws, tc.ws_bytes)
+        torch.cuda.synchronize()
+        c = int(sc.cpu()[0])
+        g_slot, g_sel = slot_idx.cpu().numpy()[0], sel.cpu().numpy()[0, :c]
+        slot_to_chunk = {int(g_slot[i]): int(kept_set[i]) for i in range(len(kept_set))}
+        chosen = np.array([slot_to_chunk[int(x)] for x in g_sel], dtype=np.int64)
+        ref = oracle.two_level(kept_set.astype(np.int32), native, k2, prob.n_chunks[0], prob.n_chunks[0])
+        assert np.array_equal(chosen, ref), f"k2 = {k2}: chunks {chosen[:8]} vs oracle {ref[:8]}"
+    log("[tier-step] ties resolved to the lower chunk ids")
