@@ -21,7 +21,9 @@
 //   of that bin staged in LDS.  Two 10-bit digit rounds over the staged
 //   entries give the exact threshold key T and the number of entries equal to
 //   T that the set needs (those with the lowest indices).  A bin with more
-//   entries than LDS holds is refined by passes over the row instead.
+//   entries than LDS holds is refined by passes over the row instead.  The
+//   first two passes read through the caches (the next pass finds part of the
+//   row in the Infinity Cache); the last one streams.
 // golden_vote_kernel -- one thread per (sequence, step, bitmap word): the
 //   votes of the L layers for 32 entries as bit-sliced counters, the theta
 //   test, an OR into the label bitmap and the golden-set size.
@@ -151,7 +153,7 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int e = entry(base, u);
-      v[u] = e < n ? __builtin_nontemporal_load(S + e) : -INFINITY;
+      v[u] = e < n ? S[e] : -INFINITY;
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) mx = fmaxf(mx, v[u]);
@@ -214,7 +216,7 @@ golden_row_kernel(GoldenTable gt, GoldenArgs a) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int e = entry(base, u);
-      v[u] = e < n ? S[e] : -INFINITY;
+      v[u] = e < n ? __builtin_nontemporal_load(S + e) : -INFINITY;
     }
     // the wavefront's kUnroll groups are 2 * kUnroll consecutive bitmap
     // words; lane j < 2 * kUnroll collects word j and stores it
