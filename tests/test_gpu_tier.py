@@ -17,6 +17,7 @@ pinned host mirror into the GPU reserve, and attention over the reserve.
 - lsa_tier_step (Level 2 over the resident set, then attention over the chosen
   slots) chooses the oracle's chunks, up to the float32 band of the k2-th
   native score, and attends over them bit for bit like the full-cache path.
+- All of the above once more at the benchmark's 1M-token size.
 """
 from __future__ import annotations
 
@@ -600,3 +601,91 @@ def test_tier_step_ties_go_to_the_lower_chunk():
         ref = oracle.two_level(kept_set.astype(np.int32), native, k2, prob.n_chunks[0], prob.n_chunks[0])
         assert np.array_equal(chosen, ref), f"k2 = {k2}: chunks {chosen[:8]} vs oracle {ref[:8]}"
     log("[tier-step] ties resolved to the lower chunk ids")
+
+
+def test_tier_full_size_1m():
+    """The host tier at its benchmark size (1,048,576 tokens, K_max 1,638,
+    reserve 3,276 slots, Level 2 keeping 1,024 with 64 native heads), in the
+    launch configuration the benchmark times: two firings of the GPU recall,
+    each planned (equal to the oracle's plan), copied by the copy kernel and
+    attended over the reserve (bitwise equal to the full-cache attention), and
+    lsa_tier_step over the second firing's resident set (the oracle's Level-2
+    set up to the float32 band, sampled rows against the oracle's attention)."""
+    import dataclasses
+    import math
+    import torch
+    import paper_2606_09079_amd as L
+    prob = dataclasses.replace(synth.make_problem("recall1m", 0), name="tier_full_1m", core_keep=[1024],
+                               nat_heads=64)
+    K = prob.keep[0]
+    slots = [2 * K]
+    log(f"[tier-1m] ctx={prob.ctx_tokens} K_max={K} slots={slots} k2=1024")
+    tc = TierCase(prob, 0, slots)
+    host, dev = tc.dev["host"], tc.dev
+    P, ix = tc.P, L.Indexer.from_synth(prob)
+    scores = torch.empty(prob.idx_layers * prob.total_chunks, dtype=torch.float32, device="cuda")
+    kept = [torch.full((1, tc.pitch), -1, dtype=torch.int32, device="cuda") for _ in range(2)]
+    cnt = [torch.zeros(1, dtype=torch.int32, device="cuda") for _ in range(2)]
+    slot_idx = [torch.full((1, tc.pitch), -1, dtype=torch.int32, device="cuda") for _ in range(2)]
+    # firing 1 uses drifted indexer queries, as the benchmark's firings do
+    rng = np.random.default_rng(77)
+    qf = synth.bf16_bits_to_f64(host["idx_q"])
+    q1 = synth.f64_to_bf16_bits(math.sqrt(0.99) * qf + math.sqrt(0.01) * rng.standard_normal(qf.shape))
+    idx_qs = [dev["idx_q"], torch.from_numpy(q1.view(np.int16)).cuda()]
+    state_owner, state_slots = [-1] * slots[0], []
+    sets = []
+    for f in range(2):
+        L.lsa_recall_scores(P, ix, idx_qs[f], dev["idx_w"], dev["idx_k"], scores)
+        L.lsa_recall_select(P, ix, scores, kept[f], cnt[f])
+        prev = (slot_idx[f - 1], cnt[f - 1]) if f else (None, None)
+        L.lsa_tier_plan(P, tc.T, kept[f], cnt[f], prev[0], prev[1], tc.owner, slot_idx[f], tc.fetch, tc.fetch_count)
+        L.lsa_tier_fetch(P, tc.T, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v)
+        torch.cuda.synchronize()
+        c = int(cnt[f].cpu()[0])
+        s_f = kept[f].cpu().numpy()[0, :c].astype(np.int64)
+        sets.append(s_f)
+        new_owner, new_slots, fetch = oracle.tier_plan(state_owner, state_slots, s_f.tolist())
+        assert tc.owner.cpu().numpy().tolist() == new_owner, f"firing {f}: owner table differs from the oracle"
+        assert slot_idx[f].cpu().numpy()[0, :c].tolist() == new_slots, f"firing {f}: slots differ from the oracle"
+        assert int(tc.fetch_count.cpu()[0]) == len(fetch), f"firing {f}: copy count differs from the oracle"
+        state_owner, state_slots = new_owner, new_slots
+        pick = rng.choice(c, size=min(48, c), replace=False)
+        for which, res in (("k", tc.res_k), ("v", tc.res_v)):
+            got = tc.blocks(res, np.asarray(new_slots)[pick])
+            want = tc.blocks(tc.dev[which], s_f[pick])
+            assert bool((got == want).all()), f"firing {f}: sampled reserve {which} blocks differ from the mirror"
+        t_out, t_lse = _tier_attention(tc, L, slot_idx[f], cnt[f])
+        d_out, d_lse = _direct_attention(tc, L, kept[f], cnt[f])
+        torch.cuda.synchronize()
+        assert torch.equal(t_out, d_out) and torch.equal(t_lse, d_lse), f"firing {f}: reserve != full-cache attention"
+        log(f"[tier-1m] firing {f}: kept {c}, copies {len(fetch)}; plan, reserve and attention match")
+    # Level 2 over the resident set of firing 1
+    s1 = sets[1]
+    sel = torch.full((1, tc.pitch), -5, dtype=torch.int32, device="cuda")
+    sc = torch.full((1,), -5, dtype=torch.int32, device="cuda")
+    shp = (1, 1, prob.n_q_heads, prob.head_dim)
+    out = torch.empty(shp, dtype=torch.float32, device="cuda")
+    lse = torch.empty(shp[:3], dtype=torch.float32, device="cuda")
+    L.lsa_tier_step(P, tc.T, L.Indexer(1, 64, prob.idx_dim), [1024], dev["nat_q"], dev["nat_w"], dev["nat_k"],
+                    kept[1], cnt[1], slot_idx[1], dev["q"], tc.res_k, tc.res_v, 0.0, out, lse, sel, sc, tc.ws,
+                    tc.ws_bytes)
+    torch.cuda.synchronize()
+    c = int(sc.cpu()[0])
+    assert c == min(len(s1), 1024)
+    slot_to_chunk = dict(zip(state_slots, s1.tolist()))
+    chosen = np.array([slot_to_chunk[int(x)] for x in sel.cpu().numpy()[0, :c]], dtype=np.int64)
+    assert np.all(np.diff(chosen) > 0), "chosen chunks not ascending"
+    native = oracle.index_score(host["nat_q"][0], host["nat_w"][0], host["nat_k"])
+    ref = oracle.two_level(s1.astype(np.int32), native, 1024, prob.n_chunks[0], prob.n_chunks[0])
+    if not np.array_equal(chosen, ref):
+        tol = parity.index_score_tolerance(host["nat_q"][0], host["nat_w"][0], host["nat_k"])
+        kth = np.sort(native[s1])[::-1][1023]
+        diff = sorted(set(chosen.tolist()) ^ set(ref.tolist()))
+        assert all(abs(native[d] - kth) <= 2 * tol[d] for d in diff), f"Level-2 set differs outside the band {diff[:8]}"
+    chosen_t = torch.full((1, tc.pitch), -1, dtype=torch.int32, device="cuda")
+    chosen_t[0, :c] = torch.from_numpy(chosen.astype(np.int32)).cuda()
+    d_out, d_lse = _direct_attention(tc, L, chosen_t, sc)
+    torch.cuda.synchronize()
+    assert torch.equal(out, d_out) and torch.equal(lse, d_lse), "tier step != full-cache attention over its chunks"
+    _oracle_rows(tc, 0, chosen, out.cpu().numpy(), lse.cpu().numpy(), [(0, h) for h in (0, 5, 17, 31)])
+    log(f"[tier-1m] Level 2 kept {c} of {len(s1)}; attention matches the full cache and the oracle")
