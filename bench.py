@@ -89,6 +89,14 @@ def code_sha(name: str) -> str:
     return hashlib.sha256(text.encode()).hexdigest()[:16]
 
 
+def history_chunks(prob, b: int) -> int:
+    """Complete chunks before the always-resident window of sequence b (the
+    Level-1 index keys a two-level step reads), for the byte count."""
+    W = prob.window_tokens[b] if prob.window_tokens else 0
+    L = prob.ctx_tokens[b]
+    return min(max(L - W, 0) // prob.chunk, L // prob.chunk)
+
+
 def measured_traffic():
     """HBM bytes per attention launch from the committed rocprofv3 counter summary,
     or None when the summary is missing or was taken on other kernel source."""
@@ -293,8 +301,8 @@ def main() -> int:
     attn_bytes = sum(kv_bytes) / len(kv_bytes) + B * Tq * Hq * d * (2 + 4) + B * Tq * Hq * 4 + max(counts) * 4
     if two_level:  # Level-1 keys of the history, native keys of (at most) K_max recalled chunks, queries, gates
         Lay, nh, c = prob.idx_layers, prob.idx_heads, prob.idx_dim
-        hist = sum(prob.history_chunks(b) for b in range(B))
-        rec = sum(min(prob.keep[b], prob.history_chunks(b)) for b in range(B))
+        hist = sum(history_chunks(prob, b) for b in range(B))
+        rec = sum(min(prob.keep[b], history_chunks(prob, b)) for b in range(B))
         emb_bytes = (Lay * hist + rec) * c * 2 + B * (Lay * nh + prob.nat_heads) * (c * 2 + 4)
     elif recall:  # index keys of every layer, plus the indexer queries and gates
         Lay, nh, c = prob.idx_layers, prob.idx_heads, prob.idx_dim
@@ -843,9 +851,9 @@ def cpu_baseline(prob, host, budget_s: float):
     what = ("full step(s) of the same workload" if full else
             "step(s) of sequence 0 of the same workload, attention for its first query token only")
     if prob.core_keep:
-        sel_what = (f"{prob.idx_layers}-layer x {prob.idx_heads}-head index scores of {prob.history_chunks(0):,} "
+        sel_what = (f"{prob.idx_layers}-layer x {prob.idx_heads}-head index scores of {history_chunks(prob, 0):,} "
                     f"history chunks, recall bounded by {prob.keep[0]:,}, native top-{prob.core_keep[0]:,}, "
-                    f"window of {prob.n_chunks[0] - prob.window_start(0)} chunks")
+                    f"window of {prob.n_chunks[0] - history_chunks(prob, 0)} chunks")
     elif prob.idx_layers > 0:
         sel_what = (f"{prob.idx_layers}-layer x {prob.idx_heads}-head index scores of {prob.n_chunks[0]:,} chunks, "
                     f"recall bounded by {prob.keep[0]:,}")

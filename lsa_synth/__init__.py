@@ -166,20 +166,6 @@ class Problem:
         """Chunks of every sequence, a partial last chunk included."""
         return [(L + self.chunk - 1) // self.chunk for L in self.ctx_tokens]
 
-    def window_start(self, b: int) -> int:
-        """First chunk of the always-resident window: the chunks holding the last
-        window_tokens[b] tokens, and always the partial last chunk."""
-        W = self.window_tokens[b] if self.window_tokens else 0
-        return min(max(self.ctx_tokens[b] - W, 0) // self.chunk, self.ctx_tokens[b] // self.chunk)
-
-    def history_chunks(self, b: int) -> int:
-        """Complete chunks before the window: what the two levels select from."""
-        return self.window_start(b)
-
-    def tail_tokens(self, b: int) -> int:
-        """Tokens in the last chunk (chunk when it is complete)."""
-        return self.ctx_tokens[b] - (self.n_chunks[b] - 1) * self.chunk
-
     @property
     def chunk_offsets(self) -> List[int]:
         off = [0]

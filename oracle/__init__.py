@@ -72,9 +72,7 @@ def bind(path: str) -> ctypes.CDLL:
     L.oracle_attention_tokens.restype = ctypes.c_int
     L.oracle_two_level.argtypes = [_P, _I64, _P, _I64, _I64, _I64, _I64, _P]
     L.oracle_two_level.restype = _I64
-    L.oracle_exp_fixed.argtypes = [ctypes.c_float]
-    L.oracle_exp_fixed.restype = ctypes.c_float
-    L.oracle_top_p.argtypes = [_P, _I64, _I64, _I64, _P]
+    L.oracle_top_p.argtypes = [_P, _I64, _I64, _I64, _P, _P, _P]
     L.oracle_top_p.restype = _I64
     L.oracle_golden_labels.argtypes = [_P, _I32, _I32, _I64, _I64, _I64, _I32, _P, _P, _P]
     L.oracle_golden_labels.restype = _I64
@@ -229,12 +227,37 @@ def two_level(recalled: np.ndarray, native: np.ndarray, k2: int, w0: int, n_tota
     return out[:m].copy()
 
 
+def window(ctx_tokens: int, window_tokens: int, chunk: int):
+    """The always-resident window and the history of one sequence.
+
+    Sec. 2.5 keeps the last window_tokens context tokens (and the decoded tail)
+    resident, and Sec. 2.1 scores only complete compressed entries.  Read per
+    chunk: chunk c covers tokens [c C, min((c + 1) C, ctx)); it belongs to the
+    window when it holds one of the last window_tokens tokens or when it is
+    partial (the context ends inside it).  The window is then a run of chunks
+    at the end, w0 .. n_total - 1, and the history is the complete chunks
+    0 .. w0 - 1 before it.  Returns (w0, n_total, tail), tail = tokens in the
+    last chunk."""
+    n_total = (ctx_tokens + chunk - 1) // chunk
+    in_window = []
+    for c in range(n_total):
+        lo, hi = c * chunk, min((c + 1) * chunk, ctx_tokens)
+        holds_recent = hi > ctx_tokens - window_tokens
+        partial = hi - lo < chunk
+        in_window.append(holds_recent or partial)
+    w0 = in_window.index(True) if True in in_window else n_total
+    if not all(in_window[w0:]):
+        raise ValueError("the window is not a run of chunks at the end")
+    return w0, n_total, ctx_tokens - (n_total - 1) * chunk
+
+
 def two_level_for_sequence(prob, inputs: Dict[str, object], b: int):
     """Level 1 (recall over the history before the window), Level 2 and the
     window for sequence b.  Returns (x [L][n_hist], recalled, native [n_hist],
     kept ascending chunk ids, token count of the last chunk)."""
     lo = prob.chunk_offsets[b]
-    n_hist, w0, n_total, tail = prob.history_chunks(b), prob.window_start(b), prob.n_chunks[b], prob.tail_tokens(b)
+    w0, n_total, tail = window(prob.ctx_tokens[b], prob.window_tokens[b] if prob.window_tokens else 0, prob.chunk)
+    n_hist = w0
     L = prob.idx_layers
     x = np.stack([index_score(inputs["idx_q"][b, l], inputs["idx_w"][b, l], inputs["idx_k"][l, lo:lo + n_hist])
                   for l in range(L)]) if n_hist > 0 else np.zeros((L, 0))
@@ -283,19 +306,20 @@ def tier_plan(owner: Sequence[int], old_slots: Sequence[int], kept: Sequence[int
 
 
 # ---------------------------------------------------------------- O4 step
-def exp_fixed(x: float) -> float:
-    """exp(x) for x <= 0 by the oracle's fixed float32 method (Cody-Waite reduction, degree-7 Taylor series)."""
-    return float(lib().oracle_exp_fixed(float(np.float32(x))))
-
-
-def top_p(S: np.ndarray, p_num: int, p_den: int):
-    """Top-p set of one row of float32 logits (Eqs. 7-8): (0/1 marks [n], set size)."""
+def top_p(S: np.ndarray, p_num: int, p_den: int, detail: bool = False):
+    """Top-p set of one row of float32 logits (Eqs. 7-8): (0/1 marks [n], set
+    size), plus, with ``detail``, the entry order (logit desc, index asc) and
+    the float64 mass fraction of every prefix of it."""
     S = _c(S, np.float32)
-    mark = np.zeros(len(S), dtype=np.uint8)
-    size = lib().oracle_top_p(S.ctypes.data, len(S), p_num, p_den, mark.ctypes.data)
+    n = len(S)
+    mark = np.zeros(n, dtype=np.uint8)
+    order = np.empty(n, dtype=np.int64) if detail else None
+    cum = np.empty(n, dtype=np.float64) if detail else None
+    size = lib().oracle_top_p(S.ctypes.data, n, p_num, p_den, mark.ctypes.data,
+                              order.ctypes.data if detail else None, cum.ctypes.data if detail else None)
     if size < 0:
         raise ValueError("oracle_top_p rejected its arguments")
-    return mark, int(size)
+    return (mark, int(size), order, cum) if detail else (mark, int(size))
 
 
 def golden_labels(logits: np.ndarray, p_num: int, p_den: int, theta: int):

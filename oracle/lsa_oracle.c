@@ -40,10 +40,11 @@
  *    the text states it, the smallest set of the most probable entries whose
  *    probability mass reaches p (entries ordered by probability, then by lower
  *    index); Eq. 8 as printed (cumulative mass <= p) would leave the set empty
- *    whenever the most probable entry alone exceeds p.  Probabilities are held
- *    as whole multiples of 2^-40 of the largest one, with the exponential
- *    evaluated by one fixed float32 method (below), so that which entries
- *    reach the mass is an exact integer decision.
+ *    whenever the most probable entry alone exceeds p.  The softmax of Eq. 7
+ *    is taken in float64 with the C library's exp, and "the first j entries
+ *    reach p" is decided in the equivalent form (1 - p) * head >= p * tail of
+ *    the two float64 sums of positive weights, so that p = 1 needs every
+ *    entry and a set whose mass is exactly p (equal weights) is enough.
  */
 #include <math.h>
 #include <stdint.h>
@@ -358,34 +359,6 @@ int64_t oracle_two_level(const int32_t* recalled, int64_t m, const double* nativ
 
 /* ------------------------------------------------------------ golden labels */
 
-/*
- * exp(x) for x <= 0 by a fixed float32 method, so that the result is one
- * determined float on any IEEE machine: Cody and Waite's reduction
- * x = k ln2 + r with k the nearest integer to x / ln2 and ln2 split into a
- * high part with trailing zero bits and a low part (the split fdlibm's expf
- * uses), the Taylor series of e^r to degree 7 (|r| <= ln2 / 2, truncation
- * below 6e-9 relative) in Horner form with fused multiply-adds, and an exact
- * scaling by 2^k.  Below -64 the result is 0 (its weight would be far below
- * 2^-40 anyway).  float32 is the precision in which the GPU takes the same
- * decision.
- */
-float oracle_exp_fixed(float x) {
-  if (x > 0.0f) x = 0.0f;
-  if (x < -64.0f) return 0.0f;
-  const float log2e = 1.44269502e+00f;
-  const float ln2_hi = 6.9314575195e-01f;
-  const float ln2_lo = 1.4286067653e-06f;
-  const float k = rintf(x * log2e);
-  float r = fmaf(-k, ln2_hi, x);
-  r = fmaf(-k, ln2_lo, r);
-  /* 1 / j! for j = 7 down to 0 */
-  const float inv_fact[8] = {1.0f / 5040.0f, 1.0f / 720.0f, 1.0f / 120.0f, 1.0f / 24.0f,
-                             1.0f / 6.0f,    1.0f / 2.0f,   1.0f,          1.0f};
-  float p = inv_fact[0];
-  for (int j = 1; j < 8; ++j) p = fmaf(p, r, inv_fact[j]);
-  return ldexpf(p, (int)k);
-}
-
 typedef struct { float s; int64_t c; } logit_entry;
 
 /* Larger logit first (so larger probability first); equal logits, -0.0 and
@@ -399,40 +372,51 @@ static int by_logit_desc(const void* a, const void* b) {
 }
 
 /*
- * Top-p set of one row of logits (Eq. 7 softmax, Eq. 8 nucleus): mark[s] = 1
- * for the entries of the smallest prefix, in (probability desc, index asc)
- * order, whose mass reaches p_num / p_den.  Returns the size of the set, or -1
- * on a bad argument or allocation failure.  Logits must be finite.
+ * Top-p set of one row of logits (Eq. 7 softmax, Eq. 8 nucleus).  Entries are
+ * ordered by (logit desc, index asc); w_j = exp(S_j - max S) in float64 is the
+ * softmax numerator of the j-th of them (dividing by the sum does not change
+ * which prefix reaches p).  The set is the shortest prefix j = 0 .. J whose
+ * mass head = w_0 + .. + w_J reaches p of the total head + tail, tail =
+ * w_{J+1} + .. + w_{n-1}, i.e. (p_den - p_num) * head >= p_num * tail.
+ * mark[s] = 1 for the entries of the set.  order (nullable) receives the entry
+ * order and cum (nullable) the mass fraction head / (head + tail) of every
+ * prefix.  Returns the size of the set, or -1 on a bad argument or allocation
+ * failure.  Logits must be finite; a weight below the smallest double (a
+ * logit more than about 745 below the maximum) counts as 0.
  */
-int64_t oracle_top_p(const float* S, int64_t n, int64_t p_num, int64_t p_den, uint8_t* mark) {
+int64_t oracle_top_p(const float* S, int64_t n, int64_t p_num, int64_t p_den, uint8_t* mark, int64_t* order,
+                     double* cum) {
   if (n < 1 || p_num < 1 || p_den < p_num) return -1;
-  float m = S[0];
+  double m = (double)S[0];
   for (int64_t s = 1; s < n; ++s)
-    if (S[s] > m) m = S[s];
-  uint64_t* q = (uint64_t*)malloc((size_t)n * sizeof *q);
+    if ((double)S[s] > m) m = (double)S[s];
   logit_entry* v = (logit_entry*)malloc((size_t)n * sizeof *v);
-  if (!q || !v) { free(q); free(v); return -1; }
-  uint64_t Z = 0;
+  double* w = (double*)malloc((size_t)n * sizeof *w);
+  double* tail = (double*)malloc((size_t)(n + 1) * sizeof *tail);
+  if (!v || !w || !tail) { free(v); free(w); free(tail); return -1; }
   for (int64_t s = 0; s < n; ++s) {
-    const float w = oracle_exp_fixed(S[s] - m);
-    q[s] = (uint64_t)((double)w * 1099511627776.0); /* floor(w * 2^40) */
-    Z += q[s];
     v[s].s = S[s];
     v[s].c = s;
   }
   qsort(v, (size_t)n, sizeof *v, by_logit_desc);
+  for (int64_t j = 0; j < n; ++j) w[j] = exp((double)v[j].s - m);
+  tail[n] = 0.0; /* tail[j] = w_j + .. + w_{n-1}, summed from the smallest */
+  for (int64_t j = n - 1; j >= 0; --j) tail[j] = tail[j + 1] + w[j];
   memset(mark, 0, (size_t)n);
-  const unsigned __int128 need = (unsigned __int128)Z * (uint64_t)p_num;
-  uint64_t cum = 0;
-  int64_t size = 0;
+  double head = 0.0;
+  int64_t size = -1;
   for (int64_t j = 0; j < n; ++j) {
-    cum += q[v[j].c];
-    mark[v[j].c] = 1;
-    ++size;
-    if ((unsigned __int128)cum * (uint64_t)p_den >= need) break;
+    head += w[j];
+    if (order) order[j] = v[j].c;
+    if (cum) cum[j] = head / (head + tail[j + 1]);
+    if (size < 0) {
+      mark[v[j].c] = 1;
+      if ((double)(p_den - p_num) * head >= (double)p_num * tail[j + 1]) size = j + 1;
+    }
   }
-  free(q);
   free(v);
+  free(w);
+  free(tail);
   return size;
 }
 
@@ -456,7 +440,7 @@ int64_t oracle_golden_labels(const float* logits, int32_t tau, int32_t L, int64_
   for (int32_t i = 0; i < tau; ++i) {
     memset(votes, 0, (size_t)n * sizeof *votes);
     for (int32_t l = 0; l < L; ++l) {
-      const int64_t size = oracle_top_p(logits + ((int64_t)i * L + l) * n, n, p_num, p_den, mark);
+      const int64_t size = oracle_top_p(logits + ((int64_t)i * L + l) * n, n, p_num, p_den, mark, NULL, NULL);
       if (size < 0) { free(mark); free(votes); return -1; }
       if (nucleus_size) nucleus_size[(int64_t)i * L + l] = (int32_t)size;
       for (int64_t s = 0; s < n; ++s) votes[s] += mark[s];

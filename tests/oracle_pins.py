@@ -414,6 +414,35 @@ def pin_two_level_bruteforce():
         assert got == want, f"two-level brute force rec={rec} native={native.tolist()} k2={k2}"
 
 
+def pin_window_worked_example():
+    """The hand-worked windows of tests/golden/window_worked.json (tails of 1 to
+    63 tokens, windows of 0, 1, 64, 65 tokens and wider than the context, both
+    chunk sizes, the 1M-token two-level workload)."""
+    g = json.load(open(os.path.join(GOLDEN, "window_worked.json")))
+    for case in g["cases"]:
+        got = oracle.window(case["ctx"], case["window"], case["chunk"])
+        assert got == (case["w0"], case["n_total"], case["tail"]), (case, got)
+
+
+def pin_window_token_count():
+    """On random shapes: the window and the history partition the chunks; the
+    window holds every one of the last window_tokens tokens and every token of
+    a partial last chunk; the history's chunks are all complete, and its last
+    one holds no recent token."""
+    rng = np.random.default_rng(23)
+    for _ in range(300):
+        C = int(rng.choice([64, 128]))
+        ctx = int(rng.integers(1, 40 * C))
+        W = int(rng.choice([0, rng.integers(0, 3 * C), rng.integers(0, 50 * C)]))
+        w0, n_total, tail = oracle.window(ctx, W, C)
+        assert n_total * C >= ctx > (n_total - 1) * C and tail == ctx - (n_total - 1) * C
+        assert 0 <= w0 <= n_total
+        assert w0 * C <= max(ctx - W, 0) or w0 == 0, "a history chunk holds a recent token"
+        if w0 < n_total:
+            assert (w0 + 1) * C > ctx - W or (tail < C and w0 == n_total - 1), "the first window chunk is needed"
+        assert w0 * C <= ctx and (w0 < n_total or ctx % C == 0), "a partial chunk is in the history"
+
+
 # ---------------------------------------------------------------- host tier
 def pin_tier_plan_invariants():
     """What the reserve must guarantee, checked on random firings: every kept
@@ -452,6 +481,55 @@ def pin_tier_plan_invariants():
         pass
 
 
+def pin_tier_plan_worked_example():
+    """The hand-worked firings of tests/golden/tier_plan_worked.json: resident
+    chunks keep their slots, slots of the previous set stay protected, free
+    slots go out in ascending order after reuse, a reserve too small raises."""
+    g = json.load(open(os.path.join(GOLDEN, "tier_plan_worked.json")))
+    owner, old = [-1] * g["slots"], []
+    for f in g["firings"]:
+        if f.get("too_small"):
+            try:
+                oracle.tier_plan(owner, old, f["kept"])
+            except ValueError:
+                continue
+            raise AssertionError("a reserve too small must raise")
+        owner, slots, fetch = oracle.tier_plan(owner, old, f["kept"])
+        assert owner == f["owner"] and slots == f["slot_idx"], (f, owner, slots)
+        assert [list(x) for x in fetch] == f["fetch"], (f, fetch)
+        old = slots
+
+
+def pin_tier_plan_bruteforce():
+    """After a few random firings (so the reserve is partly full): among every
+    assignment of the missing kept chunks (ascending) to distinct slots that
+    neither hold a kept chunk nor are read by the previous set, the plan makes
+    the lexicographically smallest one; resident chunks keep their slots."""
+    rng = np.random.default_rng(29)
+    checked = 0
+    for trial in range(120):
+        n, n_slots = int(rng.integers(2, 12)), int(rng.integers(2, 8))
+        owner, old = [-1] * n_slots, []
+        for firing in range(4):
+            kept = sorted(rng.choice(n, size=int(rng.integers(0, min(n, n_slots // 2) + 1)), replace=False).tolist())
+            where = {c: s for s, c in enumerate(owner) if c >= 0}
+            taken = set(old) | {where[c] for c in kept if c in where}
+            missing = [c for c in kept if c not in where]
+            cands = [s for s in range(n_slots) if s not in taken]
+            best = min(itertools.permutations(cands, len(missing)), default=None)
+            try:
+                new_owner, slots, fetch = oracle.tier_plan(owner, old, kept)
+            except ValueError:
+                assert best is None, "a plan exists but the oracle raised"
+                break
+            assert best is not None
+            assert [s for _, s in fetch] == list(best) and [c for c, _ in fetch] == missing
+            assert all(slots[i] == where[c] for i, c in enumerate(kept) if c in where)
+            owner, old = new_owner, slots
+            checked += firing > 0
+    assert checked > 100
+
+
 # ------------------------------------------------------------ golden labels
 def _golden_logits(weights) -> np.ndarray:
     return np.log(np.asarray(weights, dtype=np.float64)).astype(np.float32)
@@ -468,18 +546,6 @@ def pin_golden_worked_example():
         assert golden.tolist() == case["golden_count"], golden
 
 
-def pin_exp_fixed_accuracy():
-    """The oracle's fixed float32 exponential against the float64 exp of the
-    same float32 argument: within 3 * 2^-24 relative (a few float32 rounding
-    steps) on [-64, 0], exactly 1 at 0, 0 below -64."""
-    xs = np.concatenate([-np.linspace(0.0, 64.0, 4001), -np.logspace(-40, 1.8, 400), [-0.34657359, -0.34657360]])
-    for x in xs.astype(np.float32):
-        got, want = oracle.exp_fixed(float(x)), math.exp(float(x))
-        assert abs(got - want) <= 3.0 * 2.0 ** -24 * want, (x, got, want)
-    assert oracle.exp_fixed(0.0) == 1.0
-    assert oracle.exp_fixed(-64.5) == 0.0 and oracle.exp_fixed(-1000.0) == 0.0
-
-
 def _numpy_nucleus(S: np.ndarray, p: float):
     """Top-p set from numpy: float64 softmax, stable sort by (logit desc, index
     asc), cumulative mass; returns (set, cumulative masses in that order)."""
@@ -492,10 +558,9 @@ def _numpy_nucleus(S: np.ndarray, p: float):
 
 
 def pin_top_p_library_softmax():
-    """Random rows against numpy's softmax, sort and cumulative sum.  The two
-    may differ only where numpy's cumulative mass sits within 1e-6 of p at the
-    cut (the oracle's weights are float32, held in units of 2^-40 of the
-    largest)."""
+    """Random rows against scipy's softmax, numpy's stable sort and cumulative
+    sum.  The two may differ only where numpy's cumulative mass sits within
+    1e-12 of p at the cut (float64 rounding of the two sums)."""
     rng = np.random.default_rng(41)
     for trial in range(300):
         n = int(rng.integers(1, 3000))
@@ -510,50 +575,57 @@ def pin_top_p_library_softmax():
         assert size == len(got)
         if got != want:
             k = len(want)
-            near = abs(cum[k - 1] - num / den) <= 1e-6 or (k >= 2 and abs(cum[k - 2] - num / den) <= 1e-6) \
-                or (num == den and S.max() - S.min() > 27.0)
+            near = abs(cum[k - 1] - num / den) <= 1e-12 or (k >= 2 and abs(cum[k - 2] - num / den) <= 1e-12)
             assert near, (trial, n, scale, len(got), len(want))
 
 
 def pin_top_p_bruteforce():
-    """Tiny rows with integer weights: over all subsets whose probability mass
-    reaches p, the smallest ones; among those the most probable; among equals
-    the lexicographically smallest index list -- the top-p set by its own
-    definition, with exact fractions."""
+    """Tiny rows: over all subsets whose probability mass reaches p, the
+    smallest ones; among those the most probable; among equals the
+    lexicographically smallest index list -- the top-p set by its own
+    definition, in exact rational arithmetic over the float64 weights
+    exp(S - max S).  Rows where some subset's mass lies within 1e-12 of p
+    (but not on it) are skipped: there float64 sums may round either way."""
     from fractions import Fraction
     rng = np.random.default_rng(43)
     checked = 0
     for trial in range(400):
         n = int(rng.integers(1, 8))
-        wts = [int(x) for x in rng.integers(1, 6, size=n)]
-        num, den = [(3, 5), (1, 2), (2, 3), (1, 7), (6, 7)][trial % 5]
-        p, tot = Fraction(num, den), sum(wts)
+        if trial % 3 == 0:  # a coarse grid of logits: ties, masses that are exact multiples
+            S = (rng.integers(-4, 3, size=n) * 0.5).astype(np.float32)
+        else:
+            S = (rng.standard_normal(n) * float(rng.choice([0.3, 1.0, 3.0]))).astype(np.float32)
+        num, den = [(3, 5), (1, 2), (2, 3), (1, 7), (6, 7), (1, 1)][trial % 6]
+        p = Fraction(num, den)
+        m = max(float(x) for x in S)
+        wts = [Fraction(math.exp(float(x) - m)) for x in S]
+        tot = sum(wts)
+        masses = {}
         best = None
         for mask in range(1, 1 << n):
             idx = [s for s in range(n) if mask >> s & 1]
-            mass = Fraction(sum(wts[s] for s in idx), tot)
+            mass = sum(wts[s] for s in idx) / tot
+            masses[mask] = mass
             if mass < p:
                 continue
             key = (len(idx), -mass, idx)
             if best is None or key < best[0]:
                 best = (key, idx)
-        # skip rows where some subset's mass lies within float rounding of p,
-        # exactly on it included: logits ln(w) round, so such a mass can land on
-        # either side (equal logits, whose masses are exact, are pinned below)
-        masses = {Fraction(sum(wts[s] for s in range(n) if m >> s & 1), tot) for m in range(1 << n)}
-        if any(abs(float(x - p)) < 1e-6 for x in masses):
+        if any(0 < abs(float(x - p)) < 1e-12 for x in masses.values()):
             continue
-        mark, size = oracle.top_p(_golden_logits(wts), num, den)
-        assert np.nonzero(mark)[0].tolist() == best[1], (wts, num, den, best[1])
+        mark, size = oracle.top_p(S, num, den)
+        assert np.nonzero(mark)[0].tolist() == best[1], (S.tolist(), num, den, best[1])
+        assert size == len(best[1])
         checked += 1
-    assert checked > 150
+    assert checked > 200
 
 
 def pin_top_p_boundaries():
     """Equal logits make every mass exact: a set that reaches p exactly is
     enough (3 of 5 equal entries at p = 3/5, the lower indices); the most
-    probable entry alone when it exceeds p; the whole support at p = 1; the
-    first maximum alone for a tiny p."""
+    probable entry alone when it exceeds p; at p = 1 every entry, however small
+    its weight; the first maximum alone for a tiny p; and the order of the
+    prefix with its mass fractions."""
     mark, size = oracle.top_p(np.zeros(5, np.float32), 3, 5)
     assert mark.tolist() == [1, 1, 1, 0, 0] and size == 3
     mark, size = oracle.top_p(np.zeros(5, np.float32), 61, 100)
@@ -561,10 +633,16 @@ def pin_top_p_boundaries():
     mark, size = oracle.top_p(np.array([0.0, 5.0, 1.0], np.float32), 3, 5)
     assert mark.tolist() == [0, 1, 0]
     S = np.array([0.0, -40.0, -1.0, 0.0], np.float32)
-    mark, size = oracle.top_p(S, 1, 1)  # weights below 2^-40 of the largest hold no mass
-    assert mark.tolist() == [1, 0, 1, 1]
+    mark, size = oracle.top_p(S, 1, 1)  # every weight is positive: p = 1 needs them all
+    assert mark.tolist() == [1, 1, 1, 1] and size == 4
     mark, size = oracle.top_p(np.array([2.0, 3.0, 3.0, -0.0, 0.0], np.float32), 1, 1 << 30)
     assert mark.tolist() == [0, 1, 0, 0, 0]
+    # order (logit desc, index asc; -0.0 equal to +0.0) and prefix masses
+    mark, size, order, cum = oracle.top_p(np.array([0.0, 1.0, -0.0, 1.0], np.float32), 1, 2, detail=True)
+    assert order.tolist() == [1, 3, 0, 2]
+    e = math.e
+    assert np.allclose(cum, [e / (2 * e + 2), 2 * e / (2 * e + 2), (2 * e + 1) / (2 * e + 2), 1.0], rtol=1e-15)
+    assert size == 2 and mark.tolist() == [0, 1, 0, 1]  # 2e / (2e + 2) = 0.731 >= 1/2, e / (2e + 2) < 1/2
 
 
 def pin_golden_votes_and_union():
@@ -599,7 +677,8 @@ ALL_PINS = [
     pin_recall_worked_example, pin_index_score_single_head, pin_index_score_relu_identities,
     pin_index_score_head_permutation, pin_recall_sigmoid_threshold, pin_recall_or_bruteforce,
     pin_recall_boundaries, pin_attention_tokens_reduces_to_chunks, pin_two_level_worked_example,
-    pin_two_level_bruteforce, pin_tier_plan_invariants,
-    pin_golden_worked_example, pin_exp_fixed_accuracy, pin_top_p_library_softmax, pin_top_p_bruteforce,
+    pin_two_level_bruteforce, pin_window_worked_example, pin_window_token_count, pin_tier_plan_invariants,
+    pin_tier_plan_worked_example, pin_tier_plan_bruteforce,
+    pin_golden_worked_example, pin_top_p_library_softmax, pin_top_p_bruteforce,
     pin_top_p_boundaries, pin_golden_votes_and_union,
 ]

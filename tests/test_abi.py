@@ -185,11 +185,15 @@ def test_two_level_sizes_and_validation():
 
 def test_two_level_presets_size():
     import lsa_synth
+    import oracle
     for name in lsa_synth.TWO_LEVEL_PRESETS:
         prob = lsa_synth.make_problem(name, 0)
         ms, ws = L.lsa_two_level_sizes(L.Problem.from_synth(prob), L.TwoLevel.from_synth(prob))
-        assert ms == max(min(prob.core_keep[b], prob.keep[b], prob.history_chunks(b)) + prob.n_chunks[b]
-                         - prob.window_start(b) for b in range(prob.batch))
+        want = 0
+        for b in range(prob.batch):
+            w0, n_total, _ = oracle.window(prob.ctx_tokens[b], prob.window_tokens[b], prob.chunk)
+            want = max(want, min(prob.core_keep[b], prob.keep[b], w0) + n_total - w0)
+        assert ms == want
 
 
 def test_tier_sizes_and_validation():

@@ -2,7 +2,9 @@
 
 Each mutant is a one-line textual change to ``oracle/lsa_oracle.c`` -- a
 reversed tie-break, a dropped scale, a wrong sign, a wrong token or dimension
-index, a dropped term -- compiled on the CPU into a throw-away library.  The
+index, a dropped term -- compiled on the CPU into a throw-away library, or to
+the plain-Python parts of ``oracle/__init__.py`` (the two-level window and the
+host tier's residency plan), executed into a throw-away module.  The
 test passes when at least one pin fails for every mutant, which shows the pins
 can tell a plausible slip in the oracle from the real thing.
 """
@@ -18,18 +20,22 @@ import oracle_pins as P
 SRC = os.path.join(os.path.dirname(oracle.__file__), "lsa_oracle.c")
 
 MUTANTS = {
-    "top_p_strict_mass": ("if ((unsigned __int128)cum * (uint64_t)p_den >= need) break;",
-                          "if ((unsigned __int128)cum * (uint64_t)p_den > need) break;"),
+    "top_p_strict_mass": ("if ((double)(p_den - p_num) * head >= (double)p_num * tail[j + 1]) size = j + 1;",
+                          "if ((double)(p_den - p_num) * head > (double)p_num * tail[j + 1]) size = j + 1;"),
+    "top_p_tail_includes_entry": ("if ((double)(p_den - p_num) * head >= (double)p_num * tail[j + 1]) size = j + 1;",
+                                  "if ((double)(p_den - p_num) * head >= (double)p_num * tail[j]) size = j + 1;"),
+    "top_p_head_for_total": ("if ((double)(p_den - p_num) * head >= (double)p_num * tail[j + 1]) size = j + 1;",
+                             "if ((double)p_den * head >= (double)p_num * tail[j + 1]) size = j + 1;"),
     "top_p_tie_reversed": ("  return (x->c > y->c) - (x->c < y->c);\n}\n\n/*\n * Top-p set",
                            "  return (x->c < y->c) - (x->c > y->c);\n}\n\n/*\n * Top-p set"),
     "top_p_least_probable_first": ("  if (x->s > y->s) return -1;\n  if (x->s < y->s) return 1;\n"
                                    "  return (x->c > y->c) - (x->c < y->c);\n}\n\n/*\n * Top-p set",
                                    "  if (x->s > y->s) return 1;\n  if (x->s < y->s) return -1;\n"
                                    "  return (x->c > y->c) - (x->c < y->c);\n}\n\n/*\n * Top-p set"),
-    "top_p_mass_not_summed": ("    Z += q[s];\n", "    Z = q[s];\n"),
-    "exp_fixed_no_low_part": ("  r = fmaf(-k, ln2_lo, r);\n", ""),
-    "exp_fixed_short_series": ("for (int j = 1; j < 8; ++j) p = fmaf(p, r, inv_fact[j]);",
-                               "for (int j = 1; j < 7; ++j) p = fmaf(p, r, inv_fact[j]);"),
+    "top_p_tail_not_summed": ("for (int64_t j = n - 1; j >= 0; --j) tail[j] = tail[j + 1] + w[j];",
+                              "for (int64_t j = n - 1; j >= 0; --j) tail[j] = w[j];"),
+    "top_p_logits_doubled": ("for (int64_t j = 0; j < n; ++j) w[j] = exp((double)v[j].s - m);",
+                                       "for (int64_t j = 0; j < n; ++j) w[j] = exp(2.0 * ((double)v[j].s - m));"),
     "golden_vote_strict": ("if (votes[s] >= theta) {", "if (votes[s] > theta) {"),
     "golden_union_last_step": ("    memset(votes, 0, (size_t)n * sizeof *votes);\n",
                                "    memset(votes, 0, (size_t)n * sizeof *votes);\n    memset(label, 0, (size_t)n);\n"),
@@ -91,6 +97,50 @@ MUTANTS = {
     "two_level_budget_ignored": ("    if (m > k2) {", "    if (m > n_hist) {"),
     "two_level_window_short": ("  for (int64_t c = w0; c < n_total; ++c)", "  for (int64_t c = w0 + 1; c < n_total; ++c)"),
 }
+
+
+# Mutants of the plain-Python parts of the oracle (oracle/__init__.py): the
+# window of the two-level path and the host tier's residency plan.
+PY_MUTANTS = {
+    "window_whole_chunks_only": ("        holds_recent = hi > ctx_tokens - window_tokens\n",
+                                 "        holds_recent = lo >= ctx_tokens - window_tokens\n"),
+    "window_partial_not_resident": ("        in_window.append(holds_recent or partial)\n",
+                                    "        in_window.append(holds_recent)\n"),
+    "window_tail_off_by_one": ("    return w0, n_total, ctx_tokens - (n_total - 1) * chunk\n",
+                               "    return w0, n_total, ctx_tokens - n_total * chunk + chunk - 1\n"),
+    "tier_free_slots_descending": ("    free = [s for s in range(len(owner)) if s not in protected]\n",
+                                   "    free = [s for s in reversed(range(len(owner))) if s not in protected]\n"),
+    "tier_previous_set_unprotected": ("    protected = set(old_slots) | {where[c] for c in kept if c in where}\n",
+                                      "    protected = {where[c] for c in kept if c in where}\n"),
+    "tier_missing_descending": ("    fetch = list(zip(missing, free))\n", "    fetch = list(zip(reversed(missing), free))\n"),
+    "tier_resident_recopied": ("    missing = [c for c in kept if c not in where]\n", "    missing = list(kept)\n"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PY_MUTANTS))
+def test_python_mutant_is_caught(name):
+    import types
+    old, new = PY_MUTANTS[name]
+    path = os.path.join(os.path.dirname(oracle.__file__), "__init__.py")
+    src = open(path).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique/present"
+    mod = types.ModuleType("oracle_mutant")
+    mod.__file__ = path
+    exec(compile(src.replace(old, new), path, "exec"), mod.__dict__)
+    saved = {f: getattr(oracle, f) for f in ("window", "tier_plan")}
+    for f in saved:
+        setattr(oracle, f, getattr(mod, f))
+    failed = []
+    try:
+        for pin in P.ALL_PINS:
+            try:
+                pin()
+            except (AssertionError, ValueError, KeyError):
+                failed.append(pin.__name__)
+    finally:
+        for f, fn in saved.items():
+            setattr(oracle, f, fn)
+    assert failed, f"no pin catches mutant {name}"
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))

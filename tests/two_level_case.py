@@ -77,12 +77,13 @@ def run_two_level_case(prob, seed: int, rows: Optional[Sequence[Tuple[int, int]]
         assert 0 <= c <= max_sel, f"seq {b}: kept count {c}"
         got = g_sel[b, :c].astype(np.int64)
         assert np.all(np.diff(got) > 0), f"seq {b}: kept ids not strictly ascending"
-        w0, n_total = prob.window_start(b), prob.n_chunks[b]
+        w0, n_total, _ = oracle.window(prob.ctx_tokens[b], prob.window_tokens[b] if prob.window_tokens else 0,
+                                       prob.chunk)
         assert np.array_equal(got[got >= w0], np.arange(w0, n_total)), f"seq {b}: window chunks differ"
         if np.array_equal(got, kept):
             modes[b] = "exact"
         else:
-            n_hist = prob.history_chunks(b)
+            n_hist = w0
             tol_x = np.stack([parity.index_score_tolerance(host["idx_q"][b, l], host["idx_w"][b, l],
                                                            host["idx_k"][l, lo:lo + n_hist])
                               for l in range(prob.idx_layers)])
