@@ -94,6 +94,7 @@ extern "C" {
 #define LSA_MAX_TIER_SLOTS 65536   /* reserve slots per sequence */
 #define LSA_MAX_GOLDEN_ENTRIES 4194304 /* entries per sequence of the golden-label pipeline */
 #define LSA_MAX_GOLDEN_LAYERS 63   /* layers voting in the golden-label pipeline */
+#define LSA_SCRATCH_BYTES (64u << 20) /* device scratch of lsa_decode_step_noalloc, per GPU */
 
 typedef enum {
   LSA_OK = 0,
@@ -225,6 +226,26 @@ lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const vo
                            const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
                            float softmax_scale, float* out, float* lse, int32_t* sel_idx,
                            int32_t* sel_count, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * lsa_decode_step for callers that cannot allocate device memory (code under
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same step, with the same kernels and results, but no workspace argument.
+ * Its scratch (scores, kept ids when sel_idx is NULL, split-K partials) lives
+ * in one file-scope device array of LSA_SCRATCH_BYTES bytes, which every GPU
+ * the library runs on holds until the process ends.  The call allocates and
+ * frees nothing; on its first call on a device (the current one) it looks up
+ * that device's address of the array.  A problem whose lsa_workspace_size
+ * exceeds LSA_SCRATCH_BYTES returns LSA_ERR_WORKSPACE before any launch.
+ * Every call on one GPU uses that GPU's one array: calls that overlap in time
+ * on one GPU (other streams, other host threads) race, and the caller must
+ * order them.  The array keeps the last call's contents; no call depends on
+ * them.
+ */
+lsa_status lsa_decode_step_noalloc(const lsa_problem* p, const void* query_emb, const void* chunk_emb,
+                                   const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                   float softmax_scale, float* out, float* lse, int32_t* sel_idx,
+                                   int32_t* sel_count, void* stream);
 
 /*
  * Recall path.  Shapes: the problem must have n_lookahead == 1 (one query token

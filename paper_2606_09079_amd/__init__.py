@@ -13,6 +13,7 @@ ctypes binding in :mod:`.lsa`; importing it loads ``liblsa.so`` and raises if
 that is not possible.
 """
 from .lsa import (LIB, Golden, Indexer, LsaError, Problem, Tier, TwoLevel, lsa_decode_step,  # noqa: F401
+                  lsa_decode_step_noalloc,
                   lsa_golden_labels, lsa_golden_sizes, lsa_max_keep, lsa_max_sel, lsa_recall_scores,
                   lsa_recall_select, lsa_recall_step, lsa_score_chunks, lsa_sparse_decode_attn, lsa_tier_attend,
                   lsa_tier_fetch, lsa_tier_fetch_dma, lsa_tier_plan, lsa_tier_reset, lsa_tier_sizes, lsa_tier_step,

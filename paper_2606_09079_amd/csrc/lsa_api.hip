@@ -7,6 +7,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "lsa_internal.h"
 
@@ -464,6 +465,33 @@ lsa_status make_golden_plan(const lsa_golden* g, GoldenPlan* gp) {
   return LSA_OK;
 }
 
+// Scratch of lsa_decode_step_noalloc: one array per GPU, held until the
+// process ends.  In host code `scratch` only names the symbol; its device
+// address on each GPU comes from hipGetSymbolAddress with that GPU current.
+__device__ __align__(256) uint8_t scratch[LSA_SCRATCH_BYTES];
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+lsa_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(LSA_ERR_UNSUPPORTED, "device %d: the scratch array serves devices 0 .. %d", dev,
+                kMaxScratchDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (ptr == nullptr) return fail(LSA_ERR_HIP, "hipGetSymbolAddress(scratch) gave no address");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return LSA_OK;
+}
+
 }  // namespace
 }  // namespace lsa
 
@@ -598,6 +626,21 @@ lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const vo
   LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, true, s), "score launch");
   LSA_TRY(run_topk(p, P, true, scores, sel, cnt, nullptr, ws, s));
   return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
+}
+
+lsa_status lsa_decode_step_noalloc(const lsa_problem* p, const void* query_emb, const void* chunk_emb,
+                                   const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                   float softmax_scale, float* out, float* lse, int32_t* sel_idx,
+                                   int32_t* sel_count, void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P));
+  if (P.ws_total > LSA_SCRATCH_BYTES)
+    return fail(LSA_ERR_WORKSPACE, "the step needs %zu bytes of scratch; the allocation-free call has %zu", P.ws_total,
+                (size_t)LSA_SCRATCH_BYTES);
+  void* ws = nullptr;
+  LSA_TRY(scratch_of_current_device(&ws));
+  return lsa_decode_step(p, query_emb, chunk_emb, q, k_cache, v_cache, softmax_scale, out, lse, sel_idx, sel_count,
+                         ws, LSA_SCRATCH_BYTES, stream);
 }
 
 lsa_status lsa_recall_scores(const lsa_problem* p, const lsa_indexer* ix, const void* idx_q, const float* idx_w,

@@ -33,7 +33,7 @@ EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_valida
            "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
            "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step", "lsa_tier_sizes", "lsa_tier_reset",
            "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_fetch_dma", "lsa_tier_attend", "lsa_tier_step",
-           "lsa_golden_sizes", "lsa_golden_labels")
+           "lsa_golden_sizes", "lsa_golden_labels", "lsa_decode_step_noalloc")
 
 
 class lsa_problem(ctypes.Structure):
@@ -111,6 +111,7 @@ def _load() -> ctypes.CDLL:
     lib.lsa_tier_step.argtypes = [pp, rp, ip, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P,
                                   _P, _P, ctypes.c_size_t, _P]
     lib.lsa_tier_attend.argtypes = [pp, rp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
+    lib.lsa_decode_step_noalloc.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P]
     gp = ctypes.POINTER(lsa_golden)
     lib.lsa_golden_sizes.argtypes = [gp, ctypes.POINTER(ctypes.c_size_t)]
     lib.lsa_golden_labels.argtypes = [gp, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
@@ -300,6 +301,13 @@ def lsa_decode_step(p: Problem, query_emb, chunk_emb, q, k_cache, v_cache, softm
     _check(LIB.lsa_decode_step(p.ref, _ptr(query_emb), _ptr(chunk_emb), _ptr(q), _ptr(k_cache), _ptr(v_cache),
                                float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx), _ptr(sel_count), _ptr(ws),
                                ws_bytes, _stream(stream)), "lsa_decode_step")
+
+
+def lsa_decode_step_noalloc(p: Problem, query_emb, chunk_emb, q, k_cache, v_cache, softmax_scale: float, out,
+                            lse=None, sel_idx=None, sel_count=None, stream=None) -> None:
+    _check(LIB.lsa_decode_step_noalloc(p.ref, _ptr(query_emb), _ptr(chunk_emb), _ptr(q), _ptr(k_cache),
+                                       _ptr(v_cache), float(softmax_scale), _ptr(out), _ptr(lse), _ptr(sel_idx),
+                                       _ptr(sel_count), _stream(stream)), "lsa_decode_step_noalloc")
 
 
 def lsa_recall_scores(p: Problem, ix: Indexer, idx_q, idx_w, idx_k, scores, stream=None) -> None:

@@ -324,3 +324,17 @@ def test_golden_sizes_and_validation():
     assert lib.lsa_golden_labels(g.ref, FAKE, FAKE, FAKE, FAKE + 4, None, FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
     assert lib.lsa_golden_labels(g.ref, FAKE, FAKE, FAKE, None, None, FAKE, ws - 1, None) == B.LSA_ERR_WORKSPACE
     assert lib.lsa_golden_labels(g.ref, FAKE, FAKE, FAKE, None, None, None, ws, None) == B.LSA_ERR_WORKSPACE
+
+
+def test_noalloc_rejects_a_step_beyond_its_scratch():
+    """lsa_decode_step_noalloc refuses, before any launch, a problem whose
+    workspace would not fit LSA_SCRATCH_BYTES (64 MiB), and names both sizes."""
+    big = L.Problem([64 * 262144] * 64, 64, [1000] * 64, 8, 8)
+    assert L.lsa_workspace_size(big) > 64 << 20
+    rc = L.LIB.lsa_decode_step_noalloc(big.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None, None)
+    assert rc == B.LSA_ERR_WORKSPACE
+    assert b"67108864" in L.LIB.lsa_last_error()
+    # a bad problem is still reported as such, ahead of the size
+    bad = L.Problem([100], 64, [1], 8, 8)
+    assert L.LIB.lsa_decode_step_noalloc(bad.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None,
+                                         None) == B.LSA_ERR_INVALID_ARG
