@@ -89,6 +89,55 @@ def code_sha(name: str) -> str:
     return hashlib.sha256(text.encode()).hexdigest()[:16]
 
 
+def part_times(L, prob, P, ix, dev, rot, max_sel, stream, attn_us: float, n: int):
+    """Average microseconds of the step's parts, each entry point launched on
+    its own between HIP events on the launch stream: scoring, selection (with
+    the union for several lookahead queries), attention (split + combine,
+    measured with the roofline).  Recall workloads score with lsa_recall_scores
+    and select with lsa_recall_select."""
+    import torch
+    B, Q = prob.batch, prob.n_lookahead
+    recall = prob.idx_layers > 0
+    if recall:
+        scores = torch.empty(prob.idx_layers * prob.total_chunks, dtype=torch.float32, device="cuda")
+    else:
+        scores = torch.empty(Q * prob.total_chunks, dtype=torch.int32 if prob.emb_dtype == "i8" else torch.float32,
+                             device="cuda")
+    sel = torch.empty(B, max_sel, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(B, dtype=torch.int32, device="cuda")
+    pq = torch.empty(B, Q, L.lsa_max_keep(P), dtype=torch.int32, device="cuda") if Q > 1 else None
+
+    def score(i):
+        r = rot[i % len(rot)]
+        if recall:
+            L.lsa_recall_scores(P, ix, r["idx_q"], r["idx_w"], dev["idx_k"], scores, stream)
+        else:
+            L.lsa_score_chunks(P, r["qe"], dev["E"], scores, stream)
+
+    def select(i):
+        if recall:
+            L.lsa_recall_select(P, ix, scores, sel, cnt, stream)
+        else:
+            L.lsa_topk_chunks(P, scores, sel, cnt, pq, stream=stream)
+
+    res = {}
+    for name, fn in (("score", score), ("select", select)):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for i in range(n):
+            if name == "select":
+                score(i)
+            evs[i][0].record(stream)
+            fn(i)
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        res[name] = round(1e3 * sum(a.elapsed_time(b) for a, b in evs) / n, 2)
+    res["attention"] = round(attn_us, 2)
+    res["how"] = ("each entry point on its own between HIP events (score: lsa_score_chunks / lsa_recall_scores, "
+                  "which write scores where the fused step writes order keys; select: lsa_topk_chunks / "
+                  "lsa_recall_select; attention: lsa_sparse_decode_attn, split kernel + combine)")
+    return res
+
+
 def history_chunks(prob, b: int) -> int:
     """Complete chunks before the always-resident window of sequence b (the
     Level-1 index keys a two-level step reads), for the byte count."""
@@ -262,6 +311,11 @@ def main() -> int:
     att_ms = [a.elapsed_time(b) for a, b in evs]
     att_avg_us = 1e3 * sum(att_ms) / len(att_ms)
 
+    # ---- the step's parts, each entry point on its own with HIP events around
+    # it (the fused step runs the same kernels back to back)
+    parts_us = part_times(L, prob, P, ix, dev, rot, max_sel, stream, attn_us=att_avg_us,
+                          n=max(20, min(args.steps, 200))) if not two_level else None
+
     counts = [int(c.cpu().sum()) for c in cnts]
     C_, Hkv_ = prob.chunk, prob.n_kv_heads
     approx_step_bytes = sum(counts) / len(counts) * C_ * Hkv_ * d * 4
@@ -328,8 +382,16 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": WORKLOADS[args.workload], "global_batch": B, "seq_len": prob.ctx_tokens[0],
                    "parallelism": "single GPU", "kept_chunks_per_step": counts[0], "rotations": len(rot)},
+        # the whole fused step against the HBM roofline: chunk embeddings (or
+        # index keys) + kept K/V + q, out, lse and ids over the timed step time
+        "step_roofline": {"bound": "hbm", "achieved": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "algorithmic_bytes_per_step": int(step_bytes), "us_per_step": round(ms_per_step * 1e3, 2),
+                          "us_per_step_at_70pct": round(step_bytes / (0.7 * HBM_PEAK_GBS * 1e9) * 1e6, 2)},
         "step_gbs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "step_roofline_frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "parts_us": parts_us,
         "step_us": {"p10": pct(0.10), "median": pct(0.50), "p90": pct(0.90), "samples": n_dist,
                     "flush_mib_between_samples": flush_mib},
         "step_gbs_at_median": round(step_bytes / (pct(0.50) * 1e-6) / 1e9, 1),
@@ -337,7 +399,8 @@ def main() -> int:
         "step_frac_of_read_ceiling": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / read_gbs, 4) if read_gbs else None,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "attn_kernel (lsa_sparse_decode_attn)", "avg_launch_us": round(att_avg_us, 2),
+                     "kernel": "attention: split kernel + combine (one lsa_sparse_decode_attn call)",
+                     "avg_launch_us": round(att_avg_us, 2),
                      "algorithmic_bytes_per_launch": int(attn_bytes),
                      "frac_of_read_ceiling": round(achieved / read_gbs, 4) if read_gbs else None},
     }
@@ -800,7 +863,11 @@ def golden_cpu_baseline(gp, budget_s: float):
 def cpu_baseline(prob, host, budget_s: float):
     """The CPU oracle, as it stands, on one full step of the same workload
     (score all chunks, top-k, attention for every query head), repeated while
-    the time bound allows.  Independent KV-head groups run on parallel threads."""
+    the time bound allows.  The attention of each KV-head group runs as token
+    ranges on parallel threads, one task per (group, range) and as many tasks
+    as the process has cores; the ranges' outputs merge through their
+    log-sum-exps, out = sum_r exp(lse_r - lse) out_r with lse the logsumexp of
+    the lse_r."""
     import numpy as np
 
     import lsa_synth as synth
@@ -818,19 +885,29 @@ def cpu_baseline(prob, host, budget_s: float):
     Hkv, G = prob.n_kv_heads, prob.group
     kv = {(w, g): synth.kv_head_sparse(prob, 0, w, 0, g, kept) for g in range(Hkv) for w in ("k", "v")}
     log(f"[bench] cpu baseline inputs prepared in {time.time() - t_prep:.1f}s")
-    threads = min(Hkv, os.cpu_count() or 1)
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    ranges = max(1, -(-cores // Hkv))
+    threads = min(cores, Hkv * ranges)
 
     def one_step():
         kept_s = select()
-
         toks = oracle.kept_tokens(kept_s, prob.chunk, prob.ctx_tokens[0])
+        cuts = [len(toks) * r // ranges for r in range(ranges + 1)]
 
-        def head(g):
+        def part(task):
+            g, r = divmod(task, ranges)
             qr = np.stack([host["q"][0, 0, g * G + j] for j in range(G)])
-            return oracle.attention_tokens(qr, kv[("k", g)], kv[("v", g)], toks)
+            return oracle.attention_tokens(qr, kv[("k", g)], kv[("v", g)], toks[cuts[r]:cuts[r + 1]])
 
         with cf.ThreadPoolExecutor(threads) as ex:
-            list(ex.map(head, range(Hkv)))
+            res = list(ex.map(part, range(Hkv * ranges)))
+        for g in range(Hkv):
+            outs = np.stack([res[g * ranges + r][0] for r in range(ranges)])
+            lses = np.stack([res[g * ranges + r][1] for r in range(ranges)])
+            lse = np.logaddexp.reduce(lses, axis=0)
+            w = np.exp(lses - lse[None, :])
+            w[~np.isfinite(w)] = 0.0
+            (w[:, :, None] * outs).sum(axis=0)
 
     reps, t0 = 0, time.perf_counter()
     while True:
@@ -861,8 +938,9 @@ def cpu_baseline(prob, host, budget_s: float):
         sel_what = f"score {prob.n_chunks[0]:,} chunks, top-{prob.keep[0]:,}"
     return {"value": round(reps / el, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} {what} ({sel_what}, fp64 attention for {prob.n_q_heads} query heads) in {el:.1f}s; "
-                      f"KV-head groups on {threads} threads (os.cpu_count() = {os.cpu_count()}, OMP_NUM_THREADS = "
-                      f"{os.environ.get('OMP_NUM_THREADS', 'unset')})",
+                      f"{Hkv} KV-head groups x {ranges} token ranges on {threads} threads (cores available "
+                      f"{cores}, os.cpu_count() = {os.cpu_count()}, OMP_NUM_THREADS = "
+                      f"{os.environ.get('OMP_NUM_THREADS', 'unset')}); selection on one thread",
             "one_thread": {"value": round(1.0 / one_thread_s, 4), "unit": "steps/s",
                            "sample": "one more step with the KV-head groups in turn on one thread"}}
 

@@ -118,7 +118,9 @@ typedef struct lsa_problem {
   int32_t n_qtok;       /* Tq, attention query tokens per sequence, 1 .. 16 */
   int32_t emb_dtype;    /* lsa_dtype of E and of the query embeddings */
   int32_t reserved;     /* must be 0 */
-  const int64_t* ctx_tokens; /* HOST [B]: context tokens of each sequence, a positive multiple of C */
+  const int64_t* ctx_tokens; /* HOST [B]: context tokens of each sequence, a positive multiple of C
+                                (lsa_sparse_decode_attn and lsa_two_level_step also take any positive
+                                count: the last chunk may be partial) */
   const int32_t* keep;       /* HOST [B]: keep budget k_b, 1 <= k_b <= n_b (per query when Q > 1) */
   int64_t kv_chunk_stride;   /* elements between chunks in K and V; 0 selects n_kv_heads*C*d */
   int64_t kv_head_stride;    /* elements between KV heads in K and V; 0 selects C*d */
@@ -208,8 +210,7 @@ lsa_status lsa_topk_chunks(const lsa_problem* p, const void* scores, int32_t* se
  * recall path produces) gives out = 0 and lse = -inf.  Unlike the other
  * entry points of steps 1 and 2 this one also takes a context that ends
  * inside a chunk (n_b = ceil(ctx_tokens[b] / chunk_size)); tokens past the
- * context end get no weight, which needs n_qtok * n_q_heads / n_kv_heads <= 16
- * (LSA_ERR_UNSUPPORTED otherwise).
+ * context end get no weight.
  */
 lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const uint16_t* k_cache,
                                   const uint16_t* v_cache, const int32_t* sel_idx,
@@ -300,9 +301,7 @@ lsa_status lsa_recall_step(const lsa_problem* p, const lsa_indexer* ix, const vo
  *   kept     those chunks, ascending, then w0_b .. n_b - 1
  * then step 3 over the kept chunks; tokens past ctx_tokens[b] in the last
  * chunk get no weight.  Layouts: nat_q bf16 [B][native_heads][key_dim],
- * nat_w float32 [B][native_heads], nat_k bf16 [sum_b n_b][key_dim].  A context
- * that ends inside a chunk needs n_qtok * n_q_heads / n_kv_heads <= 16
- * (LSA_ERR_UNSUPPORTED otherwise).
+ * nat_w float32 [B][native_heads], nat_k bf16 [sum_b n_b][key_dim].
  */
 /* Row pitch of sel_idx and the workspace size of lsa_two_level_step (either
  * output pointer may be NULL). */

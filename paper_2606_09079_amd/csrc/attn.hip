@@ -407,7 +407,10 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
 
   // chunk id of the next tile to issue, loaded one issue ahead
   int c_next = nT > 0 ? sel[Tb / TPC] : 0;
-  auto issue = [&](int i, uint4(&dst)[16][64]) {  // this wave's pieces of tile i -> dst
+  // this wave's pieces of tile i -> dst; returns how many of the tile's tokens
+  // exist: 32, or fewer in the last chunk of a context that ends inside it
+  // (<= 0 for a tile past the end)
+  auto issue = [&](int i, uint4(&dst)[16][64]) -> int {
     const int T = Tb + i;
     const int tt = T % TPC;
     const int c = min(max(c_next, 0), n_b - 1);
@@ -417,6 +420,7 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     for (int q = 0; q < 4; ++q)
       __builtin_amdgcn_global_load_lds((const void*)(p + goff[q]),
                                        (void __attribute__((address_space(3)))*)&dst[4 * wave + q][0], 16, 0, 0);
+    return c == n_b - 1 ? t.tail[b] - 32 * tt : 32;
   };
 
   // Software pipeline over tiles.  Step j (after the barrier that makes tile j
@@ -449,10 +453,16 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     }
   };
 
-  auto softmax_pv = [&](const f32x16& x0, const f32x16& x1, const uint4(&tb)[16][64]) {
+  auto softmax_pv = [&](const f32x16& x0, const f32x16& x1, const uint4(&tb)[16][64], int lim) {
+    if (lim <= 0) return;  // wave-uniform: the tile lies past the context end
     bf16x8 vp[8];
     read_pieces(tb, 8, lane, vp);
-    const f32x16 x = x0 + x1;
+    f32x16 x = x0 + x1;
+    if (lim < 32) {  // the context ends inside this tile: register r holds token 16 (r / 8) + 8 (lane / 32) + r % 8
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (16 * (r / 8) + 8 * (lane >> 5) + r % 8 >= lim) x[r] = -INFINITY;
+    }
     // online softmax: lanes j and j ^ 32 share row j % 32 and split its tokens
     float mx = x[0];
 #pragma unroll
@@ -491,7 +501,10 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     }
   };
 
-  auto step = [&](int j, const uint4(&cur)[16][64], const uint4(&prev)[16][64], uint4(&dma)[16][64]) {
+  // lims[k]: the token count of the tile staged in buffer k
+  int lims[kRowBufs] = {32, 32, 32, 32, 32};
+  auto step = [&](int j, const uint4(&cur)[16][64], const uint4(&prev)[16][64], uint4(&dma)[16][64], int kcur,
+                  int kprev, int kdma) {
     // tile j has landed once at most `ahead` younger tiles of this wave are in flight
     const int ahead = min(nT - 1 - j, kRowBufs - 3);
     if (ahead >= 2)
@@ -505,38 +518,38 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     __asm__ volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     __asm__ volatile("" ::: "memory");
-    if (j + kRowBufs - 2 < nT) issue(j + kRowBufs - 2, dma);
+    if (j + kRowBufs - 2 < nT) lims[kdma] = issue(j + kRowBufs - 2, dma);
     if (!live) return;
     f32x16 n0, n1;
-    qk(cur, n0, n1);
-    if (j > 0) softmax_pv(s_cur0, s_cur1, prev);
+    if (lims[kcur] > 0) qk(cur, n0, n1);
+    if (j > 0) softmax_pv(s_cur0, s_cur1, prev, lims[kprev]);
     s_cur0 = n0;
     s_cur1 = n1;
   };
 
-  if (nT > 0) issue(0, buf0);
-  if (nT > 1) issue(1, buf1);
-  if (nT > 2) issue(2, buf2);
+  if (nT > 0) lims[0] = issue(0, buf0);
+  if (nT > 1) lims[1] = issue(1, buf1);
+  if (nT > 2) lims[2] = issue(2, buf2);
   int j = 0;
   for (; j + 5 <= nT; j += 5) {
-    step(j, buf0, buf4, buf3);
-    step(j + 1, buf1, buf0, buf4);
-    step(j + 2, buf2, buf1, buf0);
-    step(j + 3, buf3, buf2, buf1);
-    step(j + 4, buf4, buf3, buf2);
+    step(j, buf0, buf4, buf3, 0, 4, 3);
+    step(j + 1, buf1, buf0, buf4, 1, 0, 4);
+    step(j + 2, buf2, buf1, buf0, 2, 1, 0);
+    step(j + 3, buf3, buf2, buf1, 3, 2, 1);
+    step(j + 4, buf4, buf3, buf2, 4, 3, 2);
   }
-  if (j < nT) step(j, buf0, buf4, buf3);
-  if (j + 1 < nT) step(j + 1, buf1, buf0, buf4);
-  if (j + 2 < nT) step(j + 2, buf2, buf1, buf0);
-  if (j + 3 < nT) step(j + 3, buf3, buf2, buf1);
+  if (j < nT) step(j, buf0, buf4, buf3, 0, 4, 3);
+  if (j + 1 < nT) step(j + 1, buf1, buf0, buf4, 1, 0, 4);
+  if (j + 2 < nT) step(j + 2, buf2, buf1, buf0, 2, 1, 0);
+  if (j + 3 < nT) step(j + 3, buf3, buf2, buf1, 3, 2, 1);
   // the last tile's softmax and PV (its buffer is nT - 1 mod 5)
   if (nT > 0 && live) {
     switch ((nT - 1) % 5) {
-      case 0: softmax_pv(s_cur0, s_cur1, buf0); break;
-      case 1: softmax_pv(s_cur0, s_cur1, buf1); break;
-      case 2: softmax_pv(s_cur0, s_cur1, buf2); break;
-      case 3: softmax_pv(s_cur0, s_cur1, buf3); break;
-      default: softmax_pv(s_cur0, s_cur1, buf4); break;
+      case 0: softmax_pv(s_cur0, s_cur1, buf0, lims[0]); break;
+      case 1: softmax_pv(s_cur0, s_cur1, buf1, lims[1]); break;
+      case 2: softmax_pv(s_cur0, s_cur1, buf2, lims[2]); break;
+      case 3: softmax_pv(s_cur0, s_cur1, buf3, lims[3]); break;
+      default: softmax_pv(s_cur0, s_cur1, buf4, lims[4]); break;
     }
   }
 

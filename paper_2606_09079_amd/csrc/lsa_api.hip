@@ -120,6 +120,7 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = n
   int64_t sel_total = 0;
   for (int b = 0; b < B; ++b) sel_total += kept_bound(b);
   const int tpc = C / 32;
+  const int target = rows <= 16 && B <= kFewSequences ? kTargetWorkgroupsFew : kTargetWorkgroups;
   int64_t chunk_off = 0, wg_off = 0, swg_off = 0;
   for (int b = 0; b < B; ++b) {
     const int64_t L = p->ctx_tokens[b];
@@ -148,8 +149,8 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = n
     t.tail[b] = (int32_t)(L - (n - 1) * C);
     const int32_t msel = (int32_t)kept_bound(b);
     // splits of sequence b in proportion to its share of the kept chunks, so the
-    // whole grid is about kTargetWorkgroups; at least one 32-token tile per split
-    const double share = (double)kTargetWorkgroups * (double)msel /
+    // whole grid is about `target`; at least one 32-token tile per split
+    const double share = (double)target * (double)msel /
                          ((double)p->n_kv_heads * (double)std::max<int64_t>(sel_total, 1));
     const int32_t ns = (int32_t)std::max<int64_t>(
         1, std::min<int64_t>({std::llround(share), (int64_t)kMaxSplits, (int64_t)msel * tpc}));
@@ -283,17 +284,6 @@ lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, cons
   a.rows = P.rows;
   a.rows_pad = P.rows_pad;
   LSA_HIP(launch_attn(P.t, a, p->chunk_size, s), "attention launch");
-  return LSA_OK;
-}
-
-// A context that ends inside a chunk is masked by the attention kernel for at
-// most 16 query rows per KV head.
-lsa_status check_partial_rows(const lsa_problem* p, const Plan& P) {
-  if (P.rows > 16)
-    for (int b = 0; b < p->batch; ++b)
-      if (P.t.tail[b] != p->chunk_size)
-        return fail(LSA_ERR_UNSUPPORTED, "sequence %d ends inside a chunk; that needs at most 16 query rows per "
-                    "KV head (n_qtok * n_q_heads / n_kv_heads = %d)", b, P.rows);
   return LSA_OK;
 }
 
@@ -580,7 +570,6 @@ lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const
                                   void* stream) {
   Plan P;
   LSA_TRY(make_plan(p, &P, nullptr, true));
-  LSA_TRY(check_partial_rows(p, P));
   LSA_TRY(check_ptr(q, "q"));
   LSA_TRY(check_ptr(k_cache, "k_cache"));
   LSA_TRY(check_ptr(v_cache, "v_cache"));
@@ -745,7 +734,6 @@ lsa_status lsa_two_level_step(const lsa_problem* p, const lsa_indexer* ix, const
     LSA_TRY(check_ptr(sel_count, "sel_count"));
   }
   if (!std::isfinite(softmax_scale)) return fail(LSA_ERR_INVALID_ARG, "softmax_scale is not finite");
-  LSA_TRY(check_partial_rows(p, P));
   LSA_TRY(check_ws(P, ws, ws_bytes));
   const hipStream_t s = (hipStream_t)stream;
   const int B = p->batch;

@@ -176,11 +176,6 @@ def test_two_level_sizes_and_validation():
                                   FAKE, None, None, None, FAKE, ws, None) == B.LSA_ERR_INVALID_ARG
     assert lib.lsa_two_level_step(p.ref, ix.ref, tl.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0,
                                   FAKE, None, None, None, FAKE, ws - 1, None) == B.LSA_ERR_WORKSPACE
-    rows32 = L.Problem([64 * 40 + 3], 64, [10], 16, 2, n_qtok=4)
-    t1 = L.TwoLevel(32, [4], [256])
-    _, ws32 = L.lsa_two_level_sizes(rows32, t1)
-    assert lib.lsa_two_level_step(rows32.ref, ix.ref, t1.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                  0.0, FAKE, None, None, None, FAKE, ws32, None) == B.LSA_ERR_UNSUPPORTED
 
 
 def test_two_level_presets_size():

@@ -50,23 +50,14 @@ def test_two_level_nothing_recalled_no_window():
     assert r["cnt"].tolist() == [0, 0]
 
 
-def test_two_level_rows_above_16_need_full_chunks():
-    """More than 16 query rows per KV head run with full chunks (the many-rows
-    attention kernel) and are rejected when a context ends inside a chunk."""
-    import torch
-    import paper_2606_09079_amd as L
-    ok = T("rows32_full", [64 * 40], [10], [4], [256], hq=16, hkv=2, Tq=4)
-    run_two_level_case(ok, seed=7)
-    bad = T("rows32_partial", [64 * 40 + 3], [10], [4], [256], hq=16, hkv=2, Tq=4)
-    dev = synth.device_inputs(bad, 7)
-    P, ix, tl = L.Problem.from_synth(bad), L.Indexer.from_synth(bad), L.TwoLevel.from_synth(bad)
-    max_sel, ws_bytes = L.lsa_two_level_sizes(P, tl)
-    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
-    out = torch.empty(1, 4, 16, 128, device="cuda")
-    with pytest.raises(L.LsaError) as e:
-        L.lsa_two_level_step(P, ix, tl, dev["idx_q"], dev["idx_w"], dev["idx_k"], dev["nat_q"], dev["nat_w"],
-                             dev["nat_k"], dev["q"], dev["k"], dev["v"], 0.0, out, None, None, None, ws, ws_bytes)
-    assert e.value.status == 2
+def test_two_level_rows_above_16_partial_chunk():
+    """More than 16 query rows per KV head (the many-rows attention kernel), with
+    full chunks and with a context that ends inside its last chunk, whose
+    missing tokens get no weight."""
+    run_two_level_case(T("rows32_full", [64 * 40], [10], [4], [256], hq=16, hkv=2, Tq=4), seed=7)
+    run_two_level_case(T("rows32_partial", [64 * 40 + 3], [10], [4], [256], hq=16, hkv=2, Tq=4), seed=7)
+    run_two_level_case(T("rows128_partial_c128", [128 * 50 + 77, 128 * 20 + 1], [12, 6], [5, 3], [300, 0],
+                         chunk=128, hq=64, hkv=8, Tq=16), seed=9, rows=[(t, h) for t in (0, 7, 15) for h in range(64)])
 
 
 def _sample_rows(prob, n_rows):
@@ -86,6 +77,45 @@ def test_preset_two_level_1m():
     prob = synth.make_problem("twolevel1m", 0)
     r = run_two_level_case(prob, 0, rows=_sample_rows(prob, 6))
     log(f"[twolevel1m] kept {r['cnt'].tolist()} chunks of {prob.n_chunks[0]}")
+
+
+@pytest.mark.parametrize("chunk,tail", [(64, 1), (64, 32), (64, 33), (64, 63), (128, 1), (128, 64), (128, 65),
+                                        (128, 127)])
+def test_attention_alone_partial_context_many_rows(chunk, tail):
+    """The lookahead head shape (64 query heads on 8 KV heads, 16 query tokens:
+    128 rows per KV head) on a context that ends inside its last chunk, through
+    lsa_sparse_decode_attn, token by token against the oracle; the partial
+    chunk sits last, in the middle of a split and alone."""
+    import torch
+    import oracle
+    import parity
+    import paper_2606_09079_amd as L
+    Hq, Hkv, Tq = 64, 8, 16
+    prob = synth.Problem("partial_rows", [chunk * 40 + tail], chunk, [8], Hq, Hkv, n_qtok=Tq)
+    host = synth.host_inputs(prob, 12)
+    dev = synth.device_inputs(prob, 12, host=host)
+    n = prob.n_chunks[0]
+    G = Hq // Hkv
+    for kept in (np.array([0, 5, 17, 33, n - 3, n - 1], dtype=np.int32), np.array([n - 1], dtype=np.int32)):
+        P = L.Problem(prob.ctx_tokens, chunk, [len(kept)], Hq, Hkv, n_qtok=Tq)
+        ws_bytes = L.lsa_workspace_size(L.Problem([chunk * n], chunk, [len(kept)], Hq, Hkv, n_qtok=Tq))
+        ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+        sel = torch.from_numpy(kept[None, :].copy()).cuda()
+        cnt = torch.tensor([len(kept)], dtype=torch.int32, device="cuda")
+        out = torch.full((1, Tq, Hq, 128), float("nan"), device="cuda")
+        lse = torch.full((1, Tq, Hq), float("nan"), device="cuda")
+        L.lsa_sparse_decode_attn(P, dev["q"], dev["k"], dev["v"], sel, cnt, 0.0, out, lse, ws, ws_bytes)
+        torch.cuda.synchronize()
+        g_out, g_lse = out.cpu().numpy(), lse.cpu().numpy()
+        toks = oracle.kept_tokens(kept, chunk, prob.ctx_tokens[0])
+        for g in (0, 3, 7):
+            Kh = synth.kv_head_sparse(prob, 12, "k", 0, g, kept)
+            Vh = synth.kv_head_sparse(prob, 12, "v", 0, g, kept)
+            rows = [(t, g * G + j) for t in range(Tq) for j in range(G)]
+            qr = np.stack([host["q"][0, t, h] for (t, h) in rows])
+            r_out, r_lse = oracle.attention_tokens(qr, Kh, Vh, toks)
+            parity.check_attention(np.stack([g_out[0, t, h] for (t, h) in rows]), [g_lse[0, t, h] for (t, h) in rows],
+                                   r_out, r_lse, f"partial context C={chunk}, tail {tail}, {len(kept)} kept, KV head {g}")
 
 
 @pytest.mark.parametrize("tail", [1, 31, 32, 33, 63])
