@@ -89,6 +89,22 @@ def code_sha(name: str) -> str:
     return hashlib.sha256(text.encode()).hexdigest()[:16]
 
 
+def calibration_copy(args, stream) -> None:
+    """Profiling aid: one plain 16-byte copy of a known size, whose counter
+    readings calibrate the traffic counters of the same run."""
+    if not args.copy_calibration_mib:
+        return
+    import torch
+
+    import lsa_synth as synth
+    nbytes = args.copy_calibration_mib << 20
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    synth.copy_device(src.data_ptr(), dst.data_ptr(), nbytes, stream.cuda_stream)
+    torch.cuda.synchronize()
+    log(f"[bench] calibration copy of {nbytes} bytes done")
+
+
 def part_times(L, prob, P, ix, dev, rot, max_sel, stream, attn_us: float, n: int):
     """Average microseconds of the step's parts, each entry point launched on
     its own between HIP events on the launch stream: scoring, selection (with
@@ -261,13 +277,7 @@ def main() -> int:
         step(i)
     torch.cuda.synchronize()
 
-    if args.copy_calibration_mib:
-        nbytes = args.copy_calibration_mib << 20
-        src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-        dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-        synth.copy_device(src.data_ptr(), dst.data_ptr(), nbytes, stream.cuda_stream)
-        torch.cuda.synchronize()
-        log(f"[bench] calibration copy of {nbytes} bytes done")
+    calibration_copy(args, stream)
 
     fn = attn if args.only == "attn" else step
     for i in range(args.warmup):
@@ -768,6 +778,7 @@ def bench_golden(args) -> int:
     import paper_2606_09079_amd as L
 
     main = torch.cuda.current_stream()
+    calibration_copy(args, main)
     gp = synth.make_golden_problem(args.workload)
     t_setup = time.time()
     logits = synth.golden_logits_device(gp, 0)
