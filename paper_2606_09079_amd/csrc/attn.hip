@@ -4,8 +4,9 @@
 //
 // Flash-decoding with split-K over the kept-chunk list.  The kept list of
 // each (sequence b, KV head g) is cut into 32-token tiles, and each split owns
-// a contiguous, equal share of them; the split count is sized so that the whole
-// grid is one resident round on MI355X (256 CUs x 2 workgroups).  All G * Tq
+// a contiguous share of them, weighted by the XCD its workgroup runs on; the
+// split count is sized so that the whole grid is one resident round on MI355X
+// (one workgroup per CU for a few sequences, two for more).  All G * Tq
 // query rows that read KV head g are handled by the same workgroup, so every
 // K/V byte is fetched from HBM once.  Logits, the running max / sum and O stay
 // fp32; the softmax weights P enter the PV product as bf16 hi + lo parts (two
@@ -95,6 +96,26 @@ struct Unit {
   int b, g, s, ns;
 };
 
+// Static split boundaries weighted by the XCD of each split's workgroup.  The
+// dispatcher places workgroup i on XCD i % 8, and per-workgroup timestamps on
+// MI355X show the odd-numbered XCDs streaming 7-8% slower than the even ones
+// (every run measured); giving even-XCD workgroups 6/5 of the tiles of their
+// odd neighbours took the 1M-token step from 84.6 to 82.9 us.  (The many-rows
+// kernel, two workgroups per CU, measured 1% slower with it and keeps equal
+// splits.)  Returns the first tile of split s of (b, g), so that split s
+// covers [first(s), first(s + 1)).
+constexpr int kEvenXcdWeight = 6;
+constexpr int kOddXcdWeight = 5;
+
+__device__ __forceinline__ int split_first(const SeqTable& t, int b, int g, int s, int ns, int n_tiles) {
+  const int base = t.wg_off[b] + g * ns;  // workgroup of split 0 of (b, g)
+  auto weight_below = [&](int j) -> int64_t {  // the weights of splits 0 .. j - 1
+    const int64_t even = (int64_t)((base + j + 1) / 2 - (base + 1) / 2);
+    return even * kEvenXcdWeight + (int64_t)(j - even) * kOddXcdWeight;
+  };
+  return (int)((int64_t)n_tiles * weight_below(s) / weight_below(ns));
+}
+
 __device__ __forceinline__ Unit unit_of(const SeqTable& t, int wg) {
   Unit u;
   int b = 0;
@@ -127,7 +148,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   const int cnt = min(max(a.sel_count[b], 0), a.sel_pitch);
   const int n_b = t.n[b];
   const int nTall = cnt * TPC;
-  const int T0 = (int)(((int64_t)s * nTall) / ns), T1 = (int)(((int64_t)(s + 1) * nTall) / ns);
+  const int T0 = split_first(t, b, g, s, ns, nTall), T1 = split_first(t, b, g, s + 1, ns, nTall);
   const int Tb = T0 + (int)(((int64_t)wave * (T1 - T0)) / kAttnWaves);
   const int Te = T0 + (int)(((int64_t)(wave + 1) * (T1 - T0)) / kAttnWaves);
 
