@@ -67,11 +67,15 @@ WORKLOADS = {
     "golden512k": "golden512k: golden-label window of a 512K-token context, 131,072 compressed entries x 64 decoding "
                   "steps x 21 layers of float32 indexer logits (704 MB), top-p 0.6, votes >= 3, union over the window",
     "golden_batch": "golden_batch: 8 golden-label windows of 4,096-131,072 entries (log-uniform), 64 steps x 21 layers",
+    "kvpack1m": "kvpack1m: re-layout of the paper1m context's token-major K/V ([1,048,576 tokens][8 KV heads][128] "
+                "bf16 each) into the chunk-paged blocks the attention reads (lsa_kv_pack, every token), plus the "
+                "per-step append of one decoded token to paper1m and to each of the 32 batch32 sequences",
     "twolevel_tiny": "twolevel_tiny: 4,133 tokens (65 chunks, the last one 37 tokens), Level 1 3 x 16 x 64 with "
                      "K_max 24, Level 2 keeps 6, window 512 tokens, 8 query / 8 KV heads, head_dim 128, bf16 K/V",
 }
 EMB_BYTES = {"f32": 4, "bf16": 2, "i8": 1}
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "attn_kernel_paper1m_traffic.md")
+PACK_SUMMARY = os.path.join(ROOT, "profiles", "kvpack_kernel_kvpack1m.md")
 
 
 def log(msg: str) -> None:
@@ -162,15 +166,16 @@ def history_chunks(prob, b: int) -> int:
     return min(max(L - W, 0) // prob.chunk, L // prob.chunk)
 
 
-def measured_traffic():
-    """HBM bytes per attention launch from the committed rocprofv3 counter summary,
-    or None when the summary is missing or was taken on other kernel source."""
-    if not os.path.exists(PMC_SUMMARY):
+def measured_traffic(summary: str = PMC_SUMMARY, source: str = "attn.hip"):
+    """HBM bytes per launch of the dominant kernel from a committed rocprofv3
+    counter summary, or None when the summary is missing or was taken on other
+    kernel source."""
+    if not os.path.exists(summary):
         return None
-    text = open(PMC_SUMMARY).read()
-    m = re.search(r"attn\.hip code sha256\[:16\]:\s*([0-9a-f]{16})", text)
+    text = open(summary).read()
+    m = re.search(re.escape(source) + r" code sha256\[:16\]:\s*([0-9a-f]{16})", text)
     t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m or not t or m.group(1) != code_sha("attn.hip"):
+    if not m or not t or m.group(1) != code_sha(source):
         return None
     return float(t.group(1))
 
@@ -215,6 +220,8 @@ def main() -> int:
         return bench_tier(args)
     if args.workload.startswith("golden"):
         return bench_golden(args)
+    if args.workload == "kvpack1m":
+        return bench_kvpack(args)
     stream = torch.cuda.current_stream()
     prob = synth.make_problem(args.workload, 0)
     t_setup = time.time()
@@ -763,6 +770,121 @@ def bench_tier(args) -> int:
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(prob, host0, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def bench_kvpack(args) -> int:
+    """Tokens per second of the re-layout of a token-major cache into the paged
+    blocks (lsa_kv_pack over the whole paper1m context, K and V), and the time
+    of the per-step append of one decoded token per sequence."""
+    import numpy as np
+    import torch
+
+    import lsa_synth as synth
+    import paper_2606_09079_amd as L
+
+    main = torch.cuda.current_stream()
+    sp = main.cuda_stream
+    calibration_copy(args, main)
+    prob = synth.make_problem("paper1m", 0)
+    P = L.Problem.from_synth(prob)
+    T, H, d = prob.ctx_tokens[0], prob.n_kv_heads, prob.head_dim
+    t_setup = time.time()
+    table = torch.from_numpy(synth.normal_table_bf16().view(np.int16)).cuda()
+    tau = torch.from_numpy(synth.token_rows(prob, [0], T)).cuda()
+    src = {w: torch.empty(T * H * d, dtype=torch.int16, device="cuda") for w in "kv"}
+    for w in "kv":
+        synth.fill_kv_tokens_device(prob, 0, w, src[w].data_ptr(), table.data_ptr(), tau.data_ptr(), T,
+                                    stream_ptr=sp)
+    del tau
+    n = prob.kv_elems()
+    dst = {w: torch.empty(n, dtype=torch.int16, device="cuda") for w in "kv"}
+    offs = torch.zeros(1, dtype=torch.int64, device="cuda")
+
+    def pack():
+        L.lsa_kv_pack(P, src["k"], src["v"], offs, dst["k"], dst["v"], stream=main)
+
+    pack()
+    for w in "kv":  # the packed cache is the paged fill's, byte for byte
+        ref = torch.empty(n, dtype=torch.int16, device="cuda")
+        synth.fill_kv_device(prob, 0, w, ref.data_ptr(), table.data_ptr(), sp)
+        if not torch.equal(ref, dst[w]):
+            raise RuntimeError(f"lsa_kv_pack: packed {w.upper()} differs from the paged fill")
+        del ref
+    log(f"[kvpack] setup and check {time.time() - t_setup:.1f}s")
+    for _ in range(args.warmup):
+        pack()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(main)
+    for _ in range(args.steps):
+        pack()
+    e1.record(main)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    call_bytes = 2 * 2 * T * H * d * 2  # K and V, each read once and written once
+
+    def append_us(p_, first, src_rows, offsets, k_cache, v_cache, reps=100):
+        # one small launch per call: replayed from a HIP graph of `reps` calls,
+        # so that the host's time per call does not count
+        def call(st):
+            L.lsa_kv_pack(p_, src_rows, src_rows, offsets, k_cache, v_cache, first_token=first, stream=st)
+        call(main)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cs = torch.cuda.current_stream()
+            for _ in range(reps):
+                call(cs)
+        graph.replay()
+        torch.cuda.synchronize()
+        a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a_.record(main)
+        for _ in range(5):
+            graph.replay()
+        b_.record(main)
+        torch.cuda.synchronize()
+        return round(1e3 * a_.elapsed_time(b_) / (5 * reps), 2)
+
+    # one decoded token: its K/V rows sit in a buffer of the new rows only
+    new1 = torch.zeros(H * d, dtype=torch.int16, device="cuda")
+    ap1 = append_us(P, [T - 1], new1, torch.tensor([-(T - 1)], dtype=torch.int64, device="cuda"), dst["k"], dst["v"])
+    del src
+    b32 = synth.make_problem("batch32", 0)
+    P32 = L.Problem.from_synth(b32)
+    new32 = torch.zeros(b32.batch * H * d, dtype=torch.int16, device="cuda")
+    first32 = [Lb - 1 for Lb in b32.ctx_tokens]
+    offs32 = torch.tensor([b - f for b, f in enumerate(first32)], dtype=torch.int64, device="cuda")
+    del dst
+    k32 = torch.empty(b32.kv_elems(), dtype=torch.int16, device="cuda")
+    v32 = torch.empty(b32.kv_elems(), dtype=torch.int16, device="cuda")
+    ap32 = append_us(P32, first32, new32, offs32, k32, v32)
+    achieved = call_bytes / (ms * 1e-3) / 1e9
+    log(f"[kvpack] {args.steps} packs: {ms * 1e3:.1f} us each (wall {wall:.3f}s), {achieved:.0f} GB/s; "
+        f"append {ap1} us (1 sequence), {ap32} us (32 sequences)")
+    result = {
+        "metric": "tokens/s re-laid from a token-major cache into the paged blocks (K and V, 8 KV heads)",
+        "value": round(T / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 (bit copy)",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.workload], "global_batch": 1, "seq_len": T, "parallelism": "single GPU"},
+        "append_us": {"paper1m_one_token": ap1, "batch32_one_token_each": ap32},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(PACK_SUMMARY, "kvpack.hip"),
+                     "kernel": "kv_pack_kernel (one lsa_kv_pack call over the whole context)",
+                     "avg_launch_us": round(ms * 1e3, 2), "algorithmic_bytes_per_launch": int(call_bytes)},
+    }
     print(json.dumps(result), flush=True)
     return 0
 

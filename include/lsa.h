@@ -210,12 +210,41 @@ lsa_status lsa_topk_chunks(const lsa_problem* p, const void* scores, int32_t* se
  * recall path produces) gives out = 0 and lse = -inf.  Unlike the other
  * entry points of steps 1 and 2 this one also takes a context that ends
  * inside a chunk (n_b = ceil(ctx_tokens[b] / chunk_size)); tokens past the
- * context end get no weight.
+ * context end get no weight, and their K and V slots may hold any bits,
+ * NaN included.
  */
 lsa_status lsa_sparse_decode_attn(const lsa_problem* p, const uint16_t* q, const uint16_t* k_cache,
                                   const uint16_t* v_cache, const int32_t* sel_idx,
                                   const int32_t* sel_count, float softmax_scale, float* out,
                                   float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Cache re-layout for callers whose K/V are token-major (the paged cache of
+ * Sec. 2.1 and the KV layout of Sec. 2.5, one row per token): write the K and
+ * V rows of tokens first_token[b] .. ctx_tokens[b] - 1 of every sequence b into
+ * the chunk-paged, MFMA-ordered blocks that lsa_sparse_decode_attn and the
+ * fused steps read (layout above, strides kv_chunk_stride / kv_head_stride of
+ * p).  Once at prefill with first_token NULL (every token), then each step
+ * for the tokens decoded since (first_token[b] = the old ctx_tokens[b]).
+ *   k_tok, v_tok   bf16 source rows: token i of sequence b, KV head g starts at
+ *                  element (token_offsets[b] + i) * tok_stride + g * tok_head_stride
+ *                  and holds head_dim contiguous values.  tok_stride 0 selects
+ *                  n_kv_heads * head_dim, tok_head_stride 0 selects head_dim
+ *                  ([tokens][Hkv][d]); both non-negative multiples of 8.
+ *   token_offsets  DEVICE int64 [B]: source row of token 0 of sequence b (a
+ *                  [B + 1] prefix sum of the context lengths works as is; for a
+ *                  buffer holding only the new rows it is the row of the first
+ *                  new token minus first_token[b], which may be negative).
+ *   first_token    HOST int64 [B], 0 <= first_token[b] <= ctx_tokens[b], or NULL
+ *                  for 0.  Sequences with first_token[b] == ctx_tokens[b] are
+ *                  left alone.
+ * ctx_tokens may end inside a chunk: the positions of that block past the
+ * context end are set to zero (a later call fills them).  No other position
+ * changes; source rows must not overlap the caches.
+ */
+lsa_status lsa_kv_pack(const lsa_problem* p, const uint16_t* k_tok, const uint16_t* v_tok,
+                       const int64_t* token_offsets, int64_t tok_stride, int64_t tok_head_stride,
+                       const int64_t* first_token, uint16_t* k_cache, uint16_t* v_cache, void* stream);
 
 /*
  * The whole step: score -> select -> attend on one stream with no host

@@ -428,6 +428,10 @@ def dev_lib() -> ctypes.CDLL:
                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
         lib.synth_fill_kv_device.restype = ctypes.c_int
+        lib.synth_fill_kv_tokens_device.argtypes = [ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                                    ctypes.c_int64, ctypes.c_void_p]
+        lib.synth_fill_kv_tokens_device.restype = ctypes.c_int
         lib.synth_copy_device.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
         lib.synth_copy_device.restype = ctypes.c_int
         lib.synth_read_device.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
@@ -457,6 +461,34 @@ def fill_kv_device(prob: Problem, seed: int, which: str, out_ptr: int, table_ptr
                                         cs, hs, 0 if which == "k" else 1, stream_ptr)
     if rc != 0:
         raise RuntimeError(f"synth_fill_kv_device failed with code {rc}")
+
+
+def token_rows(prob: Problem, row_off: Sequence[int], n_rows: int) -> np.ndarray:
+    """Global token of each row of a token-major cache whose sequence b starts
+    at row row_off[b] and holds its ctx_tokens[b] tokens; other rows get -1.
+
+    The global token of token i of sequence b is chunk_offsets[b] * chunk + i,
+    the token whose values the paged fill puts at that position."""
+    tau = np.full(n_rows, -1, dtype=np.int64)
+    for b, L in enumerate(prob.ctx_tokens):
+        r0 = int(row_off[b])
+        tau[r0:r0 + int(L)] = prob.chunk_offsets[b] * prob.chunk + np.arange(int(L), dtype=np.int64)
+    return tau
+
+
+def fill_kv_tokens_device(prob: Problem, seed: int, which: str, out_ptr: int, table_ptr: int, tau_ptr: int,
+                          n_rows: int, tok_stride: Optional[int] = None, head_stride: Optional[int] = None,
+                          stream_ptr: int = 0) -> None:
+    """Fill a device token-major K or V cache: row r holds global token tau[r]
+    (:func:`token_rows`), KV head h at r * tok_stride + h * head_stride."""
+    d, H = prob.head_dim, prob.n_kv_heads
+    hs = d if head_stride is None else head_stride
+    ts = H * hs if tok_stride is None else tok_stride
+    stream = STREAM_K if which == "k" else STREAM_V
+    rc = dev_lib().synth_fill_kv_tokens_device(stream_key(seed, stream), table_ptr, out_ptr, tau_ptr, n_rows, H, d,
+                                               ts, hs, stream_ptr)
+    if rc != 0:
+        raise RuntimeError(f"synth_fill_kv_tokens_device failed with code {rc}")
 
 
 def block_offset(which: str, t, e):

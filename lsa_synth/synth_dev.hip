@@ -67,6 +67,39 @@ fill_kv(uint64_t key, const uint16_t* __restrict__ table, uint16_t* __restrict__
   }
 }
 
+// Token-major fill: row r of out holds the hkv x d values of global token
+// tau_of_row[r] (the same values the paged fill puts in that token's
+// positions), KV head h at r*tok_stride + h*head_stride; rows with a negative
+// tau are left alone.
+__global__ void __launch_bounds__(256)
+fill_kv_tokens(uint64_t key, const uint16_t* __restrict__ table, uint16_t* __restrict__ out,
+               const int64_t* __restrict__ tau_of_row, int64_t n_rows, int32_t hkv, int32_t d,
+               int64_t tok_stride, int64_t head_stride) {
+  const int64_t per_row = (int64_t)hkv * (d / 8);
+  const int64_t total = n_rows * per_row;
+  for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < total;
+       w += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = w / per_row;
+    const int64_t rem = w - r * per_row;
+    const int32_t h = (int32_t)(rem / (d / 8));
+    const int64_t e0 = (rem - (int64_t)h * (d / 8)) * 8;
+    const int64_t tau = tau_of_row[r];
+    if (tau < 0) continue;
+    uint16_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint64_t idx = (uint64_t)((tau * hkv + h) * d + e0 + j);
+      v[j] = table[mix64(key + (idx + 1ULL) * kGamma) >> 48];
+    }
+    uint4 packed;
+    packed.x = (uint32_t)v[0] | ((uint32_t)v[1] << 16);
+    packed.y = (uint32_t)v[2] | ((uint32_t)v[3] << 16);
+    packed.z = (uint32_t)v[4] | ((uint32_t)v[5] << 16);
+    packed.w = (uint32_t)v[6] | ((uint32_t)v[7] << 16);
+    *reinterpret_cast<uint4*>(out + r * tok_stride + h * head_stride + e0) = packed;
+  }
+}
+
 // Plain 16-byte copy, used only to calibrate hardware byte counters against a
 // kernel whose traffic is known exactly (n16 * 16 bytes read and written).
 __global__ void __launch_bounds__(256) copy16(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n16) {
@@ -153,6 +186,22 @@ extern "C" int synth_fill_golden_device(uint64_t key_noise, uint64_t key_rel, ui
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(fill_golden, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, key_noise, key_rel,
                      key_boost, table, start, total, n, b, sigma, beta, rel_thr, boost_thr, out);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
+
+// Returns 0 on success, 1 on a bad argument, 2 on a HIP launch error.
+extern "C" int synth_fill_kv_tokens_device(uint64_t key, const uint16_t* table, uint16_t* out,
+                                           const int64_t* tau_of_row, int64_t n_rows, int32_t hkv, int32_t d,
+                                           int64_t tok_stride, int64_t head_stride, void* stream) {
+  if (!table || !out || !tau_of_row || n_rows <= 0 || hkv <= 0 || d != 128) return 1;
+  if (tok_stride % 8 != 0 || head_stride % 8 != 0 || head_stride < d || tok_stride < (int64_t)hkv * head_stride)
+    return 1;
+  if ((reinterpret_cast<uintptr_t>(out) & 15) != 0) return 1;
+  const int64_t total = n_rows * hkv * (d / 8);
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(fill_kv_tokens, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, key, table, out,
+                     tau_of_row, n_rows, hkv, d, tok_stride, head_stride);
   return hipGetLastError() == hipSuccess ? 0 : 2;
 }
 

@@ -7,7 +7,7 @@ CSRC = os.path.join(HERE, "csrc")
 # LSA_LIB points the binding at another build of the same sources (for example an
 # installed copy); by default the in-tree library is used.
 LIB_PATH = os.environ.get("LSA_LIB") or os.path.join(HERE, "liblsa.so")
-SOURCES = ("score.hip", "topk.hip", "attn.hip", "recall.hip", "tier.hip", "golden.hip", "lsa_api.hip")
+SOURCES = ("score.hip", "topk.hip", "attn.hip", "recall.hip", "tier.hip", "golden.hip", "kvpack.hip", "lsa_api.hip")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          # no packed-fp32 instructions anywhere in the device code

@@ -253,6 +253,21 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
     }
     bf16x8 ph, pl;
     split_bf16(p, ph, pl);
+    if (lim < 32) {
+      // the V slots of tokens past the context end may hold anything, NaN
+      // included (not yet written): zero them, as a zero weight cancels only
+      // finite values.  Lane element i is token 8 kg + i.
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        bf16x8 vm = vt[nb];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (8 * kg + i >= lim) vm[i] = (__bf16)0.0f;
+        o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vm, o[nb], 0, 0, 0);
+        o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vm, o[nb], 0, 0, 0);
+      }
+      return;
+    }
 #pragma unroll
     for (int nb = 0; nb < 8; ++nb) {
       o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vt[nb], o[nb], 0, 0, 0);
@@ -482,7 +497,13 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     if (lim < 32) {  // the context ends inside this tile: register r holds token 16 (r / 8) + 8 (lane / 32) + r % 8
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        if (16 * (r / 8) + 8 * (lane >> 5) + r % 8 >= lim) x[r] = -INFINITY;
+        if (16 * (r / 8) + 8 * (lane >> 5) + r % 8 >= lim) {
+          x[r] = -INFINITY;
+          // that token's V slots may hold anything, NaN included (not yet
+          // written): zero them, as a zero weight cancels only finite values
+#pragma unroll
+          for (int n = 0; n < 4; ++n) vp[(r / 8) * 4 + n][r % 8] = (__bf16)0.0f;
+        }
     }
     // online softmax: lanes j and j ^ 32 share row j % 32 and split its tokens
     float mx = x[0];

@@ -540,6 +540,54 @@ lsa_status lsa_workspace_init(void* ws, size_t ws_bytes, void* stream) {
   return LSA_OK;
 }
 
+lsa_status lsa_kv_pack(const lsa_problem* p, const uint16_t* k_tok, const uint16_t* v_tok,
+                       const int64_t* token_offsets, int64_t tok_stride, int64_t tok_head_stride,
+                       const int64_t* first_token, uint16_t* k_cache, uint16_t* v_cache, void* stream) {
+  Plan P;
+  LSA_TRY(make_plan(p, &P, nullptr, /*partial=*/true));
+  LSA_TRY(check_ptr(k_tok, "k_tok"));
+  LSA_TRY(check_ptr(v_tok, "v_tok"));
+  LSA_TRY(check_ptr(token_offsets, "token_offsets"));
+  LSA_TRY(check_ptr(k_cache, "k_cache"));
+  LSA_TRY(check_ptr(v_cache, "v_cache"));
+  const int64_t hs = tok_head_stride ? tok_head_stride : kHeadDim;
+  const int64_t ts = tok_stride ? tok_stride : (int64_t)p->n_kv_heads * hs;
+  if (ts < 0 || hs < 0 || ts % 8 || hs % 8)
+    return fail(LSA_ERR_INVALID_ARG, "token-major strides (token %lld, head %lld) must be non-negative multiples of 8",
+                (long long)ts, (long long)hs);
+  PackArgs a{};
+  a.k_tok = k_tok;
+  a.v_tok = v_tok;
+  a.tok_off = token_offsets;
+  a.tok_stride = ts;
+  a.tok_head_stride = hs;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.chunk_stride = P.chunk_stride;
+  a.head_stride = P.head_stride;
+  a.n_kv_heads = p->n_kv_heads;
+  a.chunk = p->chunk_size;
+  a.batch = p->batch;
+  const int64_t C = p->chunk_size;
+  int64_t units = 0;
+  for (int b = 0; b < p->batch; ++b) {
+    const int64_t L = p->ctx_tokens[b], f = first_token ? first_token[b] : 0;
+    if (f < 0 || f > L)
+      return fail(LSA_ERR_INVALID_ARG, "first_token[%d] = %lld not in [0, ctx_tokens = %lld]", b, (long long)f,
+                  (long long)L);
+    a.first[b] = f;
+    a.ctx[b] = L;
+    a.chunk_off[b] = P.t.chunk_off[b];
+    a.unit_off[b] = units;
+    if (f < L) units += (L - 1) / C - f / C + 1;
+  }
+  a.unit_off[p->batch] = units;
+  if (units * p->n_kv_heads > INT32_MAX)
+    return fail(LSA_ERR_UNSUPPORTED, "%lld chunk blocks to write in one launch", (long long)(units * p->n_kv_heads));
+  LSA_HIP(launch_kv_pack(a, units, (hipStream_t)stream), "kv pack launch");
+  return LSA_OK;
+}
+
 lsa_status lsa_score_chunks(const lsa_problem* p, const void* query_emb, const void* chunk_emb, void* scores,
                             void* stream) {
   Plan P;

@@ -116,6 +116,25 @@ hipError_t launch_union(const SeqTable& t, const int32_t* per_query, int32_t k_p
 
 hipError_t launch_attn(const SeqTable& t, const AttnArgs& a, int32_t chunk_size, hipStream_t s);
 
+// Re-layout of token-major K/V rows into the chunk-paged blocks; a unit is
+// one chunk of a sequence's range, one workgroup per (unit, KV head).
+struct PackArgs {
+  const uint16_t* k_tok;
+  const uint16_t* v_tok;
+  const int64_t* tok_off;         // device [B]: source row of token 0 of sequence b
+  int64_t tok_stride;             // source elements between tokens
+  int64_t tok_head_stride;        // source elements between KV heads
+  uint16_t* k;
+  uint16_t* v;
+  int64_t chunk_stride, head_stride;  // destination block strides
+  int32_t n_kv_heads, chunk, batch;
+  int64_t unit_off[LSA_MAX_BATCH + 1];  // first unit of sequence b
+  int64_t first[LSA_MAX_BATCH];         // first token written
+  int64_t ctx[LSA_MAX_BATCH];           // one past the last token written
+  int64_t chunk_off[LSA_MAX_BATCH];     // first global chunk id of sequence b
+};
+hipError_t launch_kv_pack(const PackArgs& a, int64_t units, hipStream_t s);
+
 // Recall path: the full Memory Indexer score of L layers.
 constexpr int kMaxIdxLayers = LSA_MAX_IDX_LAYERS;
 constexpr int kRecallRowsPerWg = 64;  // entries per scoring workgroup (4 waves x 16)

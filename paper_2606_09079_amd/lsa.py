@@ -33,7 +33,7 @@ EXPORTS = ("lsa_abi_version", "lsa_status_string", "lsa_last_error", "lsa_valida
            "lsa_sparse_decode_attn", "lsa_decode_step", "lsa_recall_scores", "lsa_recall_select",
            "lsa_recall_step", "lsa_two_level_sizes", "lsa_two_level_step", "lsa_tier_sizes", "lsa_tier_reset",
            "lsa_tier_plan", "lsa_tier_fetch", "lsa_tier_fetch_dma", "lsa_tier_attend", "lsa_tier_step",
-           "lsa_golden_sizes", "lsa_golden_labels", "lsa_decode_step_noalloc")
+           "lsa_golden_sizes", "lsa_golden_labels", "lsa_decode_step_noalloc", "lsa_kv_pack")
 
 
 class lsa_problem(ctypes.Structure):
@@ -91,6 +91,7 @@ def _load() -> ctypes.CDLL:
     lib.lsa_score_chunks.argtypes = [pp, _P, _P, _P, _P]
     lib.lsa_topk_chunks.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
     lib.lsa_sparse_decode_attn.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]
+    lib.lsa_kv_pack.argtypes = [pp, _P, _P, _P, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, _P]
     lib.lsa_decode_step.argtypes = [pp, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
     ip = ctypes.POINTER(lsa_indexer)
     lib.lsa_recall_scores.argtypes = [pp, ip, _P, _P, _P, _P, _P]
@@ -287,6 +288,21 @@ def lsa_topk_chunks(p: Problem, scores, sel_idx, sel_count, per_query_idx=None, 
                     stream=None) -> None:
     _check(LIB.lsa_topk_chunks(p.ref, _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(per_query_idx), _ptr(ws),
                                ws_bytes, _stream(stream)), "lsa_topk_chunks")
+
+
+def lsa_kv_pack(p: Problem, k_tok, v_tok, token_offsets, k_cache, v_cache, first_token=None, tok_stride: int = 0,
+                tok_head_stride: int = 0, stream=None) -> None:
+    """Write tokens first_token[b] .. ctx_tokens[b] - 1 of token-major K/V rows into the paged caches.
+
+    first_token: host sequence of per-sequence first tokens, or None for 0.
+    """
+    if first_token is None:
+        ft = None
+    else:
+        ft = (ctypes.c_int64 * max(len(first_token), 1))(*[int(x) for x in first_token])
+    _check(LIB.lsa_kv_pack(p.ref, _ptr(k_tok), _ptr(v_tok), _ptr(token_offsets), int(tok_stride),
+                           int(tok_head_stride), None if ft is None else ctypes.cast(ft, ctypes.c_void_p),
+                           _ptr(k_cache), _ptr(v_cache), _stream(stream)), "lsa_kv_pack")
 
 
 def lsa_sparse_decode_attn(p: Problem, q, k_cache, v_cache, sel_idx, sel_count, softmax_scale: float, out,
