@@ -36,7 +36,9 @@ from typing import Callable, Dict, List, Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SO = os.path.join(_HERE, "liblsa_oracle.so")
+# LSA_ORACLE_SO points the tests at another build of the same source (the
+# sanitised one); by default the in-tree library is used.
+_SO = os.environ.get("LSA_ORACLE_SO") or os.path.join(_HERE, "liblsa_oracle.so")
 _lib: Optional[ctypes.CDLL] = None
 
 _P = ctypes.c_void_p
@@ -45,7 +47,8 @@ _I32, _I64, _F64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
 
 def build() -> None:
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math",
-                           os.path.join(_HERE, "lsa_oracle.c"), "-o", _SO, "-lm"])
+                           os.path.join(_HERE, "lsa_oracle.c"), "-o", os.path.join(_HERE, "liblsa_oracle.so"),
+                           "-lm"])
 
 
 def bind(path: str) -> ctypes.CDLL:

@@ -333,3 +333,28 @@ def test_noalloc_rejects_a_step_beyond_its_scratch():
     bad = L.Problem([100], 64, [1], 8, 8)
     assert L.LIB.lsa_decode_step_noalloc(bad.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None,
                                          None) == B.LSA_ERR_INVALID_ARG
+
+
+def _no_device():
+    import torch
+    return torch.cuda.device_count() == 0
+
+
+@pytest.mark.skipif(not _no_device(), reason="forces the HIP failure by calling where no device exists")
+def test_hip_failure_is_reported_as_lsa_err_hip():
+    # With no device the HIP runtime refuses every launch on the host, so a
+    # call that passes validation must come back as LSA_ERR_HIP with the
+    # runtime's message, and the Python binding must raise with that status.
+    # The pointers are never dereferenced: the launch itself is refused.
+    p = good()
+    ws = L.lsa_workspace_size(p)
+    lib = L.LIB
+    assert lib.lsa_workspace_init(FAKE, 4096, None) == B.LSA_ERR_HIP
+    assert "zero-fill launch" in B.last_error()
+    assert lib.lsa_score_chunks(p.ref, FAKE, FAKE, FAKE, None) == B.LSA_ERR_HIP
+    assert "score launch" in B.last_error()
+    assert lib.lsa_decode_step(p.ref, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None, FAKE, ws,
+                               None) == B.LSA_ERR_HIP
+    with pytest.raises(L.LsaError) as e:
+        L.lsa_score_chunks(p, FAKE, FAKE, FAKE, stream=0)
+    assert e.value.status == B.LSA_ERR_HIP
