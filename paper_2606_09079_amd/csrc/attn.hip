@@ -145,8 +145,8 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   // sel_count and the chunk ids are clamped so that malformed device inputs
   // can only give wrong numbers, never an out-of-bounds access.
   constexpr int TPC = C / 32;  // 32-token tiles per chunk
-  const int cnt = min(max(a.sel_count[b], 0), a.sel_pitch);
   const int n_b = t.n[b];
+  const int cnt = a.count_is_keep ? min(t.keep[b], n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
   const int nTall = cnt * TPC;
   const int T0 = split_first(t, b, g, s, ns, nTall), T1 = split_first(t, b, g, s + 1, ns, nTall);
   const int Tb = T0 + (int)(((int64_t)wave * (T1 - T0)) / kAttnWaves);
@@ -206,7 +206,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
     return c == n_b - 1 ? t.tail[b] - 32 * tt : 32;
   };
 
-  auto compute_tile = [&](const bf16x8(&kt)[8], const bf16x8(&vt)[8], int lim) {
+  auto compute_tile = [&](const bf16x8(&kt)[8], bf16x8(&vt)[8], int lim) {
     if (lim <= 0) return;  // wave-uniform: the tile lies past the context end
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -256,17 +256,14 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
     if (lim < 32) {
       // the V slots of tokens past the context end may hold anything, NaN
       // included (not yet written): zero them, as a zero weight cancels only
-      // finite values.  Lane element i is token 8 kg + i.
+      // finite values.  Lane element i is token 8 kg + i; dword j holds
+      // elements 2j (low half) and 2j + 1.
+      u32x4 keep;
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) {
-        bf16x8 vm = vt[nb];
+      for (int j = 0; j < 4; ++j)
+        keep[j] = (8 * kg + 2 * j < lim ? 0x0000FFFFu : 0u) | (8 * kg + 2 * j + 1 < lim ? 0xFFFF0000u : 0u);
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (8 * kg + i >= lim) vm[i] = (__bf16)0.0f;
-        o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vm, o[nb], 0, 0, 0);
-        o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vm, o[nb], 0, 0, 0);
-      }
-      return;
+      for (int nb = 0; nb < 8; ++nb) vt[nb] = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, vt[nb]) & keep);
     }
 #pragma unroll
     for (int nb = 0; nb < 8; ++nb) {
@@ -390,8 +387,8 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   const int b = u.b, g = u.g, s = u.s, ns = u.ns;
 
   constexpr int TPC = C / 32;
-  const int cnt = min(max(a.sel_count[b], 0), a.sel_pitch);
   const int n_b = t.n[b];
+  const int cnt = a.count_is_keep ? min(t.keep[b], n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
   const int nTall = cnt * TPC;
   const int Tb = (int)(((int64_t)s * nTall) / ns), Te = (int)(((int64_t)(s + 1) * nTall) / ns);
   const int nT = Te > Tb ? Te - Tb : 0;
@@ -497,13 +494,22 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     if (lim < 32) {  // the context ends inside this tile: register r holds token 16 (r / 8) + 8 (lane / 32) + r % 8
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        if (16 * (r / 8) + 8 * (lane >> 5) + r % 8 >= lim) {
-          x[r] = -INFINITY;
-          // that token's V slots may hold anything, NaN included (not yet
-          // written): zero them, as a zero weight cancels only finite values
+        if (16 * (r / 8) + 8 * (lane >> 5) + r % 8 >= lim) x[r] = -INFINITY;
+      // those tokens' V slots may hold anything, NaN included (not yet
+      // written): zero them, as a zero weight cancels only finite values.
+      // Element i of vp[4 s + n] is token 16 s + 8 (lane / 32) + i; dword j
+      // holds elements 2j (low half) and 2j + 1.
 #pragma unroll
-          for (int n = 0; n < 4; ++n) vp[(r / 8) * 4 + n][r % 8] = (__bf16)0.0f;
-        }
+      for (int sh = 0; sh < 2; ++sh) {
+        const int t0 = 16 * sh + 8 * (lane >> 5);
+        u32x4 keep;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          keep[j] = (t0 + 2 * j < lim ? 0x0000FFFFu : 0u) | (t0 + 2 * j + 1 < lim ? 0xFFFF0000u : 0u);
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+          vp[4 * sh + n] = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, vp[4 * sh + n]) & keep);
+      }
     }
     // online softmax: lanes j and j ^ 32 share row j % 32 and split its tokens
     float mx = x[0];

@@ -259,9 +259,11 @@ lsa_status run_topk(const lsa_problem* p, const Plan& P, bool keys_ready, const 
   return LSA_OK;
 }
 
+// count_is_keep: sel_count[b] is known to be min(keep[b], n_b) (the top-k of a
+// fused step with one query embedding wrote it).
 lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, const uint16_t* k,
                     const uint16_t* v, const int32_t* sel_idx, const int32_t* sel_count, float scale,
-                    float* out, float* lse, void* ws, hipStream_t s) {
+                    float* out, float* lse, void* ws, hipStream_t s, bool count_is_keep = false) {
   AttnArgs a;
   a.q = q;
   a.k = k;
@@ -277,6 +279,7 @@ lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, cons
   const double sc = scale > 0.f ? (double)scale : 1.0 / std::sqrt((double)kHeadDim);
   a.scale_log2e = (float)(sc * 1.4426950408889634);
   a.sel_pitch = P.max_sel;
+  a.count_is_keep = count_is_keep ? 1 : 0;
   a.n_q_heads = p->n_q_heads;
   a.n_kv_heads = p->n_kv_heads;
   a.group = P.group;
@@ -662,7 +665,7 @@ lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const vo
   // order keys and the selection reads them without converting
   LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, true, s), "score launch");
   LSA_TRY(run_topk(p, P, true, scores, sel, cnt, nullptr, ws, s));
-  return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s);
+  return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s, p->n_lookahead == 1);
 }
 
 lsa_status lsa_decode_step_noalloc(const lsa_problem* p, const void* query_emb, const void* chunk_emb,

@@ -41,6 +41,8 @@ struct AttnArgs {
   int64_t head_stride;
   float scale_log2e;     // softmax scale * log2(e)
   int32_t sel_pitch;
+  int32_t count_is_keep; // 1: sel_count[b] is min(keep[b], n_b), known on the host (the fused step with Q = 1),
+                         // so the kernel need not wait for it
   int32_t n_q_heads;
   int32_t n_kv_heads;
   int32_t group;         // G = Hq / Hkv
