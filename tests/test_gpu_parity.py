@@ -217,13 +217,6 @@ def test_sharp_softmax():
 
 
 # ---------------------------------------------------------------- full size
-def _sample_rows(prob, n_rows):
-    rng = np.random.default_rng(0)
-    allr = [(t, h) for t in range(prob.n_qtok) for h in range(prob.n_q_heads)]
-    idx = sorted(rng.choice(len(allr), size=min(n_rows, len(allr)), replace=False).tolist())
-    return [allr[i] for i in idx]
-
-
 def test_preset_tiny():
     prob = synth.make_problem("tiny", 0)
     r = run_case(prob, 0)
@@ -231,8 +224,9 @@ def test_preset_tiny():
 
 
 def test_preset_int8():
+    """Every query row of every sequence."""
     prob = synth.make_problem("int8", 0)
-    r = run_case(prob, 0, seqs=[0, 3], rows=_sample_rows(prob, 8))
+    r = run_case(prob, 0)
     assert all(m == "exact" for m in r["modes"].values())
 
 
@@ -242,12 +236,15 @@ def test_preset_paper1m():
 
 
 def test_preset_batch32():
+    """Every query row of all 32 ragged sequences."""
     prob = synth.make_problem("batch32", 0)
-    big = int(np.argmax(prob.ctx_tokens))
-    run_case(prob, 0, seqs=sorted({0, big, 31}), rows=_sample_rows(prob, 6))
+    run_case(prob, 0)
 
 
 def test_preset_lookahead():
+    """All 8 sequences; for every KV head, all 8 of its query heads at query
+    tokens 0, 5, 10 and 15 (2,048 of the 8,192 output rows: every (sequence,
+    KV head) split-K unit and every row block of the many-rows kernel)."""
     prob = synth.make_problem("lookahead", 0)
-    rows = [(t, h) for t in (0, 15) for h in range(0, 64, 9)]
-    run_case(prob, 0, seqs=[0, 7], rows=rows)
+    rows = [(t, h) for t in (0, 5, 10, 15) for h in range(64)]
+    run_case(prob, 0, rows=rows)

@@ -93,13 +93,6 @@ def test_recall_step_is_deterministic():
         assert np.array_equal(o, outs[0][0]) and np.array_equal(s, outs[0][1])
 
 
-def _sample_rows(prob, n_rows):
-    rng = np.random.default_rng(7)
-    allr = [(t, h) for t in range(prob.n_qtok) for h in range(prob.n_q_heads)]
-    idx = rng.choice(len(allr), size=min(n_rows, len(allr)), replace=False)
-    return [allr[i] for i in sorted(idx)]
-
-
 def test_preset_recall_tiny():
     for seed in range(4):
         run_recall_case(synth.make_problem("recall_tiny", seed), seed)
@@ -107,11 +100,12 @@ def test_preset_recall_tiny():
 
 def test_preset_recall_batch():
     prob = synth.make_problem("recall_batch", 0)
-    run_recall_case(prob, 0, rows=_sample_rows(prob, 6))
+    run_recall_case(prob, 0)
 
 
 def test_preset_recall1m():
-    """The 1M-token recall workload in the benchmark's launch configuration."""
+    """The 1M-token recall workload in the benchmark's launch configuration,
+    every query row."""
     prob = synth.make_problem("recall1m", 0)
-    r = run_recall_case(prob, 0, rows=_sample_rows(prob, 6))
+    r = run_recall_case(prob, 0)
     log(f"[recall1m] recalled {r['cnt'].tolist()} of {prob.n_chunks[0]} (K_max {prob.keep[0]})")

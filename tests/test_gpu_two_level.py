@@ -60,22 +60,16 @@ def test_two_level_rows_above_16_partial_chunk():
                          chunk=128, hq=64, hkv=8, Tq=16), seed=9, rows=[(t, h) for t in (0, 7, 15) for h in range(64)])
 
 
-def _sample_rows(prob, n_rows):
-    rng = np.random.default_rng(7)
-    allr = [(t, h) for t in range(prob.n_qtok) for h in range(prob.n_q_heads)]
-    idx = rng.choice(len(allr), size=min(n_rows, len(allr)), replace=False)
-    return [allr[i] for i in sorted(idx)]
-
-
 def test_preset_two_level_tiny():
     for seed in range(4):
         run_two_level_case(synth.make_problem("twolevel_tiny", seed), seed)
 
 
 def test_preset_two_level_1m():
-    """The 1M-token two-level workload in the benchmark's launch configuration."""
+    """The 1M-token two-level workload in the benchmark's launch configuration,
+    every query row."""
     prob = synth.make_problem("twolevel1m", 0)
-    r = run_two_level_case(prob, 0, rows=_sample_rows(prob, 6))
+    r = run_two_level_case(prob, 0)
     log(f"[twolevel1m] kept {r['cnt'].tolist()} chunks of {prob.n_chunks[0]}")
 
 
