@@ -198,6 +198,8 @@ def main() -> int:
                     help="untimed streaming read between the per-step samples of the step-time distribution, "
                          "so that the 256 MB Infinity Cache cannot serve a previous step's bytes "
                          "(a multiple of 32; default: 1024 for workloads below 1 GB per step, else 0)")
+    ap.add_argument("--tier-fetch-wgs", type=int, default=8, choices=(4, 8, 16, 32),
+                    help="tier1m / tier2l1m: workgroups of the copy kernel in the steady-state side band")
     ap.add_argument("--tier-lag", type=int, default=48,
                     help="tier1m: decode steps from a firing until its kept set is read (1 .. 63)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -498,8 +500,7 @@ def bench_tier(args) -> int:
             qf = math.sqrt(TIER_RHO) * qf + math.sqrt(1.0 - TIER_RHO) * rng.standard_normal(qf.shape)
         idx_q.append(up(synth.f64_to_bf16_bits(qf)))
     # unrelated queries: a full change of the kept set
-    fresh_q = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))
-    fresh_q2 = up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape)))
+    fresh_qs = [up(synth.f64_to_bf16_bits(rng.standard_normal(qf.shape))) for _ in range(5)]
     rot = [synth.host_inputs(prob, 1000 + r) for r in range(1, 4)]
     qs = [dev["q"]] + [up(h["q"]) for h in rot]
     nat_qs = [dev["nat_q"]] + [up(h["nat_q"]) for h in rot] if level2 else []
@@ -532,9 +533,12 @@ def bench_tier(args) -> int:
         L.lsa_tier_plan(P, T, kept[new], cnt[new], slots[prev] if prev is not None else None,
                         cnt[prev] if prev is not None else None, owner, slots[new], fetch, fcount, s)
 
-    def fire(q_idx, prev, new, s):
+    # the copy kernel beside decode runs on fewer workgroups than the cold fill
+    T_side = {w: L.Tier([2 * K] * B, fetch_workgroups=w) for w in (4, 8, 16, 32)}
+
+    def fire(q_idx, prev, new, s, wgs=None):
         select_and_plan(q_idx, prev, new, s)
-        L.lsa_tier_fetch(P, T, host_k, host_v, fetch, fcount, res_k, res_v, s)
+        L.lsa_tier_fetch(P, T_side[wgs or args.tier_fetch_wgs], host_k, host_v, fetch, fcount, res_k, res_v, s)
 
     def decode(buf, i, s):
         if level2:
@@ -621,13 +625,16 @@ def bench_tier(args) -> int:
     # ---- a full change of the kept set, copied on the side stream while decode
     # goes on over the old set, by the copy kernel and by the DMA engines
     full = {}
-    for mode, q_full in (("kernel", fresh_q), ("dma", fresh_q2)):
+    for mode, q_full in zip([f"kernel_{w}wg" for w in (4, 8, 16, 32)] + ["dma"], fresh_qs):
         fe = [ev(), ev()]
         side.wait_stream(main)
         fe[0].record(side)
-        (fire if mode == "kernel" else fire_dma)(q_full, 0, 1, side)
+        if mode == "dma":
+            fire_dma(q_full, 0, 1, side)
+        else:
+            fire(q_full, 0, 1, side, wgs=int(mode.split("_")[1][:-2]))
         fe[1].record(side)
-        n_during = 400 if mode == "dma" else 120
+        n_during = 700
         dd = [(ev(), ev()) for _ in range(n_during)]
         for i in range(n_during):
             dd[i][0].record(main)

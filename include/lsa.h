@@ -138,7 +138,10 @@ typedef struct lsa_indexer {
 typedef struct lsa_tier {
   const int32_t* slots;  /* HOST [B]: reserve slots of sequence b, 2 * keep[b] .. LSA_MAX_TIER_SLOTS */
   int32_t reserved;      /* must be 0 */
-  int32_t reserved2;     /* must be 0 */
+  int32_t fetch_workgroups; /* workgroups of lsa_tier_fetch's copy kernel, 0 .. 1024; 0 selects 32, the
+                               fastest copy (for a cold fill).  The copy reads the mirror through the memory
+                               path a concurrent decode uses, and each copy workgroup slows that decode:
+                               fewer move less per second but disturb it less. */
 } lsa_tier;
 
 /* Golden-label pipeline.  Host memory only; read during the call. */

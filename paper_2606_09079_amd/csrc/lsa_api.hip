@@ -353,7 +353,9 @@ struct TierPlan {
 lsa_status make_tier_plan(const lsa_problem* p, const lsa_tier* tr, TierPlan* tp) {
   LSA_TRY(make_plan(p, &tp->P));
   if (tr == nullptr) return fail(LSA_ERR_INVALID_ARG, "tier is NULL");
-  if (tr->reserved != 0 || tr->reserved2 != 0) return fail(LSA_ERR_INVALID_ARG, "tier reserved fields must be 0");
+  if (tr->reserved != 0) return fail(LSA_ERR_INVALID_ARG, "tier reserved field must be 0");
+  if (tr->fetch_workgroups < 0 || tr->fetch_workgroups > 1024)
+    return fail(LSA_ERR_INVALID_ARG, "tier fetch_workgroups %d not in [0, 1024]", tr->fetch_workgroups);
   if (tr->slots == nullptr) return fail(LSA_ERR_INVALID_ARG, "tier slots must be a host array of batch entries");
   if (p->n_lookahead != 1)
     return fail(LSA_ERR_INVALID_ARG, "the host tier takes one query token: n_lookahead %d != 1", p->n_lookahead);
@@ -957,6 +959,7 @@ lsa_status lsa_tier_fetch(const lsa_problem* p, const lsa_tier* tr, const uint16
   a.n_kv_heads = p->n_kv_heads;
   for (int b = 0; b < p->batch; ++b) a.slots[b] = tr->slots[b];
   memcpy(a.slot_off, T.slot_off, sizeof a.slot_off);
+  a.workgroups = tr->fetch_workgroups;
   LSA_HIP(launch_tier_fetch(P.t, a, p->chunk_size, (hipStream_t)stream), "tier fetch launch");
   return LSA_OK;
 }

@@ -212,6 +212,7 @@ struct TierFetchArgs {
   int64_t res_slot_stride;            // n_kv_heads * C * 128
   int32_t pitch;
   int32_t n_kv_heads;
+  int32_t workgroups;                 // copy workgroups per launch, 0: the default
   int32_t slots[LSA_MAX_BATCH];
   int32_t slot_off[LSA_MAX_BATCH + 1];
 };

@@ -27,7 +27,7 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kChunkWords = kMaxTierChunks / 32;
 constexpr int kSlotWords = kMaxTierSlots / 32;
-constexpr int kFetchWorkgroups = 32;  // copy workgroups per launch (at least one per sequence)
+constexpr int kFetchWorkgroups = 32;  // default copy workgroups per launch (at least one per sequence)
 
 // Exclusive prefix sum over the workgroup (one value per thread); *total
 // receives the sum of all values.
@@ -209,7 +209,8 @@ hipError_t launch_tier_plan(const SeqTable& t, const TierArgs& a, hipStream_t s)
 hipError_t launch_tier_fetch(const SeqTable& t, const TierFetchArgs& a, int32_t chunk_size, hipStream_t s) {
   const int64_t blocks = (int64_t)a.pitch * a.n_kv_heads * 2;
   if (blocks == 0) return hipSuccess;
-  const int64_t per_seq = std::min<int64_t>(blocks, std::max(1, kFetchWorkgroups / t.batch));
+  const int wgs = a.workgroups > 0 ? a.workgroups : kFetchWorkgroups;
+  const int64_t per_seq = std::min<int64_t>(blocks, std::max(1, wgs / t.batch));
   const dim3 grid((unsigned)per_seq, (unsigned)t.batch);
   if (chunk_size == 64)
     hipLaunchKernelGGL(tier_fetch_kernel<64>, grid, dim3(256), 0, s, t, a);

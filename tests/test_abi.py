@@ -206,6 +206,8 @@ def test_tier_sizes_and_validation():
     bad = L.Tier([80, 200])
     bad.c.reserved = 1
     assert lib.lsa_tier_sizes(p.ref, bad.ref, None, None, None) == B.LSA_ERR_INVALID_ARG
+    for wgs, status in ((-1, B.LSA_ERR_INVALID_ARG), (1025, B.LSA_ERR_INVALID_ARG), (1024, 0), (4, 0)):
+        assert lib.lsa_tier_sizes(p.ref, L.Tier([80, 200], fetch_workgroups=wgs).ref, None, None, None) == status
     la = L.Problem([64 * 300], 64, [40], 8, 2, n_lookahead=2)
     assert lib.lsa_tier_sizes(la.ref, L.Tier([80]).ref, None, None, None) == B.LSA_ERR_INVALID_ARG
     part = L.Problem([64 * 300 + 5], 64, [40], 8, 2)
