@@ -85,6 +85,13 @@ __device__ __forceinline__ uint32_t order_key(uint32_t bits) {
   }
 }
 
+// Order key of an exact int32 score of int8 embeddings, |s| <= 512 * 128^2 =
+// 2^23: (s + 2^24) << 7 is increasing and spreads the scores over the 32-bit
+// range, so the selection's first 12-bit digit tells them apart.  (With the
+// sign flip of order_key, every score below 2^20 in magnitude falls in one of
+// two bins, and the last digits then run over all the keys.)
+__device__ __forceinline__ uint32_t int_score_key(int32_t s) { return ((uint32_t)s + (1u << 24)) << 7; }
+
 // keys == true writes order keys instead of scores (for the fused step).
 hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,
                         const void* E, void* scores, bool keys, hipStream_t s);

@@ -125,7 +125,7 @@ score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restri
         for (int off = G::lanes / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
         bits = __float_as_uint(acc);
       }
-      if constexpr (KEYS) bits = order_key<DT == LSA_I8 ? kKeysFromI32 : kKeysFromF32>(bits);
+      if constexpr (KEYS) bits = DT == LSA_I8 ? int_score_key((int32_t)bits) : order_key<kKeysFromF32>(bits);
       if (sub == 0 && r < n) out_b[(int64_t)j * n + r] = bits;
     }
   }

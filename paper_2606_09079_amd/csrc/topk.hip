@@ -13,7 +13,7 @@
 // topk_select_kernel (up to 16384 chunks) runs on one compute unit, where every
 // instruction executed by all 1024 threads costs 16 cycles, so the design
 // minimises per-key work:
-//   - keys stay in registers (16 per thread, coalesced buffer loads);
+//   - keys stay in registers (up to 16 per thread, coalesced buffer loads);
 //   - first digit: top 12 bits into an LDS histogram whose atomic return
 //     values double as each key's rank in its bin, so the keys of the
 //     threshold bin are packed into a candidate list without a scan;
@@ -202,6 +202,9 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelMaxN = 16384;
 constexpr int kSelKPT = kSelMaxN / kSelThreads;  // 16 keys per thread
+// topk_select_kernel holds KPT keys per thread: 16 up to 16384 keys, 4 up to
+// 4096, 2 up to 2048.  On one CU every per-key instruction of the 1024 threads
+// costs 16 cycles, so a short sequence does not pay for 16 slots of padding.
 constexpr int kSelCand = 4096;                   // threshold-bin keys packed for the last digits
 constexpr int kSelSub = 4;                       // sub-histograms of the first digit (lane / 16)
 
@@ -272,7 +275,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(const void* p, uint
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-template <int MODE, bool RECALL>
+template <int MODE, bool RECALL, int KPT>
 __global__ void __launch_bounds__(kSelThreads)
 topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __restrict__ out_idx,
                    int64_t pitch_seq, int64_t pitch_q, int32_t* __restrict__ sel_count, SelectArgs sa) {
@@ -306,27 +309,27 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   // few real keys they would all land in bin 0 and serialise its atomics),
   // never fall in the threshold bin, and the emission drops their chunk ids.
   const __amdgpu_buffer_rsrc_t src = raw_buffer(s, (uint32_t)n * 4u);
-  uint32_t kk[kSelKPT];
+  uint32_t kk[KPT];
 #pragma unroll
-  for (int q = 0; q < kSelKPT; ++q)
+  for (int q = 0; q < KPT; ++q)
     kk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
   // mapped mode: the ids that the keys stand for, loaded with them and staged
   // in LDS (in the histogram's space, once it is free) for the emission
-  uint32_t mp[kSelKPT];
+  uint32_t mp[KPT];
   if (sa.map != nullptr) {
     const __amdgpu_buffer_rsrc_t msrc = raw_buffer(sa.map + b * sa.map_pitch, (uint32_t)n * 4u);
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q)
+    for (int q = 0; q < KPT; ++q)
       mp[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(msrc, tid * 4, q * kSelThreads * 4, 0);
   }
   if constexpr (RECALL) {
     // keys of the first layer, then the largest over the other indexer layers
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
+    for (int q = 0; q < KPT; ++q) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
     for (int l = 1; l < sa.n_layers; ++l) {
       const __amdgpu_buffer_rsrc_t srcl = raw_buffer(s + l * sa.layer_stride, (uint32_t)n * 4u);
 #pragma unroll
-      for (int q = 0; q < kSelKPT; ++q) {
+      for (int q = 0; q < KPT; ++q) {
         const uint32_t v = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(srcl, tid * 4, q * kSelThreads * 4, 0);
         if (q * kSelThreads + tid < n) kk[q] = max(kk[q], order_key<MODE>(v));
       }
@@ -346,16 +349,16 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   if constexpr (RECALL) {
     uint32_t nn = 0;
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q) {
+    for (int q = 0; q < KPT; ++q) {
       nn += (uint32_t)__popcll(__ballot(kk[q] >= 0x80000000u));
       kk[q] = kk[q] >= 0x80000000u ? kk[q] : 0u;
     }
     if (lane == 0) nonneg[wave] = nn;
   }
-  uint32_t bin[kSelKPT], rk[kSelKPT];
-  bool in[kSelKPT];
+  uint32_t bin[KPT], rk[KPT];
+  bool in[KPT];
 #pragma unroll
-  for (int q = 0; q < kSelKPT; ++q) {
+  for (int q = 0; q < KPT; ++q) {
     if constexpr (MODE != kKeysReady && !RECALL) kk[q] = q * kSelThreads + tid < n ? order_key<MODE>(kk[q]) : 0u;
     in[q] = RECALL ? kk[q] != 0u : q * kSelThreads + tid < n;
     bin[q] = kk[q] >> 20;
@@ -410,11 +413,11 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
     const uint4 bc = reinterpret_cast<const uint4*>(hist)[B0];
     const uint32_t off = (sub > 0 ? bc.x : 0u) + (sub > 1 ? bc.y : 0u) + (sub > 2 ? bc.z : 0u);
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q)
+    for (int q = 0; q < KPT; ++q)
       if (in[q] && bin[q] == B0) cand[off + rk[q]] = kk[q];
   } else {
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q) keys[q * kSelThreads + tid] = kk[q];
+    for (int q = 0; q < KPT; ++q) keys[q * kSelThreads + tid] = kk[q];
   }
   __syncthreads();
 
@@ -444,12 +447,12 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   uint32_t* map_lds = hist;  // free from here on
   if (sa.map != nullptr) {
 #pragma unroll
-    for (int q = 0; q < kSelKPT; ++q) map_lds[q * kSelThreads + tid] = mp[q];
+    for (int q = 0; q < KPT; ++q) map_lds[q * kSelThreads + tid] = mp[q];
   }
   uint64_t* gdst = reinterpret_cast<uint64_t*>(bm_gt) + wave;
   uint64_t* edst = reinterpret_cast<uint64_t*>(bm_eq) + wave;
 #pragma unroll
-  for (int q = 0; q < kSelKPT; ++q) {
+  for (int q = 0; q < KPT; ++q) {
     const uint64_t g = __ballot(kk[q] > T);
     const uint64_t e = __ballot(kk[q] == T);
     if (lane == 0) {
@@ -745,9 +748,15 @@ hipError_t launch_topk_keys(const SeqTable& t, const uint32_t* scores, int32_t* 
   int n_max = 0;
   for (int b = 0; b < t.batch; ++b) n_max = max(n_max, t.n[b]);
   const dim3 grid(t.batch * t.n_lookahead);
-  if (n_max <= kSelMaxN)
-    hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
+  if (n_max <= 2 * kSelThreads)
+    hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL, 2>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
                        pitch_seq, pitch_q, sel_count, sa);
+  else if (n_max <= 4 * kSelThreads)
+    hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL, 4>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
+                       pitch_seq, pitch_q, sel_count, sa);
+  else if (n_max <= kSelMaxN)
+    hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL, kSelKPT>), grid, dim3(kSelThreads), 0, s, t, scores,
+                       out_idx, pitch_seq, pitch_q, sel_count, sa);
   else
     hipLaunchKernelGGL((topk_kernel<MODE, RECALL>), grid, dim3(kThreads), 0, s, t, scores, out_idx, pitch_seq,
                        pitch_q, sel_count, sa);
