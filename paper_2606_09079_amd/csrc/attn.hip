@@ -96,22 +96,23 @@ struct Unit {
   int b, g, s, ns;
 };
 
-// Static split boundaries weighted by the XCD of each split's workgroup.  The
-// dispatcher places workgroup i on XCD i % 8, and per-workgroup timestamps on
-// MI355X show the odd-numbered XCDs streaming 7-8% slower than the even ones
-// (every run measured); giving even-XCD workgroups 6/5 of the tiles of their
-// odd neighbours took the 1M-token step from 84.6 to 82.9 us.  (The many-rows
-// kernel, two workgroups per CU, measured 1% slower with it and keeps equal
-// splits.)  Returns the first tile of split s of (b, g), so that split s
-// covers [first(s), first(s + 1)).
-constexpr int kEvenXcdWeight = 6;
-constexpr int kOddXcdWeight = 5;
+// Static split boundaries: even-numbered units get 6/5 of the tiles of odd
+// ones.  In the split kernel a unit is its workgroup, which the dispatcher
+// places on XCD i % 8, and per-workgroup timestamps on MI355X show the
+// odd-numbered XCDs streaming 7-8% slower than the even ones (every run
+// measured); the weighting took the 1M-token step from 84.6 to 82.9 us.  The
+// many-rows kernel runs two workgroups per CU and maps units so that even
+// units sit in the first slot of a CU, which runs faster than the second (1.8%
+// on the lookahead step).  Returns the first tile of split s of (b, g), so that
+// split s covers [first(s), first(s + 1)).
+constexpr int kEvenUnitWeight = 6;
+constexpr int kOddUnitWeight = 5;
 
 __device__ __forceinline__ int split_first(const SeqTable& t, int b, int g, int s, int ns, int n_tiles) {
   const int base = t.wg_off[b] + g * ns;  // workgroup of split 0 of (b, g)
   auto weight_below = [&](int j) -> int64_t {  // the weights of splits 0 .. j - 1
     const int64_t even = (int64_t)((base + j + 1) / 2 - (base + 1) / 2);
-    return even * kEvenXcdWeight + (int64_t)(j - even) * kOddXcdWeight;
+    return even * kEvenUnitWeight + (int64_t)(j - even) * kOddUnitWeight;
   };
   return (int)((int64_t)n_tiles * weight_below(s) / weight_below(ns));
 }
@@ -383,14 +384,21 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.group;
-  const Unit u = unit_of(t, blockIdx.x);
+  // Two workgroups share each CU, and the dispatcher fills the first slot of
+  // every CU (the first half of a grid of two per CU) before the second, whose
+  // workgroups run slower.  So consecutive units (the splits of one (b, g))
+  // alternate between the first and the second half of the grid, and the even
+  // ones, in the first half, get 6/5 of the tiles of the odd ones (split_first).
+  const int half = (int)(gridDim.x + 1) / 2;
+  const int unit_id = (int)blockIdx.x < half ? 2 * (int)blockIdx.x : 2 * ((int)blockIdx.x - half) + 1;
+  const Unit u = unit_of(t, unit_id);
   const int b = u.b, g = u.g, s = u.s, ns = u.ns;
 
   constexpr int TPC = C / 32;
   const int n_b = t.n[b];
   const int cnt = a.count_is_keep ? min(t.keep[b], n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
   const int nTall = cnt * TPC;
-  const int Tb = (int)(((int64_t)s * nTall) / ns), Te = (int)(((int64_t)(s + 1) * nTall) / ns);
+  const int Tb = split_first(t, b, g, s, ns, nTall), Te = split_first(t, b, g, s + 1, ns, nTall);
   const int nT = Te > Tb ? Te - Tb : 0;
 
   // this wave's 32 query rows: lane j serves row 32 * wave + j % 32
@@ -607,7 +615,7 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run), false, false);
     const float l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
     if (row < a.rows) {
-      const int64_t rbase = (int64_t)blockIdx.x * a.rows_pad + row;
+      const int64_t rbase = (int64_t)unit_id * a.rows_pad + row;
       float* po = a.part_o + rbase * kHeadDim + 4 * (lane >> 5);
 #pragma unroll
       for (int n = 0; n < 4; ++n)
