@@ -202,8 +202,8 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelMaxN = 16384;
 constexpr int kSelKPT = kSelMaxN / kSelThreads;  // 16 keys per thread
-// topk_select_kernel holds KPT keys per thread: 16 up to 16384 keys, 4 up to
-// 4096, 2 up to 2048.  On one CU every per-key instruction of the 1024 threads
+// topk_select_kernel holds KPT keys per thread: 16 up to 16384 keys, 8 up to
+// 8192, 4 up to 4096, 2 up to 2048.  On one CU every per-key instruction of the 1024 threads
 // costs 16 cycles, so a short sequence does not pay for 16 slots of padding.
 constexpr int kSelCand = 4096;                   // threshold-bin keys packed for the last digits
 constexpr int kSelSub = 4;                       // sub-histograms of the first digit (lane / 16)
@@ -753,6 +753,9 @@ hipError_t launch_topk_keys(const SeqTable& t, const uint32_t* scores, int32_t* 
                        pitch_seq, pitch_q, sel_count, sa);
   else if (n_max <= 4 * kSelThreads)
     hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL, 4>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
+                       pitch_seq, pitch_q, sel_count, sa);
+  else if (n_max <= 8 * kSelThreads)
+    hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL, 8>), grid, dim3(kSelThreads), 0, s, t, scores, out_idx,
                        pitch_seq, pitch_q, sel_count, sa);
   else if (n_max <= kSelMaxN)
     hipLaunchKernelGGL((topk_select_kernel<MODE, RECALL, kSelKPT>), grid, dim3(kSelThreads), 0, s, t, scores,
