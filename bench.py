@@ -728,7 +728,7 @@ def bench_tier(args) -> int:
         fire_ms = [a.elapsed_time(b) for a, b, timed in fire_ev if timed]
         n_copies = [int(c.cpu()[0]) for c in copies]
         log(f"[tier] {mode} copies, lag {lag}: {args.steps} steps, {ms * 1e3:.2f} us/step (wall {wall:.3f}s); "
-            f"firings {[round(x, 3) for x in fire_ms]} ms; copies {n_copies}; side-band host ms {side_host[-4:]}")
+            f"firings {[round(x, 3) for x in fire_ms]} ms; copies {n_copies}; side-band host ms {side_host[-len(fire_ms):] if fire_ms else side_host}")
         return {"us_per_step": round(ms * 1e3, 2), "lag_steps": lag, "firings_timed": len(fire_ms),
                 "firing_ms": round(sum(fire_ms) / len(fire_ms), 3) if fire_ms else None,
                 "copies_per_firing": n_copies[-len(fire_ms):] if fire_ms else [],
