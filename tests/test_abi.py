@@ -337,6 +337,33 @@ def test_noalloc_rejects_a_step_beyond_its_scratch():
                                          None) == B.LSA_ERR_INVALID_ARG
 
 
+def test_kv_pack_rejects_bad_arguments_without_launching():
+    """lsa_kv_pack validates on the host: first tokens outside [0, ctx], strides
+    that are not non-negative multiples of 8 elements, missing or misaligned
+    buffers, and a problem the attention would refuse."""
+    lib = L.LIB
+    p = good(ctx_tokens=[64 * 100 + 5, 64 * 10])  # a partial last chunk is accepted here
+    i64 = lambda *v: ctypes.cast((ctypes.c_int64 * len(v))(*v), ctypes.c_void_p)
+    ok_first = i64(6400, 0)
+    call = lambda first=ok_first, ts=0, hs=0, ptrs=(FAKE,) * 5: lib.lsa_kv_pack(
+        p.ref, ptrs[0], ptrs[1], ptrs[2], ts, hs, first, ptrs[3], ptrs[4], None)
+    assert call(first=i64(-1, 0)) == B.LSA_ERR_INVALID_ARG
+    assert call(first=i64(6406, 0)) == B.LSA_ERR_INVALID_ARG
+    assert call(first=i64(0, 641)) == B.LSA_ERR_INVALID_ARG
+    for ts, hs in ((-8, 0), (12, 0), (0, 4), (0, -128)):
+        assert call(ts=ts, hs=hs) == B.LSA_ERR_INVALID_ARG, (ts, hs)
+    for i in range(5):
+        ptrs = [FAKE] * 5
+        ptrs[i] = None
+        assert call(ptrs=tuple(ptrs)) == B.LSA_ERR_INVALID_ARG, i
+        ptrs[i] = MISALIGNED
+        assert call(ptrs=tuple(ptrs)) == B.LSA_ERR_INVALID_ARG, i
+    assert lib.lsa_kv_pack(good(chunk_size=32).ref, FAKE, FAKE, FAKE, 0, 0, None, FAKE, FAKE, None) \
+        == B.LSA_ERR_UNSUPPORTED
+    # nothing to write (every first token at the context end): accepted with no launch at all
+    assert call(first=i64(6405, 640)) == B.LSA_OK
+
+
 def _no_device():
     import torch
     return torch.cuda.device_count() == 0
