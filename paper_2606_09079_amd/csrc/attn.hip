@@ -470,35 +470,28 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   // tile runs while the MFMA unit works on the next tile's QK.  Tile j lives in
   // buffer j % 5: the copy of tile j + 3 reuses the buffer of tile j - 2, whose
   // last reader (step j - 1) is behind the barrier.
-  // logits of the tile whose softmax is pending, as the two QK accumulators
-  // (summed only when the softmax runs, a step after the products were issued)
-  f32x16 s_cur0, s_cur1;
+  // logits of the tile whose softmax is pending.  The QK products of a tile
+  // form one chain of 8 dependent MFMAs: the softmax that reads them runs a
+  // step later, so the chain's latency is hidden, and one accumulator instead
+  // of two saves 16 registers and the 16 adds that summed them.
+  f32x16 s_cur0;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    s_cur0[r] = 0.f;
-    s_cur1[r] = 0.f;
-  }
+  for (int r = 0; r < 16; ++r) s_cur0[r] = 0.f;
 
-  auto qk = [&](const uint4(&tb)[16][64], f32x16& s0, f32x16& s1) {
+  auto qk = [&](const uint4(&tb)[16][64], f32x16& s0) {
     bf16x8 kp[8];
     read_pieces(tb, 0, lane, kp);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s0[r] = 0.f;
-      s1[r] = 0.f;
-    }
+    for (int r = 0; r < 16; ++r) s0[r] = 0.f;
 #pragma unroll
-    for (int d = 0; d < 8; d += 2) {
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kp[d], qb[d], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kp[d + 1], qb[d + 1], s1, 0, 0, 0);
-    }
+    for (int d = 0; d < 8; ++d) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kp[d], qb[d], s0, 0, 0, 0);
   };
 
-  auto softmax_pv = [&](const f32x16& x0, const f32x16& x1, const uint4(&tb)[16][64], int lim) {
+  auto softmax_pv = [&](const f32x16& x0, const uint4(&tb)[16][64], int lim) {
     if (lim <= 0) return;  // wave-uniform: the tile lies past the context end
     bf16x8 vp[8];
     read_pieces(tb, 8, lane, vp);
-    f32x16 x = x0 + x1;
+    f32x16 x = x0;
     if (lim < 32) {  // the context ends inside this tile: register r holds token 16 (r / 8) + 8 (lane / 32) + r % 8
 #pragma unroll
       for (int r = 0; r < 16; ++r)
@@ -576,11 +569,10 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     __asm__ volatile("" ::: "memory");
     if (j + kRowBufs - 2 < nT) lims[kdma] = issue(j + kRowBufs - 2, dma);
     if (!live) return;
-    f32x16 n0, n1;
-    if (lims[kcur] > 0) qk(cur, n0, n1);
-    if (j > 0) softmax_pv(s_cur0, s_cur1, prev, lims[kprev]);
+    f32x16 n0;
+    if (lims[kcur] > 0) qk(cur, n0);
+    if (j > 0) softmax_pv(s_cur0, prev, lims[kprev]);
     s_cur0 = n0;
-    s_cur1 = n1;
   };
 
   if (nT > 0) lims[0] = issue(0, buf0);
@@ -601,11 +593,11 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   // the last tile's softmax and PV (its buffer is nT - 1 mod 5)
   if (nT > 0 && live) {
     switch ((nT - 1) % 5) {
-      case 0: softmax_pv(s_cur0, s_cur1, buf0, lims[0]); break;
-      case 1: softmax_pv(s_cur0, s_cur1, buf1, lims[1]); break;
-      case 2: softmax_pv(s_cur0, s_cur1, buf2, lims[2]); break;
-      case 3: softmax_pv(s_cur0, s_cur1, buf3, lims[3]); break;
-      default: softmax_pv(s_cur0, s_cur1, buf4, lims[4]); break;
+      case 0: softmax_pv(s_cur0, buf0, lims[0]); break;
+      case 1: softmax_pv(s_cur0, buf1, lims[1]); break;
+      case 2: softmax_pv(s_cur0, buf2, lims[2]); break;
+      case 3: softmax_pv(s_cur0, buf3, lims[3]); break;
+      default: softmax_pv(s_cur0, buf4, lims[4]); break;
     }
   }
 
