@@ -112,6 +112,47 @@ def test_attention_alone_partial_context_many_rows(chunk, tail):
                                    r_out, r_lse, f"partial context C={chunk}, tail {tail}, {len(kept)} kept, KV head {g}")
 
 
+@pytest.mark.parametrize("chunk,nfull,tail", [(64, 400, 13), (128, 200, 1), (128, 200, 127)])
+def test_attention_alone_partial_context_many_rows_long(chunk, nfull, tail):
+    """The lookahead head shape on a context that ends inside its last chunk,
+    with long kept lists (every chunk, and every third chunk plus the last):
+    each split streams many full tiles before the partial chunk, which comes
+    last.  Token by token against the oracle for KV heads 0, 3 and 7."""
+    import torch
+    import oracle
+    import parity
+    import paper_2606_09079_amd as L
+    Hq, Hkv, Tq = 64, 8, 16
+    prob = synth.Problem("partial_rows_long", [chunk * nfull + tail], chunk, [8], Hq, Hkv, n_qtok=Tq)
+    host = synth.host_inputs(prob, 21)
+    dev = synth.device_inputs(prob, 21, host=host)
+    n = prob.n_chunks[0]
+    G = Hq // Hkv
+    every = np.arange(n, dtype=np.int32)
+    third = np.union1d(np.arange(0, n, 3, dtype=np.int32), [n - 1]).astype(np.int32)
+    for kept in (every, third):
+        P = L.Problem(prob.ctx_tokens, chunk, [len(kept)], Hq, Hkv, n_qtok=Tq)
+        ws_bytes = L.lsa_workspace_size(L.Problem([chunk * n], chunk, [len(kept)], Hq, Hkv, n_qtok=Tq))
+        ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+        sel = torch.from_numpy(kept[None, :].copy()).cuda()
+        cnt = torch.tensor([len(kept)], dtype=torch.int32, device="cuda")
+        out = torch.full((1, Tq, Hq, 128), float("nan"), device="cuda")
+        lse = torch.full((1, Tq, Hq), float("nan"), device="cuda")
+        L.lsa_sparse_decode_attn(P, dev["q"], dev["k"], dev["v"], sel, cnt, 0.0, out, lse, ws, ws_bytes)
+        torch.cuda.synchronize()
+        g_out, g_lse = out.cpu().numpy(), lse.cpu().numpy()
+        toks = oracle.kept_tokens(kept, chunk, prob.ctx_tokens[0])
+        for g in (0, 3, 7):
+            Kh = synth.kv_head_sparse(prob, 21, "k", 0, g, kept)
+            Vh = synth.kv_head_sparse(prob, 21, "v", 0, g, kept)
+            rows = [(t, g * G + j) for t in range(Tq) for j in range(G)]
+            qr = np.stack([host["q"][0, t, h] for (t, h) in rows])
+            r_out, r_lse = oracle.attention_tokens(qr, Kh, Vh, toks)
+            parity.check_attention(np.stack([g_out[0, t, h] for (t, h) in rows]), [g_lse[0, t, h] for (t, h) in rows],
+                                   r_out, r_lse, f"partial context C={chunk}, tail {tail}, {len(kept)} kept, KV head {g}")
+        log(f"[partial long] C={chunk} tail {tail}: {len(kept)} kept chunks, 3 KV heads x 128 rows")
+
+
 @pytest.mark.parametrize("tail", [1, 31, 32, 33, 63])
 def test_attention_alone_partial_context(tail):
     """lsa_sparse_decode_attn on a context that ends inside its last chunk:
