@@ -610,12 +610,17 @@ def bench_tier(args) -> int:
         de[i][1].record(main)
     torch.cuda.synchronize()
     dec_us = 1e3 * sum(a.elapsed_time(b) for a, b in de) / n_dec
-    # host cost of enqueueing one decode step (binding, validation, launches)
-    th = time.perf_counter()
+    # host cost of enqueueing one decode step (binding, validation, launches):
+    # the median over single calls, each into an idle queue, so that one stall
+    # of the host process does not stand for the cost of every call
+    host_t = []
     for i in range(n_dec):
+        torch.cuda.synchronize()
+        th = time.perf_counter()
         decode(0, i, main)
-    host_us = (time.perf_counter() - th) / n_dec * 1e6
+        host_t.append(time.perf_counter() - th)
     torch.cuda.synchronize()
+    host_us = float(np.median(host_t)) * 1e6
 
     # the copy list on the host, for the DMA engines
     h_fetch = torch.empty(B, pitch, 2, dtype=torch.int32, pin_memory=True)
