@@ -119,8 +119,8 @@ typedef struct lsa_problem {
   int32_t emb_dtype;    /* lsa_dtype of E and of the query embeddings */
   int32_t reserved;     /* must be 0 */
   const int64_t* ctx_tokens; /* HOST [B]: context tokens of each sequence, a positive multiple of C
-                                (lsa_sparse_decode_attn and lsa_two_level_step also take any positive
-                                count: the last chunk may be partial) */
+                                (lsa_sparse_decode_attn, lsa_two_level_step and lsa_kv_pack also take
+                                any positive count: the last chunk may be partial) */
   const int32_t* keep;       /* HOST [B]: keep budget k_b, 1 <= k_b <= n_b (per query when Q > 1) */
   int64_t kv_chunk_stride;   /* elements between chunks in K and V; 0 selects n_kv_heads*C*d */
   int64_t kv_head_stride;    /* elements between KV heads in K and V; 0 selects C*d */
