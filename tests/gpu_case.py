@@ -33,7 +33,7 @@ def _rows_all(prob) -> List[Tuple[int, int]]:
 
 
 # The oracle runs one (sequence, KV head) per thread; its C calls release the
-# interpreter lock.  At most 16 threads: a GPU machine's share of host cores.
+# interpreter lock.  At most 16 threads, so that the oracle never oversubscribes the host.
 WORKERS = max(1, min(16, os.cpu_count() or 1))
 
 
