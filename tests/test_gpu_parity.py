@@ -38,6 +38,11 @@ SMALL = [
     P("f32_d512_q2", [64 * 61], 64, [11], 8, 4, emb_dim=512, dtype="f32", Q=2),
     P("many_splits", [64 * 4000], 64, [3000], 8, 8),
     P("keys_beyond_lds", [64 * 20000], 64, [2000], 8, 8, dtype="f32"),
+    # several lookahead queries over more chunks than the one-CU select holds
+    # (per-query sets from the streaming select, then the union), up to the
+    # largest sequence the union takes (LSA_MAX_UNION_CHUNKS)
+    P("union_beyond_lds", [64 * 20000], 64, [700], 8, 2, emb_dim=128, Q=2),
+    P("union_max_chunks", [64 * 262144], 64, [300], 1, 1, emb_dim=64, Q=3),
     P("batch64", [64 * (3 + (b * 7) % 23) for b in range(64)], 64, [1 + (b % 3) for b in range(64)], 4, 1),
     P("single_chunk", [64, 128], 64, [1, 2], 4, 2),
 ]
