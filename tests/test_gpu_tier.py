@@ -176,6 +176,9 @@ def _oracle_rows(tc, b, kept, out, lse, rows):
 CASES = [
     ("ragged3", [64 * 300, 64 * 1000, 64 * 77], 64, [40, 100, 77], [80, 250, 154], 8, 2),
     ("c128_one", [128 * 500], 128, [60], [121], 16, 4),
+    # the largest sequence the residency plan takes (LSA_MAX_TIER_CHUNKS) with
+    # the largest reserve (LSA_MAX_TIER_SLOTS slots)
+    ("max_chunks_slots", [64 * 131072], 64, [300], [65536], 1, 1),
 ]
 
 
