@@ -177,6 +177,21 @@ def test_golden_boundary_bin_beyond_lds(kind):
     run_golden([x], 2, 3, 2, 3, 5)
 
 
+def test_golden_largest_row():
+    """A sequence of LSA_MAX_GOLDEN_ENTRIES entries (two rows of 4,194,304
+    logits)."""
+    rng = np.random.default_rng(17)
+    run_golden([_rows(rng, 1, 2, 4194304, "gauss")], 1, 2, 1, 3, 5)
+
+
+@pytest.mark.parametrize("theta", [1, 32, 63])
+def test_golden_most_layers(theta):
+    """LSA_MAX_GOLDEN_LAYERS layers voting, with vote thresholds from one layer
+    to all of them."""
+    rng = np.random.default_rng(23 + theta)
+    run_golden([_rows(rng, 2, 63, 500, "peaked")], 2, 63, theta, 3, 5)
+
+
 def test_golden_tiny_presets():
     import torch
     import paper_2606_09079_amd as L_
