@@ -25,8 +25,9 @@
  *    the ABI.  Device contents (scores, chunk ids) are not validated: inputs
  *    must be finite and produced by the preceding steps.
  *  - Sequences are packed back to back.  Sequence b holds n_b = ctx_tokens[b] /
- *    chunk_size chunks; its chunks have global ids chunk_off[b] .. chunk_off[b]
- *    + n_b - 1 where chunk_off is the exclusive prefix sum of n_b.
+ *    chunk_size chunks (rounded up where the context may end inside a chunk,
+ *    the last chunk then partial); its chunks have global ids chunk_off[b] ..
+ *    chunk_off[b] + n_b - 1 where chunk_off is the exclusive prefix sum of n_b.
  *  - Chunk embeddings E: [sum_b n_b][emb_dim] row-major, row = global chunk id.
  *    Query embeddings: [batch][n_lookahead][emb_dim].
  *  - Scores: sequence b's block starts at element n_lookahead * chunk_off[b] and
