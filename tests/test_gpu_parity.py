@@ -5,8 +5,8 @@ MFMA tiles, several splits, ragged batches, both chunk sizes, every embedding
 dtype and width, GQA groups of 1 to 8, several query tokens and lookahead
 queries, and the degenerate cases (k = 1, k = n, one chunk, tied and signed-zero
 scores).  The five full-size workloads run in the launch configuration the
-benchmark times and are checked on every score and kept id and on sampled
-attention rows.
+benchmark times and are checked on every score, every kept id and every
+attention row.
 """
 import numpy as np
 import pytest

@@ -6,7 +6,7 @@ Small problems cover every kernel shape (1 to 4 layers, 16/32/64 heads, key
 widths 64 and 128), ragged batches, the bound both cutting and not cutting,
 more than 16,384 entries (the streaming selection), the empty recall and the
 all-recalled extremes.  The full-size recall workloads run as the benchmark
-times them, with sampled attention rows.
+times them, with every attention row checked.
 """
 import numpy as np
 import pytest
