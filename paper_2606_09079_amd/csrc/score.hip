@@ -134,11 +134,17 @@ score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restri
 // Several lookahead queries with bf16 embeddings: the scores of a sequence are
 // the product S^T = E qe^T of its [n_b x D] chunk embeddings with the [D x Q]
 // query embeddings, a real dense contraction, so it runs on
-// v_mfma_f32_16x16x32_bf16: each wave takes 16 chunks (A operand: 16 rows of E,
-// 32 dims per step, loaded straight from HBM) against all Q <= 16 queries
-// (B operand, in registers), D / 32 steps.  E is still read exactly once.
+// v_mfma_f32_16x16x32_bf16: each wave takes groups of 16 chunks (A operand: 16
+// rows of E, 32 dims per step, loaded straight from HBM) against all Q <= 16
+// queries (B operand, in registers), D / 32 steps per group.  E is still read
+// exactly once.  A lane's four scores of a group are four consecutive chunks of
+// one query and leave as one 16-byte store.
 constexpr int kMfmaMinQueries = 4;
-constexpr int kMfmaRowsPerWg = 64;  // 4 waves x 16 chunks
+// 16-chunk groups per wave.  The groups share the wave's query operand, so the
+// query embeddings are read from L2 once per 16 x groups chunks: 4 groups up
+// to D = 256, 2 at D = 512 (4 groups of A operands would take 256 registers).
+template <int D> constexpr int mfma_groups() { return D >= 512 ? 2 : 4; }
+template <int D> constexpr int mfma_rows_per_wg() { return 4 * 16 * mfma_groups<D>(); }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -153,15 +159,19 @@ score_mfma_kernel(SeqTable t, const uint16_t* __restrict__ qe, const uint16_t* _
   while (wg >= t.score_wg_off[b + 1]) ++b;
   const int n = t.n[b], Q = t.n_lookahead;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c0 = (wg - t.score_wg_off[b]) * kMfmaRowsPerWg + wave * 16;
+  constexpr int kGroups = mfma_groups<D>();
+  const int c0 = (wg - t.score_wg_off[b]) * mfma_rows_per_wg<D>() + wave * 16 * kGroups;
   if (c0 >= n) return;
-  // A operand rows: chunk c0 + lane % 16 (clamped; its scores are not stored)
-  const int crow = min(c0 + (lane & 15), n - 1);
-  const uint16_t* er = E + (t.chunk_off[b] + crow) * (int64_t)D + 8 * (lane >> 4);
-  bf16x8 ea[kSteps];
+  // A operand rows: chunk c0 + 16 gi + lane % 16 (clamped; its scores are not stored)
+  bf16x8 ea[kGroups][kSteps];
 #pragma unroll
-  for (int st = 0; st < kSteps; ++st)
-    ea[st] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(er + 32 * st));
+  for (int gi = 0; gi < kGroups; ++gi) {
+    const int crow = min(c0 + 16 * gi + (lane & 15), n - 1);
+    const uint16_t* er = E + (t.chunk_off[b] + crow) * (int64_t)D + 8 * (lane >> 4);
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st)
+      ea[gi][st] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(er + 32 * st));
+  }
   // B operand: query lane % 16 (zero beyond Q), dims 32 st + 8 (lane / 16) .. + 7
   const int jq = lane & 15;
   bf16x8 qb[kSteps];
@@ -169,18 +179,29 @@ score_mfma_kernel(SeqTable t, const uint16_t* __restrict__ qe, const uint16_t* _
 #pragma unroll
   for (int st = 0; st < kSteps; ++st)
     qb[st] = jq < Q ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qp + 32 * st)) : bf16x8{};
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  uint32_t* out = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)jq * n;
 #pragma unroll
-  for (int st = 0; st < kSteps; ++st) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ea[st], qb[st], acc, 0, 0, 0);
-  // acc[r] = score of chunk c0 + 4 (lane / 16) + r for query lane % 16
-  if (jq < Q) {
-    uint32_t* out = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)jq * n;
+  for (int gi = 0; gi < kGroups; ++gi) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int c = c0 + 4 * (lane >> 4) + r;
-      uint32_t bits = __float_as_uint(acc[r]);
-      if constexpr (KEYS) bits = order_key<kKeysFromF32>(bits);
-      if (c < n) out[c] = bits;
+    for (int st = 0; st < kSteps; ++st) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ea[gi][st], qb[st], acc, 0, 0, 0);
+    // acc[r] = score of chunk c + r, c = c0 + 16 gi + 4 (lane / 16), for query lane % 16: four
+    // consecutive scores of one query, one 16-byte store when they are aligned and all exist
+    if (jq < Q) {
+      uint32_t bits[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        bits[r] = __float_as_uint(acc[r]);
+        if constexpr (KEYS) bits[r] = order_key<kKeysFromF32>(bits[r]);
+      }
+      const int c = c0 + 16 * gi + 4 * (lane >> 4);
+      if (((reinterpret_cast<uintptr_t>(out + c) & 15u) == 0) && c + 4 <= n) {
+        *reinterpret_cast<uint4*>(out + c) = make_uint4(bits[0], bits[1], bits[2], bits[3]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (c + r < n) out[c + r] = bits[r];
+      }
     }
   }
 }
@@ -241,7 +262,15 @@ int rows_dt(int32_t D) {
 }  // namespace
 
 int score_rows_per_wg(int32_t emb_dtype, int32_t emb_dim, int32_t n_lookahead) {
-  if (use_mfma(emb_dtype, n_lookahead)) return kMfmaRowsPerWg;
+  if (use_mfma(emb_dtype, n_lookahead)) {
+    switch (emb_dim) {
+      case 64: return mfma_rows_per_wg<64>();
+      case 128: return mfma_rows_per_wg<128>();
+      case 256: return mfma_rows_per_wg<256>();
+      case 512: return mfma_rows_per_wg<512>();
+      default: return 0;
+    }
+  }
   switch (emb_dtype) {
     case LSA_F32: return rows_dt<LSA_F32>(emb_dim);
     case LSA_BF16: return rows_dt<LSA_BF16>(emb_dim);
