@@ -505,10 +505,17 @@ union_kernel(SeqTable t, const int32_t* __restrict__ per_query, int32_t k_pitch,
   const int nw = (n + 31) / 32;
   for (int w = tid; w < nw; w += kThreads) bm[w] = 0u;
   __syncthreads();
+  // the ids of 8 queries at a time, all 8 loads in flight before their atomics
   const int32_t* pq = per_query + (int64_t)b * Q * k_pitch;
-  for (int i = tid; i < Q * k; i += kThreads) {
-    const int c = pq[(int64_t)(i / k) * k_pitch + i % k];
-    if ((unsigned)c < (unsigned)n) atomicOr(&bm[c >> 5], 1u << (c & 31));
+  for (int j0 = 0; j0 < Q; j0 += 8) {
+    for (int r = tid; r < k; r += kThreads) {
+      int c[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) c[u] = j0 + u < Q ? pq[(int64_t)(j0 + u) * k_pitch + r] : -1;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if ((unsigned)c[u] < (unsigned)n) atomicOr(&bm[c[u] >> 5], 1u << (c[u] & 31));
+    }
   }
   __syncthreads();
   const int seg = (nw + kThreads - 1) / kThreads;
