@@ -138,13 +138,7 @@ typedef struct lsa_indexer {
 /* Host tier.  Host memory only; read during the call. */
 typedef struct lsa_tier {
   const int32_t* slots;  /* HOST [B]: reserve slots of sequence b, 2 * keep[b] .. LSA_MAX_TIER_SLOTS */
-  int32_t decode_cus;    /* 0, or 8 .. 1024: the decode over the reserve (lsa_tier_attend, lsa_tier_step) runs
-                            on a stream restricted to this many CUs (hipExtStreamCreateWithCUMask), and its
-                            split-K grid is sized to fill exactly those; the other CUs are left to the side
-                            band (lsa_tier_fetch on a stream masked to them), which then takes none of the
-                            decode's CUs.  0: the decode may use every CU.  The same value must reach every
-                            lsa_tier_* call of one tier (workspace sizes follow it).  A multiple of 8 gives
-                            every XCD of MI355X the same share. */
+  int32_t reserved;      /* must be 0 */
   int32_t fetch_workgroups; /* workgroups of lsa_tier_fetch's copy kernel, 0 .. 1024; 0 selects 32, the
                                fastest copy (for a cold fill).  The copy reads the mirror through the memory
                                path a concurrent decode uses, and each copy workgroup slows that decode:

@@ -56,10 +56,7 @@ struct Plan {
 // the kept set of sequence b is at most min(core_keep, keep, history) chunks
 // plus the window.
 // partial: contexts may end inside a chunk (attention alone).
-// target_cus > 0: the attention grid is sized for that many CUs (a decode
-// stream restricted to part of the GPU) instead of all of them.
-lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = nullptr, bool partial = false,
-                     int target_cus = 0) {
+lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = nullptr, bool partial = false) {
   if (p == nullptr) return fail(LSA_ERR_INVALID_ARG, "problem is NULL");
   const int B = p->batch;
   if (B < 1 || B > LSA_MAX_BATCH) return fail(LSA_ERR_INVALID_ARG, "batch %d not in [1, %d]", B, LSA_MAX_BATCH);
@@ -123,9 +120,7 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = n
   int64_t sel_total = 0;
   for (int b = 0; b < B; ++b) sel_total += kept_bound(b);
   const int tpc = C / 32;
-  const bool few = rows <= 16 && B <= kFewSequences;  // one split workgroup per CU, else two
-  const int target = target_cus > 0 ? (few ? target_cus : 2 * target_cus)
-                                    : (few ? kTargetWorkgroupsFew : kTargetWorkgroups);
+  const int target = rows <= 16 && B <= kFewSequences ? kTargetWorkgroupsFew : kTargetWorkgroups;
   int64_t chunk_off = 0, wg_off = 0, swg_off = 0;
   for (int b = 0; b < B; ++b) {
     const int64_t L = p->ctx_tokens[b];
@@ -356,10 +351,9 @@ struct TierPlan {
 };
 
 lsa_status make_tier_plan(const lsa_problem* p, const lsa_tier* tr, TierPlan* tp) {
+  LSA_TRY(make_plan(p, &tp->P));
   if (tr == nullptr) return fail(LSA_ERR_INVALID_ARG, "tier is NULL");
-  if (tr->decode_cus != 0 && (tr->decode_cus < 8 || tr->decode_cus > 1024))
-    return fail(LSA_ERR_INVALID_ARG, "tier decode_cus %d not 0 or in [8, 1024]", tr->decode_cus);
-  LSA_TRY(make_plan(p, &tp->P, nullptr, false, tr->decode_cus));
+  if (tr->reserved != 0) return fail(LSA_ERR_INVALID_ARG, "tier reserved field must be 0");
   if (tr->fetch_workgroups < 0 || tr->fetch_workgroups > 1024)
     return fail(LSA_ERR_INVALID_ARG, "tier fetch_workgroups %d not in [0, 1024]", tr->fetch_workgroups);
   if (tr->slots == nullptr) return fail(LSA_ERR_INVALID_ARG, "tier slots must be a host array of batch entries");
@@ -385,7 +379,7 @@ lsa_status make_tier_plan(const lsa_problem* p, const lsa_tier* tr, TierPlan* tp
   r.ctx_tokens = rctx;
   r.kv_chunk_stride = 0;
   r.kv_head_stride = 0;
-  LSA_TRY(make_plan(&r, &tp->R, nullptr, false, tr->decode_cus));
+  LSA_TRY(make_plan(&r, &tp->R));
   if (tp->R.max_sel != tp->P.max_sel || tp->R.n_units != tp->P.n_units)
     return fail(LSA_ERR_INVALID_ARG, "reserve plan differs from the context plan");
   tp->off_keys = align_up(tp->R.ws_total);

@@ -58,7 +58,7 @@ class lsa_two_level(ctypes.Structure):
 
 
 class lsa_tier(ctypes.Structure):
-    _fields_ = [("slots", ctypes.POINTER(ctypes.c_int32)), ("decode_cus", ctypes.c_int32),
+    _fields_ = [("slots", ctypes.POINTER(ctypes.c_int32)), ("reserved", ctypes.c_int32),
                 ("fetch_workgroups", ctypes.c_int32)]
 
 
@@ -187,9 +187,9 @@ class TwoLevel:
 class Tier:
     """Host tier: reserve slots per sequence (mirrors ``lsa_tier``; keeps its host array alive)."""
 
-    def __init__(self, slots: Sequence[int], fetch_workgroups: int = 0, decode_cus: int = 0):
+    def __init__(self, slots: Sequence[int], fetch_workgroups: int = 0):
         self._slots = (ctypes.c_int32 * max(len(slots), 1))(*slots)
-        self.c = lsa_tier(ctypes.cast(self._slots, ctypes.POINTER(ctypes.c_int32)), decode_cus, fetch_workgroups)
+        self.c = lsa_tier(ctypes.cast(self._slots, ctypes.POINTER(ctypes.c_int32)), 0, fetch_workgroups)
 
     @property
     def ref(self):

@@ -203,13 +203,9 @@ def test_tier_sizes_and_validation():
     for slots in ([79, 200], [80, 199], [80, 65537]):
         assert lib.lsa_tier_sizes(p.ref, L.Tier(slots).ref, None, None, None) == B.LSA_ERR_INVALID_ARG
     assert lib.lsa_tier_sizes(p.ref, None, None, None, None) == B.LSA_ERR_INVALID_ARG
-    for cus, status in ((-1, B.LSA_ERR_INVALID_ARG), (1, B.LSA_ERR_INVALID_ARG), (7, B.LSA_ERR_INVALID_ARG),
-                        (1025, B.LSA_ERR_INVALID_ARG), (8, 0), (248, 0), (1024, 0)):
-        assert lib.lsa_tier_sizes(p.ref, L.Tier([80, 200], decode_cus=cus).ref, None, None, None) == status
-    # a decode on fewer CUs plans fewer split-K workgroups: a smaller partial region
-    _, _, ws_all = L.lsa_tier_sizes(p, L.Tier([80, 200]))
-    _, _, ws_part = L.lsa_tier_sizes(p, L.Tier([80, 200], decode_cus=64))
-    assert ws_part < ws_all
+    bad = L.Tier([80, 200])
+    bad.c.reserved = 1
+    assert lib.lsa_tier_sizes(p.ref, bad.ref, None, None, None) == B.LSA_ERR_INVALID_ARG
     for wgs, status in ((-1, B.LSA_ERR_INVALID_ARG), (1025, B.LSA_ERR_INVALID_ARG), (1024, 0), (4, 0)):
         assert lib.lsa_tier_sizes(p.ref, L.Tier([80, 200], fetch_workgroups=wgs).ref, None, None, None) == status
     la = L.Problem([64 * 300], 64, [40], 8, 2, n_lookahead=2)

@@ -692,74 +692,3 @@ def test_tier_full_size_1m():
     assert torch.equal(out, d_out) and torch.equal(lse, d_lse), "tier step != full-cache attention over its chunks"
     _oracle_rows(tc, 0, chosen, out.cpu().numpy(), lse.cpu().numpy(), [(0, h) for h in range(prob.n_q_heads)])
     log(f"[tier-1m] Level 2 kept {c} of {len(s1)}; attention matches the full cache and the oracle")
-
-
-def _masked_stream(hip, bits):
-    """A HIP stream restricted to the CUs of the given mask bits (bit i is a CU
-    of XCD i % 8 on MI355X)."""
-    import ctypes
-    m = (ctypes.c_uint32 * 8)()
-    for b in bits:
-        m[b // 32] |= 1 << (b % 32)
-    s = ctypes.c_void_p()
-    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), ctypes.c_uint32(256), m) == 0
-    return s
-
-
-def test_tier_decode_on_part_of_the_gpu():
-    """The decode over the reserve on a stream masked to 248 CUs (31 per XCD)
-    and planned for them (decode_cus = 248), the copies on a stream masked to
-    the other 8 (one per XCD): the plan equals the oracle's, every kept chunk's
-    reserve blocks equal the mirror, and every query head's attention equals the
-    oracle's."""
-    import ctypes
-    import torch
-    import paper_2606_09079_amd as L
-    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
-        pytest.skip("the CU masks assume 256 CUs in 8 XCDs")
-    hip = ctypes.CDLL("libamdhip64.so")
-    hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
-                                                 ctypes.POINTER(ctypes.c_uint32)]
-    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
-    prob = synth.Problem("tier_part", [64 * 1000, 64 * 600], 64, [100, 60], 32, 8)
-    slots = [200, 120]
-    tc = TierCase(prob, 13, slots)
-    Tp = L.Tier(slots, decode_cus=248)
-    Tf = L.Tier(slots, fetch_workgroups=8, decode_cus=248)
-    _, _, ws_part = L.lsa_tier_sizes(tc.P, Tp)
-    assert ws_part <= tc.ws_bytes
-    dec_h, side_h = _masked_stream(hip, range(8, 256)), _masked_stream(hip, range(8))
-    try:
-        dec, side = torch.cuda.ExternalStream(dec_h.value), torch.cuda.ExternalStream(side_h.value)
-        rng = np.random.default_rng(3)
-        sets = [np.sort(rng.choice(n, size=k, replace=False)) for n, k in zip(prob.n_chunks, prob.keep)]
-        kept, cnt = tc.kept_tensors(sets)
-        slot_idx = torch.full((prob.batch, tc.pitch), -9, dtype=torch.int32, device="cuda")
-        shp = (prob.batch, prob.n_qtok, prob.n_q_heads, prob.head_dim)
-        out = torch.full(shp, float("nan"), dtype=torch.float32, device="cuda")
-        lse = torch.full(shp[:3], float("nan"), dtype=torch.float32, device="cuda")
-        torch.cuda.synchronize()
-        L.lsa_tier_plan(tc.P, Tp, kept, cnt, None, None, tc.owner, slot_idx, tc.fetch, tc.fetch_count, dec)
-        side.wait_stream(dec)
-        L.lsa_tier_fetch(tc.P, Tf, tc.host_k, tc.host_v, tc.fetch, tc.fetch_count, tc.res_k, tc.res_v, side)
-        dec.wait_stream(side)
-        L.lsa_tier_attend(tc.P, Tp, tc.dev["q"], tc.res_k, tc.res_v, slot_idx, cnt, 0.0, out, lse, tc.ws,
-                          ws_part, dec)
-        torch.cuda.synchronize()
-        g_owner, g_slots = tc.owner.cpu().numpy(), slot_idx.cpu().numpy()
-        slot_lists = []
-        for b, s in enumerate(sets):
-            new_owner, new_slots, _ = oracle.tier_plan([-1] * slots[b], [], [int(c) for c in s])
-            lo, hi = tc.slot_off[b], tc.slot_off[b + 1]
-            assert g_owner[lo:hi].tolist() == new_owner, f"seq {b}: owner table differs from the oracle"
-            assert g_slots[b, :len(s)].tolist() == new_slots, f"seq {b}: slots differ from the oracle"
-            slot_lists.append(new_slots)
-        _check_reserve(tc, sets, slot_lists)
-        o, s_ = out.cpu().numpy(), lse.cpu().numpy()
-        for b in range(prob.batch):
-            _oracle_rows(tc, b, sets[b], o, s_, [(0, h) for h in range(prob.n_q_heads)])
-        log("[tier-part] decode on 248 CUs, copies on 8: plan, reserve and attention match the oracle")
-    finally:
-        torch.cuda.synchronize()
-        hip.hipStreamDestroy(dec_h)
-        hip.hipStreamDestroy(side_h)
