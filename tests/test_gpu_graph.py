@@ -1,6 +1,7 @@
 """The fused decode step replayed from a HIP graph, as a serving loop runs it.
 
-One capture of lsa_decode_step; then, for several seeds, new query embeddings
+One capture of lsa_decode_step (with a caller workspace, and as
+lsa_decode_step_noalloc on the library's scratch); then, for several seeds, new query embeddings
 and queries are copied into the captured input buffers and the graph is
 replayed twice, with eager work and a synchronisation between the replays.
 Every replay must equal, bit for bit, the eager call on the same inputs
@@ -24,8 +25,9 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("noalloc", [False, True], ids=["workspace", "noalloc"])
 @pytest.mark.parametrize("prob", CASES, ids=[p.name for p in CASES])
-def test_fused_step_graph_replays_equal_eager(prob):
+def test_fused_step_graph_replays_equal_eager(prob, noalloc):
     import torch
     import paper_2606_09079_amd as L
     P = L.Problem.from_synth(prob)
@@ -45,7 +47,10 @@ def test_fused_step_graph_replays_equal_eager(prob):
     out_g, lse_g, sel_g, cnt_g, ws_g = buffers()
 
     def step(qe, q, out, lse, sel, cnt, ws):
-        L.lsa_decode_step(P, qe, dev["E"], q, dev["k"], dev["v"], 0.0, out, lse, sel, cnt, ws, wsb)
+        if noalloc:  # the step on the library's own scratch (its address is looked up by the first, eager call)
+            L.lsa_decode_step_noalloc(P, qe, dev["E"], q, dev["k"], dev["v"], 0.0, out, lse, sel, cnt)
+        else:
+            L.lsa_decode_step(P, qe, dev["E"], q, dev["k"], dev["v"], 0.0, out, lse, sel, cnt, ws, wsb)
 
     # warm up on a side stream, then capture
     s = torch.cuda.Stream()
@@ -78,4 +83,4 @@ def test_fused_step_graph_replays_equal_eager(prob):
                 n = int(cnt_e[bb])
                 assert torch.equal(sel_g[bb, :n], sel_e[bb, :n]), f"{prob.name} seed {seed} replay {rep}: kept ids"
         del new
-    log(f"[graph] {prob.name}: 3 input sets x 2 replays equal the eager step")
+    log(f"[graph] {prob.name} ({'noalloc' if noalloc else 'workspace'}): 3 input sets x 2 replays equal the eager step")
