@@ -84,3 +84,110 @@ def test_fused_step_graph_replays_equal_eager(prob, noalloc):
                 assert torch.equal(sel_g[bb, :n], sel_e[bb, :n]), f"{prob.name} seed {seed} replay {rep}: kept ids"
         del new
     log(f"[graph] {prob.name} ({'noalloc' if noalloc else 'workspace'}): 3 input sets x 2 replays equal the eager step")
+
+
+RECALL = synth.Problem("graph_recall", [64 * 300, 64 * 120], 64, [40, 30], 16, 4, n_qtok=2, idx_layers=2,
+                       idx_heads=32, idx_dim=128, idx_rate=0.08)
+TWO_LEVEL = synth.Problem("graph_two_level", [64 * 200 + 17, 64 * 90], 64, [30, 20], 32, 8, n_qtok=4, idx_layers=2,
+                          idx_heads=16, idx_dim=64, idx_rate=0.1, core_keep=[12, 9], nat_heads=32,
+                          window_tokens=[300, 100])
+
+
+def _replays_equal_eager(name, step, inputs, fresh, outs_g, outs_e):
+    """Capture step(bufs) once with the captured inputs, then for each fresh
+    input set replay twice and compare the outputs with an eager call: out,
+    lse and the counts bit for bit, and the written kept ids of each row."""
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(inputs, outs_g)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(inputs, outs_g)
+    torch.cuda.synchronize()
+    for k, new in enumerate(fresh):
+        for key, t in new.items():
+            inputs[key].copy_(t)
+        torch.cuda.synchronize()
+        step(inputs, outs_e)
+        torch.cuda.synchronize()
+        for rep in range(2):
+            for t in outs_g.values():
+                t.fill_(-7 if t.dtype == torch.int32 else float("nan"))
+            graph.replay()
+            torch.cuda.synchronize()
+            for key in ("out", "lse", "cnt"):
+                assert torch.equal(outs_g[key], outs_e[key]), f"{name} input set {k} replay {rep}: {key} differs"
+            # the kept ids: the first cnt[b] entries of each row are written
+            for b in range(outs_e["cnt"].numel()):
+                c = int(outs_e["cnt"][b])
+                assert torch.equal(outs_g["sel"][b, :c], outs_e["sel"][b, :c]), \
+                    f"{name} input set {k} replay {rep}: kept ids of sequence {b} differ"
+    log(f"[graph] {name}: {len(fresh)} input sets x 2 replays equal the eager step")
+
+
+def test_recall_step_graph_replays_equal_eager():
+    import torch
+    import paper_2606_09079_amd as L
+    prob = RECALL
+    P, ix = L.Problem.from_synth(prob), L.Indexer.from_synth(prob)
+    dev = synth.device_inputs(prob, 0)
+    B, Tq, Hq = prob.batch, prob.n_qtok, prob.n_q_heads
+    wsb, max_sel = L.lsa_workspace_size(P), L.lsa_max_sel(P)
+    ws = {"g": torch.zeros(max(wsb, 256), dtype=torch.uint8, device="cuda"),
+          "e": torch.zeros(max(wsb, 256), dtype=torch.uint8, device="cuda")}
+
+    def outs():
+        return {"out": torch.empty(B, Tq, Hq, 128, dtype=torch.float32, device="cuda"),
+                "lse": torch.empty(B, Tq, Hq, dtype=torch.float32, device="cuda"),
+                "sel": torch.full((B, max_sel), -1, dtype=torch.int32, device="cuda"),
+                "cnt": torch.empty(B, dtype=torch.int32, device="cuda")}
+
+    og, oe = outs(), outs()
+    inputs = {"idx_q": dev["idx_q"].clone(), "q": dev["q"].clone()}
+
+    def step(i, o):
+        w = ws["g"] if o is og else ws["e"]
+        L.lsa_recall_step(P, ix, i["idx_q"], dev["idx_w"], dev["idx_k"], i["q"], dev["k"], dev["v"], 0.0, o["out"],
+                          o["lse"], o["sel"], o["cnt"], w, wsb)
+
+    fresh = []
+    for seed in (1, 2, 3):
+        d = synth.device_inputs(prob, seed)
+        fresh.append({"idx_q": d["idx_q"], "q": d["q"]})
+    _replays_equal_eager("recall", step, inputs, fresh, og, oe)
+
+
+def test_two_level_step_graph_replays_equal_eager():
+    import torch
+    import paper_2606_09079_amd as L
+    prob = TWO_LEVEL
+    P, ix, tl = L.Problem.from_synth(prob), L.Indexer.from_synth(prob), L.TwoLevel.from_synth(prob)
+    dev = synth.device_inputs(prob, 0)
+    B, Tq, Hq = prob.batch, prob.n_qtok, prob.n_q_heads
+    max_sel, wsb = L.lsa_two_level_sizes(P, tl)
+    ws = {"g": torch.zeros(max(wsb, 256), dtype=torch.uint8, device="cuda"),
+          "e": torch.zeros(max(wsb, 256), dtype=torch.uint8, device="cuda")}
+
+    def outs():
+        return {"out": torch.empty(B, Tq, Hq, 128, dtype=torch.float32, device="cuda"),
+                "lse": torch.empty(B, Tq, Hq, dtype=torch.float32, device="cuda"),
+                "sel": torch.full((B, max_sel), -1, dtype=torch.int32, device="cuda"),
+                "cnt": torch.empty(B, dtype=torch.int32, device="cuda")}
+
+    og, oe = outs(), outs()
+    inputs = {"idx_q": dev["idx_q"].clone(), "nat_q": dev["nat_q"].clone(), "q": dev["q"].clone()}
+
+    def step(i, o):
+        w = ws["g"] if o is og else ws["e"]
+        L.lsa_two_level_step(P, ix, tl, i["idx_q"], dev["idx_w"], dev["idx_k"], i["nat_q"], dev["nat_w"], dev["nat_k"],
+                             i["q"], dev["k"], dev["v"], 0.0, o["out"], o["lse"], o["sel"], o["cnt"], w, wsb)
+
+    fresh = []
+    for seed in (1, 2, 3):
+        d = synth.device_inputs(prob, seed)
+        fresh.append({"idx_q": d["idx_q"], "nat_q": d["nat_q"], "q": d["q"]})
+    _replays_equal_eager("two-level", step, inputs, fresh, og, oe)
