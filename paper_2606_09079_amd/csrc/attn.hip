@@ -41,7 +41,12 @@
 // attn_combine_few_kernel (at most 16 splits) -- the same merge with one thread
 //   per (output row, float4 slice of O) walking every split itself.
 // The summation order of both combines is fixed, so results are bitwise
-// reproducible.
+// reproducible.  In the fused step with at most 16 splits and one workgroup
+// per CU, the split kernel merges instead: its workgroups store their partials
+// with device-scope (write-through) stores and count themselves in on a
+// per-(b, g) counter that the scoring kernel zeroed; the last to arrive reads
+// every partial with device-scope loads and runs the few-split merge, with no
+// fence and no combine launch.
 #include "lsa_internal.h"
 
 namespace lsa {
@@ -130,7 +135,132 @@ __device__ __forceinline__ Unit unit_of(const SeqTable& t, int wg) {
   return u;
 }
 
-template <int C>
+// s_waitcnt immediates (gfx9 encoding) that wait for the vector-memory counter
+// only: at most N of this wave's loads still outstanding.
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+// ---------------------------------------------------------------------------
+// Merge of the split partials (m, l, O) of one (b, g): weights exp2(m_s - M),
+// O as the weighted sum of the split outputs, divided by
+// L = sum_s exp2(m_s - M) l_s.  Two fixed summation orders, chosen by the
+// largest split count of the call: at most kFewSplits, one thread walks every
+// split of a (row, float4 slice) in order (merge_few); more, 8 split groups
+// and then the groups in order (attn_combine_kernel).  Results are bitwise
+// reproducible.  merge_few serves both the few-split combine kernel and the
+// split kernel's last workgroup, so the fused step and the separate entry
+// points give the same bits.
+
+// Wave-wide reductions with DPP row shifts and row broadcasts; the result is
+// read from lane 63.
+__device__ __forceinline__ float wave_max(float x) {
+  const int ninf = (int)0xFF800000u;
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x111, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x112, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x114, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x118, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x142, 0xA, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x143, 0xC, 0xF, false)));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x111, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x112, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x114, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x118, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xA, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xC, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
+constexpr int kSlices = kHeadDim / 4;        // float4 slices of an output row
+constexpr int kGroups = kThreads / kSlices;  // split groups of the many-split merge (8)
+
+// Partials as the combine kernels read them: plain loads (the split kernel
+// has ended, so its writes are visible).  Offsets in floats.
+struct CachedParts {
+  const float* o;
+  const float* ml;
+  __device__ explicit CachedParts(const AttnArgs& a) : o(a.part_o), ml(a.part_ml) {}
+  __device__ float4 o4(int64_t i) const { return *reinterpret_cast<const float4*>(o + i); }
+  __device__ float2 ml2(int64_t i) const { return *reinterpret_cast<const float2*>(ml + i); }
+};
+
+// Partials as the split kernel's last workgroup reads them: device-scope
+// buffer loads (cache policy sc1), coherent across the XCDs' L2 caches like
+// the device-scope stores that wrote them.
+constexpr int kScopeDevice = 16;  // the sc1 bit of a buffer instruction's cache policy on gfx950
+
+struct DeviceParts {
+  __amdgpu_buffer_rsrc_t ro, rm;
+  __device__ DeviceParts(const SeqTable& t, const AttnArgs& a) {
+    const uint32_t rows = (uint32_t)t.wg_off[t.batch] * (uint32_t)a.rows_pad;
+    ro = __builtin_amdgcn_make_buffer_rsrc(a.part_o, (short)0, (int)(rows * kHeadDim * 4u), 0x00020000);
+    rm = __builtin_amdgcn_make_buffer_rsrc(a.part_ml, (short)0, (int)(rows * 8u), 0x00020000);
+  }
+  __device__ float4 o4(int64_t i) const {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(ro, (int)(i * 4), 0, kScopeDevice);
+    return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
+  }
+  __device__ float2 ml2(int64_t i) const {
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rm, (int)(i * 4), 0, kScopeDevice);
+    return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
+  }
+};
+
+// Row r of the (b, g) group is query token r / G of query head g G + r % G.
+__device__ __forceinline__ int64_t out_row(const AttnArgs& a, int b, int g, int r) {
+  const int tq = r / a.group, h = g * a.group + r % a.group;
+  return ((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h;
+}
+
+// At most kFewSplits splits: one thread merges float4 slice `slice` of row r
+// of (b, g), walking every split itself.
+template <class Parts>
+__device__ __forceinline__ void merge_few(const SeqTable& t, const AttnArgs& a, const Parts& pp, int b, int g, int r,
+                                          int slice) {
+  const int ns = min(t.nsplit[b], kFewSplits);
+  const int64_t unit0 = (int64_t)t.wg_off[b] + (int64_t)g * ns;
+  const int64_t rows_pad = a.rows_pad;
+  float2 v[kFewSplits];
+  float4 ov[kFewSplits];
+#pragma unroll
+  for (int sp = 0; sp < kFewSplits; ++sp) {
+    if (sp < ns) {
+      const int64_t pr = (unit0 + sp) * rows_pad + r;
+      v[sp] = pp.ml2(pr * 2);
+      ov[sp] = pp.o4(pr * kHeadDim + 4 * slice);
+    }
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int sp = 0; sp < kFewSplits; ++sp)
+    if (sp < ns) M = fmaxf(M, v[sp].x);
+  float L = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int sp = 0; sp < kFewSplits; ++sp) {
+    if (sp < ns && v[sp].x != -INFINITY) {
+      const float w = fast_exp2(v[sp].x - M);
+      L += w * v[sp].y;
+      acc.x += w * ov[sp].x;
+      acc.y += w * ov[sp].y;
+      acc.z += w * ov[sp].z;
+      acc.w += w * ov[sp].w;
+    }
+  }
+  const float invL = L > 0.f ? 1.f / L : 0.f;  // an empty kept set gives out = 0, lse = -inf
+  acc.x *= invL;
+  acc.y *= invL;
+  acc.z *= invL;
+  acc.w *= invL;
+  const int64_t orow = out_row(a, b, g, r);
+  *reinterpret_cast<float4*>(a.out + orow * kHeadDim + 4 * slice) = acc;
+  if (slice == 0 && a.lse != nullptr) a.lse[orow] = (M + __log2f(L)) * kLn2;
+}
+
+template <int C, bool MERGE>
 __global__ void __launch_bounds__(kThreads, 2)  // 2 waves per SIMD: <= 256 registers
 attn_split_kernel(SeqTable t, AttnArgs a) {
   __shared__ float sm_o[kAttnWaves][16][kOPad];
@@ -315,18 +445,44 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
           L += f * sm_l[w][r];
         }
       }
-      a.part_o[(unit * rows_pad + r) * kHeadDim + e] = acc;
-      if (e == 0) {
-        a.part_ml[(unit * rows_pad + r) * 2 + 0] = M;
-        a.part_ml[(unit * rows_pad + r) * 2 + 1] = L;
+      float* po = a.part_o + (unit * rows_pad + r) * kHeadDim + e;
+      float* pml = a.part_ml + (unit * rows_pad + r) * 2;
+      if constexpr (MERGE) {
+        // device-scope stores, written through to where every XCD reads them
+        __hip_atomic_store(po, acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (e == 0) {
+          __hip_atomic_store(pml + 0, M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(pml + 1, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      } else {
+        *po = acc;
+        if (e == 0) {
+          pml[0] = M;
+          pml[1] = L;
+        }
       }
     }
   }
+  if constexpr (!MERGE) return;  // a combine kernel merges the splits
+
+  // The last of the ns workgroups of (b, g) to arrive merges the splits.  A
+  // workgroup counts itself in only once its partials are stored (every
+  // thread waits for its stores, then the barrier), so the last one finds
+  // all of them; it reads them with device-scope loads.  No fence is needed:
+  // the partials never sit in a non-coherent cache.
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  __shared__ int sh_last;
+  __syncthreads();
+  if (tid == 0)
+    sh_last = __hip_atomic_fetch_add(a.arrive + b * a.n_kv_heads + g, 1u, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(ns - 1);
+  __syncthreads();
+  if (!sh_last) return;
+  // (the host sets arrive only with at most kFewSplits splits: merge_few's order)
+  const DeviceParts pp(t, a);
+  for (int role = tid; role < a.rows * kSlices; role += kThreads) merge_few(t, a, pp, b, g, role / kSlices, role % kSlices);
 }
 
-// s_waitcnt immediates (gfx9 encoding) that wait for the vector-memory counter
-// only: at most N of this wave's loads still outstanding.
-constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
 // More than 16 query rows per KV head (rows = G * n_qtok, up to 128).  One
 // workgroup per (sequence, kv head, split) serves all the rows, so each K/V
@@ -623,34 +779,15 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   }
 }
 
-// Wave-wide reductions with DPP row shifts and row broadcasts; the result is
-// read from lane 63.
-__device__ __forceinline__ float wave_max(float x) {
-  const int ninf = (int)0xFF800000u;
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x111, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x112, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x114, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x118, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x142, 0xA, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(x), 0x143, 0xC, 0xF, false)));
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
-}
-
-__device__ __forceinline__ float wave_sum(float x) {
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x111, 0xF, 0xF, false));
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x112, 0xF, 0xF, false));
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x114, 0xF, 0xF, false));
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x118, 0xF, 0xF, false));
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xA, 0xF, false));
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xC, 0xF, false));
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
-}
-
+// attn_combine_kernel (more than kFewSplits splits): one workgroup per output
+// row (b, t, h).  Every wave computes M and L itself from all splits' (m, l)
+// (lane l takes splits l, l + 64, ...), so the loads of (m, l) and of the
+// thread's O slices go out in one round; thread (sg, slice) sums splits sg,
+// sg + 8, ... of its slice, and only the final merge of the 8 split groups
+// needs a barrier.
 __global__ void __launch_bounds__(kThreads)
 attn_combine_kernel(SeqTable t, AttnArgs a) {
-  constexpr int kSlices = kHeadDim / 4;              // float4 slices of a row
-  constexpr int kGroups = kThreads / kSlices;        // split groups (8)
-  constexpr int kBatch = 8;                          // splits per thread and round of loads
+  constexpr int kBatch = 8;  // splits per thread and round of loads
   __shared__ float4 sm_red[kGroups][kSlices];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -738,63 +875,19 @@ attn_combine_kernel(SeqTable t, AttnArgs a) {
   if (tid == 0 && a.lse != nullptr) a.lse[orow] = (M + __log2f(L)) * kLn2;
 }
 
-// Few splits per row (at most kFewSplits): one thread per (output row, float4
-// slice of the head dim) walks every split itself -- (m, l) of all splits for
-// M and L, then its own O slices -- so a row needs no cross-thread reduction
-// and a 256-thread workgroup merges 8 rows.  Same arithmetic order for every
-// thread of a row, so results stay bitwise reproducible.
-constexpr int kFewSplits = 16;
-
+// attn_combine_few_kernel (at most kFewSplits splits): one thread per (output
+// row, float4 slice of the head dim), so a 256-thread workgroup merges 8 rows
+// with no cross-thread reduction.
 __global__ void __launch_bounds__(kThreads)
 attn_combine_few_kernel(SeqTable t, AttnArgs a, int n_rows) {
-  constexpr int kSlices = kHeadDim / 4;
   const int gid = blockIdx.x * kThreads + threadIdx.x;
   const int orow = gid / kSlices, slice = gid % kSlices;
   if (orow >= n_rows) return;
-  const int G = a.group;
   const int rows_per_b = a.n_qtok * a.n_q_heads;
   const int b = orow / rows_per_b;
   const int rem = orow - b * rows_per_b;
   const int tq = rem / a.n_q_heads, h = rem - tq * a.n_q_heads;
-  const int g = h / G, r = tq * G + h % G;  // row within the (b, g) group
-  const int ns = min(t.nsplit[b], kFewSplits);
-  const int64_t unit0 = (int64_t)t.wg_off[b] + (int64_t)g * ns;
-  const int64_t rows_pad = a.rows_pad;
-  const float2* ml = reinterpret_cast<const float2*>(a.part_ml) + unit0 * rows_pad + r;
-  const float* po = a.part_o + (unit0 * rows_pad + r) * kHeadDim + 4 * slice;
-  float2 v[kFewSplits];
-  float4 ov[kFewSplits];
-#pragma unroll
-  for (int sp = 0; sp < kFewSplits; ++sp) {
-    if (sp < ns) {
-      v[sp] = ml[sp * rows_pad];
-      ov[sp] = *reinterpret_cast<const float4*>(po + sp * rows_pad * kHeadDim);
-    }
-  }
-  float M = -INFINITY;
-#pragma unroll
-  for (int sp = 0; sp < kFewSplits; ++sp)
-    if (sp < ns) M = fmaxf(M, v[sp].x);
-  float L = 0.f;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-  for (int sp = 0; sp < kFewSplits; ++sp) {
-    if (sp < ns && v[sp].x != -INFINITY) {
-      const float w = fast_exp2(v[sp].x - M);
-      L += w * v[sp].y;
-      acc.x += w * ov[sp].x;
-      acc.y += w * ov[sp].y;
-      acc.z += w * ov[sp].z;
-      acc.w += w * ov[sp].w;
-    }
-  }
-  const float invL = L > 0.f ? 1.f / L : 0.f;  // an empty kept set gives out = 0, lse = -inf
-  acc.x *= invL;
-  acc.y *= invL;
-  acc.z *= invL;
-  acc.w *= invL;
-  *reinterpret_cast<float4*>(a.out + (int64_t)orow * kHeadDim + 4 * slice) = acc;
-  if (slice == 0 && a.lse != nullptr) a.lse[orow] = (M + __log2f(L)) * kLn2;
+  merge_few(t, a, CachedParts(a), b, h / a.group, tq * a.group + h % a.group, slice);
 }
 
 template <int C>
@@ -802,14 +895,15 @@ hipError_t launch_c(const SeqTable& t, const AttnArgs& a, hipStream_t s) {
   const dim3 grid(t.wg_off[t.batch]);
   if (a.rows > 16)
     hipLaunchKernelGGL((attn_rows_kernel<C>), grid, dim3(kThreads), 0, s, t, a);
+  else if (a.arrive != nullptr)
+    hipLaunchKernelGGL((attn_split_kernel<C, true>), grid, dim3(kThreads), 0, s, t, a);
   else
-    hipLaunchKernelGGL((attn_split_kernel<C>), grid, dim3(kThreads), 0, s, t, a);
+    hipLaunchKernelGGL((attn_split_kernel<C, false>), grid, dim3(kThreads), 0, s, t, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.arrive != nullptr && a.rows <= kAttnRowsPerWave) return hipSuccess;  // the split kernel merged the splits
   const int n_rows = t.batch * a.n_qtok * a.n_q_heads;
-  int ns_max = 0;
-  for (int b = 0; b < t.batch; ++b) ns_max = max(ns_max, t.nsplit[b]);
-  if (ns_max <= kFewSplits) {
+  if (a.few_splits) {
     const int per_wg = kThreads / (kHeadDim / 4);
     hipLaunchKernelGGL(attn_combine_few_kernel, dim3((n_rows + per_wg - 1) / per_wg), dim3(kThreads), 0, s, t,
                        a, n_rows);

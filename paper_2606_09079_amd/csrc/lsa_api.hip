@@ -47,7 +47,7 @@ struct Plan {
   int32_t n_hist[LSA_MAX_BATCH] = {};
   int32_t rec_pitch = 0;
   // workspace layout (byte offsets)
-  size_t off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0;
+  size_t off_scores = 0, off_sel = 0, off_cnt = 0, off_pq = 0, off_ml = 0, off_o = 0, off_arrive = 0;
   size_t off_rec = 0, off_rec_cnt = 0, off_nat = 0, off_nat_all = 0;
   size_t ws_total = 0;
 };
@@ -212,6 +212,8 @@ lsa_status make_plan(const lsa_problem* p, Plan* pl, const lsa_two_level* tl = n
     P.off_nat_all = off;  // native keys of every chunk (the fused selection)
     off = align_up(off + (size_t)P.total_chunks * 4);
   }
+  P.off_arrive = off;  // split arrival counters of the fused step, one per (b, g)
+  off = align_up(off + (size_t)B * p->n_kv_heads * 4);
   P.ws_total = off;
   return LSA_OK;
 }
@@ -259,6 +261,22 @@ lsa_status run_topk(const lsa_problem* p, const Plan& P, bool keys_ready, const 
   return LSA_OK;
 }
 
+int max_splits(const Plan& P) {
+  int ns_max = 0;
+  for (int b = 0; b < P.t.batch; ++b) ns_max = std::max(ns_max, P.t.nsplit[b]);
+  return ns_max;
+}
+
+// Whether the split kernel merges its own splits (its last workgroup of each
+// (b, g)) when an earlier kernel of the call zeroes the arrival counters: only
+// where that measured faster than the combine launch, i.e. the split kernel
+// (at most 16 rows) on the one-workgroup-per-CU grid with at most kFewSplits
+// splits.  The merge of 32 splits in one workgroup, and one more wait in each
+// of two workgroups per CU, cost more than the launch.
+bool merge_in_split(const Plan& P) {
+  return P.rows <= kAttnRowsPerWave && P.t.batch <= kFewSequences && max_splits(P) <= kFewSplits;
+}
+
 // count_is_keep: sel_count[b] is known to be min(keep[b], n_b) (the top-k of a
 // fused step with one query embedding wrote it).
 lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, const uint16_t* k,
@@ -286,6 +304,8 @@ lsa_status run_attn(const lsa_problem* p, const Plan& P, const uint16_t* q, cons
   a.n_qtok = p->n_qtok;
   a.rows = P.rows;
   a.rows_pad = P.rows_pad;
+  a.few_splits = max_splits(P) <= kFewSplits ? 1 : 0;
+  a.arrive = P.t.arrive;  // set (and zeroed by the scoring kernel) only where merge_in_split(P)
   LSA_HIP(launch_attn(P.t, a, p->chunk_size, s), "attention launch");
   return LSA_OK;
 }
@@ -664,7 +684,13 @@ lsa_status lsa_decode_step(const lsa_problem* p, const void* query_emb, const vo
   int32_t* sel = sel_idx ? sel_idx : reinterpret_cast<int32_t*>(at(ws, P.off_sel));
   int32_t* cnt = sel_count ? sel_count : reinterpret_cast<int32_t*>(at(ws, P.off_cnt));
   // the scores stay in the workspace, so the scoring kernel writes them as
-  // order keys and the selection reads them without converting
+  // order keys and the selection reads them without converting; it also
+  // zeroes the split arrival counters, so that the attention's last split
+  // workgroup of each (b, g) merges the splits without a combine launch
+  if (merge_in_split(P)) {
+    P.t.arrive = reinterpret_cast<uint32_t*>(at(ws, P.off_arrive));
+    P.t.n_arrive = p->batch * p->n_kv_heads;
+  }
   LSA_HIP(launch_score(P.t, p->emb_dtype, p->emb_dim, query_emb, chunk_emb, scores, true, s), "score launch");
   LSA_TRY(run_topk(p, P, true, scores, sel, cnt, nullptr, ws, s));
   return run_attn(p, P, q, k_cache, v_cache, sel, cnt, softmax_scale, out, lse, ws, s, p->n_lookahead == 1);

@@ -24,6 +24,8 @@ struct SeqTable {
   int32_t wg_off[LSA_MAX_BATCH + 1];   // first attention workgroup of sequence b
   int32_t score_wg_off[LSA_MAX_BATCH + 1];  // first scoring workgroup of sequence b
   int64_t chunk_off[LSA_MAX_BATCH + 1];     // first global chunk id of sequence b
+  uint32_t* arrive;                    // fused step: split arrival counters, zeroed by the scoring kernel
+  int32_t n_arrive;                    //   (B * Hkv words; NULL / 0 otherwise)
 };
 
 // Attention launch parameters.
@@ -49,6 +51,9 @@ struct AttnArgs {
   int32_t n_qtok;
   int32_t rows;          // G * n_qtok
   int32_t rows_pad;      // partial rows per (b, g, split): rows rounded up to 16
+  uint32_t* arrive;      // NULL: a combine kernel merges the splits.  Else one counter per (b, g), zero on
+                         // entry: the last split workgroup of (b, g) to finish merges them (split kernel only)
+  int32_t few_splits;    // 1: every sequence has at most 16 splits (the merge order of the few-split combine)
 };
 
 // Geometry of the attention launch shared by dispatch and kernels.
@@ -64,6 +69,7 @@ constexpr int kHeadDim = 128;
 constexpr int kTargetWorkgroups = 512;
 constexpr int kTargetWorkgroupsFew = 256;
 constexpr int kFewSequences = 8;
+constexpr int kFewSplits = 16;   // splits per (sequence, kv head) up to which the few-split merge order holds
 constexpr int kMaxSplits = 256;  // splits per (sequence, kv head, row group)
 
 // How the selection reads its scores: raw float32 scores, raw int32 scores, or
@@ -91,6 +97,16 @@ __device__ __forceinline__ uint32_t order_key(uint32_t bits) {
 // sign flip of order_key, every score below 2^20 in magnitude falls in one of
 // two bins, and the last digits then run over all the keys.)
 __device__ __forceinline__ uint32_t int_score_key(int32_t s) { return ((uint32_t)s + (1u << 24)) << 7; }
+
+// The fused step's first kernel (the scoring) zeroes the attention's split
+// arrival counters of the same call: wave 0 of workgroup 0, at its end (so
+// that the check does not delay the kernel's first loads), with stores that
+// are coherent across the XCDs' caches.
+__device__ __forceinline__ void zero_arrivals(const SeqTable& t) {
+  if (blockIdx.x == 0 && threadIdx.x < 64 && t.arrive != nullptr)
+    for (int i = threadIdx.x; i < t.n_arrive; i += 64)
+      __hip_atomic_store(t.arrive + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // keys == true writes order keys instead of scores (for the fused step).
 hipError_t launch_score(const SeqTable& t, int32_t emb_dtype, int32_t emb_dim, const void* qe,

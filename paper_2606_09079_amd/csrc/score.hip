@@ -129,6 +129,7 @@ score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restri
       if (sub == 0 && r < n) out_b[(int64_t)j * n + r] = bits;
     }
   }
+  zero_arrivals(t);
 }
 
 // Several lookahead queries with bf16 embeddings: the scores of a sequence are
@@ -204,6 +205,7 @@ score_mfma_kernel(SeqTable t, const uint16_t* __restrict__ qe, const uint16_t* _
       }
     }
   }
+  zero_arrivals(t);  // wave 0 of workgroup 0 never returns early (c0 = 0)
 }
 
 template <int D>

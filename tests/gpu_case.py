@@ -168,6 +168,13 @@ def run_case(prob, seed: int, seqs: Optional[Sequence[int]] = None,
             kept = f_sel[b, :f_cnt[b]].astype(np.int64)
             if modes[b] == "exact":
                 assert np.array_equal(kept, ref_kept[b])
+            if np.array_equal(kept, ref_kept[b]):
+                # same kept set as the attention call above: the fused step merges its splits in
+                # the attention kernel, in the combine's order, so the bits are the same
+                assert np.array_equal(f_out[b].view(np.uint32), g_out[b].view(np.uint32)), \
+                    f"{prob.name} seq {b}: fused output differs from lsa_sparse_decode_attn"
+                assert np.array_equal(f_lse[b].view(np.uint32), g_lse[b].view(np.uint32)), \
+                    f"{prob.name} seq {b}: fused lse differs from lsa_sparse_decode_attn"
             res = band_attn[b] if b in band_attn else ref_attn[b]
             keys = list(res.keys())
             worst_fused = max(worst_fused, parity.check_attention(

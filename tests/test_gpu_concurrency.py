@@ -11,7 +11,9 @@ from gpu_case import log
 
 pytestmark = pytest.mark.gpu
 
-A = synth.Problem("conc_a", [64 * 900, 64 * 300], 64, [90, 30], 32, 8)                    # split kernel
+A = synth.Problem("conc_a", [64 * 900, 64 * 300], 64, [90, 30], 32, 8)                    # split kernel + combine
+# split kernel with at most 16 splits per (b, g): its last workgroups merge them on arrival counters
+M = synth.Problem("conc_m", [64 * 300, 64 * 200, 64 * 250, 64 * 100], 64, [30, 20, 25, 10], 32, 8)
 B = synth.Problem("conc_b", [128 * 200, 128 * 80], 128, [12, 9], 64, 8, n_lookahead=4, n_qtok=16)  # union + many rows
 
 
@@ -40,9 +42,10 @@ class Case:
                                    o["cnt"], o["ws"], self.wsb, stream)
 
 
-def test_two_threads_two_streams_equal_each_step_alone():
+@pytest.mark.parametrize("first", [A, M], ids=["split_combine", "split_merge"])
+def test_two_threads_two_streams_equal_each_step_alone(first):
     import torch
-    a, b = Case(A, 4), Case(B, 5)
+    a, b = Case(first, 4), Case(B, 5)
     ref = {}
     for name, c in (("a", a), ("b", b)):
         o = c.buffers()
@@ -74,4 +77,4 @@ def test_two_threads_two_streams_equal_each_step_alone():
         for bb in range(r["cnt"].numel()):
             n = int(r["cnt"][bb])
             assert torch.equal(o["sel"][bb, :n], r["sel"][bb, :n]), f"step {name}: kept ids of sequence {bb} differ"
-    log("[concurrency] two threads on two streams: both steps equal the steps run alone")
+    log(f"[concurrency] {first.name} and {B.name} on two threads and streams: both equal the steps run alone")

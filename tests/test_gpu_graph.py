@@ -6,7 +6,9 @@ and queries are copied into the captured input buffers and the graph is
 replayed twice, with eager work and a synchronisation between the replays.
 Every replay must equal, bit for bit, the eager call on the same inputs
 (outputs, lse, kept ids and counts).  The step launches only kernels (no
-memory fills), so nothing in it depends on being recorded once.
+memory fills), so nothing in it depends on being recorded once: the arrival
+counters of the split kernel's own merge are zeroed by the scoring kernel of
+the same replay.
 """
 import pytest
 
@@ -22,6 +24,9 @@ CASES = [
     synth.Problem("graph_lookahead", [128 * 200, 128 * 90], 128, [12, 9], 16, 4, n_lookahead=4, n_qtok=4),
     # int8 embeddings, 32 rows per KV head (many-rows kernel)
     synth.Problem("graph_int8_rows", [64 * 256, 64 * 128], 64, [32, 16], 32, 4, emb_dtype="i8", n_qtok=4),
+    # four sequences, at most 16 splits each: the split kernel's last workgroups merge the splits
+    # on arrival counters that the scoring kernel zeroes in every replay
+    synth.Problem("graph_split_merge", [64 * 300, 64 * 200, 64 * 250, 64 * 100], 64, [30, 20, 25, 10], 32, 8),
 ]
 
 
