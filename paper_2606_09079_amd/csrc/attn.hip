@@ -13,10 +13,12 @@
 // MFMAs per product), which keeps ~16 significant bits.
 //
 // attn_split_kernel (rows <= 16) on v_mfma_f32_16x16x32_bf16.  The 4 waves of
-//   a workgroup take consecutive quarters of the split's tiles, each streaming
-//   its own tiles straight into registers (1 KiB per load instruction,
-//   nontemporal hint, two tiles in flight per wave), and merge their (m, l, O)
-//   states through LDS.
+//   a workgroup take every fourth tile of the split (wave w: tiles w, w + 4,
+//   ...), each streaming its own tiles straight into registers (1 KiB per load
+//   instruction, nontemporal hint, two tiles in flight per wave), and merge
+//   their (m, l, O) states through LDS.  Interleaved tiles keep the four waves
+//   of a workgroup within a tile of each other where consecutive quarters left
+//   them waiting for the slowest at the merge.
 //   * QK computes S^T = K Q^T with 16 tokens as M and 16 query rows as N.  The
 //     cache stores each (chunk, head) block in MFMA operand order, and the M
 //     rows of the two 16-token MFMAs of a tile are tokens 8a+0..3 and 8a+4..7,
@@ -280,8 +282,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   const int cnt = a.count_is_keep ? min(t.keep[b], n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
   const int nTall = cnt * TPC;
   const int T0 = split_first(t, b, g, s, ns, nTall), T1 = split_first(t, b, g, s + 1, ns, nTall);
-  const int Tb = T0 + (int)(((int64_t)wave * (T1 - T0)) / kAttnWaves);
-  const int Te = T0 + (int)(((int64_t)(wave + 1) * (T1 - T0)) / kAttnWaves);
+  // wave w takes tiles T0 + w, T0 + w + 4, ... of the split
 
   // ---- query operand: row n16 (rows <= 16 here)
   bf16x8 qb[4];
@@ -303,12 +304,13 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   for (int nb = 0; nb < 8; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  // Tiles Tb..Te-1 of the kept list; tile T is tile T % TPC of kept chunk T / TPC.
-  // Chunk ids are fetched 64 at a time into a register (one per lane) and read
-  // back with readlane, so no scalar load sits between consecutive tiles.
-  const int nT = Te > Tb ? Te - Tb : 0;
-  const int pos0 = Tb / TPC;
-  const int npos = nT > 0 ? (Te - 1) / TPC - pos0 + 1 : 0;
+  // Tiles T0 + wave + 4 i of the kept list (i < nT); tile T is tile T % TPC of
+  // kept chunk T / TPC.  The split's chunk ids are fetched 64 at a time into a
+  // register (one per lane) and read back with readlane, so no scalar load
+  // sits between consecutive tiles.
+  const int nT = T1 - T0 > wave ? (T1 - T0 - wave + kAttnWaves - 1) / kAttnWaves : 0;
+  const int pos0 = T0 / TPC;
+  const int npos = nT > 0 ? (T1 - 1) / TPC - pos0 + 1 : 0;
   const int32_t* sel = a.sel_idx + (int64_t)b * a.sel_pitch + pos0;
   int sel_base = 0;
   int sel_lane = lane < npos ? sel[lane] : 0;
@@ -320,7 +322,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   // Returns how many of the tile's tokens exist: 32, or fewer in the last
   // chunk of a context that ends inside it (and <= 0 for a tile past the end).
   auto load_tile = [&](int i, bf16x8(&kt)[8], bf16x8(&vt)[8]) -> int {
-    const int T = Tb + i;
+    const int T = T0 + wave + kAttnWaves * i;
     const int j = T / TPC - pos0, tt = T % TPC;
     if (j - sel_base >= 64) {  // wave-uniform: next window of chunk ids
       sel_base = j & ~63;
