@@ -115,8 +115,8 @@ struct Unit {
 constexpr int kEvenUnitWeight = 6;
 constexpr int kOddUnitWeight = 5;
 
-__device__ __forceinline__ int split_first(const SeqTable& t, int b, int g, int s, int ns, int n_tiles) {
-  const int base = t.wg_off[b] + g * ns;  // workgroup of split 0 of (b, g)
+__device__ __forceinline__ int split_first(int base, int s, int ns, int n_tiles) {
+  // base: the workgroup of split 0 of (b, g)
   auto weight_below = [&](int j) -> int64_t {  // the weights of splits 0 .. j - 1
     const int64_t even = (int64_t)((base + j + 1) / 2 - (base + 1) / 2);
     return even * kEvenUnitWeight + (int64_t)(j - even) * kOddUnitWeight;
@@ -124,16 +124,13 @@ __device__ __forceinline__ int split_first(const SeqTable& t, int b, int g, int 
   return (int)((int64_t)n_tiles * weight_below(s) / weight_below(ns));
 }
 
-__device__ __forceinline__ Unit unit_of(const SeqTable& t, int wg) {
+__device__ __forceinline__ Unit unit_of(const SeqData& sd, int wg) {
   Unit u;
-  int b = 0;
-  while (wg >= t.wg_off[b + 1]) ++b;
-  const int ns = t.nsplit[b];
-  const int local = wg - t.wg_off[b];
-  u.b = b;
-  u.ns = ns;
-  u.g = local / ns;
-  u.s = local % ns;
+  const int local = wg - sd.wg0;
+  u.b = sd.b;
+  u.ns = sd.ns;
+  u.g = local / sd.ns;
+  u.s = local % sd.ns;
   return u;
 }
 
@@ -272,16 +269,17 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n16 = lane & 15, kg = lane >> 4;
   const int G = a.group;
-  const Unit u = unit_of(t, blockIdx.x);
+  const SeqData sd = seq_data(t, t.wg_off, blockIdx.x);
+  const Unit u = unit_of(sd, blockIdx.x);
   const int b = u.b, g = u.g, s = u.s, ns = u.ns;
 
   // sel_count and the chunk ids are clamped so that malformed device inputs
   // can only give wrong numbers, never an out-of-bounds access.
   constexpr int TPC = C / 32;  // 32-token tiles per chunk
-  const int n_b = t.n[b];
-  const int cnt = a.count_is_keep ? min(t.keep[b], n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
+  const int n_b = sd.n;
+  const int cnt = a.count_is_keep ? min(sd.keep, n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
   const int nTall = cnt * TPC;
-  const int T0 = split_first(t, b, g, s, ns, nTall), T1 = split_first(t, b, g, s + 1, ns, nTall);
+  const int T0 = split_first(sd.wg0 + g * ns, s, ns, nTall), T1 = split_first(sd.wg0 + g * ns, s + 1, ns, nTall);
   // wave w takes tiles T0 + w, T0 + w + 4, ... of the split
 
   // ---- query operand: row n16 (rows <= 16 here)
@@ -314,8 +312,8 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   const int32_t* sel = a.sel_idx + (int64_t)b * a.sel_pitch + pos0;
   int sel_base = 0;
   int sel_lane = lane < npos ? sel[lane] : 0;
-  const uint16_t* kbase = a.k + t.chunk_off[b] * a.chunk_stride + g * a.head_stride + lane * 8;
-  const uint16_t* vbase = a.v + t.chunk_off[b] * a.chunk_stride + g * a.head_stride + lane * 8;
+  const uint16_t* kbase = a.k + sd.chunk_off * a.chunk_stride + g * a.head_stride + lane * 8;
+  const uint16_t* vbase = a.v + sd.chunk_off * a.chunk_stride + g * a.head_stride + lane * 8;
 
   // K and V tiles are 8 KiB each and contiguous in the MFMA-ordered block
   // layout: load instruction q of a tile reads bytes [1024 q, 1024 q + 1024).
@@ -336,7 +334,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
     for (int q = 0; q < 8; ++q) kt[q] = load8_stream(kp + q * 512);
 #pragma unroll
     for (int q = 0; q < 8; ++q) vt[q] = load8_stream(vp + q * 512);
-    return c == n_b - 1 ? t.tail[b] - 32 * tt : 32;
+    return c == n_b - 1 ? sd.tail - 32 * tt : 32;
   };
 
   auto compute_tile = [&](const bf16x8(&kt)[8], bf16x8(&vt)[8], int lim) {
@@ -422,7 +420,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
 
   // ---- this split's partials: rows of the (b, g) group, [unit][rows_pad]
   const int rows_pad = a.rows_pad;
-  const int64_t unit = (int64_t)t.wg_off[b] + (int64_t)g * ns + s;
+  const int64_t unit = (int64_t)sd.wg0 + (int64_t)g * ns + s;
   {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
@@ -549,14 +547,15 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   // ones, in the first half, get 6/5 of the tiles of the odd ones (split_first).
   const int half = (int)(gridDim.x + 1) / 2;
   const int unit_id = (int)blockIdx.x < half ? 2 * (int)blockIdx.x : 2 * ((int)blockIdx.x - half) + 1;
-  const Unit u = unit_of(t, unit_id);
+  const SeqData sd = seq_data(t, t.wg_off, unit_id);
+  const Unit u = unit_of(sd, unit_id);
   const int b = u.b, g = u.g, s = u.s, ns = u.ns;
 
   constexpr int TPC = C / 32;
-  const int n_b = t.n[b];
-  const int cnt = a.count_is_keep ? min(t.keep[b], n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
+  const int n_b = sd.n;
+  const int cnt = a.count_is_keep ? min(sd.keep, n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
   const int nTall = cnt * TPC;
-  const int Tb = split_first(t, b, g, s, ns, nTall), Te = split_first(t, b, g, s + 1, ns, nTall);
+  const int Tb = split_first(sd.wg0 + g * ns, s, ns, nTall), Te = split_first(sd.wg0 + g * ns, s + 1, ns, nTall);
   const int nT = Te > Tb ? Te - Tb : 0;
 
   // this wave's 32 query rows: lane j serves row 32 * wave + j % 32
@@ -602,7 +601,7 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
   // (wave-uniform loads), so the tile copies are the only vector loads in flight
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   const kept_ids_t sel = (kept_ids_t)(uintptr_t)(a.sel_idx + (int64_t)b * a.sel_pitch);
-  const uint16_t* src = (wave < 2 ? a.k : a.v) + t.chunk_off[b] * a.chunk_stride + g * a.head_stride;
+  const uint16_t* src = (wave < 2 ? a.k : a.v) + sd.chunk_off * a.chunk_stride + g * a.head_stride;
 
   // chunk id of the next tile to issue, loaded one issue ahead
   int c_next = nT > 0 ? sel[Tb / TPC] : 0;
@@ -619,7 +618,7 @@ attn_rows_kernel(SeqTable t, AttnArgs a) {
     for (int q = 0; q < 4; ++q)
       __builtin_amdgcn_global_load_lds((const void*)(p + goff[q]),
                                        (void __attribute__((address_space(3)))*)&dst[4 * wave + q][0], 16, 0, 0);
-    return c == n_b - 1 ? t.tail[b] - 32 * tt : 32;
+    return c == n_b - 1 ? sd.tail - 32 * tt : 32;
   };
 
   // Software pipeline over tiles.  Step j (after the barrier that makes tile j

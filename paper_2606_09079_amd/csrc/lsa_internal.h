@@ -98,6 +98,31 @@ __device__ __forceinline__ uint32_t order_key(uint32_t bits) {
 // two bins, and the last digits then run over all the keys.)
 __device__ __forceinline__ uint32_t int_score_key(int32_t s) { return ((uint32_t)s + (1u << 24)) << 7; }
 
+// Sequence b of workgroup wg of a grid laid out by wg_off (first workgroup
+// of each sequence, wg_off[0] = 0) and the per-sequence numbers the kernels
+// read.  Those of sequence 0 are loaded together with the search's first
+// bound (the empty asm statements keep the compiler from deferring the loads
+// past the branch), so a workgroup of sequence 0 -- every one, with one
+// sequence -- waits for one round of kernel-argument loads before it can
+// address memory, not two or three.
+struct SeqData {
+  int b, n, keep, tail, ns, wg0;
+  int64_t chunk_off;
+};
+__device__ __forceinline__ SeqData seq_data(const SeqTable& t, const int32_t* wg_off, int wg) {
+  int n0 = t.n[0], k0 = t.keep[0], tl0 = t.tail[0], ns0 = t.nsplit[0], off1 = wg_off[1];
+  int64_t c0 = t.chunk_off[0];
+  asm volatile("" : "+s"(n0), "+s"(k0), "+s"(tl0), "+s"(ns0), "+s"(off1));
+  asm volatile("" : "+s"(c0));
+  SeqData r{0, n0, k0, tl0, ns0, 0, c0};
+  if (wg >= off1) {
+    int b = 1;
+    while (wg >= wg_off[b + 1]) ++b;
+    r = SeqData{b, t.n[b], t.keep[b], t.tail[b], t.nsplit[b], wg_off[b], t.chunk_off[b]};
+  }
+  return r;
+}
+
 // The fused step's first kernel (the scoring) zeroes the attention's split
 // arrival counters of the same call: wave 0 of workgroup 0, at its end (so
 // that the check does not delay the kernel's first loads), with stores that

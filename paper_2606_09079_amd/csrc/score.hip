@@ -76,14 +76,13 @@ score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restri
   using G = Geo<DT, D>;
   constexpr int es = Elem<DT>::size;
   const int wg = blockIdx.x;
-  int b = 0;
-  while (wg >= t.score_wg_off[b + 1]) ++b;
-  const int n = t.n[b];
+  const SeqData sq = seq_data(t, t.score_wg_off, wg);
+  const int b = sq.b, n = sq.n;
   const int Q = t.n_lookahead;
-  const int row0 = (wg - t.score_wg_off[b]) * G::rows_per_wg;
+  const int row0 = (wg - sq.wg0) * G::rows_per_wg;
   const int sub = threadIdx.x % G::lanes;       // piece index within the row
   const int rw = threadIdx.x / G::lanes;        // row within a pass
-  const uint8_t* Eb = E + t.chunk_off[b] * (int64_t)(D * es);
+  const uint8_t* Eb = E + sq.chunk_off * (int64_t)(D * es);
 
   uint4 e[kPasses][G::ppl];
 #pragma unroll
@@ -98,7 +97,7 @@ score_kernel(SeqTable t, const uint8_t* __restrict__ qe, const uint8_t* __restri
     }
   }
 
-  uint32_t* out_b = scores + (int64_t)Q * t.chunk_off[b];
+  uint32_t* out_b = scores + (int64_t)Q * sq.chunk_off;
   for (int j = 0; j < Q; ++j) {
     const uint8_t* qj = qe + ((int64_t)b * Q + j) * (D * es);
     uint4 qv[G::ppl];
@@ -156,19 +155,18 @@ score_mfma_kernel(SeqTable t, const uint16_t* __restrict__ qe, const uint16_t* _
                   uint32_t* __restrict__ scores) {
   constexpr int kSteps = D / 32;
   const int wg = blockIdx.x;
-  int b = 0;
-  while (wg >= t.score_wg_off[b + 1]) ++b;
-  const int n = t.n[b], Q = t.n_lookahead;
+  const SeqData sq = seq_data(t, t.score_wg_off, wg);
+  const int b = sq.b, n = sq.n, Q = t.n_lookahead;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr int kGroups = mfma_groups<D>();
-  const int c0 = (wg - t.score_wg_off[b]) * mfma_rows_per_wg<D>() + wave * 16 * kGroups;
+  const int c0 = (wg - sq.wg0) * mfma_rows_per_wg<D>() + wave * 16 * kGroups;
   if (c0 >= n) return;
   // A operand rows: chunk c0 + 16 gi + lane % 16 (clamped; its scores are not stored)
   bf16x8 ea[kGroups][kSteps];
 #pragma unroll
   for (int gi = 0; gi < kGroups; ++gi) {
     const int crow = min(c0 + 16 * gi + (lane & 15), n - 1);
-    const uint16_t* er = E + (t.chunk_off[b] + crow) * (int64_t)D + 8 * (lane >> 4);
+    const uint16_t* er = E + (sq.chunk_off + crow) * (int64_t)D + 8 * (lane >> 4);
 #pragma unroll
     for (int st = 0; st < kSteps; ++st)
       ea[gi][st] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(er + 32 * st));
@@ -180,7 +178,7 @@ score_mfma_kernel(SeqTable t, const uint16_t* __restrict__ qe, const uint16_t* _
 #pragma unroll
   for (int st = 0; st < kSteps; ++st)
     qb[st] = jq < Q ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qp + 32 * st)) : bf16x8{};
-  uint32_t* out = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)jq * n;
+  uint32_t* out = scores + (int64_t)Q * sq.chunk_off + (int64_t)jq * n;
 #pragma unroll
   for (int gi = 0; gi < kGroups; ++gi) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};

@@ -290,13 +290,25 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   __shared__ uint32_t sh[4];
   __shared__ uint32_t nonneg[kSelWaves];  // recall: keys >= the key of +0.0, per wave
 
-  const int Q = t.n_lookahead;
-  const int b = blockIdx.x / Q, j = blockIdx.x % Q;
-  // keys of this (sequence, query): t.n[b], or fewer when the count is on the device
-  const int n = sa.dev_n != nullptr ? min(t.n[b], max(sa.dev_n[b], 0)) : t.n[b];
-  int k = min(t.keep[b], n);
+  // (sequence, query) of this workgroup; the numbers of sequence 0 are loaded
+  // with the query count, in one round (see seq_data)
+  int Q = t.n_lookahead, nb = t.n[0], kb = t.keep[0];
+  int64_t cb = t.chunk_off[0];
+  asm volatile("" : "+s"(Q), "+s"(nb), "+s"(kb));
+  asm volatile("" : "+s"(cb));
+  int b = 0, j = blockIdx.x;
+  if (j >= Q) {
+    b = j / Q;
+    j -= b * Q;
+    nb = t.n[b];
+    kb = t.keep[b];
+    cb = t.chunk_off[b];
+  }
+  // keys of this (sequence, query): n_b, or fewer when the count is on the device
+  const int n = sa.dev_n != nullptr ? min(nb, max(sa.dev_n[b], 0)) : nb;
+  int k = min(kb, n);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane >> 4;
-  const uint32_t* s = scores + (int64_t)Q * t.chunk_off[b] + (int64_t)j * t.n[b];
+  const uint32_t* s = scores + (int64_t)Q * cb + (int64_t)j * nb;
   int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
   if (k == 0) {  // no keys (uniform across the workgroup)
     finish_count(t, sa, b, 0, out, sel_count, tid, kSelThreads);
