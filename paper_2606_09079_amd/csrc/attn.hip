@@ -268,7 +268,13 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n16 = lane & 15, kg = lane >> 4;
-  const int G = a.group;
+  // the arguments every workgroup needs before its first loads, in the same
+  // round of kernel-argument loads as its sequence's numbers (see seq_data)
+  int G = a.group, rows = a.rows, n_qtok = a.n_qtok, n_q_heads = a.n_q_heads, sel_pitch = a.sel_pitch;
+  int count_is_keep = a.count_is_keep;
+  int64_t chunk_stride = a.chunk_stride, head_stride = a.head_stride;
+  asm volatile("" : "+s"(G), "+s"(rows), "+s"(n_qtok), "+s"(n_q_heads), "+s"(sel_pitch), "+s"(count_is_keep));
+  asm volatile("" : "+s"(chunk_stride), "+s"(head_stride));
   const SeqData sd = seq_data(t, t.wg_off, blockIdx.x);
   const Unit u = unit_of(sd, blockIdx.x);
   const int b = u.b, g = u.g, s = u.s, ns = u.ns;
@@ -277,7 +283,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   // can only give wrong numbers, never an out-of-bounds access.
   constexpr int TPC = C / 32;  // 32-token tiles per chunk
   const int n_b = sd.n;
-  const int cnt = a.count_is_keep ? min(sd.keep, n_b) : min(max(a.sel_count[b], 0), a.sel_pitch);
+  const int cnt = count_is_keep ? min(sd.keep, n_b) : min(max(a.sel_count[b], 0), sel_pitch);
   const int nTall = cnt * TPC;
   const int T0 = split_first(sd.wg0 + g * ns, s, ns, nTall), T1 = split_first(sd.wg0 + g * ns, s + 1, ns, nTall);
   // wave w takes tiles T0 + w, T0 + w + 4, ... of the split
@@ -286,9 +292,9 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   bf16x8 qb[4];
   {
     const int row = n16;
-    if (row < a.rows) {
+    if (row < rows) {
       const int tq = row / G, h = g * G + row % G;
-      const uint16_t* qp = a.q + (((int64_t)b * a.n_qtok + tq) * a.n_q_heads + h) * kHeadDim + 8 * kg;
+      const uint16_t* qp = a.q + (((int64_t)b * n_qtok + tq) * n_q_heads + h) * kHeadDim + 8 * kg;
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) qb[jj] = load8(qp + 32 * jj);
     } else {
@@ -309,11 +315,11 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   const int nT = T1 - T0 > wave ? (T1 - T0 - wave + kAttnWaves - 1) / kAttnWaves : 0;
   const int pos0 = T0 / TPC;
   const int npos = nT > 0 ? (T1 - 1) / TPC - pos0 + 1 : 0;
-  const int32_t* sel = a.sel_idx + (int64_t)b * a.sel_pitch + pos0;
+  const int32_t* sel = a.sel_idx + (int64_t)b * sel_pitch + pos0;
   int sel_base = 0;
   int sel_lane = lane < npos ? sel[lane] : 0;
-  const uint16_t* kbase = a.k + sd.chunk_off * a.chunk_stride + g * a.head_stride + lane * 8;
-  const uint16_t* vbase = a.v + sd.chunk_off * a.chunk_stride + g * a.head_stride + lane * 8;
+  const uint16_t* kbase = a.k + sd.chunk_off * chunk_stride + g * head_stride + lane * 8;
+  const uint16_t* vbase = a.v + sd.chunk_off * chunk_stride + g * head_stride + lane * 8;
 
   // K and V tiles are 8 KiB each and contiguous in the MFMA-ordered block
   // layout: load instruction q of a tile reads bytes [1024 q, 1024 q + 1024).
@@ -327,7 +333,7 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
       sel_lane = sel_base + lane < npos ? sel[sel_base + lane] : 0;
     }
     const int c = min(max(__builtin_amdgcn_readlane(sel_lane, j - sel_base), 0), n_b - 1);
-    const int64_t off = (int64_t)c * a.chunk_stride + tt * (32 * kHeadDim);
+    const int64_t off = (int64_t)c * chunk_stride + tt * (32 * kHeadDim);
     const uint16_t* kp = kbase + off;
     const uint16_t* vp = vbase + off;
 #pragma unroll
@@ -792,18 +798,27 @@ attn_combine_kernel(SeqTable t, AttnArgs a) {
   __shared__ float4 sm_red[kGroups][kSlices];
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int G = a.group;
-  const int rows_per_b = a.n_qtok * a.n_q_heads;
-  const int b = blockIdx.x / rows_per_b;
-  const int rem = blockIdx.x - b * rows_per_b;
-  const int tq = rem / a.n_q_heads, h = rem - tq * a.n_q_heads;
+  // output row (b, t, h) of this workgroup; sequence 0's split numbers come in
+  // the first round of kernel-argument loads (see seq_data)
+  int G = a.group, n_q_heads = a.n_q_heads, rows_per_b = a.n_qtok * a.n_q_heads, ns = t.nsplit[0];
+  int64_t rows_pad = a.rows_pad;
+  const float* part_o = a.part_o;
+  const float* part_ml = a.part_ml;
+  asm volatile("" : "+s"(G), "+s"(n_q_heads), "+s"(rows_per_b), "+s"(ns));
+  asm volatile("" : "+s"(rows_pad), "+s"(part_o), "+s"(part_ml));
+  int b = 0, wg0 = 0, rem = blockIdx.x;
+  if (rem >= rows_per_b) {
+    b = rem / rows_per_b;
+    rem -= b * rows_per_b;
+    ns = t.nsplit[b];
+    wg0 = t.wg_off[b];
+  }
+  const int tq = rem / n_q_heads, h = rem - tq * n_q_heads;
   const int g = h / G, r = tq * G + h % G;  // row within the (b, g) group
-  const int ns = t.nsplit[b];
-  const int64_t unit0 = (int64_t)t.wg_off[b] + (int64_t)g * ns;
-  const int64_t rows_pad = a.rows_pad;
-  const float2* ml = reinterpret_cast<const float2*>(a.part_ml) + unit0 * rows_pad + r;  // split s at s * rows_pad
+  const int64_t unit0 = (int64_t)wg0 + (int64_t)g * ns;
+  const float2* ml = reinterpret_cast<const float2*>(part_ml) + unit0 * rows_pad + r;  // split s at s * rows_pad
   const int sg = tid / kSlices, e4 = (tid % kSlices) * 4;
-  const float* po = a.part_o + (unit0 * rows_pad + r) * kHeadDim + e4;
+  const float* po = part_o + (unit0 * rows_pad + r) * kHeadDim + e4;
   const int64_t ostride = rows_pad * kHeadDim;
 
   // Every load of the first round is issued up front: (m, l) of all splits

@@ -293,9 +293,11 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   // (sequence, query) of this workgroup; the numbers of sequence 0 are loaded
   // with the query count, in one round (see seq_data)
   int Q = t.n_lookahead, nb = t.n[0], kb = t.keep[0];
-  int64_t cb = t.chunk_off[0];
+  int64_t cb = t.chunk_off[0], ps = pitch_seq, pq = pitch_q;
+  const uint32_t* sc = scores;
+  int32_t* oi = out_idx;
   asm volatile("" : "+s"(Q), "+s"(nb), "+s"(kb));
-  asm volatile("" : "+s"(cb));
+  asm volatile("" : "+s"(cb), "+s"(ps), "+s"(pq), "+s"(sc), "+s"(oi));
   int b = 0, j = blockIdx.x;
   if (j >= Q) {
     b = j / Q;
@@ -308,8 +310,8 @@ topk_select_kernel(SeqTable t, const uint32_t* __restrict__ scores, int32_t* __r
   const int n = sa.dev_n != nullptr ? min(nb, max(sa.dev_n[b], 0)) : nb;
   int k = min(kb, n);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane >> 4;
-  const uint32_t* s = scores + (int64_t)Q * cb + (int64_t)j * nb;
-  int32_t* out = out_idx + b * pitch_seq + j * pitch_q;
+  const uint32_t* s = sc + (int64_t)Q * cb + (int64_t)j * nb;
+  int32_t* out = oi + b * ps + j * pq;
   if (k == 0) {  // no keys (uniform across the workgroup)
     finish_count(t, sa, b, 0, out, sel_count, tid, kSelThreads);
     return;
