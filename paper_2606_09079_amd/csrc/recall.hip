@@ -81,15 +81,15 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
   const int NAT = (OUT == kOutKeys && r.nat_out != nullptr) ? 1 : 0;
   const int LT = L + NAT;
   const int wg = blockIdx.x;
-  int b = 0;
-  while (wg >= t.score_wg_off[b + 1]) ++b;
+  const SeqData sd = seq_data(t, t.score_wg_off, wg);
+  const int b = sd.b;
   // entries of sequence b; in list mode t.n[b] is the list capacity and the
   // count is on the device
-  const int n = OUT == kOutListKeys ? min(t.n[b], max(r.list_count[b], 0)) : t.n[b];
-  if ((wg - t.score_wg_off[b]) * kRecallRowsPerWg >= n) return;  // the whole workgroup: nothing to score
+  const int n = OUT == kOutListKeys ? min(sd.n, max(r.list_count[b], 0)) : sd.n;
+  if ((wg - sd.wg0) * kRecallRowsPerWg >= n) return;  // the whole workgroup: nothing to score
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int e0 = (wg - t.score_wg_off[b]) * kRecallRowsPerWg + wave * 16;
+  const int e0 = (wg - sd.wg0) * kRecallRowsPerWg + wave * 16;
   const int hi = lane >> 4;  // this lane's k-slice 8 hi .. 8 hi + 7 of every 32-wide step
 
   // queries -> LDS in operand order: lane i of block (l, hb, st) holds
@@ -117,10 +117,10 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
     const int pos = min(e0 + (lane & 15), n - 1);
     // a list id is clamped into the key array (its score is then meaningless)
     const int ent = OUT == kOutListKeys
-                        ? min(max(r.list[b * r.list_pitch + pos], 0), (int)(r.total - 1 - t.chunk_off[b]))
+                        ? min(max(r.list[b * r.list_pitch + pos], 0), (int)(r.total - 1 - sd.chunk_off))
                         : pos;
-    const uint16_t* kp = r.k + (t.chunk_off[b] + ent) * CD + 8 * hi;
-    const uint16_t* kn = NAT ? r.nat_k + (t.chunk_off[b] + ent) * CD + 8 * hi : kp;
+    const uint16_t* kp = r.k + (sd.chunk_off + ent) * CD + 8 * hi;
+    const uint16_t* kn = NAT ? r.nat_k + (sd.chunk_off + ent) * CD + 8 * hi : kp;
 #pragma unroll
     for (int l = 0; l < kMaxIdxLayers; ++l) {
       const uint16_t* kl = l < L ? kp + l * r.layer_stride : l == L ? kn : kp;
@@ -164,17 +164,17 @@ recall_score_kernel(SeqTable t, RecallArgs r, void* __restrict__ out) {
     x += __shfl_xor(x, 32);
     if constexpr (OUT == kOutScores) {
       if (lane < 16 && e0 + lane < n)
-        static_cast<float*>(out)[l * r.total + t.chunk_off[b] + e0 + lane] = x;
+        static_cast<float*>(out)[l * r.total + sd.chunk_off + e0 + lane] = x;
     }
     if (l < L) best = fmaxf(best, x);
     else native = x;
   }
   if constexpr (OUT != kOutScores) {
-    const int64_t base = OUT == kOutListKeys ? b * r.list_pitch : t.chunk_off[b];
+    const int64_t base = OUT == kOutListKeys ? b * r.list_pitch : sd.chunk_off;
     if (lane < 16 && e0 + lane < n)
       static_cast<uint32_t*>(out)[base + e0 + lane] = order_key<kKeysFromF32>(__float_as_uint(best));
     if (NAT && lane < 16 && e0 + lane < n)
-      r.nat_out[t.chunk_off[b] + e0 + lane] = order_key<kKeysFromF32>(__float_as_uint(native));
+      r.nat_out[sd.chunk_off + e0 + lane] = order_key<kKeysFromF32>(__float_as_uint(native));
   }
 }
 

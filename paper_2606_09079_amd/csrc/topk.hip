@@ -696,13 +696,20 @@ two_level_select_kernel(SeqTable t, TwoLevelSelArgs a) {
   const SelLds S{hist, cand, keys, tot, bm_gt, bm_eq, sh};
 
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n = min(t.n[b], kSelMaxN);
+  // the table entries and arguments needed before the first loads, in one
+  // round of kernel-argument loads (see seq_data)
+  int nb = t.n[b];
+  int64_t cb = t.chunk_off[b];
+  const uint32_t* l1 = a.l1;
+  const uint32_t* l2 = a.l2;
+  asm volatile("" : "+s"(nb), "+s"(cb), "+s"(l1), "+s"(l2));
+  const int n = min(nb, kSelMaxN);
   int32_t* out = a.out + b * a.pitch;
 
   // Level-1 keys; slots past n read 0 (buffer loads past the end)
   uint32_t kk[kSelKPT];
   {
-    const __amdgpu_buffer_rsrc_t src = raw_buffer(a.l1 + t.chunk_off[b], (uint32_t)n * 4u);
+    const __amdgpu_buffer_rsrc_t src = raw_buffer(l1 + cb, (uint32_t)n * 4u);
 #pragma unroll
     for (int q = 0; q < kSelKPT; ++q)
       kk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
@@ -710,7 +717,7 @@ two_level_select_kernel(SeqTable t, TwoLevelSelArgs a) {
   // the native keys are loaded now too, and masked once the recall is known
   uint32_t nk[kSelKPT];
   {
-    const __amdgpu_buffer_rsrc_t src = raw_buffer(a.l2 + t.chunk_off[b], (uint32_t)n * 4u);
+    const __amdgpu_buffer_rsrc_t src = raw_buffer(l2 + cb, (uint32_t)n * 4u);
 #pragma unroll
     for (int q = 0; q < kSelKPT; ++q)
       nk[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(src, tid * 4, q * kSelThreads * 4, 0);
