@@ -475,7 +475,13 @@ attn_split_kernel(SeqTable t, AttnArgs a) {
   // workgroup counts itself in only once its partials are stored (every
   // thread waits for its stores, then the barrier), so the last one finds
   // all of them; it reads them with device-scope loads.  No fence is needed:
-  // the partials never sit in a non-coherent cache.
+  // the partials never sit in a non-coherent cache.  (On gfx950 an
+  // agent-scope release is an L2 writeback plus a wait for the vector-memory
+  // counter; the writeback exists for ordinary stores held in an XCD's L2,
+  // and these stores are device-scope (sc1) stores that write through, so
+  // the wait alone remains.  The acquire side's device-scope (sc1) loads
+  // are what agent-scope atomic loads compile to, so no L2 invalidate is
+  // needed either.)
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __shared__ int sh_last;
   __syncthreads();
